@@ -1,0 +1,270 @@
+/*
+ * mesa_oracle.c -- plain fp64 CPU reference of the Mesa layer.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path (libmesa, its kernels
+ * or its Python binding) may include, link or call this file.  Only the test
+ * suite, the smoke check and the benchmark's CPU-baseline leg use it.  It
+ * shares no code, header, table or helper with the HIP path.
+ *
+ * What it computes (MesaNet, arXiv 2506.05233):
+ *   For each (batch, head) independently, starting from H_0 = G_0 = 0:
+ *     H_t = gamma_t H_{t-1} + beta_t k_t k_t^T          (Sec. 3, state recurrences;
+ *     G_t = gamma_t G_{t-1} + beta_t v_t k_t^T           App. E, gated form)
+ *     q*_t = (H_t + Lambda)^{-1} q_t                     (Eq. mesa-layer-final)
+ *     o_t  = G_t q*_t                                    (App. D, Eq. app-mesa-dynamics)
+ *   The solve is either
+ *     - fixed-step conjugate gradients following App. C, Alg. 1 with tolerance
+ *       zero: Jacobi-scaled start x0 = q / diag(H_t + Lambda) (App. C text),
+ *       one matrix-vector product for the first residual, then n_cg loop
+ *       iterations, or
+ *     - an exact Cholesky solve (the closed form of Eq. mesa-layer-objective).
+ *   Nothing is chunked: this is the sequential recurrence, token by token.
+ *
+ * Readings adopted where the paper is ambiguous (all listed in the design doc):
+ *   - the Jacobi diagonal is that of the system being solved, H_t + Lambda;
+ *   - n_cg counts loop iterations, so a solve does n_cg + 1 products;
+ *   - with tolerance zero the loop stops when the new squared residual is
+ *     exactly zero; it also stops, keeping x, when the squared residual is zero
+ *     before a step or when p^T A p <= 0 (guards for q = 0 and breakdown);
+ *   - beta enters once: H += beta k k^T, G += beta v k^T;
+ *   - decode updates the state with the new token first, then solves.
+ *
+ * All arrays are dense, row-major, fp64, host memory, owned by the caller.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { ORACLE_SOLVE_CG = 0, ORACLE_SOLVE_CHOLESKY = 1 };
+enum { ORACLE_INIT_JACOBI = 0, ORACLE_INIT_QUERY = 1 };
+
+/* Fixed-step CG on the SPD system A x = b (App. C, Alg. 1, epsilon = 0).
+ * init = ORACLE_INIT_JACOBI: x0 = b / diag(A)  (the paper's choice);
+ * init = ORACLE_INIT_QUERY : x0 = b            (the "zero CG steps gives GLA"
+ *                                               remark of Sec. 4; tests only).
+ * work must hold 3n doubles.  Returns the number of loop iterations done. */
+int oracle_cg(const double* A, const double* b, int64_t n, int n_cg, int init,
+              double* x, double* work)
+{
+    double* r = work;
+    double* p = work + n;
+    double* w = work + 2 * n;
+    for (int64_t i = 0; i < n; ++i)
+        x[i] = (init == ORACLE_INIT_QUERY) ? b[i] : b[i] / A[i * n + i];
+    double delta = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        double ax = 0.0;
+        for (int64_t j = 0; j < n; ++j) ax += A[i * n + j] * x[j];
+        r[i] = b[i] - ax;
+        p[i] = r[i];
+        delta += r[i] * r[i];
+    }
+    int it = 0;
+    for (; it < n_cg; ++it) {
+        if (delta == 0.0) break;
+        double pw = 0.0;
+        for (int64_t i = 0; i < n; ++i) {
+            double s = 0.0;
+            for (int64_t j = 0; j < n; ++j) s += A[i * n + j] * p[j];
+            w[i] = s;
+            pw += p[i] * s;
+        }
+        if (!(pw > 0.0)) break;
+        double alpha = delta / pw;
+        double delta_new = 0.0;
+        for (int64_t i = 0; i < n; ++i) {
+            x[i] += alpha * p[i];
+            r[i] -= alpha * w[i];
+            delta_new += r[i] * r[i];
+        }
+        if (delta_new == 0.0) { ++it; break; }
+        double beta_cg = delta_new / delta;
+        for (int64_t i = 0; i < n; ++i) p[i] = r[i] + beta_cg * p[i];
+        delta = delta_new;
+    }
+    return it;
+}
+
+/* Exact solve of the SPD system A x = b by Cholesky, A = L L^T.
+ * work must hold n*n doubles.  Returns 0, or -1 if A is not positive definite. */
+int oracle_cholesky_solve(const double* A, const double* b, int64_t n, double* x, double* work)
+{
+    double* L = work;
+    memset(L, 0, (size_t)(n * n) * sizeof(double));
+    for (int64_t j = 0; j < n; ++j) {
+        double d = A[j * n + j];
+        for (int64_t m = 0; m < j; ++m) d -= L[j * n + m] * L[j * n + m];
+        if (!(d > 0.0)) return -1;
+        double ljj = sqrt(d);
+        L[j * n + j] = ljj;
+        for (int64_t i = j + 1; i < n; ++i) {
+            double s = A[i * n + j];
+            for (int64_t m = 0; m < j; ++m) s -= L[i * n + m] * L[j * n + m];
+            L[i * n + j] = s / ljj;
+        }
+    }
+    /* forward: L y = b (y stored in x) */
+    for (int64_t i = 0; i < n; ++i) {
+        double s = b[i];
+        for (int64_t m = 0; m < i; ++m) s -= L[i * n + m] * x[m];
+        x[i] = s / L[i * n + i];
+    }
+    /* backward: L^T x = y */
+    for (int64_t i = n - 1; i >= 0; --i) {
+        double s = x[i];
+        for (int64_t m = i + 1; m < n; ++m) s -= L[m * n + i] * x[m];
+        x[i] = s / L[i * n + i];
+    }
+    return 0;
+}
+
+/* One token of the recurrence on one (batch, head): update, solve, read out.
+ * H [dk*dk], G [dv*dk] are updated in place.  A_work holds dk*dk, solve_work
+ * holds max(3*dk, dk*dk), xq holds dk (returns q*).  Returns 0 or -1. */
+static int mesa_token(double* H, double* G, const double* q, const double* k, const double* v,
+                      double gamma, double beta, const double* lambda, int64_t dk, int64_t dv,
+                      int n_cg, int solver, int init, double* o, double* xq,
+                      double* A_work, double* solve_work)
+{
+    for (int64_t a = 0; a < dk; ++a)
+        for (int64_t b = 0; b < dk; ++b)
+            H[a * dk + b] = gamma * H[a * dk + b] + beta * k[a] * k[b];
+    for (int64_t a = 0; a < dv; ++a)
+        for (int64_t b = 0; b < dk; ++b)
+            G[a * dk + b] = gamma * G[a * dk + b] + beta * v[a] * k[b];
+    for (int64_t a = 0; a < dk; ++a)
+        for (int64_t b = 0; b < dk; ++b)
+            A_work[a * dk + b] = H[a * dk + b] + (a == b ? lambda[a] : 0.0);
+    if (solver == ORACLE_SOLVE_CHOLESKY) {
+        if (oracle_cholesky_solve(A_work, q, dk, xq, solve_work) != 0) return -1;
+    } else {
+        oracle_cg(A_work, q, dk, n_cg, init, xq, solve_work);
+    }
+    for (int64_t a = 0; a < dv; ++a) {
+        double s = 0.0;
+        for (int64_t b = 0; b < dk; ++b) s += G[a * dk + b] * xq[b];
+        o[a] = s;
+    }
+    return 0;
+}
+
+typedef struct {
+    const double *q, *k, *v, *gamma, *beta, *lambda;
+    int64_t B, Hh, T, dk, dv;
+    int n_cg, solver, init;
+    double *out, *qstar, *final_H, *final_G;
+    double *state_H, *state_G;   /* decode: in/out states; forward: NULL */
+    int n_threads, tid;
+    int status;
+} oracle_job;
+
+static void* forward_worker(void* arg)
+{
+    oracle_job* j = (oracle_job*)arg;
+    const int64_t dk = j->dk, dv = j->dv, T = j->T;
+    double* H = (double*)malloc((size_t)(dk * dk) * sizeof(double));
+    double* G = (double*)malloc((size_t)(dv * dk) * sizeof(double));
+    double* A = (double*)malloc((size_t)(dk * dk) * sizeof(double));
+    double* sw = (double*)malloc((size_t)(dk * dk + 3 * dk) * sizeof(double));
+    double* xq = (double*)malloc((size_t)dk * sizeof(double));
+    j->status = 0;
+    for (int64_t bh = j->tid; bh < j->B * j->Hh; bh += j->n_threads) {
+        const int64_t h = bh % j->Hh;
+        memset(H, 0, (size_t)(dk * dk) * sizeof(double));
+        memset(G, 0, (size_t)(dv * dk) * sizeof(double));
+        for (int64_t t = 0; t < T; ++t) {
+            const int64_t tok = bh * T + t;
+            if (mesa_token(H, G, j->q + tok * dk, j->k + tok * dk, j->v + tok * dv,
+                           j->gamma[tok], j->beta[tok], j->lambda + h * dk, dk, dv,
+                           j->n_cg, j->solver, j->init, j->out + tok * dv, xq, A, sw) != 0)
+                j->status = -1;
+            if (j->qstar) memcpy(j->qstar + tok * dk, xq, (size_t)dk * sizeof(double));
+        }
+        if (j->final_H) memcpy(j->final_H + bh * dk * dk, H, (size_t)(dk * dk) * sizeof(double));
+        if (j->final_G) memcpy(j->final_G + bh * dv * dk, G, (size_t)(dv * dk) * sizeof(double));
+    }
+    free(H); free(G); free(A); free(sw); free(xq);
+    return NULL;
+}
+
+static void* decode_worker(void* arg)
+{
+    oracle_job* j = (oracle_job*)arg;
+    const int64_t dk = j->dk, dv = j->dv;
+    double* A = (double*)malloc((size_t)(dk * dk) * sizeof(double));
+    double* sw = (double*)malloc((size_t)(dk * dk + 3 * dk) * sizeof(double));
+    double* xq = (double*)malloc((size_t)dk * sizeof(double));
+    j->status = 0;
+    for (int64_t bh = j->tid; bh < j->B * j->Hh; bh += j->n_threads) {
+        const int64_t h = bh % j->Hh;
+        if (mesa_token(j->state_H + bh * dk * dk, j->state_G + bh * dv * dk,
+                       j->q + bh * dk, j->k + bh * dk, j->v + bh * dv,
+                       j->gamma[bh], j->beta[bh], j->lambda + h * dk, dk, dv,
+                       j->n_cg, j->solver, j->init, j->out + bh * dv, xq, A, sw) != 0)
+            j->status = -1;
+        if (j->qstar) memcpy(j->qstar + bh * dk, xq, (size_t)dk * sizeof(double));
+    }
+    free(A); free(sw); free(xq);
+    return NULL;
+}
+
+static int run_jobs(oracle_job* proto, void* (*fn)(void*), int n_threads)
+{
+    const int64_t units = proto->B * proto->Hh;
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > units) n_threads = (int)(units > 0 ? units : 1);
+    oracle_job* jobs = (oracle_job*)malloc((size_t)n_threads * sizeof(oracle_job));
+    pthread_t* th = (pthread_t*)malloc((size_t)n_threads * sizeof(pthread_t));
+    for (int i = 0; i < n_threads; ++i) {
+        jobs[i] = *proto;
+        jobs[i].n_threads = n_threads;
+        jobs[i].tid = i;
+    }
+    for (int i = 1; i < n_threads; ++i) pthread_create(&th[i], NULL, fn, &jobs[i]);
+    fn(&jobs[0]);
+    int status = jobs[0].status;
+    for (int i = 1; i < n_threads; ++i) {
+        pthread_join(th[i], NULL);
+        if (jobs[i].status != 0) status = jobs[i].status;
+    }
+    free(jobs);
+    free(th);
+    return status;
+}
+
+/* Whole-sequence forward.  q,k [B,Hh,T,dk]; v [B,Hh,T,dv]; gamma,beta [B,Hh,T];
+ * lambda [Hh,dk]; out [B,Hh,T,dv]; optional (may be NULL): qstar [B,Hh,T,dk],
+ * final_H [B,Hh,dk,dk], final_G [B,Hh,dv,dk].  Returns 0, or -1 if a Cholesky
+ * solve met a non-positive pivot. */
+int oracle_forward(const double* q, const double* k, const double* v, const double* gamma,
+                   const double* beta, const double* lambda, int64_t B, int64_t Hh, int64_t T,
+                   int64_t dk, int64_t dv, int n_cg, int solver, int init, double* out,
+                   double* qstar, double* final_H, double* final_G, int n_threads)
+{
+    oracle_job proto;
+    memset(&proto, 0, sizeof(proto));
+    proto.q = q; proto.k = k; proto.v = v; proto.gamma = gamma; proto.beta = beta;
+    proto.lambda = lambda; proto.B = B; proto.Hh = Hh; proto.T = T; proto.dk = dk; proto.dv = dv;
+    proto.n_cg = n_cg; proto.solver = solver; proto.init = init; proto.out = out;
+    proto.qstar = qstar; proto.final_H = final_H; proto.final_G = final_G;
+    return run_jobs(&proto, forward_worker, n_threads);
+}
+
+/* One recurrent decode step from the given states (updated in place).
+ * state_H [N,Hh,dk,dk]; state_G [N,Hh,dv,dk]; q,k [N,Hh,dk]; v [N,Hh,dv];
+ * gamma,beta [N,Hh]; lambda [Hh,dk]; out [N,Hh,dv]; qstar [N,Hh,dk] or NULL. */
+int oracle_decode_step(double* state_H, double* state_G, const double* q, const double* k,
+                       const double* v, const double* gamma, const double* beta,
+                       const double* lambda, int64_t N, int64_t Hh, int64_t dk, int64_t dv,
+                       int n_cg, int solver, int init, double* out, double* qstar, int n_threads)
+{
+    oracle_job proto;
+    memset(&proto, 0, sizeof(proto));
+    proto.q = q; proto.k = k; proto.v = v; proto.gamma = gamma; proto.beta = beta;
+    proto.lambda = lambda; proto.B = N; proto.Hh = Hh; proto.T = 1; proto.dk = dk; proto.dv = dv;
+    proto.n_cg = n_cg; proto.solver = solver; proto.init = init; proto.out = out;
+    proto.qstar = qstar; proto.state_H = state_H; proto.state_G = state_G;
+    return run_jobs(&proto, decode_worker, n_threads);
+}
