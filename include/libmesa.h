@@ -1,0 +1,170 @@
+/*
+ * libmesa -- the chunkwise-parallel Mesa layer (MesaNet, arXiv 2506.05233) on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * For every (batch b, head h) the layer keeps two gated states, starting from
+ * H_0 = G_0 = 0 (Sec. 3, "A new parallelizable Mesa layer"; App. D, Eq.
+ * app-mesa-dynamics; App. E for the input gate):
+ *
+ *     H_t = gamma_t H_{t-1} + beta_t k_t k_t^T        (d_k x d_k, symmetric)
+ *     G_t = gamma_t G_{t-1} + beta_t v_t k_t^T        (d_v x d_k)
+ *     q*_t ~= (H_t + Lambda)^{-1} q_t                 (fixed-step CG, App. C, Alg. 1)
+ *     o_t  = G_t q*_t                                 (Eq. mesa-layer-final)
+ *
+ * The solve is Alg. 1 with tolerance zero: x0 = q_t / diag(H_t + Lambda), one
+ * product for the first residual, then n_cg iterations (n_cg + 1 products).
+ * An iteration stops a column, keeping its x, when its squared residual is
+ * exactly zero or when p^T A p <= 0.
+ *
+ * The forward pass is evaluated chunkwise (Sec. 3, Eq. gla_matrix; App. D,
+ * Eq. gla and Eq. q_star_parallel): states are materialised only at chunk
+ * boundaries, and every CG product (H_t + Lambda) p inside a chunk is an
+ * inter-chunk state term plus a causally masked, gate-weighted K K^T term.
+ *
+ * Conventions for every entry point
+ *   - Every array pointer is a DEVICE pointer owned by the caller.  The library
+ *     allocates and frees nothing and keeps no state between calls.
+ *   - Arrays are dense and row-major (C order) with the shapes given below.
+ *   - q, k, v have element type `dtype` (MESA_DTYPE_F32 or MESA_DTYPE_BF16);
+ *     gates, Lambda, states and outputs are fp32.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *     the call returns without synchronising.  Errors raised while kernels run
+ *     surface at the caller's next synchronisation.
+ *   - Argument checks run on the host before any launch; a failed check
+ *     returns its status code and neither launches nor writes anything.
+ *   - Value ranges are preconditions and are not checked (that would read
+ *     device memory): gamma, beta in [0, 1], Lambda > 0, finite inputs.
+ *   - Outputs must not overlap inputs.  Calls on different streams are
+ *     independent; calls that share output or workspace memory must not overlap.
+ */
+#ifndef LIBMESA_H
+#define LIBMESA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of q, k and v. */
+#define MESA_DTYPE_F32 0
+#define MESA_DTYPE_BF16 1
+
+/* Arithmetic of the matrix products inside CG and the read-out.
+ *   MESA_PREC_AUTO : MESA_PREC_F32 for fp32 inputs, MESA_PREC_BF16 for bf16 inputs.
+ *   MESA_PREC_F32  : fp32 products with fp32 accumulation (fp32-accurate).
+ *   MESA_PREC_BF16 : matrix-core products with bf16 operands (the fp32 state and
+ *                    the fp32 CG direction are rounded to bf16 as operands) and
+ *                    fp32 accumulation; every CG vector, scalar and reduction
+ *                    stays fp32 (App. H.5 keeps the solver in fp32; this mode
+ *                    trades operand precision for matrix-core throughput). */
+#define MESA_PREC_AUTO 0
+#define MESA_PREC_F32 1
+#define MESA_PREC_BF16 2
+
+/* Status codes. */
+#define MESA_OK 0
+#define MESA_ERR_NULL 1          /* a required pointer is NULL                         */
+#define MESA_ERR_SHAPE 2         /* a size is negative or the sizes are inconsistent  */
+#define MESA_ERR_UNSUPPORTED 3   /* d_k, d_v, chunk, dtype or precision not supported */
+#define MESA_ERR_ARG 4           /* n_cg out of range, or outputs overlap inputs       */
+#define MESA_ERR_WORKSPACE 5     /* workspace too small                                */
+#define MESA_ERR_HIP 6           /* the HIP runtime refused a launch                   */
+
+/* Supported sizes: d_k, d_v in {64, 128}; chunk in {16, 32, 64}; 0 <= n_cg <= 1024.
+ * Any seq_len >= 0 is accepted; a last chunk shorter than `chunk` is handled.
+ * batch, heads or seq_len equal to 0 is a no-op that returns MESA_OK. */
+#define MESA_MAX_NCG 1024
+
+/* Bytes of device workspace mesa_forward needs: the fp32 states entering every
+ * chunk, H_c [batch, heads, ceil(seq_len/chunk), d_k, d_k] and the transposed
+ * value-key state G_c^T [..., d_k, d_v] (App. D: states are kept only at chunk
+ * boundaries c = 0, C, 2C, ...).  Returns 0 for unsupported or empty sizes. */
+size_t mesa_forward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
+                                    int64_t d_v, int chunk);
+
+/* Sequence forward pass of the Mesa layer (Eq. mesa-layer-final, chunkwise
+ * form of App. D).
+ *   q, k    [batch, heads, seq_len, d_k]   dtype
+ *   v       [batch, heads, seq_len, d_v]   dtype
+ *   gamma   [batch, heads, seq_len]        fp32, forget gates in [0, 1]
+ *   beta    [batch, heads, seq_len]        fp32, input gates in [0, 1]
+ *   lambda  [heads, d_k]                   fp32, diagonal of Lambda, > 0
+ *   n_cg    CG loop iterations (Alg. 1's k_max), 0 <= n_cg <= MESA_MAX_NCG
+ *   chunk   chunk size C
+ *   out     [batch, heads, seq_len, d_v]   fp32, o_t = G_t q*_t
+ *   workspace / workspace_bytes: at least mesa_forward_workspace_bytes(...)
+ *   stream  hipStream_t
+ * Uses MESA_PREC_AUTO. */
+int mesa_forward(const void* q, const void* k, const void* v, const float* gamma,
+                 const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                 int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
+                 float* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* mesa_forward with a chosen precision and optional extra outputs (each may be NULL):
+ *   qstar_out [batch, heads, seq_len, d_k]  fp32, the CG solutions q*_t
+ *   final_H   [batch, heads, d_k, d_k]      fp32, H_T after the last token
+ *   final_G   [batch, heads, d_v, d_k]      fp32, G_T after the last token
+ * final_H and final_G are the recurrent state that mesa_decode_step continues
+ * from (prefill -> decode).  If out is NULL only the state scan runs: then
+ * qstar_out must be NULL, final_H and final_G must be given, and workspace may
+ * be NULL with workspace_bytes 0. */
+int mesa_forward_ex(const void* q, const void* k, const void* v, const float* gamma,
+                    const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                    int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
+                    int precision, float* out, float* qstar_out, float* final_H, float* final_G,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* The two launches of mesa_forward_ex, callable one at a time (same argument
+ * meanings and checks).  mesa_forward_ex(out != NULL) == mesa_forward_states
+ * followed by mesa_forward_solve on the same workspace and stream.
+ *
+ * mesa_forward_states: step (a), the chunk-state scan.  Writes the states
+ * entering every chunk into the workspace (layout as described for
+ * mesa_forward_workspace_bytes) and, when non-NULL, final_H / final_G.
+ * One kernel launch. */
+int mesa_forward_states(const void* k, const void* v, const float* gamma, const float* beta,
+                        int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v,
+                        int dtype, int chunk, float* final_H, float* final_G, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/* mesa_forward_solve: steps (b) and (c), the chunked CG solve and the
+ * read-out o_t = G_t q*_t, from the states a previous mesa_forward_states
+ * call left in the workspace (same sizes, dtype, chunk, k, v, gamma, beta).
+ * qstar_out may be NULL.  One kernel launch. */
+int mesa_forward_solve(const void* q, const void* k, const void* v, const float* gamma,
+                       const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                       int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
+                       int precision, float* out, float* qstar_out, const void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* One recurrent decode step for `batch` independent sequences (Sec. 3,
+ * recurrent inference mode; App. C last paragraph: CG is applied to H_t + Lambda
+ * directly).  For each (sequence, head), in place:
+ *     H <- gamma H + beta k k^T;  G <- gamma G + beta v k^T;
+ *     q* = CG_{n_cg}(H + Lambda, q);  out = G q*.
+ *   state_H [batch, heads, d_k, d_k]  fp32, in/out
+ *   state_G [batch, heads, d_v, d_k]  fp32, in/out
+ *   q, k    [batch, heads, d_k]       dtype
+ *   v       [batch, heads, d_v]       dtype
+ *   gamma, beta [batch, heads]        fp32
+ *   lambda  [heads, d_k]              fp32
+ *   out     [batch, heads, d_v]       fp32
+ * Arithmetic is fp32 throughout. */
+int mesa_decode_step(float* state_H, float* state_G, const void* q, const void* k, const void* v,
+                     const float* gamma, const float* beta, const float* lambda, int64_t batch,
+                     int64_t heads, int64_t d_k, int64_t d_v, int dtype, int n_cg, float* out,
+                     void* stream);
+
+/* Static text for a status code (never NULL). */
+const char* mesa_status_string(int status);
+
+/* Library ABI version (major * 100 + minor). */
+int mesa_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBMESA_H */

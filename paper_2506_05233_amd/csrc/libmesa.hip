@@ -1,0 +1,264 @@
+// libmesa C ABI: argument validation, workspace sizing and kernel launches.
+// The contract of every entry point is documented in include/libmesa.h.
+#include "libmesa.h"
+
+#include <stdint.h>
+#include <string.h>
+
+#include "mesa_kernels.hpp"
+
+namespace {
+
+using mesa::ForwardShape;
+
+bool dim_ok(int64_t d) { return d == 64 || d == 128; }
+bool chunk_ok(int c) { return c == 16 || c == 32 || c == 64; }
+
+int64_t n_chunks_of(int64_t seq_len, int chunk) { return (seq_len + chunk - 1) / chunk; }
+
+// Byte range [p, p + n) of a device array, for overlap checks.
+struct Range {
+    uintptr_t lo, hi;
+};
+Range range_of(const void* p, int64_t bytes) { return {uintptr_t(p), uintptr_t(p) + uintptr_t(bytes)}; }
+bool overlaps(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+int check_sizes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v,
+                int dtype, int n_cg)
+{
+    if (batch < 0 || heads < 0 || seq_len < 0 || d_k < 0 || d_v < 0) return MESA_ERR_SHAPE;
+    if (!dim_ok(d_k) || !dim_ok(d_v)) return MESA_ERR_UNSUPPORTED;
+    if (dtype != MESA_DTYPE_F32 && dtype != MESA_DTYPE_BF16) return MESA_ERR_UNSUPPORTED;
+    if (n_cg < 0 || n_cg > MESA_MAX_NCG) return MESA_ERR_ARG;
+    // Grid sizes are 32-bit: batch * heads * chunks (and tiles) must stay well inside.
+    if (batch > 0 && heads > (int64_t(1) << 30) / batch) return MESA_ERR_SHAPE;
+    return MESA_OK;
+}
+
+}  // namespace
+
+namespace {
+
+// Checks shared by the forward entry points.  `need_ws` is the workspace the
+// call reads or writes (0 when it uses none).  Returns a status code.
+struct FwdCall {
+    const void *q, *k, *v;
+    const float *gamma, *beta, *lambda;
+    int64_t batch, heads, seq_len, d_k, d_v;
+    int dtype, n_cg, chunk, precision;
+    float *out, *qstar, *final_H, *final_G;
+    const void* workspace;
+    size_t workspace_bytes;
+    bool needs_q;       // the solve reads q and lambda
+    bool needs_ws;      // the call uses the chunk-state workspace
+};
+
+int validate_forward(const FwdCall& c)
+{
+    int st = check_sizes(c.batch, c.heads, c.seq_len, c.d_k, c.d_v, c.dtype, c.n_cg);
+    if (st != MESA_OK) return st;
+    if (!chunk_ok(c.chunk)) return MESA_ERR_UNSUPPORTED;
+    if (c.precision != MESA_PREC_AUTO && c.precision != MESA_PREC_F32 && c.precision != MESA_PREC_BF16)
+        return MESA_ERR_UNSUPPORTED;
+    const ForwardShape probe{c.batch, c.heads, c.seq_len, int(c.d_k), int(c.d_v), c.chunk, 0,
+                             c.dtype == MESA_DTYPE_BF16};
+    if (c.precision == MESA_PREC_BF16 && !mesa::chunk_cg_bf16_supported(probe)) return MESA_ERR_UNSUPPORTED;
+    if (c.batch == 0 || c.heads == 0) return MESA_OK;
+    if (!c.k || !c.v || !c.gamma || !c.beta) return MESA_ERR_NULL;
+    if (c.needs_q && (!c.q || !c.lambda || !c.out)) return MESA_ERR_NULL;
+    const int64_t nc = n_chunks_of(c.seq_len, c.chunk);
+    if (nc * c.batch * c.heads > (int64_t(1) << 31) / 16) return MESA_ERR_SHAPE;
+    const size_t need = c.needs_ws ? mesa_forward_workspace_bytes(c.batch, c.heads, c.seq_len, c.d_k,
+                                                                  c.d_v, c.chunk)
+                                   : 0;
+    if (need > 0) {
+        if (!c.workspace) return MESA_ERR_NULL;
+        if (c.workspace_bytes < need) return MESA_ERR_WORKSPACE;
+    }
+    const int64_t tokens = c.batch * c.heads * c.seq_len;
+    const int64_t in_sz = c.dtype == MESA_DTYPE_BF16 ? 2 : 4;
+    // Outputs must overlap neither an input nor each other.  The workspace is an
+    // output of the state scan and an input of the solve; either way no other
+    // output may touch it.
+    const Range ins[] = {range_of(c.q, c.q ? tokens * c.d_k * in_sz : 0),
+                         range_of(c.k, tokens * c.d_k * in_sz),
+                         range_of(c.v, tokens * c.d_v * in_sz),
+                         range_of(c.gamma, tokens * 4),
+                         range_of(c.beta, tokens * 4),
+                         range_of(c.lambda, c.lambda ? c.heads * c.d_k * 4 : 0),
+                         range_of(c.workspace, int64_t(need))};
+    const Range outs[] = {range_of(c.out, c.out ? tokens * c.d_v * 4 : 0),
+                          range_of(c.qstar, c.qstar ? tokens * c.d_k * 4 : 0),
+                          range_of(c.final_H, c.final_H ? c.batch * c.heads * c.d_k * c.d_k * 4 : 0),
+                          range_of(c.final_G, c.final_G ? c.batch * c.heads * c.d_v * c.d_k * 4 : 0)};
+    for (const Range& o : outs) {
+        if (o.lo == o.hi) continue;
+        for (const Range& i : ins)
+            if (i.lo != i.hi && overlaps(o, i)) return MESA_ERR_ARG;
+    }
+    for (int x = 0; x < 4; ++x)
+        for (int y = x + 1; y < 4; ++y)
+            if (outs[x].lo != outs[x].hi && outs[y].lo != outs[y].hi && overlaps(outs[x], outs[y]))
+                return MESA_ERR_ARG;
+    return MESA_OK;
+}
+
+ForwardShape shape_of(const FwdCall& c)
+{
+    return ForwardShape{c.batch, c.heads, c.seq_len, int(c.d_k), int(c.d_v), c.chunk,
+                        int(n_chunks_of(c.seq_len, c.chunk)), c.dtype == MESA_DTYPE_BF16};
+}
+
+float* ws_H(const FwdCall& c) { return static_cast<float*>(const_cast<void*>(c.workspace)); }
+float* ws_GT(const FwdCall& c)
+{
+    const ForwardShape s = shape_of(c);
+    return ws_H(c) + size_t(s.batch * s.heads * s.n_chunks) * size_t(s.d_k) * size_t(s.d_k);
+}
+
+int launch_states(const FwdCall& c, bool store_chunks, hipStream_t s)
+{
+    if (c.seq_len == 0) {
+        // No tokens: the final states are the initial ones, H_0 = G_0 = 0.
+        if (c.final_H && mesa::launch_fill_zero(c.final_H, c.batch * c.heads * c.d_k * c.d_k, s) != hipSuccess)
+            return MESA_ERR_HIP;
+        if (c.final_G && mesa::launch_fill_zero(c.final_G, c.batch * c.heads * c.d_v * c.d_k, s) != hipSuccess)
+            return MESA_ERR_HIP;
+        return MESA_OK;
+    }
+    mesa::StateArgs sa{shape_of(c), c.k, c.v, c.gamma, c.beta,
+                       store_chunks ? ws_H(c) : nullptr, store_chunks ? ws_GT(c) : nullptr,
+                       c.final_H, c.final_G, store_chunks};
+    return mesa::launch_chunk_state(sa, s) == hipSuccess ? MESA_OK : MESA_ERR_HIP;
+}
+
+int launch_solve(const FwdCall& c, hipStream_t s)
+{
+    if (c.seq_len == 0) return MESA_OK;
+    const ForwardShape shape = shape_of(c);
+    int prec = c.precision;
+    if (prec == MESA_PREC_AUTO)
+        prec = shape.bf16 && mesa::chunk_cg_bf16_supported(shape) ? MESA_PREC_BF16 : MESA_PREC_F32;
+    mesa::CgArgs ca{shape, c.q, c.k, c.v, c.gamma, c.beta, c.lambda, ws_H(c), ws_GT(c), c.n_cg, c.out, c.qstar};
+    const hipError_t e = prec == MESA_PREC_BF16 ? mesa::launch_chunk_cg_bf16(ca, s)
+                                                : mesa::launch_chunk_cg_f32(ca, s);
+    return e == hipSuccess ? MESA_OK : MESA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mesa_version(void) { return 100; }
+
+const char* mesa_status_string(int status)
+{
+    switch (status) {
+        case MESA_OK: return "ok";
+        case MESA_ERR_NULL: return "a required pointer is NULL";
+        case MESA_ERR_SHAPE: return "a size is negative or the sizes are inconsistent";
+        case MESA_ERR_UNSUPPORTED: return "d_k, d_v, chunk, dtype or precision not supported";
+        case MESA_ERR_ARG: return "n_cg out of range, or an output overlaps an input";
+        case MESA_ERR_WORKSPACE: return "workspace too small";
+        case MESA_ERR_HIP: return "the HIP runtime refused a launch";
+        default: return "unknown status";
+    }
+}
+
+size_t mesa_forward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
+                                    int64_t d_v, int chunk)
+{
+    if (batch <= 0 || heads <= 0 || seq_len <= 0) return 0;
+    if (!dim_ok(d_k) || !dim_ok(d_v) || !chunk_ok(chunk)) return 0;
+    const int64_t nc = n_chunks_of(seq_len, chunk);
+    return size_t(batch) * size_t(heads) * size_t(nc) * size_t(d_k) * size_t(d_k + d_v) * sizeof(float);
+}
+
+int mesa_forward_ex(const void* q, const void* k, const void* v, const float* gamma,
+                    const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                    int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
+                    int precision, float* out, float* qstar_out, float* final_H, float* final_G,
+                    void* workspace, size_t workspace_bytes, void* stream)
+{
+    const bool states_only = out == nullptr;
+    if (states_only && (qstar_out || !final_H || !final_G)) return MESA_ERR_NULL;
+    FwdCall c{q, k, v, gamma, beta, lambda, batch, heads, seq_len, d_k, d_v, dtype, n_cg, chunk,
+              precision, out, qstar_out, final_H, final_G, workspace, workspace_bytes,
+              !states_only, !states_only};
+    int st = validate_forward(c);
+    if (st != MESA_OK || batch == 0 || heads == 0) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = launch_states(c, !states_only, s);
+    if (st != MESA_OK || states_only) return st;
+    return launch_solve(c, s);
+}
+
+int mesa_forward(const void* q, const void* k, const void* v, const float* gamma,
+                 const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                 int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
+                 float* out, void* workspace, size_t workspace_bytes, void* stream)
+{
+    if (!out) return MESA_ERR_NULL;
+    return mesa_forward_ex(q, k, v, gamma, beta, lambda, batch, heads, seq_len, d_k, d_v, dtype,
+                           n_cg, chunk, MESA_PREC_AUTO, out, nullptr, nullptr, nullptr, workspace,
+                           workspace_bytes, stream);
+}
+
+int mesa_forward_states(const void* k, const void* v, const float* gamma, const float* beta,
+                        int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v,
+                        int dtype, int chunk, float* final_H, float* final_G, void* workspace,
+                        size_t workspace_bytes, void* stream)
+{
+    FwdCall c{nullptr, k, v, gamma, beta, nullptr, batch, heads, seq_len, d_k, d_v, dtype, 0, chunk,
+              MESA_PREC_AUTO, nullptr, nullptr, final_H, final_G, workspace, workspace_bytes, false,
+              true};
+    int st = validate_forward(c);
+    if (st != MESA_OK || batch == 0 || heads == 0) return st;
+    return launch_states(c, true, static_cast<hipStream_t>(stream));
+}
+
+int mesa_forward_solve(const void* q, const void* k, const void* v, const float* gamma,
+                       const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                       int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
+                       int precision, float* out, float* qstar_out, const void* workspace,
+                       size_t workspace_bytes, void* stream)
+{
+    FwdCall c{q, k, v, gamma, beta, lambda, batch, heads, seq_len, d_k, d_v, dtype, n_cg, chunk,
+              precision, out, qstar_out, nullptr, nullptr, workspace, workspace_bytes, true, true};
+    int st = validate_forward(c);
+    if (st != MESA_OK || batch == 0 || heads == 0) return st;
+    return launch_solve(c, static_cast<hipStream_t>(stream));
+}
+
+int mesa_decode_step(float* state_H, float* state_G, const void* q, const void* k, const void* v,
+                     const float* gamma, const float* beta, const float* lambda, int64_t batch,
+                     int64_t heads, int64_t d_k, int64_t d_v, int dtype, int n_cg, float* out,
+                     void* stream)
+{
+    int st = check_sizes(batch, heads, 1, d_k, d_v, dtype, n_cg);
+    if (st != MESA_OK) return st;
+    if (batch == 0 || heads == 0) return MESA_OK;
+    if (!state_H || !state_G || !q || !k || !v || !gamma || !beta || !lambda || !out)
+        return MESA_ERR_NULL;
+    const int64_t pairs = batch * heads;
+    if (pairs > (int64_t(1) << 31) - 1) return MESA_ERR_SHAPE;
+    const int64_t in_sz = dtype == MESA_DTYPE_BF16 ? 2 : 4;
+    {
+        const Range ins[] = {range_of(q, pairs * d_k * in_sz), range_of(k, pairs * d_k * in_sz),
+                             range_of(v, pairs * d_v * in_sz), range_of(gamma, pairs * 4),
+                             range_of(beta, pairs * 4), range_of(lambda, heads * d_k * 4)};
+        const Range outs[] = {range_of(state_H, pairs * d_k * d_k * 4),
+                              range_of(state_G, pairs * d_v * d_k * 4), range_of(out, pairs * d_v * 4)};
+        for (const Range& o : outs)
+            for (const Range& i : ins)
+                if (overlaps(o, i)) return MESA_ERR_ARG;
+        if (overlaps(outs[0], outs[1]) || overlaps(outs[0], outs[2]) || overlaps(outs[1], outs[2]))
+            return MESA_ERR_ARG;
+    }
+    mesa::DecodeArgs da{batch, heads, int(d_k), int(d_v), dtype == MESA_DTYPE_BF16, state_H, state_G,
+                        q, k, v, gamma, beta, lambda, n_cg, out};
+    return mesa::launch_decode_step(da, static_cast<hipStream_t>(stream)) == hipSuccess ? MESA_OK
+                                                                                       : MESA_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,77 @@
+// Host-side launchers of the libmesa kernels.  Each kernel source file defines
+// its kernels and the launcher declared here; the C ABI (libmesa.hip) validates
+// arguments and calls the launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mesa {
+
+// Shapes of one forward call.  Token (b, h, t) lives at row (b*heads + h)*seq_len + t.
+struct ForwardShape {
+    int64_t batch, heads, seq_len;
+    int d_k, d_v, chunk;
+    int n_chunks;  // ceil(seq_len / chunk)
+    bool bf16;     // q, k, v element type
+};
+
+// Chunk-state scan: writes the fp32 states entering every chunk,
+//   Hs  [B*H, n_chunks, d_k, d_k]   and   GTs [B*H, n_chunks, d_k, d_v] (G transposed),
+// when store_chunks, and the states after the last token (final_H [B*H, d_k, d_k],
+// final_G [B*H, d_v, d_k]) when those pointers are non-null.
+struct StateArgs {
+    ForwardShape s;
+    const void* k;
+    const void* v;
+    const float* gamma;
+    const float* beta;
+    float* Hs;
+    float* GTs;
+    float* final_H;
+    float* final_G;
+    bool store_chunks;
+};
+hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream);
+
+// dst[0 .. n) = 0 with a fill kernel (no memset node, so the call can be graph-captured).
+hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream);
+
+// Chunked CG + read-out: q*_t for every token and o_t = G_t q*_t.
+struct CgArgs {
+    ForwardShape s;
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* gamma;
+    const float* beta;
+    const float* lambda;
+    const float* Hs;
+    const float* GTs;
+    int n_cg;
+    float* out;
+    float* qstar;  // may be null
+};
+hipError_t launch_chunk_cg_f32(const CgArgs& a, hipStream_t stream);
+hipError_t launch_chunk_cg_bf16(const CgArgs& a, hipStream_t stream);
+bool chunk_cg_bf16_supported(const ForwardShape& s);
+
+// One recurrent decode step for batch*heads pairs.
+struct DecodeArgs {
+    int64_t batch, heads;
+    int d_k, d_v;
+    bool bf16;
+    float* H;
+    float* G;
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* gamma;
+    const float* beta;
+    const float* lambda;
+    int n_cg;
+    float* out;
+};
+hipError_t launch_decode_step(const DecodeArgs& a, hipStream_t stream);
+
+}  // namespace mesa

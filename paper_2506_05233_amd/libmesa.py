@@ -1,0 +1,279 @@
+"""Thin ctypes binding of libmesa (include/libmesa.h).
+
+Argument marshalling only: tensors are checked for device, dtype, shape and
+contiguity, then their data pointers and torch's current HIP stream go to the C
+ABI.  Every step of the layer runs in libmesa's HIP kernels; there is no
+fallback.  Loading fails loudly when the built library is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_lib", "libmesa.so")
+
+MESA_DTYPE_F32 = 0
+MESA_DTYPE_BF16 = 1
+MESA_PREC_AUTO = 0
+MESA_PREC_F32 = 1
+MESA_PREC_BF16 = 2
+MESA_OK = 0
+MESA_ERR_NULL = 1
+MESA_ERR_SHAPE = 2
+MESA_ERR_UNSUPPORTED = 3
+MESA_ERR_ARG = 4
+MESA_ERR_WORKSPACE = 5
+MESA_ERR_HIP = 6
+MESA_MAX_NCG = 1024
+
+EXPORTED = ("mesa_forward", "mesa_forward_ex", "mesa_forward_states", "mesa_forward_solve",
+            "mesa_forward_workspace_bytes", "mesa_decode_step", "mesa_status_string",
+            "mesa_version")
+
+_lib = None
+
+
+class MesaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s (status %d)" % (where, status_string(status), status))
+
+
+def load():
+    """Load libmesa.so (built by paper_2506_05233_amd/build.py); raise if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libmesa is not built: %s is missing (run __graft_entry__.build())" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, fp, i64, ci, sz = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+    lib.mesa_forward_workspace_bytes.argtypes = [i64, i64, i64, i64, i64, ci]
+    lib.mesa_forward_workspace_bytes.restype = sz
+    lib.mesa_forward.argtypes = [vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, fp, vp, sz, vp]
+    lib.mesa_forward.restype = ci
+    lib.mesa_forward_ex.argtypes = [vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, ci,
+                                    fp, fp, fp, fp, vp, sz, vp]
+    lib.mesa_forward_ex.restype = ci
+    lib.mesa_forward_states.argtypes = [vp, vp, fp, fp, i64, i64, i64, i64, i64, ci, ci, fp, fp, vp, sz, vp]
+    lib.mesa_forward_states.restype = ci
+    lib.mesa_forward_solve.argtypes = [vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, ci,
+                                       fp, fp, vp, sz, vp]
+    lib.mesa_forward_solve.restype = ci
+    lib.mesa_decode_step.argtypes = [fp, fp, vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, ci, ci, fp, vp]
+    lib.mesa_decode_step.restype = ci
+    lib.mesa_status_string.argtypes = [ci]
+    lib.mesa_status_string.restype = ctypes.c_char_p
+    lib.mesa_version.argtypes = []
+    lib.mesa_version.restype = ci
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().mesa_status_string(int(status)).decode()
+
+
+def version() -> int:
+    return load().mesa_version()
+
+
+def forward_workspace_bytes(batch, heads, seq_len, d_k, d_v, chunk) -> int:
+    return load().mesa_forward_workspace_bytes(batch, heads, seq_len, d_k, d_v, chunk)
+
+
+def bf16_path_available(d_k, d_v, chunk, seq_len=2048) -> bool:
+    """Whether MESA_PREC_BF16 (the matrix-core path) supports this shape: a
+    zero-batch solve call validates the arguments and launches nothing."""
+    st = load().mesa_forward_solve(None, None, None, None, None, None, 0, 1, seq_len, d_k, d_v,
+                                   MESA_DTYPE_BF16, 1, chunk, MESA_PREC_BF16, None, None, None, 0,
+                                   None)
+    return st == MESA_OK
+
+
+# ---------------------------------------------------------------- torch glue
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return MESA_DTYPE_F32
+    if t.dtype == torch.bfloat16:
+        return MESA_DTYPE_BF16
+    raise TypeError("q, k, v must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _check(t, name, shape, dtype=None, device=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def forward(q, k, v, gamma, beta, lam, n_cg, chunk=64, precision=MESA_PREC_AUTO, want_qstar=False,
+            want_states=False, out=None, workspace=None):
+    """Mesa forward over q, k [B,H,T,d_k], v [B,H,T,d_v] (fp32 or bf16, same dtype),
+    gamma, beta [B,H,T] fp32, lam [H,d_k] fp32.  Returns out [B,H,T,d_v] fp32, or a
+    dict with "out" and, if asked, "qstar" [B,H,T,d_k], "H" [B,H,d_k,d_k], "G" [B,H,d_v,d_k].
+    Runs on torch's current stream of q's device."""
+    torch = _torch()
+    lib = load()
+    B, H, T, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    _check(q, "q", (B, H, T, dk), device=dev)
+    _check(k, "k", (B, H, T, dk), q.dtype, dev)
+    _check(v, "v", (B, H, T, dv), q.dtype, dev)
+    _check(gamma, "gamma", (B, H, T), torch.float32, dev)
+    _check(beta, "beta", (B, H, T), torch.float32, dev)
+    _check(lam, "lam", (H, dk), torch.float32, dev)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
+    _check(out, "out", (B, H, T, dv), torch.float32, dev)
+    need = lib.mesa_forward_workspace_bytes(B, H, T, dk, dv, chunk)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    qstar = torch.empty((B, H, T, dk), dtype=torch.float32, device=dev) if want_qstar else None
+    fH = torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev) if want_states else None
+    fG = torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev) if want_states else None
+    st = lib.mesa_forward_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam), B, H, T,
+                             dk, dv, code, int(n_cg), int(chunk), int(precision), _ptr(out),
+                             _ptr(qstar), _ptr(fH), _ptr(fG), _ptr(workspace),
+                             workspace.numel() * workspace.element_size(), _stream(dev))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_forward_ex")
+    if not (want_qstar or want_states):
+        return out
+    res = {"out": out}
+    if want_qstar:
+        res["qstar"] = qstar
+    if want_states:
+        res["H"] = fH
+        res["G"] = fG
+    return res
+
+
+class ForwardPlan:
+    """Pre-checked arguments of one forward shape, for repeated calls of the two
+    launches (mesa_forward_states, then mesa_forward_solve) on torch's current
+    stream.  Holds the output and workspace tensors; used by the benchmark to
+    time each launch with events on the launch stream."""
+
+    def __init__(self, q, k, v, gamma, beta, lam, n_cg, chunk=64, precision=MESA_PREC_AUTO):
+        torch = _torch()
+        self.lib = load()
+        B, H, T, dk = q.shape
+        dv = v.shape[-1]
+        dev = q.device
+        _check(q, "q", (B, H, T, dk), device=dev)
+        _check(k, "k", (B, H, T, dk), q.dtype, dev)
+        _check(v, "v", (B, H, T, dv), q.dtype, dev)
+        _check(gamma, "gamma", (B, H, T), torch.float32, dev)
+        _check(beta, "beta", (B, H, T), torch.float32, dev)
+        _check(lam, "lam", (H, dk), torch.float32, dev)
+        self.tensors = (q, k, v, gamma, beta, lam)
+        self.dims = (B, H, T, dk, dv)
+        self.code = _dtype_code(q)
+        self.n_cg, self.chunk, self.precision = int(n_cg), int(chunk), int(precision)
+        self.device = dev
+        self.out = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
+        self.ws_bytes = self.lib.mesa_forward_workspace_bytes(B, H, T, dk, dv, chunk)
+        self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
+
+    def states(self):
+        q, k, v, gamma, beta, lam = self.tensors
+        B, H, T, dk, dv = self.dims
+        st = self.lib.mesa_forward_states(_ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), B, H, T, dk, dv,
+                                          self.code, self.chunk, None, None, _ptr(self.workspace),
+                                          self.ws_bytes, _stream(self.device))
+        if st != MESA_OK:
+            raise MesaError(st, "mesa_forward_states")
+
+    def solve(self):
+        q, k, v, gamma, beta, lam = self.tensors
+        B, H, T, dk, dv = self.dims
+        st = self.lib.mesa_forward_solve(_ptr(q), _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam),
+                                         B, H, T, dk, dv, self.code, self.n_cg, self.chunk,
+                                         self.precision, _ptr(self.out), None, _ptr(self.workspace),
+                                         self.ws_bytes, _stream(self.device))
+        if st != MESA_OK:
+            raise MesaError(st, "mesa_forward_solve")
+        return self.out
+
+    def __call__(self):
+        self.states()
+        return self.solve()
+
+
+def prefill_states(k, v, gamma, beta, chunk=64):
+    """States after the last token only (mesa_forward_ex with out = NULL):
+    returns (H [B,H,d_k,d_k], G [B,H,d_v,d_k]) fp32, the input of decode_step."""
+    torch = _torch()
+    lib = load()
+    B, H, T, dk = k.shape
+    dv = v.shape[-1]
+    dev = k.device
+    _check(k, "k", (B, H, T, dk), device=dev)
+    _check(v, "v", (B, H, T, dv), k.dtype, dev)
+    _check(gamma, "gamma", (B, H, T), torch.float32, dev)
+    _check(beta, "beta", (B, H, T), torch.float32, dev)
+    code = _dtype_code(k)
+    fH = torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev)
+    fG = torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev)
+    st = lib.mesa_forward_ex(None, _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), None, B, H, T, dk, dv,
+                             code, 0, int(chunk), MESA_PREC_AUTO, None, None, _ptr(fH), _ptr(fG),
+                             None, 0, _stream(dev))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_forward_ex(states only)")
+    return fH, fG
+
+
+def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, out=None):
+    """One recurrent step, in place on state_H [N,H,d_k,d_k] and state_G [N,H,d_v,d_k].
+    q, k [N,H,d_k], v [N,H,d_v] fp32 or bf16; gamma, beta [N,H]; lam [H,d_k].
+    Returns out [N,H,d_v] fp32."""
+    torch = _torch()
+    lib = load()
+    N, H, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    _check(state_H, "state_H", (N, H, dk, dk), torch.float32, dev)
+    _check(state_G, "state_G", (N, H, dv, dk), torch.float32, dev)
+    _check(q, "q", (N, H, dk), device=dev)
+    _check(k, "k", (N, H, dk), q.dtype, dev)
+    _check(v, "v", (N, H, dv), q.dtype, dev)
+    _check(gamma, "gamma", (N, H), torch.float32, dev)
+    _check(beta, "beta", (N, H), torch.float32, dev)
+    _check(lam, "lam", (H, dk), torch.float32, dev)
+    if out is None:
+        out = torch.empty((N, H, dv), dtype=torch.float32, device=dev)
+    _check(out, "out", (N, H, dv), torch.float32, dev)
+    st = lib.mesa_decode_step(_ptr(state_H), _ptr(state_G), _ptr(q), _ptr(k), _ptr(v), _ptr(gamma),
+                              _ptr(beta), _ptr(lam), N, H, dk, dv, _dtype_code(q), int(n_cg),
+                              _ptr(out), _stream(dev))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_decode_step")
+    return out

@@ -1,0 +1,152 @@
+"""The C ABI on the host: the library loads, exports every entry point that
+include/libmesa.h declares, and rejects bad arguments before any launch.
+
+No test here reaches a kernel launch: every call fails validation, so the
+suite runs without a GPU.  Fake device pointers are plain integers.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2506_05233_amd import libmesa as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "libmesa.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(L.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return L.load()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?(?:int|size_t|char\s*\*|const char\s*\*)\s*\**\s*(mesa_\w+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def _declared_constants():
+    text = open(HEADER).read()
+    return {m.group(1): int(m.group(2)) for m in re.finditer(r"#define\s+(MESA_\w+)\s+(-?\d+)", text)}
+
+
+def test_header_declares_the_expected_entry_points():
+    assert _declared_functions() == sorted(L.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_binding_constants_match_header():
+    for name, value in _declared_constants().items():
+        assert getattr(L, name) == value, name
+
+
+def test_status_strings(lib):
+    for s in range(7):
+        assert L.status_string(s)
+    assert L.status_string(99) == "unknown status"
+    assert L.version() == 100
+
+
+def test_workspace_bytes(lib):
+    # states entering every chunk: H_c (d_k x d_k) and G_c^T (d_k x d_v), fp32
+    assert L.forward_workspace_bytes(8, 16, 2048, 128, 128, 64) == 8 * 16 * 32 * 128 * 256 * 4
+    assert L.forward_workspace_bytes(1, 2, 100, 64, 128, 32) == 2 * 4 * 64 * 192 * 4
+    assert L.forward_workspace_bytes(1, 1, 0, 64, 64, 64) == 0
+    assert L.forward_workspace_bytes(1, 1, 64, 96, 64, 64) == 0
+    assert L.forward_workspace_bytes(1, 1, 64, 64, 64, 48) == 0
+
+
+# fake, non-overlapping device addresses
+P = {n: 0x10000000 * (i + 1) for i, n in enumerate(
+    ["q", "k", "v", "g", "b", "lam", "out", "qs", "fh", "fg", "ws", "H", "G"])}
+
+
+def _fwd(lib, **kw):
+    a = dict(q=P["q"], k=P["k"], v=P["v"], gamma=P["g"], beta=P["b"], lam=P["lam"], B=2, H=3, T=128,
+             dk=64, dv=64, dtype=0, n_cg=5, chunk=64, prec=0, out=P["out"], qstar=None, fH=None,
+             fG=None, ws=P["ws"], ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.mesa_forward_ex(a["q"], a["k"], a["v"], a["gamma"], a["beta"], a["lam"], a["B"],
+                               a["H"], a["T"], a["dk"], a["dv"], a["dtype"], a["n_cg"], a["chunk"],
+                               a["prec"], a["out"], a["qstar"], a["fH"], a["fG"], a["ws"],
+                               a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), L.MESA_ERR_NULL),
+    (dict(k=None), L.MESA_ERR_NULL),
+    (dict(lam=None), L.MESA_ERR_NULL),
+    (dict(ws=None), L.MESA_ERR_NULL),
+    (dict(B=-1), L.MESA_ERR_SHAPE),
+    (dict(T=-5), L.MESA_ERR_SHAPE),
+    (dict(dk=96), L.MESA_ERR_UNSUPPORTED),
+    (dict(dv=32), L.MESA_ERR_UNSUPPORTED),
+    (dict(chunk=48), L.MESA_ERR_UNSUPPORTED),
+    (dict(chunk=128), L.MESA_ERR_UNSUPPORTED),
+    (dict(dtype=2), L.MESA_ERR_UNSUPPORTED),
+    (dict(prec=7), L.MESA_ERR_UNSUPPORTED),
+    (dict(n_cg=-1), L.MESA_ERR_ARG),
+    (dict(n_cg=L.MESA_MAX_NCG + 1), L.MESA_ERR_ARG),
+    (dict(ws_bytes=100), L.MESA_ERR_WORKSPACE),
+    (dict(out=P["q"] + 64), L.MESA_ERR_ARG),          # out overlaps q
+    (dict(out=P["ws"]), L.MESA_ERR_ARG),               # out overlaps the workspace
+    (dict(qstar=P["out"]), L.MESA_ERR_ARG),            # two outputs overlap
+    (dict(out=None, fH=P["fh"], fG=None), L.MESA_ERR_NULL),    # states only needs both states
+    (dict(out=None, fH=P["fh"], fG=P["fg"], qstar=P["qs"]), L.MESA_ERR_NULL),
+])
+def test_forward_rejects_bad_arguments(lib, kw, status):
+    assert _fwd(lib, **kw) == status
+
+
+def test_forward_empty_batch_is_a_noop(lib):
+    assert _fwd(lib, B=0) == L.MESA_OK
+    assert _fwd(lib, H=0, q=None) == L.MESA_OK
+
+
+def test_plain_forward_requires_out(lib):
+    assert lib.mesa_forward(P["q"], P["k"], P["v"], P["g"], P["b"], P["lam"], 1, 1, 64, 64, 64, 0, 3,
+                            64, None, P["ws"], 1 << 30, None) == L.MESA_ERR_NULL
+
+
+def _dec(lib, **kw):
+    a = dict(H=P["H"], G=P["G"], q=P["q"], k=P["k"], v=P["v"], gamma=P["g"], beta=P["b"],
+             lam=P["lam"], N=4, Hh=2, dk=128, dv=128, dtype=1, n_cg=15, out=P["out"])
+    a.update(kw)
+    return lib.mesa_decode_step(a["H"], a["G"], a["q"], a["k"], a["v"], a["gamma"], a["beta"],
+                                a["lam"], a["N"], a["Hh"], a["dk"], a["dv"], a["dtype"], a["n_cg"],
+                                a["out"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H=None), L.MESA_ERR_NULL),
+    (dict(out=None), L.MESA_ERR_NULL),
+    (dict(lam=None), L.MESA_ERR_NULL),
+    (dict(N=-2), L.MESA_ERR_SHAPE),
+    (dict(dk=256), L.MESA_ERR_UNSUPPORTED),
+    (dict(dtype=5), L.MESA_ERR_UNSUPPORTED),
+    (dict(n_cg=-3), L.MESA_ERR_ARG),
+    (dict(out=P["q"]), L.MESA_ERR_ARG),
+    (dict(G=P["H"] + 1024), L.MESA_ERR_ARG),
+])
+def test_decode_rejects_bad_arguments(lib, kw, status):
+    assert _dec(lib, **kw) == status
+
+
+def test_decode_empty_is_a_noop(lib):
+    assert _dec(lib, N=0) == L.MESA_OK
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(L, "_lib", None)
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        L.load()

@@ -1,0 +1,240 @@
+"""GPU parity of libmesa against the fp64 oracle's same-step CG.
+
+Every call goes through the C ABI (paper_2506_05233_amd.libmesa).  The oracle
+consumes exactly the values the GPU receives (bf16 inputs widen exactly).
+Small workloads are compared element by element in full; the full-size
+workloads run in the launch configuration the benchmark times and are checked
+on sampled (batch, head) sequences, which the oracle computes from their first
+token on.
+"""
+import concurrent.futures as cf
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from mesa_testutil import TOL_BF16, TOL_F32, rel_l2, to_device
+from paper_2506_05233_amd import libmesa as L
+from paper_2506_05233_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    L.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _oracle_pairs(x, pairs, n_cg, **kw):
+    """Oracle forward on the listed (b, h) sequences, one thread each."""
+    def one(bh):
+        b, h = bh
+        sl = {n: x[n][b:b + 1, h:h + 1] for n in ("q", "k", "v", "gamma", "beta")}
+        return oracle.forward(sl["q"], sl["k"], sl["v"], sl["gamma"], sl["beta"], x["lam"][h:h + 1],
+                              n_cg, threads=1, **kw)
+    with cf.ThreadPoolExecutor(max_workers=min(16, len(pairs))) as ex:
+        return list(ex.map(one, pairs))
+
+
+def _gpu_forward(x, dtype, n_cg, chunk, **kw):
+    d = to_device(x, dtype)
+    res = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], n_cg, chunk, **kw)
+    torch.cuda.synchronize()
+    if isinstance(res, dict):
+        return {k: v.cpu().numpy() for k, v in res.items()}
+    return res.cpu().numpy()
+
+
+# ------------------------------------------------------------ small, in full
+@pytest.mark.parametrize("w", [W.TINY_F32, W.SMALL_F32], ids=lambda w: w.name)
+def test_forward_f32_workloads_full(w):
+    _say("forward parity %s" % w.name)
+    x = W.workload_inputs(w)
+    got = _gpu_forward(x, w.dtype, w.n_cg, w.chunk, want_qstar=True, want_states=True)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], w.n_cg,
+                         want_qstar=True, want_states=True)
+    e_out = rel_l2(got["out"], ref["out"])
+    e_q = rel_l2(got["qstar"], ref["qstar"])
+    _say("  out %.3e  qstar %.3e" % (e_out, e_q))
+    assert e_out <= TOL_F32 and e_q <= TOL_F32
+    assert rel_l2(got["H"], ref["H"]) <= 1e-5 and rel_l2(got["G"], ref["G"]) <= 1e-5
+
+
+def test_forward_bf16_small_full_auto_precision():
+    x = W.forward_inputs(2, 3, 320, 128, 128, "bf16", 4.0, seed=11)
+    got = _gpu_forward(x, "bf16", 15, 64)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 15)["out"]
+    e = rel_l2(got, ref)
+    _say("bf16 small auto: %.3e" % e)
+    assert e <= TOL_BF16
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 128), (128, 64), (128, 128)])
+@pytest.mark.parametrize("chunk", [16, 32, 64])
+def test_forward_shapes_ragged_tail(dk, dv, chunk):
+    """T not a multiple of the chunk: several chunks plus a ragged last one."""
+    x = W.forward_inputs(1, 2, 3 * chunk + 7, dk, dv, "f32", 3.0, seed=dk + dv + chunk)
+    got = _gpu_forward(x, "f32", 9, chunk, precision=L.MESA_PREC_F32, want_states=True)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 9, want_states=True)
+    assert rel_l2(got["out"], ref["out"]) <= TOL_F32
+    assert rel_l2(got["H"], ref["H"]) <= 1e-5 and rel_l2(got["G"], ref["G"]) <= 1e-5
+
+
+def test_chunk_size_invariance():
+    x = W.forward_inputs(1, 2, 256, 64, 64, "f32", 3.0, seed=5)
+    outs = [_gpu_forward(x, "f32", 10, c, precision=L.MESA_PREC_F32) for c in (16, 32, 64)]
+    assert rel_l2(outs[0], outs[2]) <= 1e-5 and rel_l2(outs[1], outs[2]) <= 1e-5
+
+
+def test_edge_cases_zero_gates_zero_queries_short_sequences():
+    x = W.forward_inputs(2, 2, 97, 64, 64, "f32", 3.0, seed=21)
+    x["gamma"][0, 1, 40] = 0.0      # memory reset inside a chunk
+    x["gamma"][1, 0, 64] = 0.0      # reset at a chunk start
+    x["gamma"][1, 1, 63] = 0.0      # reset at a chunk end
+    x["q"][0, 0, 10] = 0.0          # q = 0 -> o = 0
+    x["beta"][1, 0, 5:9] = 0.0      # ignored tokens
+    for n_cg in (0, 1, 12):
+        got = _gpu_forward(x, "f32", n_cg, 64, precision=L.MESA_PREC_F32)
+        ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], n_cg)["out"]
+        assert rel_l2(got, ref) <= TOL_F32, n_cg
+        assert np.all(got[0, 0, 10] == 0.0)
+    for T in (1, 2, 63, 64, 65):
+        y = W.forward_inputs(1, 1, T, 64, 64, "f32", 3.0, seed=T)
+        got = _gpu_forward(y, "f32", 6, 64, precision=L.MESA_PREC_F32)
+        ref = oracle.forward(y["q"], y["k"], y["v"], y["gamma"], y["beta"], y["lam"], 6)["out"]
+        assert rel_l2(got, ref) <= TOL_F32, T
+
+
+def test_empty_sequence_gives_zero_states():
+    d = to_device(W.forward_inputs(2, 2, 0, 64, 64, "f32", 3.0, 0), "f32")
+    H, G = L.prefill_states(d["k"], d["v"], d["gamma"], d["beta"])
+    torch.cuda.synchronize()
+    assert H.shape == (2, 2, 64, 64) and float(H.abs().max()) == 0.0 and float(G.abs().max()) == 0.0
+
+
+def test_prefill_states_match_oracle():
+    x = W.forward_inputs(2, 2, 200, 128, 64, "bf16", 4.0, seed=8)
+    d = to_device(x, "bf16")
+    H, G = L.prefill_states(d["k"], d["v"], d["gamma"], d["beta"])
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 0, want_states=True)
+    assert rel_l2(H.cpu().numpy(), ref["H"]) <= 1e-5
+    assert rel_l2(G.cpu().numpy(), ref["G"]) <= 1e-5
+
+
+def test_forward_is_bitwise_deterministic():
+    x = W.forward_inputs(2, 4, 512, 128, 128, "bf16", 4.0, seed=9)
+    a = _gpu_forward(x, "bf16", 15, 64)
+    b = _gpu_forward(x, "bf16", 15, 64)
+    assert np.array_equal(a, b)
+
+
+def test_stress_repeated_keys_f32_path():
+    """Keys from a pool of one vector, gates near one: the ill-conditioned case."""
+    x = W.repeated_key_inputs(1, 2, 512, 128, 128, pool=1, dtype="bf16")
+    got = _gpu_forward(x, "bf16", 20, 64, precision=L.MESA_PREC_F32)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 20)["out"]
+    e = rel_l2(got, ref)
+    _say("stress pool=1 f32 products: %.3e" % e)
+    assert e <= TOL_F32
+
+
+# ------------------------------------------------- full size, sampled sequences
+@pytest.mark.parametrize("w,pairs", [
+    (W.LAYER_1B_BF16, [(0, 0), (3, 7), (5, 12), (7, 15)]),
+    (W.LONG_BF16, [(0, 0), (0, 9)]),
+], ids=["layer1b", "longctx"])
+def test_forward_full_size_sampled(w, pairs):
+    _say("full-size forward %s, sampled %s" % (w.name, pairs))
+    x = W.workload_inputs(w)
+    got = _gpu_forward(x, w.dtype, w.n_cg, w.chunk)
+    assert np.isfinite(got).all()
+    refs = _oracle_pairs(x, pairs, w.n_cg)
+    g = np.stack([got[b, h] for b, h in pairs])
+    r = np.stack([ref["out"][0, 0] for ref in refs])
+    e = rel_l2(g, r)
+    _say("  sampled rel L2 %.3e" % e)
+    assert e <= (TOL_BF16 if w.dtype == "bf16" else TOL_F32)
+
+
+# ------------------------------------------------------------------- decode
+def _decode_state_pool(w, n_pool):
+    """Oracle-prefilled states of the first n_pool sequences' head-0..H-1 pairs."""
+    toks = W.decode_prefill_tokens(w, 0, n_pool)
+    H, G = oracle.unrolled_states(toks["k"], toks["v"], toks["gamma"], toks["beta"])
+    return H.astype(np.float32), G.astype(np.float32)   # [n_pool, H, d, d]
+
+
+def test_decode_full_size_sampled_steps():
+    w = W.DECODE_BF16
+    _say("decode full size %s" % w.name)
+    n_pool = 4
+    Hp, Gp = _decode_state_pool(w, n_pool)
+    # every sequence s starts from pool state s % n_pool (per head)
+    idx = np.arange(w.seqs) % n_pool
+    H0 = np.ascontiguousarray(Hp[idx])
+    G0 = np.ascontiguousarray(Gp[idx])
+    lam = W.decode_lambda(w)
+    dH = torch.from_numpy(H0).cuda()
+    dG = torch.from_numpy(G0).cuda()
+    dlam = torch.from_numpy(lam).cuda()
+    sample = [0, 1, 77, 255]
+    rH = H0[sample].astype(np.float64)
+    rG = G0[sample].astype(np.float64)
+    worst = 0.0
+    for step in range(8):
+        x = W.decode_step_inputs(w, step)
+        d = to_device(x, w.dtype)
+        out = L.decode_step(dH, dG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], dlam, w.n_cg)
+        torch.cuda.synchronize()
+        sx = {n: x[n][sample] for n in x}
+        ro, rH, rG = oracle.decode_step(rH, rG, sx["q"], sx["k"], sx["v"], sx["gamma"], sx["beta"],
+                                        lam, w.n_cg)
+        worst = max(worst, rel_l2(out.cpu().numpy()[sample], ro))
+    _say("  decode worst step rel L2 %.3e" % worst)
+    assert worst <= TOL_BF16
+    assert rel_l2(dH.cpu().numpy()[sample], rH) <= 1e-5
+    assert rel_l2(dG.cpu().numpy()[sample], rG) <= 1e-5
+
+
+def test_decode_f32_matches_oracle_tightly():
+    x = W.forward_inputs(3, 2, 1, 64, 128, "f32", 3.0, seed=3)
+    rng = np.random.default_rng(0)
+    H0, G0 = oracle.unrolled_states(rng.standard_normal((3, 2, 50, 64)) / 8,
+                                    rng.standard_normal((3, 2, 50, 128)),
+                                    np.full((3, 2, 50), 0.97), np.full((3, 2, 50), 0.5))
+    H0 = H0.astype(np.float32)
+    G0 = G0.astype(np.float32)
+    d = to_device({k: v[:, :, 0] if v.ndim == 3 else v for k, v in x.items() if k != "lam"}, "f32")
+    dH, dG = torch.from_numpy(H0).cuda(), torch.from_numpy(G0).cuda()
+    lam = torch.from_numpy(x["lam"]).cuda()
+    out = L.decode_step(dH, dG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], lam, 12)
+    ro, rH, rG = oracle.decode_step(H0, G0, x["q"][:, :, 0], x["k"][:, :, 0], x["v"][:, :, 0],
+                                    x["gamma"][:, :, 0], x["beta"][:, :, 0], x["lam"], 12)
+    assert rel_l2(out.cpu().numpy(), ro) <= TOL_F32
+    assert rel_l2(dH.cpu().numpy(), rH) <= 1e-6 and rel_l2(dG.cpu().numpy(), rG) <= 1e-6
+
+
+def test_decode_steps_from_zero_equal_forward():
+    x = W.forward_inputs(2, 2, 70, 128, 128, "bf16", 4.0, seed=12)
+    fwd = _gpu_forward(x, "bf16", 10, 64, precision=L.MESA_PREC_F32)
+    d = to_device(x, "bf16")
+    dH = torch.zeros((2, 2, 128, 128), device="cuda")
+    dG = torch.zeros((2, 2, 128, 128), device="cuda")
+    outs = []
+    for t in range(70):
+        outs.append(L.decode_step(dH, dG, d["q"][:, :, t].contiguous(), d["k"][:, :, t].contiguous(),
+                                  d["v"][:, :, t].contiguous(), d["gamma"][:, :, t].contiguous(),
+                                  d["beta"][:, :, t].contiguous(), d["lam"], 10).cpu().numpy())
+    dec = np.stack(outs, axis=2)
+    assert rel_l2(dec, fwd) <= 1e-4
