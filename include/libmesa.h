@@ -25,6 +25,8 @@
  *   - Every array pointer is a DEVICE pointer owned by the caller.  The library
  *     allocates and frees nothing and keeps no state between calls.
  *   - Arrays are dense and row-major (C order) with the shapes given below.
+ *     The forward entry points need q, k, v, lambda, out, qstar_out, final_H,
+ *     final_G and the workspace 16-byte aligned (MESA_ERR_ARG otherwise).
  *   - q, k, v have element type `dtype` (MESA_DTYPE_F32 or MESA_DTYPE_BF16);
  *     gates, Lambda, states and outputs are fp32.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
@@ -68,19 +70,22 @@ extern "C" {
 #define MESA_ERR_NULL 1          /* a required pointer is NULL                         */
 #define MESA_ERR_SHAPE 2         /* a size is negative or the sizes are inconsistent  */
 #define MESA_ERR_UNSUPPORTED 3   /* d_k, d_v, chunk, dtype or precision not supported */
-#define MESA_ERR_ARG 4           /* n_cg out of range, or outputs overlap inputs       */
+#define MESA_ERR_ARG 4           /* n_cg out of range, misaligned, or overlapping      */
 #define MESA_ERR_WORKSPACE 5     /* workspace too small                                */
 #define MESA_ERR_HIP 6           /* the HIP runtime refused a launch                   */
 
 /* Supported sizes: d_k, d_v in {64, 128}; chunk in {16, 32, 64}; 0 <= n_cg <= 1024.
  * Any seq_len >= 0 is accepted; a last chunk shorter than `chunk` is handled.
- * batch, heads or seq_len equal to 0 is a no-op that returns MESA_OK. */
+ * batch or heads equal to 0 is a no-op that returns MESA_OK.  With seq_len 0 no
+ * token is read or written (pointers to arrays with no elements may be NULL) and
+ * the final states, when asked for, are the initial ones, H_0 = G_0 = 0. */
 #define MESA_MAX_NCG 1024
 
 /* Bytes of device workspace mesa_forward needs: the fp32 states entering every
- * chunk, H_c [batch, heads, ceil(seq_len/chunk), d_k, d_k] and the transposed
- * value-key state G_c^T [..., d_k, d_v] (App. D: states are kept only at chunk
- * boundaries c = 0, C, 2C, ...).  Returns 0 for unsupported or empty sizes. */
+ * chunk, H_c [batch, heads, ceil(seq_len/chunk), d_k, d_k] followed by
+ * G_c [batch, heads, ceil(seq_len/chunk), d_v, d_k] (App. D: states are kept
+ * only at chunk boundaries c = 0, C, 2C, ...).  Returns 0 for unsupported or
+ * empty sizes. */
 size_t mesa_forward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
                                     int64_t d_v, int chunk);
 

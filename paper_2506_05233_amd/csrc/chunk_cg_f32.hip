@@ -49,7 +49,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
     const int j = tid % C;   // this thread's token (column)
     const int a0 = tid / C;  // this thread's first feature row
 
-    __shared__ float sH[DK * kLdW];   // H_c [DK][DK+1]; later G_c^T [DK][129]
+    __shared__ float sH[DK * kLdW];   // H_c [DK][DK+1]; later G_c^T as [DK][129]
     __shared__ float sKV[C * kLdW];   // K [C][DK] (row stride 129); later V [C][dv]
     __shared__ float sP[DK * LDP];    // P, q or x as [DK][C+1]
     __shared__ float sS[C * C];       // beta ⊙ Z ⊙ (K P) as [C][C]
@@ -206,8 +206,9 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
         const int i = e / dv, c = e % dv;
         sKV[i * kLdW + c] = i < valid ? to_f32(vp[(tok0 + i) * dv + c]) : 0.0f;
     }
-    const float* GT = a.GTs + (bh * s.n_chunks + n) * int64_t(DK) * dv;
-    for (int e = tid; e < DK * dv; e += kThreads) sH[(e / dv) * kLdW + e % dv] = GT[e];
+    // G_c [dv][DK] staged transposed, sH[b][e] = G_c[e][b]
+    const float* Gc = a.Gs + (bh * s.n_chunks + n) * int64_t(DK) * dv;
+    for (int e = tid; e < DK * dv; e += kThreads) sH[(e % DK) * kLdW + e / DK] = Gc[e];
     __syncthreads();
     for (int e = tid; e < C * dv; e += kThreads) {
         const int jj = e / dv, c = e % dv;

@@ -5,7 +5,7 @@
 //   G_{c+C} = zeta_{c+C,c} G_c + sum_{i in chunk} zeta_{c+C,i} beta_i v_i k_i^T
 //
 // (the gated recurrences of Sec. 3 summed over one chunk, unrolled as in App. D).
-// One workgroup owns a 16-row tile of H or of G^T for one (batch, head) and
+// One workgroup owns a 16-row tile of H or of G for one (batch, head) and
 // walks the chunks in order, so every state element is written exactly once per
 // chunk with coalesced stores.  The tile stays in registers between chunks.
 // HBM traffic per token-head: the states, 4 (d_k + d_v) d_k / C bytes, plus the
@@ -26,19 +26,20 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
 {
     const ForwardShape s = a.s;
     const int dk = s.d_k, dv = s.d_v, C = s.chunk;
-    const int ntile = dk / kTileRows;
-    const int tile = blockIdx.x % (2 * ntile);
-    const int64_t bh = blockIdx.x / (2 * ntile);
-    const bool isG = tile >= ntile;  // tiles [0, ntile): H rows; [ntile, 2 ntile): G^T rows
-    const int r0 = (isG ? tile - ntile : tile) * kTileRows;
-    const int ncol = isG ? dv : dk;
-    const int nel = kTileRows * ncol;
+    const int ntile_h = dk / kTileRows;
+    const int ntile = ntile_h + dv / kTileRows;
+    const int tile = blockIdx.x % ntile;
+    const int64_t bh = blockIdx.x / ntile;
+    const bool isG = tile >= ntile_h;  // tiles [0, d_k/16): rows of H; then rows of G
+    const int r0 = (isG ? tile - ntile_h : tile) * kTileRows;
+    const int nrow = isG ? dv : dk;    // rows of the whole state
+    const int nel = kTileRows * dk;    // a tile spans all d_k columns
     const int tid = threadIdx.x;
     const Tin* kp = static_cast<const Tin*>(a.k);
-    const Tin* bp = static_cast<const Tin*>(isG ? a.v : a.k);
+    const Tin* rp = static_cast<const Tin*>(isG ? a.v : a.k);
 
-    __shared__ float sR[64][kTileRows + 1];  // k_i[r0 + row]
-    __shared__ float sB[64][kMaxCols + 1];   // k_i (H) or v_i (G^T), all columns
+    __shared__ float sR[64][kTileRows + 1];  // rows r0.. of k_i (H) or v_i (G)
+    __shared__ float sB[64][kMaxCols + 1];   // k_i, all d_k columns
     __shared__ float sW[64];                 // beta_i * zeta_{chunk end, i}
     __shared__ float sLg[64];
     __shared__ int sZl[64];
@@ -48,26 +49,26 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
 #pragma unroll
     for (int m = 0; m < kPerThread; ++m) st[m] = 0.0f;
 
-    float* chunk_dst = isG ? a.GTs : a.Hs;
+    float* chunk_dst = isG ? a.Gs : a.Hs;
     for (int n = 0; n < s.n_chunks; ++n) {
         const int64_t t0 = int64_t(n) * C;
         const int valid = int(min<int64_t>(C, s.seq_len - t0));
         const int64_t tok0 = bh * s.seq_len + t0;
         if (a.store_chunks) {
-            float* dst = chunk_dst + ((bh * s.n_chunks + n) * dk + r0) * int64_t(ncol);
+            float* dst = chunk_dst + ((bh * s.n_chunks + n) * nrow + r0) * int64_t(dk);
 #pragma unroll
             for (int m = 0; m < kPerThread; ++m) {
                 const int e = tid + kThreads * m;
                 if (e < nel) dst[e] = st[m];
             }
         }
-        for (int e = tid; e < C * ncol; e += kThreads) {
-            const int i = e / ncol, c = e - (e / ncol) * ncol;
-            sB[i][c] = i < valid ? to_f32(bp[(tok0 + i) * ncol + c]) : 0.0f;
+        for (int e = tid; e < C * dk; e += kThreads) {
+            const int i = e / dk, c = e % dk;
+            sB[i][c] = i < valid ? to_f32(kp[(tok0 + i) * dk + c]) : 0.0f;
         }
         for (int e = tid; e < C * kTileRows; e += kThreads) {
             const int i = e / kTileRows, r = e % kTileRows;
-            sR[i][r] = i < valid ? to_f32(kp[(tok0 + i) * dk + r0 + r]) : 0.0f;
+            sR[i][r] = i < valid ? to_f32(rp[(tok0 + i) * nrow + r0 + r]) : 0.0f;
         }
         if (tid < kWave) chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
         __syncthreads();
@@ -79,7 +80,7 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
         for (int m = 0; m < kPerThread; ++m) {
             const int e = tid + kThreads * m;
             if (e < nel) {
-                const int row = e / ncol, col = e - (e / ncol) * ncol;
+                const int row = e / dk, col = e % dk;
                 float acc = 0.0f;
                 for (int i = 0; i < C; ++i) acc += sW[i] * sR[i][row] * sB[i][col];
                 st[m] = D * st[m] + acc;
@@ -89,16 +90,11 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
     }
     float* fin = isG ? a.final_G : a.final_H;
     if (fin) {
+        float* dst = fin + (bh * nrow + r0) * int64_t(dk);
 #pragma unroll
         for (int m = 0; m < kPerThread; ++m) {
             const int e = tid + kThreads * m;
-            if (e < nel) {
-                const int row = e / ncol, col = e - (e / ncol) * ncol;
-                if (isG)
-                    fin[(bh * dv + col) * dk + r0 + row] = st[m];  // G [d_v, d_k]
-                else
-                    fin[(bh * dk + r0 + row) * dk + col] = st[m];
-            }
+            if (e < nel) dst[e] = st[m];
         }
     }
 }
@@ -123,7 +119,7 @@ hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream)
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream)
 {
     const int64_t bh = a.s.batch * a.s.heads;
-    const int64_t blocks = bh * 2 * (a.s.d_k / kTileRows);
+    const int64_t blocks = bh * ((a.s.d_k + a.s.d_v) / kTileRows);
     if (a.s.bf16)
         hipLaunchKernelGGL(chunk_state_kernel<bf16_t>, dim3(unsigned(blocks)), dim3(kThreads), 0,
                            stream, a);

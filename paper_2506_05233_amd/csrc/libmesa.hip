@@ -64,10 +64,16 @@ int validate_forward(const FwdCall& c)
                              c.dtype == MESA_DTYPE_BF16};
     if (c.precision == MESA_PREC_BF16 && !mesa::chunk_cg_bf16_supported(probe)) return MESA_ERR_UNSUPPORTED;
     if (c.batch == 0 || c.heads == 0) return MESA_OK;
-    if (!c.k || !c.v || !c.gamma || !c.beta) return MESA_ERR_NULL;
-    if (c.needs_q && (!c.q || !c.lambda || !c.out)) return MESA_ERR_NULL;
+    // Arrays with no elements (seq_len == 0) may be NULL; lambda never is empty.
+    if (c.seq_len > 0 && (!c.k || !c.v || !c.gamma || !c.beta)) return MESA_ERR_NULL;
+    if (c.needs_q && (!c.lambda || (c.seq_len > 0 && (!c.q || !c.out)))) return MESA_ERR_NULL;
     const int64_t nc = n_chunks_of(c.seq_len, c.chunk);
     if (nc * c.batch * c.heads > (int64_t(1) << 31) / 16) return MESA_ERR_SHAPE;
+    // The kernels move q, k, v, Lambda, states and outputs with 16-byte accesses.
+    for (const void* ptr : {c.q, c.k, c.v, static_cast<const void*>(c.lambda), static_cast<const void*>(c.out),
+                            static_cast<const void*>(c.qstar), static_cast<const void*>(c.final_H),
+                            static_cast<const void*>(c.final_G), c.workspace})
+        if (uintptr_t(ptr) % 16 != 0) return MESA_ERR_ARG;
     const size_t need = c.needs_ws ? mesa_forward_workspace_bytes(c.batch, c.heads, c.seq_len, c.d_k,
                                                                   c.d_v, c.chunk)
                                    : 0;
@@ -110,7 +116,7 @@ ForwardShape shape_of(const FwdCall& c)
 }
 
 float* ws_H(const FwdCall& c) { return static_cast<float*>(const_cast<void*>(c.workspace)); }
-float* ws_GT(const FwdCall& c)
+float* ws_G(const FwdCall& c)
 {
     const ForwardShape s = shape_of(c);
     return ws_H(c) + size_t(s.batch * s.heads * s.n_chunks) * size_t(s.d_k) * size_t(s.d_k);
@@ -127,7 +133,7 @@ int launch_states(const FwdCall& c, bool store_chunks, hipStream_t s)
         return MESA_OK;
     }
     mesa::StateArgs sa{shape_of(c), c.k, c.v, c.gamma, c.beta,
-                       store_chunks ? ws_H(c) : nullptr, store_chunks ? ws_GT(c) : nullptr,
+                       store_chunks ? ws_H(c) : nullptr, store_chunks ? ws_G(c) : nullptr,
                        c.final_H, c.final_G, store_chunks};
     return mesa::launch_chunk_state(sa, s) == hipSuccess ? MESA_OK : MESA_ERR_HIP;
 }
@@ -139,7 +145,7 @@ int launch_solve(const FwdCall& c, hipStream_t s)
     int prec = c.precision;
     if (prec == MESA_PREC_AUTO)
         prec = shape.bf16 && mesa::chunk_cg_bf16_supported(shape) ? MESA_PREC_BF16 : MESA_PREC_F32;
-    mesa::CgArgs ca{shape, c.q, c.k, c.v, c.gamma, c.beta, c.lambda, ws_H(c), ws_GT(c), c.n_cg, c.out, c.qstar};
+    mesa::CgArgs ca{shape, c.q, c.k, c.v, c.gamma, c.beta, c.lambda, ws_H(c), ws_G(c), c.n_cg, c.out, c.qstar};
     const hipError_t e = prec == MESA_PREC_BF16 ? mesa::launch_chunk_cg_bf16(ca, s)
                                                 : mesa::launch_chunk_cg_f32(ca, s);
     return e == hipSuccess ? MESA_OK : MESA_ERR_HIP;
@@ -158,7 +164,7 @@ const char* mesa_status_string(int status)
         case MESA_ERR_NULL: return "a required pointer is NULL";
         case MESA_ERR_SHAPE: return "a size is negative or the sizes are inconsistent";
         case MESA_ERR_UNSUPPORTED: return "d_k, d_v, chunk, dtype or precision not supported";
-        case MESA_ERR_ARG: return "n_cg out of range, or an output overlaps an input";
+        case MESA_ERR_ARG: return "n_cg out of range, a misaligned pointer, or an output overlapping an input";
         case MESA_ERR_WORKSPACE: return "workspace too small";
         case MESA_ERR_HIP: return "the HIP runtime refused a launch";
         default: return "unknown status";

@@ -17,7 +17,7 @@ struct ForwardShape {
 };
 
 // Chunk-state scan: writes the fp32 states entering every chunk,
-//   Hs  [B*H, n_chunks, d_k, d_k]   and   GTs [B*H, n_chunks, d_k, d_v] (G transposed),
+//   Hs [B*H, n_chunks, d_k, d_k]   and   Gs [B*H, n_chunks, d_v, d_k],
 // when store_chunks, and the states after the last token (final_H [B*H, d_k, d_k],
 // final_G [B*H, d_v, d_k]) when those pointers are non-null.
 struct StateArgs {
@@ -27,7 +27,7 @@ struct StateArgs {
     const float* gamma;
     const float* beta;
     float* Hs;
-    float* GTs;
+    float* Gs;
     float* final_H;
     float* final_G;
     bool store_chunks;
@@ -47,7 +47,7 @@ struct CgArgs {
     const float* beta;
     const float* lambda;
     const float* Hs;
-    const float* GTs;
+    const float* Gs;
     int n_cg;
     float* out;
     float* qstar;  // may be null

@@ -98,6 +98,8 @@ def _fwd(lib, **kw):
     (dict(n_cg=L.MESA_MAX_NCG + 1), L.MESA_ERR_ARG),
     (dict(ws_bytes=100), L.MESA_ERR_WORKSPACE),
     (dict(out=P["q"] + 64), L.MESA_ERR_ARG),          # out overlaps q
+    (dict(k=P["k"] + 2), L.MESA_ERR_ARG),             # k not 16-byte aligned
+    (dict(ws=P["ws"] + 8), L.MESA_ERR_ARG),           # workspace not 16-byte aligned
     (dict(out=P["ws"]), L.MESA_ERR_ARG),               # out overlaps the workspace
     (dict(qstar=P["out"]), L.MESA_ERR_ARG),            # two outputs overlap
     (dict(out=None, fH=P["fh"], fG=None), L.MESA_ERR_NULL),    # states only needs both states
