@@ -27,42 +27,13 @@
 // beta and every reduction stay fp32.
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
+#include "mesa_mfma.hpp"
 
 namespace mesa {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
 constexpr int kC = 64;         // chunk
 constexpr int kThreads = 256;  // four waves, 16 tokens each
-
-__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c)
-{
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ bf16x8 pack8(const f32x4& lo, const f32x4& hi)
-{
-    bf16x8 r;
-    r[0] = (__bf16)lo[0];
-    r[1] = (__bf16)lo[1];
-    r[2] = (__bf16)lo[2];
-    r[3] = (__bf16)lo[3];
-    r[4] = (__bf16)hi[0];
-    r[5] = (__bf16)hi[1];
-    r[6] = (__bf16)hi[2];
-    r[7] = (__bf16)hi[3];
-    return r;
-}
-
-// Fragment of 8 bf16 from LDS: elements base[0..3] and base[16..19].
-__device__ __forceinline__ bf16x8 lds_frag(const uint16_t* base)
-{
-    const uint2 lo = *reinterpret_cast<const uint2*>(base);
-    const uint2 hi = *reinterpret_cast<const uint2*>(base + 16);
-    return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-}
 
 // Same, with every element squared (fp32 square, rounded back to bf16).
 __device__ __forceinline__ bf16x8 lds_frag_sq(const uint16_t* base)
@@ -74,14 +45,6 @@ __device__ __forceinline__ bf16x8 lds_frag_sq(const uint16_t* base)
         f[e] = (__bf16)(v * v);
     }
     return f;
-}
-
-// Fragment of 8 fp32 from global memory (rows of H_c or G_c): base[0..3], base[16..19].
-__device__ __forceinline__ bf16x8 gmem_frag(const float* base)
-{
-    const f32x4 lo = *reinterpret_cast<const f32x4*>(base);
-    const f32x4 hi = *reinterpret_cast<const f32x4*>(base + 16);
-    return pack8(lo, hi);
 }
 
 // Sum over the four lanes that hold one column (lanes n, n+16, n+32, n+48).

@@ -12,6 +12,7 @@
 // chunk's k and v, read once per tile.
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
+#include "mesa_mfma.hpp"
 
 namespace mesa {
 namespace {
@@ -99,6 +100,150 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
     }
 }
 
+// Matrix-core variant for bf16 k and v (chunk 32 or 64).  The stacked state
+// [H; G] ((d_k + d_v) x d_k) is cut into 64-row x 32-column tiles, one per
+// workgroup; wave w keeps rows 16w..16w+15 of the tile as two 16x16 MFMA
+// result tiles and updates them in place, chunk after chunk:
+//
+//   M <- zeta_{end,start} M + X^T (w ⊙ K),   w_i = beta_i zeta_{end,i},
+//
+// with X = the chunk's keys (rows of H) or values (rows of G).  X is exact in
+// bf16; w ⊙ K is split into a bf16 high part and a bf16 remainder and both are
+// multiplied (two passes), so each term carries about 2^-17 relative error and
+// the state stays fp32-accurate to ~1e-6.  The next chunk's inputs are
+// prefetched into registers while the current one is multiplied, and each wave
+// runs the gate scan itself, so a chunk costs two barriers.
+template <int C>
+__global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
+{
+    constexpr int KST = C / 32;   // 32-token contraction steps per chunk
+    constexpr int LDT = C + 8;    // row stride (elements) of the token-minor LDS tiles
+    const ForwardShape s = a.s;
+    const int dk = s.d_k, dv = s.d_v;
+    const int nrt = (dk + dv) / 64, nct = dk / 32;
+    const int ct = blockIdx.x % nct;
+    const int rt = (blockIdx.x / nct) % nrt;
+    const int64_t bh = blockIdx.x / (nct * nrt);
+    const bool isG = rt * 64 >= dk;
+    const int xr0 = isG ? rt * 64 - dk : rt * 64;  // first row of the tile within H or G
+    const int nX = isG ? dv : dk;                  // rows of that state = width of its source
+    const int col0 = ct * 32;
+    const uint16_t* xp = static_cast<const uint16_t*>(isG ? a.v : a.k);
+    const uint16_t* kp = static_cast<const uint16_t*>(a.k);
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int lane = tid % kWave;
+    const int g = lane / 16, ln = lane % 16;
+
+    __shared__ __attribute__((aligned(16))) uint16_t sA[64 * LDT];   // X[i][row], as [row][i]
+    __shared__ __attribute__((aligned(16))) uint16_t sBh[32 * LDT];  // hi(w_i K[i][c]), as [c][i]
+    __shared__ __attribute__((aligned(16))) uint16_t sBl[32 * LDT];  // remainder
+
+    // register prefetch of one chunk: X rows, K columns, gates
+    uint4 ra[KST];
+    uint4 rb = make_uint4(0, 0, 0, 0);
+    float rgam = 1.0f, rbet = 0.0f;
+    int rvalid = 0;
+    auto load_chunk = [&](int n) {
+        const int64_t t0 = int64_t(n) * C;
+        const int valid = int(min<int64_t>(C, s.seq_len - t0));
+        const int64_t tok0 = bh * s.seq_len + t0;
+        rvalid = valid;
+#pragma unroll
+        for (int m = 0; m < KST; ++m) {
+            const int e = tid + kThreads * m, i = e / 8, f8 = (e % 8) * 8;
+            ra[m] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + xr0 + f8)
+                              : make_uint4(0, 0, 0, 0);
+        }
+        if (tid < C * 4) {
+            const int i = tid / 4, f8 = (tid % 4) * 8;
+            rb = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + col0 + f8)
+                           : make_uint4(0, 0, 0, 0);
+        }
+        rgam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
+        rbet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
+    };
+
+    f32x4 acc[2] = {f32x4{0.0f, 0.0f, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}};
+    float* chunk_dst = isG ? a.Gs : a.Hs;
+    load_chunk(0);
+    for (int n = 0; n < s.n_chunks; ++n) {
+        // gate scan of this chunk, per wave (lane i = in-chunk token i)
+        float lg = (lane < rvalid && rgam > 0.0f) ? logf(rgam) : 0.0f;
+        int zl = (lane < rvalid && !(rgam > 0.0f)) ? lane : -1;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            const float lo = __shfl_up(lg, off, kWave);
+            const int zo = __shfl_up(zl, off, kWave);
+            if (lane >= off) {
+                lg += lo;
+                zl = max(zl, zo);
+            }
+        }
+        const float lgE = __shfl(lg, C - 1, kWave);
+        const int zlE = __shfl(zl, C - 1, kWave);
+        const float wl = lane < rvalid ? rbet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
+        const float D = zlE >= 0 ? 0.0f : expf(lgE);
+
+        __syncthreads();  // the previous chunk's products are done with LDS
+#pragma unroll
+        for (int m = 0; m < KST; ++m) {
+            const int e = tid + kThreads * m, i = e / 8, f8 = (e % 8) * 8;
+            const uint32_t w4[4] = {ra[m].x, ra[m].y, ra[m].z, ra[m].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                sA[(f8 + 2 * q) * LDT + i] = uint16_t(w4[q] & 0xffffu);
+                sA[(f8 + 2 * q + 1) * LDT + i] = uint16_t(w4[q] >> 16);
+            }
+        }
+        {
+            const int i = (tid / 4) % C, f8 = (tid % 4) * 8;
+            const float wi = __shfl(wl, i, kWave);
+            if (tid < C * 4) {
+                const uint32_t w4[4] = {rb.x, rb.y, rb.z, rb.w};
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const uint32_t bits = (q & 1) ? (w4[q / 2] >> 16) : (w4[q / 2] & 0xffffu);
+                    const float v = wi * bf16_bits_to_f32(bits);
+                    const __bf16 hi = (__bf16)v;
+                    const __bf16 lo = (__bf16)(v - (float)hi);
+                    sBh[(f8 + q) * LDT + i] = bf16_bits(hi);
+                    sBl[(f8 + q) * LDT + i] = bf16_bits(lo);
+                }
+            }
+        }
+        __syncthreads();
+        if (n + 1 < s.n_chunks) load_chunk(n + 1);
+
+        if (a.store_chunks) {
+            float* dst = chunk_dst + ((bh * s.n_chunks + n) * nX + xr0 + 16 * wave + 4 * g) * int64_t(dk) + col0 + ln;
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                for (int ii = 0; ii < 4; ++ii) dst[ii * dk + 16 * nt] = acc[nt][ii];
+        }
+        acc[0] *= D;
+        acc[1] *= D;
+#pragma unroll
+        for (int u = 0; u < KST; ++u) {
+            const bf16x8 af = lds_frag(sA + (16 * wave + ln) * LDT + 32 * u + 4 * g);
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                acc[nt] = mfma16(af, lds_frag(sBh + (16 * nt + ln) * LDT + 32 * u + 4 * g), acc[nt]);
+                acc[nt] = mfma16(af, lds_frag(sBl + (16 * nt + ln) * LDT + 32 * u + 4 * g), acc[nt]);
+            }
+        }
+    }
+    float* fin = isG ? a.final_G : a.final_H;
+    if (fin) {
+        float* dst = fin + (bh * nX + xr0 + 16 * wave + 4 * g) * int64_t(dk) + col0 + ln;
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) dst[ii * dk + 16 * nt] = acc[nt][ii];
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void fill_zero_kernel(float* dst, int64_t n)
 {
     const int64_t stride = int64_t(gridDim.x) * kThreads;
@@ -119,6 +264,14 @@ hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream)
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream)
 {
     const int64_t bh = a.s.batch * a.s.heads;
+    if (a.s.bf16 && (a.s.chunk == 32 || a.s.chunk == 64)) {
+        const unsigned blocks = unsigned(bh * ((a.s.d_k + a.s.d_v) / 64) * (a.s.d_k / 32));
+        if (a.s.chunk == 64)
+            hipLaunchKernelGGL(chunk_state_mfma_kernel<64>, dim3(blocks), dim3(kThreads), 0, stream, a);
+        else
+            hipLaunchKernelGGL(chunk_state_mfma_kernel<32>, dim3(blocks), dim3(kThreads), 0, stream, a);
+        return hipGetLastError();
+    }
     const int64_t blocks = bh * ((a.s.d_k + a.s.d_v) / kTileRows);
     if (a.s.bf16)
         hipLaunchKernelGGL(chunk_state_kernel<bf16_t>, dim3(unsigned(blocks)), dim3(kThreads), 0,

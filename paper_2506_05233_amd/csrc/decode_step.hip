@@ -1,129 +1,181 @@
 // Recurrent decode step of the Mesa layer (Sec. 3, recurrent inference mode;
 // App. C, last paragraph: at inference CG runs on H_t + Lambda directly).
-// One workgroup per (sequence, head):
-//   1. H <- gamma H + beta k k^T, written back in place; H + Lambda kept in LDS.
-//   2. n_cg iterations of Alg. 1 (tolerance 0) on (H + Lambda) x = q, each
-//      product a GEMV from LDS.
-//   3. G <- gamma G + beta v k^T streamed through registers and written back,
-//      with o = G x formed on the way.
-// All arithmetic is fp32.  The step is bound by HBM: each (sequence, head)
-// reads and writes its two fp32 states, 8 (d_k + d_v) d_k bytes.
+//
+// One 64-lane wave per (sequence, head); the step is bound by HBM, since each
+// pair reads and writes its two fp32 states (8 (d_k + d_v) d_k bytes).
+//   1. H <- gamma H + beta k k^T.  Lane l keeps rows R(l) = {l, l + 64, ...}
+//      of H in registers.  H is symmetric, so row r is read as column r,
+//      H[c][r] for c = 0..d_k-1, which makes every load and store one
+//      contiguous 256-byte wave access; the updated column is written back
+//      in place.
+//   2. Alg. 1 with tolerance 0 on (H + Lambda) x = q: each product is a
+//      register-resident GEMV against p broadcast through LDS; the CG scalars
+//      are wave reductions, so no barrier beyond the wave is needed.
+//   3. Lane l streams rows R(l) of G through registers: G <- gamma G +
+//      beta v k^T, written back, and o_e = sum_b G[e][b] x_b formed per row.
+// All arithmetic is fp32.
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
 
 namespace mesa {
 namespace {
 
-constexpr int kThreads = 256;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-template <typename Tin, int DK>
-__global__ __launch_bounds__(kThreads) void decode_step_kernel(DecodeArgs a)
+template <typename Tin, int DK, int DV>
+__global__ __launch_bounds__(kWave) void decode_step_kernel(DecodeArgs a)
 {
-    constexpr int TPR = kThreads / DK;  // threads per row of H in a GEMV
-    constexpr int LDA = DK + 1;
+    constexpr int RH = DK / kWave;  // rows of H per lane
+    constexpr int RG = DV / kWave;  // rows of G per lane
     const int64_t pair = blockIdx.x;
     const int h = int(pair % a.heads);
-    const int dv = a.d_v;
-    const int tid = threadIdx.x;
+    const int lane = threadIdx.x;
 
-    __shared__ float sA[DK * LDA];
-    __shared__ float sk[DK], sq[DK], sv[128], sx[DK], sp[DK];
-    __shared__ float sRed[kThreads / kWave];
-    __shared__ float sO[128 * (DK / kWave)];
+    __shared__ __attribute__((aligned(16))) float sk[DK];
+    __shared__ __attribute__((aligned(16))) float sp[DK];
 
     const Tin* qp = static_cast<const Tin*>(a.q) + pair * DK;
     const Tin* kp = static_cast<const Tin*>(a.k) + pair * DK;
-    const Tin* vp = static_cast<const Tin*>(a.v) + pair * dv;
+    const Tin* vp = static_cast<const Tin*>(a.v) + pair * DV;
     const float* lam = a.lambda + int64_t(h) * DK;
-    if (tid < DK) {
-        sk[tid] = to_f32(kp[tid]);
-        sq[tid] = to_f32(qp[tid]);
-    }
-    if (tid < dv) sv[tid] = to_f32(vp[tid]);
-    const float g = a.gamma[pair], bt = a.beta[pair];
-    __syncthreads();
+    const float gam = a.gamma[pair], bet = a.beta[pair];
 
-    float* H = a.H + pair * DK * DK;
-    for (int e = tid; e < DK * DK; e += kThreads) {
-        const int rr = e / DK, c = e % DK;
-        const float hn = g * H[e] + bt * sk[rr] * sk[c];
-        H[e] = hn;
-        sA[rr * LDA + c] = hn + (rr == c ? lam[rr] : 0.0f);
-    }
-    __syncthreads();
-
-    const int row = tid / TPR, part = tid % TPR;
-    auto gemv = [&](const float* vec) -> float {
-        float acc = 0.0f;
-        for (int b = part; b < DK; b += TPR) acc += sA[row * LDA + b] * vec[b];
+    float kr[RH], qr[RH], lr[RH], vr[RG];
 #pragma unroll
-        for (int off = TPR / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, kWave);
-        return acc;
-    };
-    // Sum of one value per row (the TPR copies of a row count once).
-    auto rowsum = [&](float v) -> float {
-        v = wave_sum(part == 0 ? v : 0.0f);
-        if ((tid & (kWave - 1)) == 0) sRed[tid / kWave] = v;
-        __syncthreads();
-        float t = 0.0f;
+    for (int u = 0; u < RH; ++u) {
+        const int r = lane + kWave * u;
+        kr[u] = to_f32(kp[r]);
+        qr[u] = to_f32(qp[r]);
+        lr[u] = lam[r];
+        sk[r] = kr[u];
+    }
 #pragma unroll
-        for (int w = 0; w < kThreads / kWave; ++w) t += sRed[w];
+    for (int u = 0; u < RG; ++u) vr[u] = to_f32(vp[lane + kWave * u]);
+    __syncthreads();
+
+    // ---- 1. state update of H, rows R(lane) held as hrow[u][c]
+    float* Hp = a.H + pair * DK * DK;
+    float hrow[RH][DK];
+    float hdiag[RH];
+#pragma unroll
+    for (int c = 0; c < DK; ++c)
+#pragma unroll
+        for (int u = 0; u < RH; ++u) hrow[u][c] = Hp[c * DK + lane + kWave * u];
+#pragma unroll
+    for (int u = 0; u < RH; ++u) {
+        const int r = lane + kWave * u;
+        hdiag[u] = gam * Hp[r * DK + r] + bet * kr[u] * kr[u] + lr[u];
+    }
+#pragma unroll
+    for (int c4 = 0; c4 < DK; c4 += 4) {
+        const f32x4 kc = *reinterpret_cast<const f32x4*>(sk + c4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int u = 0; u < RH; ++u) {
+                const float hn = gam * hrow[u][c4 + e] + bet * kr[u] * kc[e];
+                hrow[u][c4 + e] = hn;
+                Hp[(c4 + e) * DK + lane + kWave * u] = hn;
+            }
+    }
+
+    // ---- 2. CG on (H + Lambda) x = q
+    auto gemv = [&](const float (&pin)[RH], float (&wout)[RH]) {
+        __syncthreads();  // previous readers of sp are done
+#pragma unroll
+        for (int u = 0; u < RH; ++u) sp[lane + kWave * u] = pin[u];
         __syncthreads();
-        return t;
+#pragma unroll
+        for (int u = 0; u < RH; ++u) wout[u] = lr[u] * pin[u];
+#pragma unroll
+        for (int c4 = 0; c4 < DK; c4 += 4) {
+            const f32x4 pc = *reinterpret_cast<const f32x4*>(sp + c4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int u = 0; u < RH; ++u) wout[u] += hrow[u][c4 + e] * pc[e];
+        }
+    };
+    auto dot = [&](const float (&x)[RH], const float (&y)[RH]) -> float {
+        float s = 0.0f;
+#pragma unroll
+        for (int u = 0; u < RH; ++u) s += x[u] * y[u];
+        return wave_sum(s);
     };
 
-    const float qv = sq[row];
-    float x = qv / sA[row * LDA + row];
-    if (part == 0) sx[row] = x;
-    __syncthreads();
-    float r = qv - gemv(sx);
-    float p = r;
-    float delta = rowsum(r * r);
+    float x[RH], r[RH], p[RH], w[RH];
+#pragma unroll
+    for (int u = 0; u < RH; ++u) x[u] = qr[u] / hdiag[u];
+    gemv(x, w);
+#pragma unroll
+    for (int u = 0; u < RH; ++u) {
+        r[u] = qr[u] - w[u];
+        p[u] = r[u];
+    }
+    float delta = dot(r, r);
     if (delta > 0.0f) {
         for (int it = 0; it < a.n_cg; ++it) {
-            if (part == 0) sp[row] = p;
-            __syncthreads();
-            const float w = gemv(sp);
-            const float pw = rowsum(p * w);
+            gemv(p, w);
+            const float pw = dot(p, w);
             if (!(pw > 0.0f)) break;
             const float alpha = delta / pw;
-            x += alpha * p;
-            r -= alpha * w;
-            const float dn = rowsum(r * r);
+#pragma unroll
+            for (int u = 0; u < RH; ++u) {
+                x[u] += alpha * p[u];
+                r[u] -= alpha * w[u];
+            }
+            const float dn = dot(r, r);
             if (dn == 0.0f) break;
-            p = r + (dn / delta) * p;
+            const float beta_cg = dn / delta;
+#pragma unroll
+            for (int u = 0; u < RH; ++u) p[u] = r[u] + beta_cg * p[u];
             delta = dn;
         }
     }
-    if (part == 0) sx[row] = x;
-    __syncthreads();
 
-    float* G = a.G + pair * int64_t(dv) * DK;
-    for (int e = tid; e < dv * DK; e += kThreads) {
-        const int rr = e / DK, c = e % DK;
-        const float gn = g * G[e] + bt * sv[rr] * sk[c];
-        G[e] = gn;
-        const float s = wave_sum(gn * sx[c]);
-        if ((tid & (kWave - 1)) == 0) sO[rr * (DK / kWave) + c / kWave] = s;
-    }
+    // ---- 3. G update and read-out, rows R(lane) of G
     __syncthreads();
-    if (tid < dv) {
+#pragma unroll
+    for (int u = 0; u < RH; ++u) sp[lane + kWave * u] = x[u];
+    __syncthreads();
+    float* Gp = a.G + pair * int64_t(DV) * DK;
+#pragma unroll
+    for (int u = 0; u < RG; ++u) {
+        const int e = lane + kWave * u;
+        float* grow = Gp + int64_t(e) * DK;
         float o = 0.0f;
 #pragma unroll
-        for (int u = 0; u < DK / kWave; ++u) o += sO[tid * (DK / kWave) + u];
-        a.out[pair * dv + tid] = o;
+        for (int c4 = 0; c4 < DK; c4 += 4) {
+            const f32x4 gv = *reinterpret_cast<const f32x4*>(grow + c4);
+            const f32x4 kc = *reinterpret_cast<const f32x4*>(sk + c4);
+            const f32x4 xc = *reinterpret_cast<const f32x4*>(sp + c4);
+            f32x4 gn;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                gn[q] = gam * gv[q] + bet * vr[u] * kc[q];
+                o += gn[q] * xc[q];
+            }
+            *reinterpret_cast<f32x4*>(grow + c4) = gn;
+        }
+        a.out[pair * DV + e] = o;
     }
+}
+
+template <typename Tin, int DK>
+hipError_t launch_dk(const DecodeArgs& a, hipStream_t stream)
+{
+    const unsigned blocks = unsigned(a.batch * a.heads);
+    if (a.d_v == 64)
+        hipLaunchKernelGGL((decode_step_kernel<Tin, DK, 64>), dim3(blocks), dim3(kWave), 0, stream, a);
+    else
+        hipLaunchKernelGGL((decode_step_kernel<Tin, DK, 128>), dim3(blocks), dim3(kWave), 0, stream, a);
+    return hipGetLastError();
 }
 
 template <typename Tin>
 hipError_t launch_tin(const DecodeArgs& a, hipStream_t stream)
 {
-    const unsigned blocks = unsigned(a.batch * a.heads);
-    if (a.d_k == 64)
-        hipLaunchKernelGGL((decode_step_kernel<Tin, 64>), dim3(blocks), dim3(kThreads), 0, stream, a);
-    else
-        hipLaunchKernelGGL((decode_step_kernel<Tin, 128>), dim3(blocks), dim3(kThreads), 0, stream, a);
-    return hipGetLastError();
+    return a.d_k == 64 ? launch_dk<Tin, 64>(a, stream) : launch_dk<Tin, 128>(a, stream);
 }
 
 }  // namespace

@@ -1,0 +1,60 @@
+// Helpers for the gfx950 bf16 matrix-core kernels (v_mfma_f32_16x16x32_bf16).
+//
+// Operand layouts used throughout: for a 16x16 result tile, lane
+// (g = lane / 16, n = lane % 16) holds rows 4g + {0..3} of column n.  A
+// 32-long contraction takes, in lane group g, the eight k-indices
+// {4g .. 4g+3} and {16 + 4g .. 16 + 4g + 3} (element e < 4 and e >= 4 of the
+// 8-wide operand), for both the A operand (row m = lane % 16) and the B
+// operand (column n = lane % 16).  Any fixed assignment of k-indices to
+// operand elements gives the same product as long as A and B agree; this one
+// lets two stacked 16-row result tiles feed the next contraction directly.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mesa {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 pack8(const f32x4& lo, const f32x4& hi)
+{
+    bf16x8 r;
+    r[0] = (__bf16)lo[0];
+    r[1] = (__bf16)lo[1];
+    r[2] = (__bf16)lo[2];
+    r[3] = (__bf16)lo[3];
+    r[4] = (__bf16)hi[0];
+    r[5] = (__bf16)hi[1];
+    r[6] = (__bf16)hi[2];
+    r[7] = (__bf16)hi[3];
+    return r;
+}
+
+// 8 bf16 from LDS: base[0..3] and base[16..19] (the k-index map above).
+__device__ __forceinline__ bf16x8 lds_frag(const uint16_t* base)
+{
+    const uint2 lo = *reinterpret_cast<const uint2*>(base);
+    const uint2 hi = *reinterpret_cast<const uint2*>(base + 16);
+    return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+}
+
+// 8 fp32 from global memory, base[0..3] and base[16..19], rounded to bf16.
+__device__ __forceinline__ bf16x8 gmem_frag(const float* base)
+{
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(base);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(base + 16);
+    return pack8(lo, hi);
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+__device__ __forceinline__ uint16_t bf16_bits(__bf16 x) { return __builtin_bit_cast(uint16_t, x); }
+
+}  // namespace mesa

@@ -256,7 +256,7 @@ def test_decode_f32_matches_oracle_tightly():
                                     np.full((3, 2, 50), 0.97), np.full((3, 2, 50), 0.5))
     H0 = H0.astype(np.float32)
     G0 = G0.astype(np.float32)
-    d = to_device({k: v[:, :, 0] if v.ndim == 3 else v for k, v in x.items() if k != "lam"}, "f32")
+    d = to_device({k: v[:, :, 0] for k, v in x.items() if k != "lam"}, "f32")
     dH, dG = torch.from_numpy(H0).cuda(), torch.from_numpy(G0).cuda()
     lam = torch.from_numpy(x["lam"]).cuda()
     out = L.decode_step(dH, dG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], lam, 12)
