@@ -81,11 +81,12 @@ extern "C" {
  * the final states, when asked for, are the initial ones, H_0 = G_0 = 0. */
 #define MESA_MAX_NCG 1024
 
-/* Bytes of device workspace mesa_forward needs: the fp32 states entering every
- * chunk, H_c [batch, heads, ceil(seq_len/chunk), d_k, d_k] followed by
- * G_c [batch, heads, ceil(seq_len/chunk), d_v, d_k] (App. D: states are kept
- * only at chunk boundaries c = 0, C, 2C, ...).  Returns 0 for unsupported or
- * empty sizes. */
+/* Bytes of device workspace mesa_forward needs: the states entering every
+ * chunk (App. D: states are kept only at chunk boundaries c = 0, C, 2C, ...),
+ * H_c for [batch, heads, ceil(seq_len/chunk)] chunks (d_k x d_k each) followed
+ * by G_c (d_v x d_k each), as fp32 (the upper bound; the bf16 path stores them
+ * as bf16 and uses half).  The layout is internal to the library.  Returns 0
+ * for unsupported or empty sizes. */
 size_t mesa_forward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
                                     int64_t d_v, int chunk);
 
@@ -126,13 +127,15 @@ int mesa_forward_ex(const void* q, const void* k, const void* v, const float* ga
  * followed by mesa_forward_solve on the same workspace and stream.
  *
  * mesa_forward_states: step (a), the chunk-state scan.  Writes the states
- * entering every chunk into the workspace (layout as described for
- * mesa_forward_workspace_bytes) and, when non-NULL, final_H / final_G.
+ * entering every chunk into the workspace and, when non-NULL, final_H /
+ * final_G.  `precision` must be the one the following mesa_forward_solve
+ * uses: it selects the workspace layout (fp32 states for MESA_PREC_F32,
+ * bf16 states laid out as matrix-core operands for MESA_PREC_BF16).
  * One kernel launch. */
 int mesa_forward_states(const void* k, const void* v, const float* gamma, const float* beta,
                         int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v,
-                        int dtype, int chunk, float* final_H, float* final_G, void* workspace,
-                        size_t workspace_bytes, void* stream);
+                        int dtype, int chunk, int precision, float* final_H, float* final_G,
+                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* mesa_forward_solve: steps (b) and (c), the chunked CG solve and the
  * read-out o_t = G_t q*_t, from the states a previous mesa_forward_states

@@ -8,23 +8,35 @@
 //   (H_t + Lambda) p_j = H_c (zeta_j p_j) + sum_{i<=j} beta_i Z[i][j] k_i (k_i^T p_j) + Lambda p_j
 //   o_j               = G_c (zeta_j x_j) + sum_{i<=j} beta_i Z[i][j] v_i (k_i^T x_j).
 //
-// Work split: a workgroup is one chunk, each of its four waves owns 16 tokens
-// (columns j = 16w .. 16w+15) over all d_k features and runs its own CG with
-// no barrier.  Every per-token vector (x, r, p, w) lives in registers in the
-// layout of a v_mfma_f32_16x16x32_bf16 result: lane (g = lane/16, n = lane%16)
-// holds rows 16t + 4g + {0..3} of column n for each 16-row tile t.  The
-// 32-long contraction of one MFMA consumes two such tiles: k-index
-// e in 0..7 of lane group g stands for row 32s + 4g + e (e < 4) or
-// 32s + 16 + 4g + (e - 4) (e >= 4).  The A operands (H_c, the keys) are laid
-// out with the same index map, so a CG vector feeds the next product straight
-// from its accumulator registers, with no LDS round trip.
+// Work split: a workgroup is one chunk; wave w owns the 16-token sub-chunk
+// j = 16w .. 16w+15 and runs its own CG on it with no barrier.  Each wave
+// first forms the state that enters its sub-chunk,
 //
-// Per CG product and wave: H_c (zeta p) as d_k/16 x d_k/32 MFMAs with H_c held
-// as bf16 A-fragments in registers for the whole solve; S = K_c p over the
-// causal token tiles 0..w only; S' = beta Z ⊙ S in fp32; W += K_c^T S' over the
-// same tiles.  CG scalars reduce over the 4 lanes of a column with two
+//   B_w = zeta_{16w-1} H_c + sum_{i < 16w} beta_i zeta_{16w-1,i} k_i k_i^T   (B_0 = H_c),
+//
+// on the matrix cores (a rank-16w update of H_c; H and B_w are symmetric, so
+// the result tiles come out directly in the A-operand layout), and keeps it as
+// bf16 A-fragments in registers.  Inside CG every product is then
+//
+//   (H_t + Lambda) p_j = B_w (zt_j p_j) + sum_{16w <= i <= j} beta_i Z[i][j] k_i (k_i^T p_j) + Lambda p_j,
+//
+// with zt_j = zeta_{c+j, c+16w-1}: d_k/16 x d_k/32 MFMAs for the state term, a
+// 16-token S = K_w p (d_k/32 MFMAs) and W += K_w^T (beta Z ⊙ S) (d_k/16 MFMAs of
+// 16x16x16).  All four waves do the same work, and every operand of the CG
+// loop stays in registers.
+//
+// Every per-token vector (x, r, p, w) lives in registers in the layout of a
+// 16x16 MFMA result: lane (g = lane/16, n = lane%16) holds rows 16t + 4g + {0..3}
+// of column n for each 16-row tile t.  The 32-long contraction of
+// v_mfma_f32_16x16x32_bf16 takes, in lane group g, rows 32s + 4g + {0..3} and
+// 32s + 16 + 4g + {0..3}: the lane's own values of two stacked tiles, so a CG
+// vector feeds the next product straight from registers (A operands use the
+// same index map).  CG scalars reduce over the 4 lanes of a column with two
 // cross-lane shuffles.  Only the MFMA operands are bf16; x, r, p, w, alpha,
 // beta and every reduction stay fp32.
+//
+// The read-out o_j = G_c (zeta_j x_j) + sum_{i <= j} beta_i Z[i][j] v_i (k_i^T x_j)
+// runs once per chunk over the whole causal chunk.
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
 #include "mesa_mfma.hpp"
@@ -50,9 +62,12 @@ __device__ __forceinline__ bf16x8 lds_frag_sq(const uint16_t* base)
 // Sum over the four lanes that hold one column (lanes n, n+16, n+32, n+48).
 __device__ __forceinline__ float col_sum(float v)
 {
-    v += __shfl_xor(v, 16, kWave);
-    v += __shfl_xor(v, 32, kWave);
-    return v;
+    // gfx950 row swaps: odd 16-lane rows of one copy with even rows of the
+    // other, then the upper 32 lanes of one with the lower 32 of the other.
+    const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(s16[0]) + __uint_as_float(s16[1]);
+    const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
 }
 
 template <int DK, int DV>
@@ -85,6 +100,7 @@ void chunk_cg_bf16_kernel(CgArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t sQ[kC * LDK];   // q_j[b], token-major
     __shared__ float sLg[kWave], sBeta[kWave];
     __shared__ int sZl[kWave];
+    __shared__ __attribute__((aligned(16))) float sLam[DK];
 
     // ---- stage the chunk's keys, values and queries (bf16 bits) in LDS
     const uint16_t* kp = static_cast<const uint16_t*>(a.k);
@@ -122,39 +138,105 @@ void chunk_cg_bf16_kernel(CgArgs a)
         sBeta[tid] = tid < valid ? a.beta[tok0 + tid] : 0.0f;
     }
 
-    // ---- per-lane constants: H_c fragments, Lambda, decays
-    const float* Hc = a.Hs + (bh * s.n_chunks + n) * int64_t(DK) * DK;
-    bf16x8 hf[MT][KS];
+    // chunk states as bf16 A-fragments: fragment (t, s) of lane l at [(t * KS + s) * 64 + l] * 8
+    const uint16_t* Hf = static_cast<const uint16_t*>(a.Hs) + (bh * s.n_chunks + n) * int64_t(DK) * DK;
+    const uint16_t* Gf = static_cast<const uint16_t*>(a.Gs) + (bh * s.n_chunks + n) * int64_t(DV) * DK;
+    bf16x8 hc[MT][KS];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) hf[mt][ks] = gmem_frag(Hc + (16 * mt + ln) * DK + 32 * ks + 4 * g);
+        for (int ks = 0; ks < KS; ++ks)
+            hc[mt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(Hf + ((mt * KS + ks) * 64 + lane) * 8));
     const float* lam = a.lambda + int64_t(h) * DK;
-    f32x4 lamv[MT], hdiag[MT];
+    if (tid < DK) sLam[tid] = lam[tid];
+    // diag(H_c) for the rows r = 16mt + 4g + ii this lane holds
+    f32x4 hdiag[MT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        lamv[mt] = *reinterpret_cast<const f32x4*>(lam + 16 * mt + 4 * g);
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
             const int r = 16 * mt + 4 * g + ii;
-            hdiag[mt][ii] = Hc[r * DK + r];
+            const int rs = r % 32, gl = (rs % 16) / 4, e = 4 * (rs / 16) + rs % 4;
+            const int idx = (((r / 16) * KS + r / 32) * 64 + gl * 16 + r % 16) * 8 + e;
+            hdiag[mt][ii] = bf16_bits_to_f32(Hf[idx]);
         }
-    }
     __syncthreads();
 
-    const float zeta = decay_from_start(sLg, sZl, j);
-    // beta_i Z[i][j] for the rows i = 16 it + 4g + ii this lane meets in S (tiles it <= wave)
-    f32x4 zw[4];
+    // ---- decays of this sub-chunk
+    const int jb = 16 * wave - 1;  // token whose state enters the sub-chunk (-1: the chunk's H_c)
+    const float zt = wave == 0 ? decay_from_start(sLg, sZl, j) : decay_between(sLg, sZl, jb, j);
+    const float Dw = wave == 0 ? 1.0f : decay_from_start(sLg, sZl, jb);
+    f32x4 zw;  // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
 #pragma unroll
-    for (int it = 0; it < 4; ++it)
+    for (int ii = 0; ii < 4; ++ii) {
+        const int i = 16 * wave + 4 * g + ii;
+        zw[ii] = sBeta[i] * decay_between(sLg, sZl, i, j);
+    }
+    // rank-update weights u_i = beta_i zeta_{16w-1,i} for i < 16w, on this lane's k-indices
+    bf16x8 uwb[2];
+    float uw[2][8];
 #pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-            const int i = 16 * it + 4 * g + ii;
-            zw[it][ii] = (it <= wave) ? sBeta[i] * decay_between(sLg, sZl, i, j) : 0.0f;
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
+            uw[u][e] = i < 16 * wave ? sBeta[i] * decay_between(sLg, sZl, i, jb) : 0.0f;
+            uwb[u][e] = (__bf16)uw[u][e];
         }
-    bf16x8 zwb[2];
+    const int nu = (16 * wave + 31) / 32;  // 32-token steps holding tokens < 16w
+
+    // ---- B_w as bf16 A-fragments: hf[mt][s] covers rows 16mt.., columns 32s..
+    bf16x8 hf[MT][KS];
+    f32x4 dg1[MT];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) zwb[u] = pack8(zw[2 * u], zw[2 * u + 1]);
+    for (int mt = 0; mt < MT; ++mt) {
+        bf16x8 bw[2];
+        dg1[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            if (u < nu) {
+                const bf16x8 raw = lds_frag(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) bw[u][e] = (__bf16)((float)raw[e] * uw[u][e]);
+                dg1[mt] = mfma16(lds_frag_sq(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g), uwb[u], dg1[mt]);
+            }
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (nu == 0) {
+                hf[mt][ks] = hc[mt][ks];  // B_0 = H_c
+                continue;
+            }
+            f32x4 lo, hi;
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) {
+                lo[ii] = Dw * (float)hc[mt][ks][ii];
+                hi[ii] = Dw * (float)hc[mt][ks][4 + ii];
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                if (u < nu) {
+                    lo = mfma16(lds_frag(sKT + (32 * ks + ln) * LDC + 32 * u + 4 * g), bw[u], lo);
+                    hi = mfma16(lds_frag(sKT + (32 * ks + 16 + ln) * LDC + 32 * u + 4 * g), bw[u], hi);
+                }
+            }
+            hf[mt][ks] = pack8(lo, hi);
+        }
+    }
+    // ---- the sub-chunk's keys as A-fragments: rows of S (kf2), columns of W (kf3)
+    bf16x8 kf2[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf2[ks] = lds_frag(sK + (16 * wave + ln) * LDK + 32 * ks + 4 * g);
+    // kf3: the 16 sub-chunk tokens in the lower half of a 32-long contraction
+    // (elements 4..7 zero), so W += K_w^T S' stays on v_mfma_f32_16x16x32_bf16.
+    bf16x8 kf3[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const uint2 kk = *reinterpret_cast<const uint2*>(sKT + (16 * mt + ln) * LDC + 16 * wave + 4 * g);
+        kf3[mt] = __builtin_bit_cast(bf16x8, make_uint4(kk.x, kk.y, 0u, 0u));
+    }
+    const f32x4 zero4 = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    const bf16x8 zwb = pack8(zw, zero4);
 
     // W = A_j vec for this wave's 16 columns (A_j = H_t + Lambda of token j).
     auto matvec = [&](const f32x4 (&vec)[MT], f32x4 (&w)[MT]) {
@@ -162,60 +244,42 @@ void chunk_cg_bf16_kernel(CgArgs a)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             pb[ks] = pack8(vec[2 * ks], vec[2 * ks + 1]);
-            pz[ks] = pack8(zeta * vec[2 * ks], zeta * vec[2 * ks + 1]);
+            pz[ks] = pack8(zt * vec[2 * ks], zt * vec[2 * ks + 1]);
         }
-        f32x4 sacc[4];
+        f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-            sacc[it] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            if (it <= wave) {
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks)
-                    sacc[it] = mfma16(lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g), pb[ks], sacc[it]);
-            }
-        }
+        for (int ks = 0; ks < KS; ++ks) sacc = mfma16(kf2[ks], pb[ks], sacc);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             w[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) w[mt] = mfma16(hf[mt][ks], pz[ks], w[mt]);
         }
+        const bf16x8 sb = pack8(sacc * zw, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            if (2 * u <= wave) {
-                const bf16x8 sb = pack8(sacc[2 * u] * zw[2 * u], sacc[2 * u + 1] * zw[2 * u + 1]);
+        for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(kf3[mt], sb, w[mt]);
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    w[mt] = mfma16(lds_frag(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, w[mt]);
-            }
-        }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) w[mt] += lamv[mt] * vec[mt];
+        for (int mt = 0; mt < MT; ++mt) w[mt] += *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g) * vec[mt];
     };
 
-    // ---- Jacobi start x0 = q / diag(H_t + Lambda)
+    // ---- Jacobi start x0 = q / diag(H_t + Lambda),
+    //      diag(H_t) = zt_j diag(B_w) + sum_{16w <= i <= j} beta_i Z[i][j] k_i^2
     f32x4 x[MT], r[MT], p[MT], w[MT];
-    {
-        f32x4 dg[MT];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) dg[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int mt = 0; mt < MT; ++mt) {
+        bf16x8 ksq = kf3[mt];
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            if (2 * u <= wave) {
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    dg[mt] = mfma16(lds_frag_sq(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g), zwb[u], dg[mt]);
-            }
+        for (int e = 0; e < 4; ++e) {
+            const float v = (float)ksq[e];
+            ksq[e] = (__bf16)(v * v);
         }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const uint2 qq = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
-            const f32x4 qf{__uint_as_float(qq.x << 16), __uint_as_float(qq.x & 0xffff0000u),
-                           __uint_as_float(qq.y << 16), __uint_as_float(qq.y & 0xffff0000u)};
-            const f32x4 d = zeta * hdiag[mt] + dg[mt] + lamv[mt];
-            x[mt] = qf / d;
-            p[mt] = qf;  // holds q until the first residual is formed
-        }
+        const f32x4 dg2 = mfma16(ksq, zwb, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+        const uint2 qq = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
+        const f32x4 qf{bf16_bits_to_f32(qq.x & 0xffffu), bf16_bits_to_f32(qq.x >> 16),
+                       bf16_bits_to_f32(qq.y & 0xffffu), bf16_bits_to_f32(qq.y >> 16)};
+        const f32x4 d = zt * (Dw * hdiag[mt] + dg1[mt]) + dg2 + *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
+        x[mt] = qf / d;
+        p[mt] = qf;  // holds q until the first residual is formed
     }
     matvec(x, w);
     float part = 0.0f;
@@ -266,7 +330,15 @@ void chunk_cg_bf16_kernel(CgArgs a)
         for (int mt = 0; mt < MT; ++mt)
             *reinterpret_cast<f32x4*>(a.qstar + (tok0 + j) * DK + 16 * mt + 4 * g) = x[mt];
     }
-    const float* Gc = a.Gs + (bh * s.n_chunks + n) * int64_t(DV) * DK;
+    const float zeta = decay_from_start(sLg, sZl, j);
+    f32x4 zo[4];  // beta_i Z[i][j] over the causal tiles it <= wave
+#pragma unroll
+    for (int it = 0; it < 4; ++it)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+            const int i = 16 * it + 4 * g + ii;
+            zo[it][ii] = (it <= wave) ? sBeta[i] * decay_between(sLg, sZl, i, j) : 0.0f;
+        }
     bf16x8 xb[KS], xz[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -289,12 +361,13 @@ void chunk_cg_bf16_kernel(CgArgs a)
         o[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-            o[mt] = mfma16(gmem_frag(Gc + (16 * mt + ln) * DK + 32 * ks + 4 * g), xz[ks], o[mt]);
+            o[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(Gf + ((mt * KS + ks) * 64 + lane) * 8)),
+                           xz[ks], o[mt]);
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
         if (2 * u <= wave) {
-            const bf16x8 sb = pack8(sacc[2 * u] * zw[2 * u], sacc[2 * u + 1] * zw[2 * u + 1]);
+            const bf16x8 sb = pack8(sacc[2 * u] * zo[2 * u], sacc[2 * u + 1] * zo[2 * u + 1]);
 #pragma unroll
             for (int mt = 0; mt < MTV; ++mt)
                 o[mt] = mfma16(lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, o[mt]);

@@ -67,7 +67,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
         sKV[i * kLdW + c] = ok ? to_f32(kp[(tok0 + i) * DK + c]) : 0.0f;
         sP[c * LDP + i] = ok ? to_f32(qp[(tok0 + i) * DK + c]) : 0.0f;
     }
-    const float* Hc = a.Hs + (bh * s.n_chunks + n) * int64_t(DK) * DK;
+    const float* Hc = static_cast<const float*>(a.Hs) + (bh * s.n_chunks + n) * int64_t(DK) * DK;
     for (int e = tid; e < DK * DK; e += kThreads) sH[(e / DK) * LDH + e % DK] = Hc[e];
     if (tid < kWave) chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
     if (tid < C) sBeta[tid] = tid < valid ? a.beta[tok0 + tid] : 0.0f;
@@ -207,7 +207,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
         sKV[i * kLdW + c] = i < valid ? to_f32(vp[(tok0 + i) * dv + c]) : 0.0f;
     }
     // G_c [dv][DK] staged transposed, sH[b][e] = G_c[e][b]
-    const float* Gc = a.Gs + (bh * s.n_chunks + n) * int64_t(DK) * dv;
+    const float* Gc = static_cast<const float*>(a.Gs) + (bh * s.n_chunks + n) * int64_t(DK) * dv;
     for (int e = tid; e < DK * dv; e += kThreads) sH[(e % DK) * kLdW + e / DK] = Gc[e];
     __syncthreads();
     for (int e = tid; e < C * dv; e += kThreads) {

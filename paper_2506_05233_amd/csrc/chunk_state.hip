@@ -50,7 +50,7 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
 #pragma unroll
     for (int m = 0; m < kPerThread; ++m) st[m] = 0.0f;
 
-    float* chunk_dst = isG ? a.Gs : a.Hs;
+    float* chunk_dst = static_cast<float*>(isG ? a.Gs : a.Hs);
     for (int n = 0; n < s.n_chunks; ++n) {
         const int64_t t0 = int64_t(n) * C;
         const int valid = int(min<int64_t>(C, s.seq_len - t0));
@@ -165,7 +165,7 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
     };
 
     f32x4 acc[2] = {f32x4{0.0f, 0.0f, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}};
-    float* chunk_dst = isG ? a.Gs : a.Hs;
+    float* chunk_dst = static_cast<float*>(isG ? a.Gs : a.Hs);
     load_chunk(0);
     for (int n = 0; n < s.n_chunks; ++n) {
         // gate scan of this chunk, per wave (lane i = in-chunk token i)
@@ -244,6 +244,159 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
     }
 }
 
+// Fragment-layout variant (bf16 k and v, chunk 64), feeding the bf16 CG
+// kernel.  Here the state is tiled as [H | G^T] (rows = key features,
+// d_k x (d_k + d_v)): A operand = the chunk's keys, B operand = w ⊙ k (columns
+// of H) or w ⊙ v (columns of G^T), in the same hi/lo two-pass form.  After each
+// chunk a lane writes its four fp32 accumulator values, rounded to bf16, into
+// the A-fragment slots that hold them: the value at row R, column c of a 16x16
+// tile is X[c][R] of H (symmetric) or of G, i.e. fragment (c/16, R/32), lane
+// (g, c%16), element 4 (R/16 % 2) + (R%4), with g = (R%16)/4.
+__global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
+{
+    constexpr int C = 64;
+    constexpr int KST = C / 32;
+    constexpr int LDT = C + 8;
+    const ForwardShape s = a.s;
+    const int dk = s.d_k, dv = s.d_v;
+    const int nrt = dk / 64, nct = (dk + dv) / 32;
+    const int ct = blockIdx.x % nct;
+    const int rt = (blockIdx.x / nct) % nrt;
+    const int64_t bh = blockIdx.x / (nct * nrt);
+    const int row0 = rt * 64;                 // key-feature rows of the tile
+    const bool isG = ct * 32 >= dk;           // columns of G^T (value features)
+    const int colX = isG ? ct * 32 - dk : ct * 32;
+    const int nX = isG ? dv : dk;             // width of the column source
+    const uint16_t* kp = static_cast<const uint16_t*>(a.k);
+    const uint16_t* xp = static_cast<const uint16_t*>(isG ? a.v : a.k);
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int lane = tid % kWave;
+    const int g = lane / 16, ln = lane % 16;
+
+    __shared__ __attribute__((aligned(16))) uint16_t sA[64 * LDT];   // k_i[row], as [row][i]
+    __shared__ __attribute__((aligned(16))) uint16_t sBh[32 * LDT];  // hi(w_i x_i[c]), as [c][i]
+    __shared__ __attribute__((aligned(16))) uint16_t sBl[32 * LDT];
+
+    uint4 ra[KST];
+    uint4 rb = make_uint4(0, 0, 0, 0);
+    float rgam = 1.0f, rbet = 0.0f;
+    int rvalid = 0;
+    auto load_chunk = [&](int n) {
+        const int64_t t0 = int64_t(n) * C;
+        const int valid = int(min<int64_t>(C, s.seq_len - t0));
+        const int64_t tok0 = bh * s.seq_len + t0;
+        rvalid = valid;
+#pragma unroll
+        for (int m = 0; m < KST; ++m) {
+            const int e = tid + kThreads * m, i = e / 8, f8 = (e % 8) * 8;
+            ra[m] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + row0 + f8)
+                              : make_uint4(0, 0, 0, 0);
+        }
+        {
+            const int i = tid / 4, f8 = (tid % 4) * 8;
+            rb = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + colX + f8)
+                           : make_uint4(0, 0, 0, 0);
+        }
+        rgam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
+        rbet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
+    };
+
+    // fragment slot of this lane's tile values
+    const int MTX = (isG ? dv : dk) / 16, KS = dk / 32;
+    const int h = (row0 / 16 + wave) % 2;          // which half of the 32-long contraction
+    const int sidx = (row0 + 16 * wave) / 32;      // contraction step of these rows
+    uint16_t* frag_base = static_cast<uint16_t*>(isG ? a.Gs : a.Hs);
+
+    f32x4 acc[2] = {f32x4{0.0f, 0.0f, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}};
+    load_chunk(0);
+    for (int n = 0; n < s.n_chunks; ++n) {
+        float lg = (lane < rvalid && rgam > 0.0f) ? logf(rgam) : 0.0f;
+        int zl = (lane < rvalid && !(rgam > 0.0f)) ? lane : -1;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            const float lo = __shfl_up(lg, off, kWave);
+            const int zo = __shfl_up(zl, off, kWave);
+            if (lane >= off) {
+                lg += lo;
+                zl = max(zl, zo);
+            }
+        }
+        const float lgE = __shfl(lg, C - 1, kWave);
+        const int zlE = __shfl(zl, C - 1, kWave);
+        const float wl = lane < rvalid ? rbet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
+        const float D = zlE >= 0 ? 0.0f : expf(lgE);
+
+        __syncthreads();
+#pragma unroll
+        for (int m = 0; m < KST; ++m) {
+            const int e = tid + kThreads * m, i = e / 8, f8 = (e % 8) * 8;
+            const uint32_t w4[4] = {ra[m].x, ra[m].y, ra[m].z, ra[m].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                sA[(f8 + 2 * q) * LDT + i] = uint16_t(w4[q] & 0xffffu);
+                sA[(f8 + 2 * q + 1) * LDT + i] = uint16_t(w4[q] >> 16);
+            }
+        }
+        {
+            const int i = tid / 4, f8 = (tid % 4) * 8;
+            const float wi = __shfl(wl, i, kWave);
+            const uint32_t w4[4] = {rb.x, rb.y, rb.z, rb.w};
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const uint32_t bits = (q & 1) ? (w4[q / 2] >> 16) : (w4[q / 2] & 0xffffu);
+                const float v = wi * bf16_bits_to_f32(bits);
+                const __bf16 hi = (__bf16)v;
+                const __bf16 lo = (__bf16)(v - (float)hi);
+                sBh[(f8 + q) * LDT + i] = bf16_bits(hi);
+                sBl[(f8 + q) * LDT + i] = bf16_bits(lo);
+            }
+        }
+        __syncthreads();
+        if (n + 1 < s.n_chunks) load_chunk(n + 1);
+
+        if (a.store_chunks) {
+            uint16_t* base = frag_base + (bh * s.n_chunks + n) * int64_t(MTX) * KS * 512;
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                const int t = (colX + 16 * nt) / 16;
+                uint16_t* dst = base + ((t * KS + sidx) * 64 + lane) * 8 + 4 * h;
+                uint2 pk;
+                pk.x = uint32_t(bf16_bits((__bf16)acc[nt][0])) | (uint32_t(bf16_bits((__bf16)acc[nt][1])) << 16);
+                pk.y = uint32_t(bf16_bits((__bf16)acc[nt][2])) | (uint32_t(bf16_bits((__bf16)acc[nt][3])) << 16);
+                *reinterpret_cast<uint2*>(dst) = pk;
+            }
+        }
+        acc[0] *= D;
+        acc[1] *= D;
+#pragma unroll
+        for (int u = 0; u < KST; ++u) {
+            const bf16x8 af = lds_frag(sA + (16 * wave + ln) * LDT + 32 * u + 4 * g);
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                acc[nt] = mfma16(af, lds_frag(sBh + (16 * nt + ln) * LDT + 32 * u + 4 * g), acc[nt]);
+                acc[nt] = mfma16(af, lds_frag(sBl + (16 * nt + ln) * LDT + 32 * u + 4 * g), acc[nt]);
+            }
+        }
+    }
+    // final states, plain fp32: tile value (R, c) is H[R][c] or G[c][R]
+    float* fin = isG ? a.final_G : a.final_H;
+    if (fin) {
+        const int R = row0 + 16 * wave + 4 * g;
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+            const int c = colX + 16 * nt + ln;
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) {
+                if (isG)
+                    fin[(bh * dv + c) * int64_t(dk) + R + ii] = acc[nt][ii];
+                else
+                    fin[(bh * dk + R + ii) * int64_t(dk) + c] = acc[nt][ii];
+            }
+        }
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void fill_zero_kernel(float* dst, int64_t n)
 {
     const int64_t stride = int64_t(gridDim.x) * kThreads;
@@ -261,9 +414,20 @@ hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream)
     return hipGetLastError();
 }
 
+bool chunk_state_frag_supported(const ForwardShape& s)
+{
+    return s.bf16 && s.chunk == 64 && (s.d_k == 64 || s.d_k == 128) && (s.d_v == 64 || s.d_v == 128);
+}
+
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream)
 {
     const int64_t bh = a.s.batch * a.s.heads;
+    if (a.frag) {
+        if (!chunk_state_frag_supported(a.s)) return hipErrorInvalidValue;
+        const unsigned blocks = unsigned(bh * (a.s.d_k / 64) * ((a.s.d_k + a.s.d_v) / 32));
+        hipLaunchKernelGGL(chunk_state_frag_kernel, dim3(blocks), dim3(kThreads), 0, stream, a);
+        return hipGetLastError();
+    }
     if (a.s.bf16 && (a.s.chunk == 32 || a.s.chunk == 64)) {
         const unsigned blocks = unsigned(bh * ((a.s.d_k + a.s.d_v) / 64) * (a.s.d_k / 32));
         if (a.s.chunk == 64)

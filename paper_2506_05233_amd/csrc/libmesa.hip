@@ -115,11 +115,24 @@ ForwardShape shape_of(const FwdCall& c)
                         int(n_chunks_of(c.seq_len, c.chunk)), c.dtype == MESA_DTYPE_BF16};
 }
 
-float* ws_H(const FwdCall& c) { return static_cast<float*>(const_cast<void*>(c.workspace)); }
-float* ws_G(const FwdCall& c)
+// The solve path a call resolves to.  The state scan and the solve of one
+// forward must resolve to the same path: it fixes the workspace layout.
+int resolve_precision(const FwdCall& c)
 {
     const ForwardShape s = shape_of(c);
-    return ws_H(c) + size_t(s.batch * s.heads * s.n_chunks) * size_t(s.d_k) * size_t(s.d_k);
+    if (c.precision == MESA_PREC_AUTO)
+        return s.bf16 && mesa::chunk_cg_bf16_supported(s) ? MESA_PREC_BF16 : MESA_PREC_F32;
+    return c.precision;
+}
+
+// Workspace: H states then G states, fp32 plain (MESA_PREC_F32) or bf16
+// fragments (MESA_PREC_BF16, half the bytes).
+void* ws_H(const FwdCall& c) { return const_cast<void*>(c.workspace); }
+void* ws_G(const FwdCall& c)
+{
+    const ForwardShape s = shape_of(c);
+    const size_t elem = resolve_precision(c) == MESA_PREC_BF16 ? 2 : 4;
+    return static_cast<char*>(ws_H(c)) + size_t(s.batch * s.heads * s.n_chunks) * size_t(s.d_k) * size_t(s.d_k) * elem;
 }
 
 int launch_states(const FwdCall& c, bool store_chunks, hipStream_t s)
@@ -132,9 +145,10 @@ int launch_states(const FwdCall& c, bool store_chunks, hipStream_t s)
             return MESA_ERR_HIP;
         return MESA_OK;
     }
+    const bool frag = store_chunks && resolve_precision(c) == MESA_PREC_BF16;
     mesa::StateArgs sa{shape_of(c), c.k, c.v, c.gamma, c.beta,
                        store_chunks ? ws_H(c) : nullptr, store_chunks ? ws_G(c) : nullptr,
-                       c.final_H, c.final_G, store_chunks};
+                       c.final_H, c.final_G, store_chunks, frag};
     return mesa::launch_chunk_state(sa, s) == hipSuccess ? MESA_OK : MESA_ERR_HIP;
 }
 
@@ -142,9 +156,7 @@ int launch_solve(const FwdCall& c, hipStream_t s)
 {
     if (c.seq_len == 0) return MESA_OK;
     const ForwardShape shape = shape_of(c);
-    int prec = c.precision;
-    if (prec == MESA_PREC_AUTO)
-        prec = shape.bf16 && mesa::chunk_cg_bf16_supported(shape) ? MESA_PREC_BF16 : MESA_PREC_F32;
+    const int prec = resolve_precision(c);
     mesa::CgArgs ca{shape, c.q, c.k, c.v, c.gamma, c.beta, c.lambda, ws_H(c), ws_G(c), c.n_cg, c.out, c.qstar};
     const hipError_t e = prec == MESA_PREC_BF16 ? mesa::launch_chunk_cg_bf16(ca, s)
                                                 : mesa::launch_chunk_cg_f32(ca, s);
@@ -212,11 +224,11 @@ int mesa_forward(const void* q, const void* k, const void* v, const float* gamma
 
 int mesa_forward_states(const void* k, const void* v, const float* gamma, const float* beta,
                         int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v,
-                        int dtype, int chunk, float* final_H, float* final_G, void* workspace,
-                        size_t workspace_bytes, void* stream)
+                        int dtype, int chunk, int precision, float* final_H, float* final_G,
+                        void* workspace, size_t workspace_bytes, void* stream)
 {
     FwdCall c{nullptr, k, v, gamma, beta, nullptr, batch, heads, seq_len, d_k, d_v, dtype, 0, chunk,
-              MESA_PREC_AUTO, nullptr, nullptr, final_H, final_G, workspace, workspace_bytes, false,
+              precision, nullptr, nullptr, final_H, final_G, workspace, workspace_bytes, false,
               true};
     int st = validate_forward(c);
     if (st != MESA_OK || batch == 0 || heads == 0) return st;

@@ -16,22 +16,29 @@ struct ForwardShape {
     bool bf16;     // q, k, v element type
 };
 
-// Chunk-state scan: writes the fp32 states entering every chunk,
-//   Hs [B*H, n_chunks, d_k, d_k]   and   Gs [B*H, n_chunks, d_v, d_k],
-// when store_chunks, and the states after the last token (final_H [B*H, d_k, d_k],
-// final_G [B*H, d_v, d_k]) when those pointers are non-null.
+// Chunk-state scan: writes the states entering every chunk when store_chunks,
+// and the fp32 states after the last token (final_H [B*H, d_k, d_k], final_G
+// [B*H, d_v, d_k]) when those pointers are non-null.  Two layouts of the
+// chunk states:
+//   plain (frag == false): fp32 Hs [B*H, n_chunks, d_k, d_k], Gs [B*H, n_chunks, d_v, d_k];
+//   fragment (frag == true, bf16 inputs, chunk 64): bf16 MFMA A-operand
+//     fragments, Hs as [B*H, n_chunks, d_k/16, d_k/32, 64 lanes, 8] and Gs as
+//     [B*H, n_chunks, d_v/16, d_k/32, 64 lanes, 8]; fragment (t, s) lane
+//     (g, m) element e holds X[16t + m][32s + (e < 4 ? 4g + e : 16 + 4g + e - 4)].
 struct StateArgs {
     ForwardShape s;
     const void* k;
     const void* v;
     const float* gamma;
     const float* beta;
-    float* Hs;
-    float* Gs;
+    void* Hs;
+    void* Gs;
     float* final_H;
     float* final_G;
     bool store_chunks;
+    bool frag;
 };
+bool chunk_state_frag_supported(const ForwardShape& s);
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream);
 
 // dst[0 .. n) = 0 with a fill kernel (no memset node, so the call can be graph-captured).
@@ -46,8 +53,8 @@ struct CgArgs {
     const float* gamma;
     const float* beta;
     const float* lambda;
-    const float* Hs;
-    const float* Gs;
+    const void* Hs;   // chunk states, plain fp32 (fp32 path) or bf16 fragments (bf16 path)
+    const void* Gs;
     int n_cg;
     float* out;
     float* qstar;  // may be null

@@ -56,7 +56,7 @@ def load():
     lib.mesa_forward_ex.argtypes = [vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, ci,
                                     fp, fp, fp, fp, vp, sz, vp]
     lib.mesa_forward_ex.restype = ci
-    lib.mesa_forward_states.argtypes = [vp, vp, fp, fp, i64, i64, i64, i64, i64, ci, ci, fp, fp, vp, sz, vp]
+    lib.mesa_forward_states.argtypes = [vp, vp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, fp, fp, vp, sz, vp]
     lib.mesa_forward_states.restype = ci
     lib.mesa_forward_solve.argtypes = [vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, ci,
                                        fp, fp, vp, sz, vp]
@@ -207,8 +207,8 @@ class ForwardPlan:
         q, k, v, gamma, beta, lam = self.tensors
         B, H, T, dk, dv = self.dims
         st = self.lib.mesa_forward_states(_ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), B, H, T, dk, dv,
-                                          self.code, self.chunk, None, None, _ptr(self.workspace),
-                                          self.ws_bytes, _stream(self.device))
+                                          self.code, self.chunk, self.precision, None, None,
+                                          _ptr(self.workspace), self.ws_bytes, _stream(self.device))
         if st != MESA_OK:
             raise MesaError(st, "mesa_forward_states")
 
