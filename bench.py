@@ -218,6 +218,9 @@ def main():
     ap.add_argument("--cpu-sequences", type=int, default=16)
     ap.add_argument("--skip-decode", action="store_true")
     ap.add_argument("--skip-cpu", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after timing, copy this many MiB once with a plain device copy "
+                         "(reference dispatch for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (--gpus 1); the (batch, head) sharding "
@@ -234,6 +237,14 @@ def main():
 
     fw = run_forward(args, torch, L, W)
     w = fw["w"]
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     dec = None if args.skip_decode else run_decode(args, torch, L, W)
     cpu = None if args.skip_cpu else cpu_baseline(args, fw["x"], w)
 

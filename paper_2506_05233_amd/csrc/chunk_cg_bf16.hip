@@ -59,6 +59,20 @@ __device__ __forceinline__ bf16x8 lds_frag_sq(const uint16_t* base)
     return f;
 }
 
+// Gate decays with the hardware exponential (relative error ~1e-7, far below
+// the bf16 operand rounding of this path); same zero-gate rules as the
+// shared helpers.
+__device__ __forceinline__ float decay_between_hw(const float* lg, const int* zl, int i, int j)
+{
+    if (i > j || zl[j] > i) return 0.0f;
+    return __expf(lg[j] - lg[i]);
+}
+
+__device__ __forceinline__ float decay_from_start_hw(const float* lg, const int* zl, int j)
+{
+    return zl[j] >= 0 ? 0.0f : __expf(lg[j]);
+}
+
 // Sum over the four lanes that hold one column (lanes n, n+16, n+32, n+48).
 __device__ __forceinline__ float col_sum(float v)
 {
@@ -106,38 +120,32 @@ void chunk_cg_bf16_kernel(CgArgs a)
     const uint16_t* kp = static_cast<const uint16_t*>(a.k);
     const uint16_t* qp = static_cast<const uint16_t*>(a.q);
     const uint16_t* vp = static_cast<const uint16_t*>(a.v);
-    for (int e = tid; e < kC * DK / 8; e += kThreads) {
-        const int i = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
-        uint4 kv = make_uint4(0, 0, 0, 0), qv = make_uint4(0, 0, 0, 0);
-        if (i < valid) {
-            kv = *reinterpret_cast<const uint4*>(kp + (tok0 + i) * DK + c8);
-            qv = *reinterpret_cast<const uint4*>(qp + (tok0 + i) * DK + c8);
-        }
-        *reinterpret_cast<uint4*>(sK + i * LDK + c8) = kv;
-        *reinterpret_cast<uint4*>(sQ + i * LDK + c8) = qv;
-        const uint32_t w4[4] = {kv.x, kv.y, kv.z, kv.w};
+    // every global load of the chunk is issued before the first LDS write;
+    // thread t stages tokens 2p, 2p+1 (p = t % 32) for 8 features per pass
+    constexpr int NKQ = DK / 64;  // passes over the key features (8 groups of 8 per pass)
+    constexpr int NV = DV / 64;
+    const int p2 = tid % 32, fg = tid / 32;
+    const int i0 = 2 * p2, i1 = 2 * p2 + 1;
+    uint4 kv[NKQ][2], qv[NKQ][2], vv[NV][2];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            sKT[(c8 + 2 * u) * LDC + i] = uint16_t(w4[u] & 0xffffu);
-            sKT[(c8 + 2 * u + 1) * LDC + i] = uint16_t(w4[u] >> 16);
+    for (int m = 0; m < NKQ; ++m) {
+        const int f0 = 64 * m + 8 * fg;
+        kv[m][0] = kv[m][1] = qv[m][0] = qv[m][1] = make_uint4(0, 0, 0, 0);
+        if (i0 < valid) {
+            kv[m][0] = *reinterpret_cast<const uint4*>(kp + (tok0 + i0) * DK + f0);
+            qv[m][0] = *reinterpret_cast<const uint4*>(qp + (tok0 + i0) * DK + f0);
+        }
+        if (i1 < valid) {
+            kv[m][1] = *reinterpret_cast<const uint4*>(kp + (tok0 + i1) * DK + f0);
+            qv[m][1] = *reinterpret_cast<const uint4*>(qp + (tok0 + i1) * DK + f0);
         }
     }
-    for (int e = tid; e < kC * DV / 8; e += kThreads) {
-        const int i = e / (DV / 8), c8 = (e % (DV / 8)) * 8;
-        uint4 vv = make_uint4(0, 0, 0, 0);
-        if (i < valid) vv = *reinterpret_cast<const uint4*>(vp + (tok0 + i) * DV + c8);
-        const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            sVT[(c8 + 2 * u) * LDC + i] = uint16_t(w4[u] & 0xffffu);
-            sVT[(c8 + 2 * u + 1) * LDC + i] = uint16_t(w4[u] >> 16);
-        }
+    for (int m = 0; m < NV; ++m) {
+        const int f0 = 64 * m + 8 * fg;
+        vv[m][0] = i0 < valid ? *reinterpret_cast<const uint4*>(vp + (tok0 + i0) * DV + f0) : make_uint4(0, 0, 0, 0);
+        vv[m][1] = i1 < valid ? *reinterpret_cast<const uint4*>(vp + (tok0 + i1) * DV + f0) : make_uint4(0, 0, 0, 0);
     }
-    if (tid < kWave) {
-        chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
-        sBeta[tid] = tid < valid ? a.beta[tok0 + tid] : 0.0f;
-    }
-
     // chunk states as bf16 A-fragments: fragment (t, s) of lane l at [(t * KS + s) * 64 + l] * 8
     const uint16_t* Hf = static_cast<const uint16_t*>(a.Hs) + (bh * s.n_chunks + n) * int64_t(DK) * DK;
     const uint16_t* Gf = static_cast<const uint16_t*>(a.Gs) + (bh * s.n_chunks + n) * int64_t(DV) * DK;
@@ -147,8 +155,6 @@ void chunk_cg_bf16_kernel(CgArgs a)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
             hc[mt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(Hf + ((mt * KS + ks) * 64 + lane) * 8));
-    const float* lam = a.lambda + int64_t(h) * DK;
-    if (tid < DK) sLam[tid] = lam[tid];
     // diag(H_c) for the rows r = 16mt + 4g + ii this lane holds
     f32x4 hdiag[MT];
 #pragma unroll
@@ -160,17 +166,36 @@ void chunk_cg_bf16_kernel(CgArgs a)
             const int idx = (((r / 16) * KS + r / 32) * 64 + gl * 16 + r % 16) * 8 + e;
             hdiag[mt][ii] = bf16_bits_to_f32(Hf[idx]);
         }
+    const float* lam = a.lambda + int64_t(h) * DK;
+    if (tid < DK) sLam[tid] = lam[tid];
+#pragma unroll
+    for (int m = 0; m < NKQ; ++m) {
+        const int f0 = 64 * m + 8 * fg;
+        *reinterpret_cast<uint4*>(sK + i0 * LDK + f0) = kv[m][0];
+        *reinterpret_cast<uint4*>(sK + i1 * LDK + f0) = kv[m][1];
+        *reinterpret_cast<uint4*>(sQ + i0 * LDK + f0) = qv[m][0];
+        *reinterpret_cast<uint4*>(sQ + i1 * LDK + f0) = qv[m][1];
+        stage_token_pair(reinterpret_cast<uint32_t*>(sKT), LDC / 2, f0, p2, kv[m][0], kv[m][1]);
+    }
+#pragma unroll
+    for (int m = 0; m < NV; ++m)
+        stage_token_pair(reinterpret_cast<uint32_t*>(sVT), LDC / 2, 64 * m + 8 * fg, p2, vv[m][0], vv[m][1]);
+    if (tid < kWave) {
+        chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
+        sBeta[tid] = tid < valid ? a.beta[tok0 + tid] : 0.0f;
+    }
+
     __syncthreads();
 
     // ---- decays of this sub-chunk
     const int jb = 16 * wave - 1;  // token whose state enters the sub-chunk (-1: the chunk's H_c)
-    const float zt = wave == 0 ? decay_from_start(sLg, sZl, j) : decay_between(sLg, sZl, jb, j);
-    const float Dw = wave == 0 ? 1.0f : decay_from_start(sLg, sZl, jb);
+    const float zt = wave == 0 ? decay_from_start_hw(sLg, sZl, j) : decay_between_hw(sLg, sZl, jb, j);
+    const float Dw = wave == 0 ? 1.0f : decay_from_start_hw(sLg, sZl, jb);
     f32x4 zw;  // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
         const int i = 16 * wave + 4 * g + ii;
-        zw[ii] = sBeta[i] * decay_between(sLg, sZl, i, j);
+        zw[ii] = sBeta[i] * decay_between_hw(sLg, sZl, i, j);
     }
     // rank-update weights u_i = beta_i zeta_{16w-1,i} for i < 16w, on this lane's k-indices
     bf16x8 uwb[2];
@@ -180,7 +205,7 @@ void chunk_cg_bf16_kernel(CgArgs a)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
-            uw[u][e] = i < 16 * wave ? sBeta[i] * decay_between(sLg, sZl, i, jb) : 0.0f;
+            uw[u][e] = i < 16 * wave ? sBeta[i] * decay_between_hw(sLg, sZl, i, jb) : 0.0f;
             uwb[u][e] = (__bf16)uw[u][e];
         }
     const int nu = (16 * wave + 31) / 32;  // 32-token steps holding tokens < 16w
@@ -330,14 +355,14 @@ void chunk_cg_bf16_kernel(CgArgs a)
         for (int mt = 0; mt < MT; ++mt)
             *reinterpret_cast<f32x4*>(a.qstar + (tok0 + j) * DK + 16 * mt + 4 * g) = x[mt];
     }
-    const float zeta = decay_from_start(sLg, sZl, j);
+    const float zeta = decay_from_start_hw(sLg, sZl, j);
     f32x4 zo[4];  // beta_i Z[i][j] over the causal tiles it <= wave
 #pragma unroll
     for (int it = 0; it < 4; ++it)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
             const int i = 16 * it + 4 * g + ii;
-            zo[it][ii] = (it <= wave) ? sBeta[i] * decay_between(sLg, sZl, i, j) : 0.0f;
+            zo[it][ii] = (it <= wave) ? sBeta[i] * decay_between_hw(sLg, sZl, i, j) : 0.0f;
         }
     bf16x8 xb[KS], xz[KS];
 #pragma unroll

@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
     }
 }
 
-// Matrix-core variant for bf16 k and v (chunk 32 or 64).  The stacked state
+// Matrix-core variant for bf16 k and v (chunk 64).  The stacked state
 // [H; G] ((d_k + d_v) x d_k) is cut into 64-row x 32-column tiles, one per
 // workgroup; wave w keeps rows 16w..16w+15 of the tile as two 16x16 MFMA
 // result tiles and updates them in place, chunk after chunk:
@@ -113,9 +113,9 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
 // the state stays fp32-accurate to ~1e-6.  The next chunk's inputs are
 // prefetched into registers while the current one is multiplied, and each wave
 // runs the gate scan itself, so a chunk costs two barriers.
-template <int C>
 __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
 {
+    constexpr int C = 64;
     constexpr int KST = C / 32;   // 32-token contraction steps per chunk
     constexpr int LDT = C + 8;    // row stride (elements) of the token-minor LDS tiles
     const ForwardShape s = a.s;
@@ -140,8 +140,8 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t sBl[32 * LDT];  // remainder
 
     // register prefetch of one chunk: X rows, K columns, gates
-    uint4 ra[KST];
-    uint4 rb = make_uint4(0, 0, 0, 0);
+    uint4 ra[2];  // A rows of tokens 2p, 2p+1
+    uint4 rb[2];  // B columns of tokens 2p, 2p+1
     float rgam = 1.0f, rbet = 0.0f;
     int rvalid = 0;
     auto load_chunk = [&](int n) {
@@ -149,16 +149,22 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
         const int valid = int(min<int64_t>(C, s.seq_len - t0));
         const int64_t tok0 = bh * s.seq_len + t0;
         rvalid = valid;
+        // thread t: tokens 2p, 2p+1 with p = t % 32; A rows f8 = 8 (t / 32), B columns f8 = 8 (t / 32 % 4)
+        {
+            const int p = tid % 32, f8 = 8 * (tid / 32);
 #pragma unroll
-        for (int m = 0; m < KST; ++m) {
-            const int e = tid + kThreads * m, i = e / 8, f8 = (e % 8) * 8;
-            ra[m] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + xr0 + f8)
-                              : make_uint4(0, 0, 0, 0);
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const int i = 2 * p + h2;
+                ra[h2] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + xr0 + f8) : make_uint4(0, 0, 0, 0);
+            }
         }
-        if (tid < C * 4) {
-            const int i = tid / 4, f8 = (tid % 4) * 8;
-            rb = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + col0 + f8)
-                           : make_uint4(0, 0, 0, 0);
+        {
+            const int p = tid % 32, f8 = 8 * ((tid / 32) % 4);
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const int i = 2 * p + h2;
+                rb[h2] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + col0 + f8) : make_uint4(0, 0, 0, 0);
+            }
         }
         rgam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
         rbet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
@@ -186,29 +192,25 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
         const float D = zlE >= 0 ? 0.0f : expf(lgE);
 
         __syncthreads();  // the previous chunk's products are done with LDS
-#pragma unroll
-        for (int m = 0; m < KST; ++m) {
-            const int e = tid + kThreads * m, i = e / 8, f8 = (e % 8) * 8;
-            const uint32_t w4[4] = {ra[m].x, ra[m].y, ra[m].z, ra[m].w};
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                sA[(f8 + 2 * q) * LDT + i] = uint16_t(w4[q] & 0xffffu);
-                sA[(f8 + 2 * q + 1) * LDT + i] = uint16_t(w4[q] >> 16);
-            }
-        }
+        stage_token_pair(reinterpret_cast<uint32_t*>(sA), LDT / 2, 8 * (tid / 32), tid % 32, ra[0], ra[1]);
         {
-            const int i = (tid / 4) % C, f8 = (tid % 4) * 8;
-            const float wi = __shfl(wl, i, kWave);
-            if (tid < C * 4) {
-                const uint32_t w4[4] = {rb.x, rb.y, rb.z, rb.w};
+            // B = hi/lo split of w_i x_i[c] for tokens 2p, 2p+1 (threads t < 128)
+            const int p = tid % 32, f8 = 8 * ((tid / 32) % 4);
+            const float w0 = __shfl(wl, 2 * p, kWave), w1 = __shfl(wl, 2 * p + 1, kWave);
+            if (tid < 128) {
+                const uint32_t a4[4] = {rb[0].x, rb[0].y, rb[0].z, rb[0].w};
+                const uint32_t b4[4] = {rb[1].x, rb[1].y, rb[1].z, rb[1].w};
+                uint32_t* hi32 = reinterpret_cast<uint32_t*>(sBh);
+                uint32_t* lo32 = reinterpret_cast<uint32_t*>(sBl);
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
-                    const uint32_t bits = (q & 1) ? (w4[q / 2] >> 16) : (w4[q / 2] & 0xffffu);
-                    const float v = wi * bf16_bits_to_f32(bits);
-                    const __bf16 hi = (__bf16)v;
-                    const __bf16 lo = (__bf16)(v - (float)hi);
-                    sBh[(f8 + q) * LDT + i] = bf16_bits(hi);
-                    sBl[(f8 + q) * LDT + i] = bf16_bits(lo);
+                    const uint32_t ba = (q & 1) ? (a4[q / 2] >> 16) : (a4[q / 2] & 0xffffu);
+                    const uint32_t bb = (q & 1) ? (b4[q / 2] >> 16) : (b4[q / 2] & 0xffffu);
+                    const float va = w0 * bf16_bits_to_f32(ba), vb = w1 * bf16_bits_to_f32(bb);
+                    const __bf16 ha = (__bf16)va, hb = (__bf16)vb;
+                    const __bf16 la = (__bf16)(va - (float)ha), lb = (__bf16)(vb - (float)hb);
+                    hi32[(f8 + q) * (LDT / 2) + p] = uint32_t(bf16_bits(ha)) | (uint32_t(bf16_bits(hb)) << 16);
+                    lo32[(f8 + q) * (LDT / 2) + p] = uint32_t(bf16_bits(la)) | (uint32_t(bf16_bits(lb)) << 16);
                 }
             }
         }
@@ -278,8 +280,8 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t sBh[32 * LDT];  // hi(w_i x_i[c]), as [c][i]
     __shared__ __attribute__((aligned(16))) uint16_t sBl[32 * LDT];
 
-    uint4 ra[KST];
-    uint4 rb = make_uint4(0, 0, 0, 0);
+    uint4 ra[2];  // A rows of tokens 2p, 2p+1
+    uint4 rb[2];  // B columns of tokens 2p, 2p+1
     float rgam = 1.0f, rbet = 0.0f;
     int rvalid = 0;
     auto load_chunk = [&](int n) {
@@ -287,16 +289,22 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
         const int valid = int(min<int64_t>(C, s.seq_len - t0));
         const int64_t tok0 = bh * s.seq_len + t0;
         rvalid = valid;
+        // thread t: tokens 2p, 2p+1 with p = t % 32; A rows f8 = 8 (t / 32), B columns f8 = 8 (t / 32 % 4)
+        {
+            const int p = tid % 32, f8 = 8 * (tid / 32);
 #pragma unroll
-        for (int m = 0; m < KST; ++m) {
-            const int e = tid + kThreads * m, i = e / 8, f8 = (e % 8) * 8;
-            ra[m] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + row0 + f8)
-                              : make_uint4(0, 0, 0, 0);
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const int i = 2 * p + h2;
+                ra[h2] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + row0 + f8) : make_uint4(0, 0, 0, 0);
+            }
         }
         {
-            const int i = tid / 4, f8 = (tid % 4) * 8;
-            rb = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + colX + f8)
-                           : make_uint4(0, 0, 0, 0);
+            const int p = tid % 32, f8 = 8 * ((tid / 32) % 4);
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const int i = 2 * p + h2;
+                rb[h2] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + colX + f8) : make_uint4(0, 0, 0, 0);
+            }
         }
         rgam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
         rbet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
@@ -328,28 +336,26 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
         const float D = zlE >= 0 ? 0.0f : expf(lgE);
 
         __syncthreads();
-#pragma unroll
-        for (int m = 0; m < KST; ++m) {
-            const int e = tid + kThreads * m, i = e / 8, f8 = (e % 8) * 8;
-            const uint32_t w4[4] = {ra[m].x, ra[m].y, ra[m].z, ra[m].w};
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                sA[(f8 + 2 * q) * LDT + i] = uint16_t(w4[q] & 0xffffu);
-                sA[(f8 + 2 * q + 1) * LDT + i] = uint16_t(w4[q] >> 16);
-            }
-        }
+        stage_token_pair(reinterpret_cast<uint32_t*>(sA), LDT / 2, 8 * (tid / 32), tid % 32, ra[0], ra[1]);
         {
-            const int i = tid / 4, f8 = (tid % 4) * 8;
-            const float wi = __shfl(wl, i, kWave);
-            const uint32_t w4[4] = {rb.x, rb.y, rb.z, rb.w};
+            // B = hi/lo split of w_i x_i[c] for tokens 2p, 2p+1 (threads t < 128)
+            const int p = tid % 32, f8 = 8 * ((tid / 32) % 4);
+            const float w0 = __shfl(wl, 2 * p, kWave), w1 = __shfl(wl, 2 * p + 1, kWave);
+            if (tid < 128) {
+                const uint32_t a4[4] = {rb[0].x, rb[0].y, rb[0].z, rb[0].w};
+                const uint32_t b4[4] = {rb[1].x, rb[1].y, rb[1].z, rb[1].w};
+                uint32_t* hi32 = reinterpret_cast<uint32_t*>(sBh);
+                uint32_t* lo32 = reinterpret_cast<uint32_t*>(sBl);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const uint32_t bits = (q & 1) ? (w4[q / 2] >> 16) : (w4[q / 2] & 0xffffu);
-                const float v = wi * bf16_bits_to_f32(bits);
-                const __bf16 hi = (__bf16)v;
-                const __bf16 lo = (__bf16)(v - (float)hi);
-                sBh[(f8 + q) * LDT + i] = bf16_bits(hi);
-                sBl[(f8 + q) * LDT + i] = bf16_bits(lo);
+                for (int q = 0; q < 8; ++q) {
+                    const uint32_t ba = (q & 1) ? (a4[q / 2] >> 16) : (a4[q / 2] & 0xffffu);
+                    const uint32_t bb = (q & 1) ? (b4[q / 2] >> 16) : (b4[q / 2] & 0xffffu);
+                    const float va = w0 * bf16_bits_to_f32(ba), vb = w1 * bf16_bits_to_f32(bb);
+                    const __bf16 ha = (__bf16)va, hb = (__bf16)vb;
+                    const __bf16 la = (__bf16)(va - (float)ha), lb = (__bf16)(vb - (float)hb);
+                    hi32[(f8 + q) * (LDT / 2) + p] = uint32_t(bf16_bits(ha)) | (uint32_t(bf16_bits(hb)) << 16);
+                    lo32[(f8 + q) * (LDT / 2) + p] = uint32_t(bf16_bits(la)) | (uint32_t(bf16_bits(lb)) << 16);
+                }
             }
         }
         __syncthreads();
@@ -428,12 +434,9 @@ hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream)
         hipLaunchKernelGGL(chunk_state_frag_kernel, dim3(blocks), dim3(kThreads), 0, stream, a);
         return hipGetLastError();
     }
-    if (a.s.bf16 && (a.s.chunk == 32 || a.s.chunk == 64)) {
+    if (a.s.bf16 && a.s.chunk == 64) {
         const unsigned blocks = unsigned(bh * ((a.s.d_k + a.s.d_v) / 64) * (a.s.d_k / 32));
-        if (a.s.chunk == 64)
-            hipLaunchKernelGGL(chunk_state_mfma_kernel<64>, dim3(blocks), dim3(kThreads), 0, stream, a);
-        else
-            hipLaunchKernelGGL(chunk_state_mfma_kernel<32>, dim3(blocks), dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL(chunk_state_mfma_kernel, dim3(blocks), dim3(kThreads), 0, stream, a);
         return hipGetLastError();
     }
     const int64_t blocks = bh * ((a.s.d_k + a.s.d_v) / kTileRows);

@@ -57,4 +57,21 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) { return __ui
 
 __device__ __forceinline__ uint16_t bf16_bits(__bf16 x) { return __builtin_bit_cast(uint16_t, x); }
 
+// Transposed staging of two consecutive tokens (2p, 2p+1), 8 features each
+// (bf16 bits in a and b), into a feature-major LDS tile of 32-bit words:
+// word [(f0 + q) * ld32 + p] = (token 2p, token 2p+1) of feature f0 + q.
+// Lanes with consecutive p write consecutive words, so a wave's stores do not
+// collide in LDS banks.
+__device__ __forceinline__ void stage_token_pair(uint32_t* dst32, int ld32, int f0, int p, const uint4& a,
+                                                 const uint4& b)
+{
+    const uint32_t wa[4] = {a.x, a.y, a.z, a.w};
+    const uint32_t wb[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        dst32[(f0 + 2 * q) * ld32 + p] = (wa[q] & 0xffffu) | (wb[q] << 16);
+        dst32[(f0 + 2 * q + 1) * ld32 + p] = (wa[q] >> 16) | (wb[q] & 0xffff0000u);
+    }
+}
+
 }  // namespace mesa
