@@ -24,6 +24,9 @@ HIPCC_FLAGS = [
     "-Wno-unused-function",
     # keep the compiler from forming packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core accumulators in ordinary VGPRs: the CG vectors they produce are
+    # consumed by VALU code, so this avoids AGPR <-> VGPR copies
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I" + INCLUDE,
     "-I" + CSRC,
 ]

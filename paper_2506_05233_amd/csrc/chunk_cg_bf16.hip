@@ -115,6 +115,8 @@ void chunk_cg_bf16_kernel(CgArgs a)
     __shared__ float sLg[kWave], sBeta[kWave];
     __shared__ int sZl[kWave];
     __shared__ __attribute__((aligned(16))) float sLam[DK];
+    __shared__ float sT[kC * (kC + 1)];  // beta_i Z[i][j] as [i][j] (row stride 65), 0 for i > j
+    __shared__ float sZ0[kC];            // zeta_{c+j,c}: decay from the chunk's entering state
 
     // ---- stage the chunk's keys, values and queries (bf16 bits) in LDS
     const uint16_t* kp = static_cast<const uint16_t*>(a.k);
@@ -155,17 +157,14 @@ void chunk_cg_bf16_kernel(CgArgs a)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
             hc[mt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(Hf + ((mt * KS + ks) * 64 + lane) * 8));
-    // diag(H_c) for the rows r = 16mt + 4g + ii this lane holds
+    // diag(H_c) for the rows r = 16mt + 4g + ii this lane holds: fragment (mt, mt/2),
+    // lane 16g + 4g + ii, element 4 (mt % 2) + ii
     f32x4 hdiag[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-            const int r = 16 * mt + 4 * g + ii;
-            const int rs = r % 32, gl = (rs % 16) / 4, e = 4 * (rs / 16) + rs % 4;
-            const int idx = (((r / 16) * KS + r / 32) * 64 + gl * 16 + r % 16) * 8 + e;
-            hdiag[mt][ii] = bf16_bits_to_f32(Hf[idx]);
-        }
+        for (int ii = 0; ii < 4; ++ii)
+            hdiag[mt][ii] = bf16_bits_to_f32(Hf[((mt * KS + mt / 2) * 64 + 20 * g + ii) * 8 + 4 * (mt % 2) + ii]);
     const float* lam = a.lambda + int64_t(h) * DK;
     if (tid < DK) sLam[tid] = lam[tid];
 #pragma unroll
@@ -186,16 +185,22 @@ void chunk_cg_bf16_kernel(CgArgs a)
     }
 
     __syncthreads();
+    for (int e = tid; e < kC * kC; e += kThreads) {
+        const int i = e / kC, jj = e % kC;
+        sT[i * (kC + 1) + jj] = sBeta[i] * decay_between_hw(sLg, sZl, i, jj);
+    }
+    if (tid < kC) sZ0[tid] = decay_from_start_hw(sLg, sZl, tid);
+    __syncthreads();
 
     // ---- decays of this sub-chunk
     const int jb = 16 * wave - 1;  // token whose state enters the sub-chunk (-1: the chunk's H_c)
-    const float zt = wave == 0 ? decay_from_start_hw(sLg, sZl, j) : decay_between_hw(sLg, sZl, jb, j);
-    const float Dw = wave == 0 ? 1.0f : decay_from_start_hw(sLg, sZl, jb);
+    const float zt = wave == 0 ? sZ0[j] : decay_between_hw(sLg, sZl, jb, j);
+    const float Dw = wave == 0 ? 1.0f : sZ0[jb];
     f32x4 zw;  // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
         const int i = 16 * wave + 4 * g + ii;
-        zw[ii] = sBeta[i] * decay_between_hw(sLg, sZl, i, j);
+        zw[ii] = sT[i * (kC + 1) + j];
     }
     // rank-update weights u_i = beta_i zeta_{16w-1,i} for i < 16w, on this lane's k-indices
     bf16x8 uwb[2];
@@ -205,7 +210,7 @@ void chunk_cg_bf16_kernel(CgArgs a)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
-            uw[u][e] = i < 16 * wave ? sBeta[i] * decay_between_hw(sLg, sZl, i, jb) : 0.0f;
+            uw[u][e] = i < 16 * wave ? sT[i * (kC + 1) + jb] : 0.0f;
             uwb[u][e] = (__bf16)uw[u][e];
         }
     const int nu = (16 * wave + 31) / 32;  // 32-token steps holding tokens < 16w
@@ -283,8 +288,11 @@ void chunk_cg_bf16_kernel(CgArgs a)
         const bf16x8 sb = pack8(sacc * zw, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(kf3[mt], sb, w[mt]);
+        {
+            int lofs = 4 * g;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) w[mt] += *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g) * vec[mt];
+            for (int mt = 0; mt < MT; ++mt) w[mt] += *reinterpret_cast<const f32x4*>(sLam + 16 * mt + lofs) * vec[mt];
+        }
     };
 
     // ---- Jacobi start x0 = q / diag(H_t + Lambda),
@@ -355,14 +363,14 @@ void chunk_cg_bf16_kernel(CgArgs a)
         for (int mt = 0; mt < MT; ++mt)
             *reinterpret_cast<f32x4*>(a.qstar + (tok0 + j) * DK + 16 * mt + 4 * g) = x[mt];
     }
-    const float zeta = decay_from_start_hw(sLg, sZl, j);
+    const float zeta = sZ0[j];
     f32x4 zo[4];  // beta_i Z[i][j] over the causal tiles it <= wave
 #pragma unroll
     for (int it = 0; it < 4; ++it)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
             const int i = 16 * it + 4 * g + ii;
-            zo[it][ii] = (it <= wave) ? sBeta[i] * decay_between_hw(sLg, sZl, i, j) : 0.0f;
+            zo[it][ii] = (it <= wave) ? sT[i * (kC + 1) + j] : 0.0f;
         }
     bf16x8 xb[KS], xz[KS];
 #pragma unroll
