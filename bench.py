@@ -75,7 +75,7 @@ def source_hash():
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2506_05233_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        if name.startswith("chunk_cg") or name == "mesa_device.hpp":
+        if name.startswith("chunk_cg") or name in ("mesa_device.hpp", "mesa_mfma.hpp"):
             h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()
 
@@ -184,7 +184,7 @@ def cpu_baseline(args, x, w):
     import oracle
     n_seq = args.cpu_sequences
     threads = min(n_seq, oracle.default_threads(), 16)
-    pairs = [(i % w.batch, (i * 5) % w.heads) for i in range(n_seq)]
+    pairs = [(i // w.heads % w.batch, i % w.heads) for i in range(n_seq)]
     sl = {n: np.stack([x[n][b, h] for b, h in pairs])[:, None] for n in ("q", "k", "v", "gamma", "beta")}
     # one head row of lambda per sequence: run the oracle once per distinct head set
     lam_rows = np.stack([x["lam"][h] for _, h in pairs])
@@ -202,8 +202,9 @@ def cpu_baseline(args, x, w):
     token_heads = n_seq * w.seq_len
     return {
         "value": token_heads / w.heads / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-        "sample": "%d of the %d (batch, head) sequences of %s, all %d tokens each, fp64 sequential "
-                  "recurrence with %d-step CG; tokens/s = token-heads/s / %d heads; %.1f s wall"
+        "sample": "%d of the %d (batch, head) sequences of %s (all of them when equal), %d tokens "
+                  "each, fp64 sequential recurrence with %d-step CG, one sequence per thread; "
+                  "tokens/s = token-heads/s / %d heads; %.1f s wall"
                   % (n_seq, w.batch * w.heads, w.name, w.seq_len, w.n_cg, w.heads, el),
     }
 
@@ -215,7 +216,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--precision", type=int, default=0, help="MESA_PREC_* (0 = auto)")
     ap.add_argument("--decode-steps", type=int, default=1024)
-    ap.add_argument("--cpu-sequences", type=int, default=16)
+    ap.add_argument("--cpu-sequences", type=int, default=128)
     ap.add_argument("--skip-decode", action="store_true")
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,

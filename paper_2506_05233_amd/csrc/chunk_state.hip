@@ -29,8 +29,9 @@ __global__ __launch_bounds__(kThreads) void chunk_state_kernel(StateArgs a)
     const int dk = s.d_k, dv = s.d_v, C = s.chunk;
     const int ntile_h = dk / kTileRows;
     const int ntile = ntile_h + dv / kTileRows;
-    const int tile = blockIdx.x % ntile;
-    const int64_t bh = blockIdx.x / ntile;
+    const int blk = xcd_major_block(blockIdx.x, gridDim.x);
+    const int tile = blk % ntile;
+    const int64_t bh = blk / ntile;
     const bool isG = tile >= ntile_h;  // tiles [0, d_k/16): rows of H; then rows of G
     const int r0 = (isG ? tile - ntile_h : tile) * kTileRows;
     const int nrow = isG ? dv : dk;    // rows of the whole state
@@ -121,9 +122,10 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
     const ForwardShape s = a.s;
     const int dk = s.d_k, dv = s.d_v;
     const int nrt = (dk + dv) / 64, nct = dk / 32;
-    const int ct = blockIdx.x % nct;
-    const int rt = (blockIdx.x / nct) % nrt;
-    const int64_t bh = blockIdx.x / (nct * nrt);
+    const int blk = xcd_major_block(blockIdx.x, gridDim.x);
+    const int ct = blk % nct;
+    const int rt = (blk / nct) % nrt;
+    const int64_t bh = blk / (nct * nrt);
     const bool isG = rt * 64 >= dk;
     const int xr0 = isG ? rt * 64 - dk : rt * 64;  // first row of the tile within H or G
     const int nX = isG ? dv : dk;                  // rows of that state = width of its source
@@ -262,9 +264,10 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
     const ForwardShape s = a.s;
     const int dk = s.d_k, dv = s.d_v;
     const int nrt = dk / 64, nct = (dk + dv) / 32;
-    const int ct = blockIdx.x % nct;
-    const int rt = (blockIdx.x / nct) % nrt;
-    const int64_t bh = blockIdx.x / (nct * nrt);
+    const int blk = xcd_major_block(blockIdx.x, gridDim.x);
+    const int ct = blk % nct;
+    const int rt = (blk / nct) % nrt;
+    const int64_t bh = blk / (nct * nrt);
     const int row0 = rt * 64;                 // key-feature rows of the tile
     const bool isG = ct * 32 >= dk;           // columns of G^T (value features)
     const int colX = isG ? ct * 32 - dk : ct * 32;

@@ -66,4 +66,16 @@ __device__ __forceinline__ float decay_from_start(const float* lg, const int* zl
     return zl[j] >= 0 ? 0.0f : expf(lg[j]);
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin (block b runs on XCD b % 8),
+// and each XCD has its own L2.  This maps the hardware block index to a logical
+// one so that logically consecutive workgroups share an XCD: workgroups that
+// read the same inputs then hit one L2 instead of fetching them eight times.
+constexpr int kNumXcd = 8;
+__device__ __forceinline__ int xcd_major_block(int b, int n)
+{
+    const int per = n / kNumXcd, rem = n % kNumXcd;
+    const int x = b % kNumXcd, local = b / kNumXcd;
+    return x * per + min(x, rem) + local;
+}
+
 }  // namespace mesa
