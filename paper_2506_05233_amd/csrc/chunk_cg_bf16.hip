@@ -194,15 +194,21 @@ void chunk_cg_bf16_kernel(CgArgs a)
 
     // ---- decays of this sub-chunk
     const int jb = 16 * wave - 1;  // token whose state enters the sub-chunk (-1: the chunk's H_c)
-    const float zt = wave == 0 ? sZ0[j] : decay_between_hw(sLg, sZl, jb, j);
     const float Dw = wave == 0 ? 1.0f : sZ0[jb];
+    // B_w = Dw H_c + sum_{i<16w} u_i k_i k_i^T with u_i = beta_i zeta_{16w-1,i}.  It is kept as
+    // B'_w = B_w / Dw = H_c + sum (u_i / Dw) k_i k_i^T and the 1/Dw goes into the column scale:
+    // zs_j = zt_j Dw = zeta_{c+j,c}.  When Dw is negligible (<= 1e-20, e.g. a zero gate) the
+    // state term Dw H_c is dropped instead: B_w = sum u_i k_i k_i^T and zs_j = zt_j.
+    const bool keepH = wave == 0 || Dw > 1e-20f;
+    const float zs = keepH ? sZ0[j] : decay_between_hw(sLg, sZl, jb, j);
+    const float ush = keepH && wave > 0 ? 1.0f / Dw : 1.0f;
     f32x4 zw;  // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
         const int i = 16 * wave + 4 * g + ii;
         zw[ii] = sT[i * (kC + 1) + j];
     }
-    // rank-update weights u_i = beta_i zeta_{16w-1,i} for i < 16w, on this lane's k-indices
+    // rank-update weights (scaled) on this lane's k-indices
     bf16x8 uwb[2];
     float uw[2][8];
 #pragma unroll
@@ -210,12 +216,31 @@ void chunk_cg_bf16_kernel(CgArgs a)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
-            uw[u][e] = i < 16 * wave ? sT[i * (kC + 1) + jb] : 0.0f;
+            uw[u][e] = i < 16 * wave ? sT[i * (kC + 1) + jb] * ush : 0.0f;
             uwb[u][e] = (__bf16)uw[u][e];
         }
     const int nu = (16 * wave + 31) / 32;  // 32-token steps holding tokens < 16w
 
-    // ---- B_w as bf16 A-fragments: hf[mt][s] covers rows 16mt.., columns 32s..
+    // ---- B'_w as bf16 A-fragments: hf[mt][s] covers rows 16mt.., columns 32s..
+    // The A operand of the rank update for rows 32s + 16h.. does not depend on mt: load once.
+    bf16x8 ka[KS][2][2];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                if (u < nu) ka[ks][hh][u] = lds_frag(sKT + (32 * ks + 16 * hh + ln) * LDC + 32 * u + 4 * g);
+    // Identity operands that copy an A-fragment of H_c, read as a B operand, into the two
+    // 16x16 result tiles (rows 32s + {0..15} and 32s + {16..31}) it belongs to.
+    bf16x8 id_lo, id_hi;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        id_lo[e] = (__bf16)(4 * g + e == ln ? 1.0f : 0.0f);
+        id_lo[4 + e] = (__bf16)0.0f;
+        id_hi[e] = (__bf16)0.0f;
+        id_hi[4 + e] = (__bf16)(4 * g + e == ln ? 1.0f : 0.0f);
+    }
     bf16x8 hf[MT][KS];
     f32x4 dg1[MT];
 #pragma unroll
@@ -237,17 +262,16 @@ void chunk_cg_bf16_kernel(CgArgs a)
                 hf[mt][ks] = hc[mt][ks];  // B_0 = H_c
                 continue;
             }
-            f32x4 lo, hi;
-#pragma unroll
-            for (int ii = 0; ii < 4; ++ii) {
-                lo[ii] = Dw * (float)hc[mt][ks][ii];
-                hi[ii] = Dw * (float)hc[mt][ks][4 + ii];
+            f32x4 lo = f32x4{0.0f, 0.0f, 0.0f, 0.0f}, hi = lo;
+            if (keepH) {
+                lo = mfma16(id_lo, hc[mt][ks], lo);
+                hi = mfma16(id_hi, hc[mt][ks], hi);
             }
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
                 if (u < nu) {
-                    lo = mfma16(lds_frag(sKT + (32 * ks + ln) * LDC + 32 * u + 4 * g), bw[u], lo);
-                    hi = mfma16(lds_frag(sKT + (32 * ks + 16 + ln) * LDC + 32 * u + 4 * g), bw[u], hi);
+                    lo = mfma16(ka[ks][0][u], bw[u], lo);
+                    hi = mfma16(ka[ks][1][u], bw[u], hi);
                 }
             }
             hf[mt][ks] = pack8(lo, hi);
@@ -274,7 +298,7 @@ void chunk_cg_bf16_kernel(CgArgs a)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             pb[ks] = pack8(vec[2 * ks], vec[2 * ks + 1]);
-            pz[ks] = pack8(zt * vec[2 * ks], zt * vec[2 * ks + 1]);
+            pz[ks] = pack8(zs * vec[2 * ks], zs * vec[2 * ks + 1]);
         }
         f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -296,7 +320,7 @@ void chunk_cg_bf16_kernel(CgArgs a)
     };
 
     // ---- Jacobi start x0 = q / diag(H_t + Lambda),
-    //      diag(H_t) = zt_j diag(B_w) + sum_{16w <= i <= j} beta_i Z[i][j] k_i^2
+    //      diag(H_t) = zs_j diag(B'_w) + sum_{16w <= i <= j} beta_i Z[i][j] k_i^2
     f32x4 x[MT], r[MT], p[MT], w[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -310,7 +334,7 @@ void chunk_cg_bf16_kernel(CgArgs a)
         const uint2 qq = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
         const f32x4 qf{bf16_bits_to_f32(qq.x & 0xffffu), bf16_bits_to_f32(qq.x >> 16),
                        bf16_bits_to_f32(qq.y & 0xffffu), bf16_bits_to_f32(qq.y >> 16)};
-        const f32x4 d = zt * (Dw * hdiag[mt] + dg1[mt]) + dg2 + *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
+        const f32x4 d = zs * ((keepH ? 1.0f : 0.0f) * hdiag[mt] + dg1[mt]) + dg2 + *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
         x[mt] = qf / d;
         p[mt] = qf;  // holds q until the first residual is formed
     }
