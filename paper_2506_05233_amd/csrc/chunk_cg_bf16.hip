@@ -74,15 +74,7 @@ __device__ __forceinline__ float decay_from_start_hw(const float* lg, const int*
 }
 
 // Sum over the four lanes that hold one column (lanes n, n+16, n+32, n+48).
-__device__ __forceinline__ float col_sum(float v)
-{
-    // gfx950 row swaps: odd 16-lane rows of one copy with even rows of the
-    // other, then the upper 32 lanes of one with the lower 32 of the other.
-    const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = __uint_as_float(s16[0]) + __uint_as_float(s16[1]);
-    const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    return __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
-}
+__device__ __forceinline__ float col_sum(float v) { return row_pair_sums(v); }
 
 template <int DK, int DV>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))

@@ -140,24 +140,28 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t sA[64 * LDT];   // X[i][row], as [row][i]
     __shared__ __attribute__((aligned(16))) uint16_t sBh[32 * LDT];  // hi(w_i K[i][c]), as [c][i]
     __shared__ __attribute__((aligned(16))) uint16_t sBl[32 * LDT];  // remainder
+    __shared__ float sW[kWave];  // w_i = beta_i zeta_{chunk end, i} of the chunk being staged
 
     // register prefetch of one chunk: X rows, K columns, gates
-    uint4 ra[2];  // A rows of tokens 2p, 2p+1
-    uint4 rb[2];  // B columns of tokens 2p, 2p+1
-    float rgam = 1.0f, rbet = 0.0f;
-    int rvalid = 0;
-    auto load_chunk = [&](int n) {
+    // inputs of one chunk, held in registers: prefetched two chunks ahead
+    struct ChunkRegs {
+        uint4 ra[2];  // A rows of tokens 2p, 2p+1
+        uint4 rb[2];  // B columns of tokens 2p, 2p+1
+        float gam, bet;
+        int valid;
+    };
+    auto load_chunk = [&](int n, ChunkRegs& R) {
         const int64_t t0 = int64_t(n) * C;
         const int valid = int(min<int64_t>(C, s.seq_len - t0));
         const int64_t tok0 = bh * s.seq_len + t0;
-        rvalid = valid;
+        R.valid = valid;
         // thread t: tokens 2p, 2p+1 with p = t % 32; A rows f8 = 8 (t / 32), B columns f8 = 8 (t / 32 % 4)
         {
             const int p = tid % 32, f8 = 8 * (tid / 32);
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
                 const int i = 2 * p + h2;
-                ra[h2] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + xr0 + f8) : make_uint4(0, 0, 0, 0);
+                R.ra[h2] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + xr0 + f8) : make_uint4(0, 0, 0, 0);
             }
         }
         {
@@ -165,43 +169,34 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
                 const int i = 2 * p + h2;
-                rb[h2] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + col0 + f8) : make_uint4(0, 0, 0, 0);
+                R.rb[h2] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + col0 + f8) : make_uint4(0, 0, 0, 0);
             }
         }
-        rgam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
-        rbet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
+        R.gam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
+        R.bet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
     };
 
     f32x4 acc[2] = {f32x4{0.0f, 0.0f, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}};
     float* chunk_dst = static_cast<float*>(isG ? a.Gs : a.Hs);
-    load_chunk(0);
-    for (int n = 0; n < s.n_chunks; ++n) {
+    auto step = [&](int n, ChunkRegs& R) {
         // gate scan of this chunk, per wave (lane i = in-chunk token i)
-        float lg = (lane < rvalid && rgam > 0.0f) ? logf(rgam) : 0.0f;
-        int zl = (lane < rvalid && !(rgam > 0.0f)) ? lane : -1;
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            const float lo = __shfl_up(lg, off, kWave);
-            const int zo = __shfl_up(zl, off, kWave);
-            if (lane >= off) {
-                lg += lo;
-                zl = max(zl, zo);
-            }
-        }
-        const float lgE = __shfl(lg, C - 1, kWave);
-        const int zlE = __shfl(zl, C - 1, kWave);
-        const float wl = lane < rvalid ? rbet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
+        const float lg = wave_scan_add((lane < R.valid && R.gam > 0.0f) ? logf(R.gam) : 0.0f);
+        const int zl = wave_scan_max((lane < R.valid && !(R.gam > 0.0f)) ? lane : -1);
+        const float lgE = lane_value(lg, C - 1);
+        const int zlE = lane_value(zl, C - 1);
+        const float wl = lane < R.valid ? R.bet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
         const float D = zlE >= 0 ? 0.0f : expf(lgE);
 
+        if (wave == 0) sW[lane] = wl;  // all waves computed the same weights
         __syncthreads();  // the previous chunk's products are done with LDS
-        stage_token_pair(reinterpret_cast<uint32_t*>(sA), LDT / 2, 8 * (tid / 32), tid % 32, ra[0], ra[1]);
+        stage_token_pair(reinterpret_cast<uint32_t*>(sA), LDT / 2, 8 * (tid / 32), tid % 32, R.ra[0], R.ra[1]);
         {
             // B = hi/lo split of w_i x_i[c] for tokens 2p, 2p+1 (threads t < 128)
             const int p = tid % 32, f8 = 8 * ((tid / 32) % 4);
-            const float w0 = __shfl(wl, 2 * p, kWave), w1 = __shfl(wl, 2 * p + 1, kWave);
+            const float w0 = sW[2 * p], w1 = sW[2 * p + 1];
             if (tid < 128) {
-                const uint32_t a4[4] = {rb[0].x, rb[0].y, rb[0].z, rb[0].w};
-                const uint32_t b4[4] = {rb[1].x, rb[1].y, rb[1].z, rb[1].w};
+                const uint32_t a4[4] = {R.rb[0].x, R.rb[0].y, R.rb[0].z, R.rb[0].w};
+                const uint32_t b4[4] = {R.rb[1].x, R.rb[1].y, R.rb[1].z, R.rb[1].w};
                 uint32_t* hi32 = reinterpret_cast<uint32_t*>(sBh);
                 uint32_t* lo32 = reinterpret_cast<uint32_t*>(sBl);
 #pragma unroll
@@ -217,7 +212,7 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
             }
         }
         __syncthreads();
-        if (n + 1 < s.n_chunks) load_chunk(n + 1);
+        if (n + 2 < s.n_chunks) load_chunk(n + 2, R);
 
         if (a.store_chunks) {
             float* dst = chunk_dst + ((bh * s.n_chunks + n) * nX + xr0 + 16 * wave + 4 * g) * int64_t(dk) + col0 + ln;
@@ -237,6 +232,13 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
                 acc[nt] = mfma16(af, lds_frag(sBl + (16 * nt + ln) * LDT + 32 * u + 4 * g), acc[nt]);
             }
         }
+        };
+    ChunkRegs R0, R1;
+    load_chunk(0, R0);
+    if (s.n_chunks > 1) load_chunk(1, R1);
+    for (int n = 0; n < s.n_chunks; n += 2) {
+        step(n, R0);
+        if (n + 1 < s.n_chunks) step(n + 1, R1);
     }
     float* fin = isG ? a.final_G : a.final_H;
     if (fin) {
@@ -282,23 +284,27 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t sA[64 * LDT];   // k_i[row], as [row][i]
     __shared__ __attribute__((aligned(16))) uint16_t sBh[32 * LDT];  // hi(w_i x_i[c]), as [c][i]
     __shared__ __attribute__((aligned(16))) uint16_t sBl[32 * LDT];
+    __shared__ float sW[kWave];  // w_i = beta_i zeta_{chunk end, i} of the chunk being staged
 
-    uint4 ra[2];  // A rows of tokens 2p, 2p+1
-    uint4 rb[2];  // B columns of tokens 2p, 2p+1
-    float rgam = 1.0f, rbet = 0.0f;
-    int rvalid = 0;
-    auto load_chunk = [&](int n) {
+    // inputs of one chunk, held in registers: prefetched two chunks ahead
+    struct ChunkRegs {
+        uint4 ra[2];  // A rows of tokens 2p, 2p+1
+        uint4 rb[2];  // B columns of tokens 2p, 2p+1
+        float gam, bet;
+        int valid;
+    };
+    auto load_chunk = [&](int n, ChunkRegs& R) {
         const int64_t t0 = int64_t(n) * C;
         const int valid = int(min<int64_t>(C, s.seq_len - t0));
         const int64_t tok0 = bh * s.seq_len + t0;
-        rvalid = valid;
+        R.valid = valid;
         // thread t: tokens 2p, 2p+1 with p = t % 32; A rows f8 = 8 (t / 32), B columns f8 = 8 (t / 32 % 4)
         {
             const int p = tid % 32, f8 = 8 * (tid / 32);
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
                 const int i = 2 * p + h2;
-                ra[h2] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + row0 + f8) : make_uint4(0, 0, 0, 0);
+                R.ra[h2] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + row0 + f8) : make_uint4(0, 0, 0, 0);
             }
         }
         {
@@ -306,11 +312,11 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
                 const int i = 2 * p + h2;
-                rb[h2] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + colX + f8) : make_uint4(0, 0, 0, 0);
+                R.rb[h2] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + colX + f8) : make_uint4(0, 0, 0, 0);
             }
         }
-        rgam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
-        rbet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
+        R.gam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
+        R.bet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
     };
 
     // fragment slot of this lane's tile values
@@ -320,33 +326,24 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
     uint16_t* frag_base = static_cast<uint16_t*>(isG ? a.Gs : a.Hs);
 
     f32x4 acc[2] = {f32x4{0.0f, 0.0f, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}};
-    load_chunk(0);
-    for (int n = 0; n < s.n_chunks; ++n) {
-        float lg = (lane < rvalid && rgam > 0.0f) ? logf(rgam) : 0.0f;
-        int zl = (lane < rvalid && !(rgam > 0.0f)) ? lane : -1;
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            const float lo = __shfl_up(lg, off, kWave);
-            const int zo = __shfl_up(zl, off, kWave);
-            if (lane >= off) {
-                lg += lo;
-                zl = max(zl, zo);
-            }
-        }
-        const float lgE = __shfl(lg, C - 1, kWave);
-        const int zlE = __shfl(zl, C - 1, kWave);
-        const float wl = lane < rvalid ? rbet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
+    auto step = [&](int n, ChunkRegs& R) {
+        const float lg = wave_scan_add((lane < R.valid && R.gam > 0.0f) ? logf(R.gam) : 0.0f);
+        const int zl = wave_scan_max((lane < R.valid && !(R.gam > 0.0f)) ? lane : -1);
+        const float lgE = lane_value(lg, C - 1);
+        const int zlE = lane_value(zl, C - 1);
+        const float wl = lane < R.valid ? R.bet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
         const float D = zlE >= 0 ? 0.0f : expf(lgE);
 
+        if (wave == 0) sW[lane] = wl;  // all waves computed the same weights
         __syncthreads();
-        stage_token_pair(reinterpret_cast<uint32_t*>(sA), LDT / 2, 8 * (tid / 32), tid % 32, ra[0], ra[1]);
+        stage_token_pair(reinterpret_cast<uint32_t*>(sA), LDT / 2, 8 * (tid / 32), tid % 32, R.ra[0], R.ra[1]);
         {
             // B = hi/lo split of w_i x_i[c] for tokens 2p, 2p+1 (threads t < 128)
             const int p = tid % 32, f8 = 8 * ((tid / 32) % 4);
-            const float w0 = __shfl(wl, 2 * p, kWave), w1 = __shfl(wl, 2 * p + 1, kWave);
+            const float w0 = sW[2 * p], w1 = sW[2 * p + 1];
             if (tid < 128) {
-                const uint32_t a4[4] = {rb[0].x, rb[0].y, rb[0].z, rb[0].w};
-                const uint32_t b4[4] = {rb[1].x, rb[1].y, rb[1].z, rb[1].w};
+                const uint32_t a4[4] = {R.rb[0].x, R.rb[0].y, R.rb[0].z, R.rb[0].w};
+                const uint32_t b4[4] = {R.rb[1].x, R.rb[1].y, R.rb[1].z, R.rb[1].w};
                 uint32_t* hi32 = reinterpret_cast<uint32_t*>(sBh);
                 uint32_t* lo32 = reinterpret_cast<uint32_t*>(sBl);
 #pragma unroll
@@ -362,7 +359,7 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
             }
         }
         __syncthreads();
-        if (n + 1 < s.n_chunks) load_chunk(n + 1);
+        if (n + 2 < s.n_chunks) load_chunk(n + 2, R);
 
         if (a.store_chunks) {
             uint16_t* base = frag_base + (bh * s.n_chunks + n) * int64_t(MTX) * KS * 512;
@@ -387,6 +384,13 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
                 acc[nt] = mfma16(af, lds_frag(sBl + (16 * nt + ln) * LDT + 32 * u + 4 * g), acc[nt]);
             }
         }
+        };
+    ChunkRegs R0, R1;
+    load_chunk(0, R0);
+    if (s.n_chunks > 1) load_chunk(1, R1);
+    for (int n = 0; n < s.n_chunks; n += 2) {
+        step(n, R0);
+        if (n + 1 < s.n_chunks) step(n + 1, R1);
     }
     // final states, plain fp32: tile value (R, c) is H[R][c] or G[c][R]
     float* fin = isG ? a.final_G : a.final_H;

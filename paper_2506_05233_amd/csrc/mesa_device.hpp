@@ -16,13 +16,76 @@ struct bf16_t {
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16_t x) { return __uint_as_float(uint32_t(x.bits) << 16); }
 
+// Cross-lane data movement without LDS: DPP moves within 16-lane rows, and the
+// gfx950 permlane swaps between rows.  DPP control codes (GFX9 encoding).
+constexpr int kDppQuadSwap1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kDppQuadSwap2 = 0x4E;  // quad_perm [2,3,0,1]
+constexpr int kDppRowShr1 = 0x111;
+constexpr int kDppRowShr2 = 0x112;
+constexpr int kDppRowShr4 = 0x114;
+constexpr int kDppRowShr8 = 0x118;
+constexpr int kDppRowRor4 = 0x124;
+constexpr int kDppRowRor8 = 0x128;
+constexpr int kDppRowBcast15 = 0x142;  // last lane of a row to the whole next row
+constexpr int kDppRowBcast31 = 0x143;  // lane 31 to rows 2 and 3
+
+template <int Ctrl, int RowMask = 0xF>
+__device__ __forceinline__ float dpp_f32(float old, float src)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(src), Ctrl, RowMask, 0xF, false));
+}
+
+template <int Ctrl, int RowMask = 0xF>
+__device__ __forceinline__ int dpp_i32(int old, int src)
+{
+    return __builtin_amdgcn_update_dpp(old, src, Ctrl, RowMask, 0xF, false);
+}
+
+// Sum over the four 16-lane rows: every lane receives the sum of its column position.
+__device__ __forceinline__ float row_pair_sums(float v)
+{
+    const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(s16[0]) + __uint_as_float(s16[1]);
+    const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
+}
+
 // Sum over all 64 lanes of a wave; every lane receives the total.
 __device__ __forceinline__ float wave_sum(float x)
 {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, kWave);
+    x += dpp_f32<kDppQuadSwap1>(x, x);
+    x += dpp_f32<kDppQuadSwap2>(x, x);
+    x += dpp_f32<kDppRowRor4>(x, x);
+    x += dpp_f32<kDppRowRor8>(x, x);
+    return row_pair_sums(x);
+}
+
+// Inclusive prefix sum / prefix max over the 64 lanes of a wave.
+__device__ __forceinline__ float wave_scan_add(float x)
+{
+    x += dpp_f32<kDppRowShr1>(0.0f, x);
+    x += dpp_f32<kDppRowShr2>(0.0f, x);
+    x += dpp_f32<kDppRowShr4>(0.0f, x);
+    x += dpp_f32<kDppRowShr8>(0.0f, x);
+    x += dpp_f32<kDppRowBcast15, 0xA>(0.0f, x);
+    x += dpp_f32<kDppRowBcast31, 0xC>(0.0f, x);
     return x;
 }
+
+__device__ __forceinline__ int wave_scan_max(int x)
+{
+    x = max(x, dpp_i32<kDppRowShr1>(-1, x));
+    x = max(x, dpp_i32<kDppRowShr2>(-1, x));
+    x = max(x, dpp_i32<kDppRowShr4>(-1, x));
+    x = max(x, dpp_i32<kDppRowShr8>(-1, x));
+    x = max(x, dpp_i32<kDppRowBcast15, 0xA>(-1, x));
+    x = max(x, dpp_i32<kDppRowBcast31, 0xC>(-1, x));
+    return x;
+}
+
+// Value of lane `l` (a wave-uniform index) in every lane.
+__device__ __forceinline__ float lane_value(float x, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l)); }
+__device__ __forceinline__ int lane_value(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
 
 // Gate log-cumsums of one chunk (Sec. 3: zeta_{t,s} = prod_{s<i<=t} gamma_i).
 // Called by the 64 lanes of ONE wave, for C <= 64 tokens starting at `gamma`
@@ -38,17 +101,8 @@ __device__ __forceinline__ void chunk_log_decays(const float* gamma, int valid, 
 {
     const int lane = threadIdx.x & (kWave - 1);
     const float g = lane < valid ? gamma[lane] : 1.0f;
-    float s = g > 0.0f ? logf(g) : 0.0f;
-    int z = (lane < valid && !(g > 0.0f)) ? lane : -1;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const float so = __shfl_up(s, off, kWave);
-        const int zo = __shfl_up(z, off, kWave);
-        if (lane >= off) {
-            s += so;
-            z = max(z, zo);
-        }
-    }
+    const float s = wave_scan_add(g > 0.0f ? logf(g) : 0.0f);
+    const int z = wave_scan_max((lane < valid && !(g > 0.0f)) ? lane : -1);
     lg[lane] = s;
     zl[lane] = z;
 }
