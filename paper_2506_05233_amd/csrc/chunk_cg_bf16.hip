@@ -20,10 +20,11 @@
 //
 //   (H_t + Lambda) p_j = B_w (zt_j p_j) + sum_{16w <= i <= j} beta_i Z[i][j] k_i (k_i^T p_j) + Lambda p_j,
 //
-// with zt_j = zeta_{c+j, c+16w-1}: d_k/16 x d_k/32 MFMAs for the state term, a
-// 16-token S = K_w p (d_k/32 MFMAs) and W += K_w^T (beta Z ⊙ S) (d_k/16 MFMAs of
-// 16x16x16).  All four waves do the same work, and every operand of the CG
-// loop stays in registers.
+// with zt_j = zeta_{c+j, c+16w-1}: d_k/16 x d_k/32 MFMAs for the state term
+// (B_w read from the accumulation registers), a 16-token S = K_w p (d_k/32
+// MFMAs), and one MFMA per 16-row tile that adds both K_w^T (beta Z ⊙ S) and
+// Lambda p (half of its 32-long contraction each).  All four waves do the same
+// work, and every operand of the CG loop stays in registers.
 //
 // Every per-token vector (x, r, p, w) lives in registers in the layout of a
 // 16x16 MFMA result: lane (g = lane/16, n = lane%16) holds rows 16t + 4g + {0..3}
@@ -269,29 +270,40 @@ void chunk_cg_bf16_kernel(CgArgs a)
             hf[mt][ks] = pack8(lo, hi);
         }
     }
+    // B'_w is read only as the A operand of the state products.  Those accept the
+    // accumulation registers directly, so keep it there: the loop's fp32 vectors
+    // then have the ordinary vector registers to themselves.
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) asm volatile("" : "=a"(hf[mt][ks]) : "0"(hf[mt][ks]));
     // ---- the sub-chunk's keys as A-fragments: rows of S (kf2), columns of W (kf3)
     bf16x8 kf2[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) kf2[ks] = lds_frag(sK + (16 * wave + ln) * LDK + 32 * ks + 4 * g);
-    // kf3: the 16 sub-chunk tokens in the lower half of a 32-long contraction
-    // (elements 4..7 zero), so W += K_w^T S' stays on v_mfma_f32_16x16x32_bf16.
+    // kf3: one 32-long contraction per row tile adds both remaining terms of the
+    // product: its lower half holds the 16 sub-chunk tokens (K_w^T, met by S'),
+    // its upper half diag(lambda) of the tile's rows (met by the tile's own rows
+    // of the vector), so W += K_w^T S' + Lambda vec is one v_mfma_f32_16x16x32_bf16.
     bf16x8 kf3[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         const uint2 kk = *reinterpret_cast<const uint2*>(sKT + (16 * mt + ln) * LDC + 16 * wave + 4 * g);
         kf3[mt] = __builtin_bit_cast(bf16x8, make_uint4(kk.x, kk.y, 0u, 0u));
+        const float lrow = sLam[16 * mt + ln];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) kf3[mt][4 + e] = (__bf16)(4 * g + e == ln ? lrow : 0.0f);
     }
     const f32x4 zero4 = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     const bf16x8 zwb = pack8(zw, zero4);
 
-    // W = A_j vec for this wave's 16 columns (A_j = H_t + Lambda of token j).
+    // W = A_j vec for this wave's 16 columns (A_j = H_t + Lambda of token j):
+    // W = zs_j (B'_w vec) + K_w^T S' + Lambda vec, the column scale applied to the
+    // state products' accumulators.
     auto matvec = [&](const f32x4 (&vec)[MT], f32x4 (&w)[MT]) {
-        bf16x8 pb[KS], pz[KS];
+        bf16x8 pb[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            pb[ks] = pack8(vec[2 * ks], vec[2 * ks + 1]);
-            pz[ks] = pack8(zs * vec[2 * ks], zs * vec[2 * ks + 1]);
-        }
+        for (int ks = 0; ks < KS; ++ks) pb[ks] = pack8(vec[2 * ks], vec[2 * ks + 1]);
         f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) sacc = mfma16(kf2[ks], pb[ks], sacc);
@@ -299,16 +311,11 @@ void chunk_cg_bf16_kernel(CgArgs a)
         for (int mt = 0; mt < MT; ++mt) {
             w[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) w[mt] = mfma16(hf[mt][ks], pz[ks], w[mt]);
+            for (int ks = 0; ks < KS; ++ks) w[mt] = mfma16(hf[mt][ks], pb[ks], w[mt]);
         }
-        const bf16x8 sb = pack8(sacc * zw, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+        const f32x4 sz = sacc * zw;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(kf3[mt], sb, w[mt]);
-        {
-            int lofs = 4 * g;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) w[mt] += *reinterpret_cast<const f32x4*>(sLam + 16 * mt + lofs) * vec[mt];
-        }
+        for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(kf3[mt], pack8(sz, vec[mt]), zs * w[mt]);
     };
 
     // ---- Jacobi start x0 = q / diag(H_t + Lambda),
@@ -350,16 +357,18 @@ void chunk_cg_bf16_kernel(CgArgs a)
             part += p[mt][0] * w[mt][0] + p[mt][1] * w[mt][1] + p[mt][2] * w[mt][2] + p[mt][3] * w[mt][3];
         const float pw = col_sum(part);
         if (!(pw > 0.0f)) active = false;
-        const float alpha = active ? delta / pw : 0.0f;
-        part = 0.0f;
+        if (active) {
+            const float alpha = delta / pw;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            if (active) {
+            for (int mt = 0; mt < MT; ++mt) {
                 x[mt] += alpha * p[mt];
                 r[mt] -= alpha * w[mt];
             }
-            part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
         }
+        part = 0.0f;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
         const float dn = col_sum(part);
         if (active) {
             if (dn == 0.0f) {
