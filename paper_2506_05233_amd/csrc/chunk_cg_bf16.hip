@@ -60,18 +60,34 @@ __device__ __forceinline__ bf16x8 lds_frag_sq(const uint16_t* base)
     return f;
 }
 
-// Gate decays with the hardware exponential (relative error ~1e-7, far below
-// the bf16 operand rounding of this path); same zero-gate rules as the
-// shared helpers.
+// Gate decay with the hardware exponential (relative error ~1e-7, far below
+// the bf16 operand rounding of this path); same zero-gate rule as the shared
+// helper.
 __device__ __forceinline__ float decay_between_hw(const float* lg, const int* zl, int i, int j)
 {
     if (i > j || zl[j] > i) return 0.0f;
     return __expf(lg[j] - lg[i]);
 }
 
-__device__ __forceinline__ float decay_from_start_hw(const float* lg, const int* zl, int j)
+
+// v if c, else zero (per component, so the operands stay in registers)
+__device__ __forceinline__ uint4 keep_if(bool c, const uint4& v)
 {
-    return zl[j] >= 0 ? 0.0f : __expf(lg[j]);
+    return make_uint4(c ? v.x : 0u, c ? v.y : 0u, c ? v.z : 0u, c ? v.w : 0u);
+}
+
+// Decays below this are treated as zero where a chunk-relative weight would need
+// their reciprocal (see the sub-chunk states below).
+constexpr float kMinDecay = 1e-20f;
+
+// 8 bf16 (bits in v) times u, rounded back to bf16.
+__device__ __forceinline__ uint4 scale_bf16x8(const uint4& v, float u)
+{
+    const bf16x8 x = __builtin_bit_cast(bf16x8, v);
+    bf16x8 y;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = (__bf16)((float)x[e] * u);
+    return __builtin_bit_cast(uint4, y);
 }
 
 // Sum over the four lanes that hold one column (lanes n, n+16, n+32, n+48).
@@ -88,9 +104,10 @@ void chunk_cg_bf16_kernel(CgArgs a)
     constexpr int LDC = kC + 8;    // row stride of feature-major tiles
 
     const ForwardShape s = a.s;
-    const int n = blockIdx.x % s.n_chunks;
-    const int64_t bh = blockIdx.x / s.n_chunks;
-    const int h = int(bh % s.heads);
+    // the grid has fewer than 2^31 blocks (checked at launch): 32-bit index arithmetic
+    const int n = int(blockIdx.x % unsigned(s.n_chunks));
+    const int64_t bh = blockIdx.x / unsigned(s.n_chunks);
+    const int h = int(unsigned(bh) % unsigned(s.heads));
     const int64_t t0 = int64_t(n) * kC;
     const int valid = int(min<int64_t>(kC, s.seq_len - t0));
     const int64_t tok0 = bh * s.seq_len + t0;
@@ -105,61 +122,98 @@ void chunk_cg_bf16_kernel(CgArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t sKT[DK * LDC];  // k_i[b], feature-major
     __shared__ __attribute__((aligned(16))) uint16_t sVT[DV * LDC];  // v_i[e], feature-major
     __shared__ __attribute__((aligned(16))) uint16_t sQ[kC * LDK];   // q_j[b], token-major
+    __shared__ __attribute__((aligned(16))) uint16_t sHf[DK * DK];   // H_c as A-fragments
+    __shared__ __attribute__((aligned(16))) uint16_t sGf[DV * DK];   // G_c as A-fragments
+    __shared__ __attribute__((aligned(16))) uint16_t sKU[DK * LDC];  // u_i k_i[b], feature-major
     __shared__ float sLg[kWave], sBeta[kWave];
     __shared__ int sZl[kWave];
     __shared__ __attribute__((aligned(16))) float sLam[DK];
-    __shared__ float sT[kC * (kC + 1)];  // beta_i Z[i][j] as [i][j] (row stride 65), 0 for i > j
     __shared__ float sZ0[kC];            // zeta_{c+j,c}: decay from the chunk's entering state
+    __shared__ __attribute__((aligned(16))) float sDiag[kThreads / kWave][DK + kWave];  // diag(B'_w) per wave, spare slots
 
     // ---- stage the chunk's keys, values and queries (bf16 bits) in LDS
     const uint16_t* kp = static_cast<const uint16_t*>(a.k);
     const uint16_t* qp = static_cast<const uint16_t*>(a.q);
     const uint16_t* vp = static_cast<const uint16_t*>(a.v);
-    // every global load of the chunk is issued before the first LDS write;
+    // Every global load of the chunk is issued before the first use of any of them,
+    // gates first (the first ones needed; vector memory returns in order).  Loads
+    // never sit behind a branch: tokens past the end of the sequence read the last
+    // valid token (valid >= 1) and are zeroed once the data is in registers.
+    const int lt = min(lane, valid - 1);
+    const float g_raw = a.gamma[tok0 + lt];
+    const float b_raw = a.beta[tok0 + lt];
     // thread t stages tokens 2p, 2p+1 (p = t % 32) for 8 features per pass
     constexpr int NKQ = DK / 64;  // passes over the key features (8 groups of 8 per pass)
     constexpr int NV = DV / 64;
     const int p2 = tid % 32, fg = tid / 32;
     const int i0 = 2 * p2, i1 = 2 * p2 + 1;
+    const int64_t r0 = tok0 + min(i0, valid - 1), r1 = tok0 + min(i1, valid - 1);
     uint4 kv[NKQ][2], qv[NKQ][2], vv[NV][2];
 #pragma unroll
     for (int m = 0; m < NKQ; ++m) {
         const int f0 = 64 * m + 8 * fg;
-        kv[m][0] = kv[m][1] = qv[m][0] = qv[m][1] = make_uint4(0, 0, 0, 0);
-        if (i0 < valid) {
-            kv[m][0] = *reinterpret_cast<const uint4*>(kp + (tok0 + i0) * DK + f0);
-            qv[m][0] = *reinterpret_cast<const uint4*>(qp + (tok0 + i0) * DK + f0);
-        }
-        if (i1 < valid) {
-            kv[m][1] = *reinterpret_cast<const uint4*>(kp + (tok0 + i1) * DK + f0);
-            qv[m][1] = *reinterpret_cast<const uint4*>(qp + (tok0 + i1) * DK + f0);
-        }
+        kv[m][0] = *reinterpret_cast<const uint4*>(kp + r0 * DK + f0);
+        qv[m][0] = *reinterpret_cast<const uint4*>(qp + r0 * DK + f0);
+        kv[m][1] = *reinterpret_cast<const uint4*>(kp + r1 * DK + f0);
+        qv[m][1] = *reinterpret_cast<const uint4*>(qp + r1 * DK + f0);
     }
 #pragma unroll
     for (int m = 0; m < NV; ++m) {
         const int f0 = 64 * m + 8 * fg;
-        vv[m][0] = i0 < valid ? *reinterpret_cast<const uint4*>(vp + (tok0 + i0) * DV + f0) : make_uint4(0, 0, 0, 0);
-        vv[m][1] = i1 < valid ? *reinterpret_cast<const uint4*>(vp + (tok0 + i1) * DV + f0) : make_uint4(0, 0, 0, 0);
+        vv[m][0] = *reinterpret_cast<const uint4*>(vp + r0 * DV + f0);
+        vv[m][1] = *reinterpret_cast<const uint4*>(vp + r1 * DV + f0);
     }
-    // chunk states as bf16 A-fragments: fragment (t, s) of lane l at [(t * KS + s) * 64 + l] * 8
+    // Chunk states as bf16 A-fragments, fragment f of lane l at [f * 64 + l] * 8: one
+    // fragment is 1 KiB, so each is one direct global -> LDS load of the whole wave
+    // (lane l's 16 bytes land at byte 16 l of the fragment).  Every wave needs all of
+    // H_c and G_c; they cross the vector caches once per workgroup this way.  H_c is
+    // needed first; G_c only by the read-out, so its loads go out after the barrier.
     const uint16_t* Hf = static_cast<const uint16_t*>(a.Hs) + (bh * s.n_chunks + n) * int64_t(DK) * DK;
     const uint16_t* Gf = static_cast<const uint16_t*>(a.Gs) + (bh * s.n_chunks + n) * int64_t(DV) * DK;
-    bf16x8 hc[MT][KS];
+    constexpr int NHF = DK * DK / (8 * kWave) / 4;  // H_c fragments per wave
+    constexpr int NGF = DV * DK / (8 * kWave) / 4;  // G_c fragments per wave
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int u = 0; u < NHF; ++u) {
+        const int f = wave * NHF + u;
+        load_lds16(Hf + (f * kWave + lane) * 8, sHf + f * kWave * 8);
+    }
+    // gates and write strengths of the chunk, one token per lane, in every wave;
+    // absent tokens have gate 1 and strength 0
+    const float gl = lane < valid ? g_raw : 1.0f;
+    const float bl = lane < valid ? b_raw : 0.0f;
+    if (valid < kC) {
+        const bool k0 = i0 < valid, k1 = i1 < valid;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            hc[mt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(Hf + ((mt * KS + ks) * 64 + lane) * 8));
-    // diag(H_c) for the rows r = 16mt + 4g + ii this lane holds: fragment (mt, mt/2),
-    // lane 16g + 4g + ii, element 4 (mt % 2) + ii
-    f32x4 hdiag[MT];
+        for (int m = 0; m < NKQ; ++m) {
+            kv[m][0] = keep_if(k0, kv[m][0]);
+            qv[m][0] = keep_if(k0, qv[m][0]);
+            kv[m][1] = keep_if(k1, kv[m][1]);
+            qv[m][1] = keep_if(k1, qv[m][1]);
+        }
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int ii = 0; ii < 4; ++ii)
-            hdiag[mt][ii] = bf16_bits_to_f32(Hf[((mt * KS + mt / 2) * 64 + 20 * g + ii) * 8 + 4 * (mt % 2) + ii]);
+        for (int m = 0; m < NV; ++m) {
+            vv[m][0] = keep_if(k0, vv[m][0]);
+            vv[m][1] = keep_if(k1, vv[m][1]);
+        }
+    }
     const float* lam = a.lambda + int64_t(h) * DK;
     if (tid < DK) sLam[tid] = lam[tid];
+    // Gate log-cumsums of the chunk in registers (lane = token; the same rules as
+    // chunk_log_decays: a zero gate resets memory through zl instead of log 0).
+    const float lgl = wave_scan_add(gl > 0.0f ? logf(gl) : 0.0f);
+    const int zll = wave_scan_max((lane < valid && !(gl > 0.0f)) ? lane : -1);
+    const float zeta_l = zll >= 0 ? 0.0f : __expf(lgl);  // zeta_{c+l,c}
+    if (wave == 0) {
+        sLg[lane] = lgl;
+        sZl[lane] = zll;
+        sZ0[lane] = zeta_l;
+        sBeta[lane] = bl;
+    }
+    // Rank-update weight of token i relative to the chunk's entering state,
+    // u_i = beta_i / zeta_{c+i,c}; 0 where zeta_{c+i,c} <= kMinDecay (those tokens
+    // only enter sub-chunk states built without H_c, below).
+    const float u_l = zeta_l > kMinDecay ? bl * __expf(-lgl) : 0.0f;
+    const float u0 = __shfl(u_l, i0), u1 = __shfl(u_l, i1);
 #pragma unroll
     for (int m = 0; m < NKQ; ++m) {
         const int f0 = 64 * m + 8 * fg;
@@ -168,106 +222,120 @@ void chunk_cg_bf16_kernel(CgArgs a)
         *reinterpret_cast<uint4*>(sQ + i0 * LDK + f0) = qv[m][0];
         *reinterpret_cast<uint4*>(sQ + i1 * LDK + f0) = qv[m][1];
         stage_token_pair(reinterpret_cast<uint32_t*>(sKT), LDC / 2, f0, p2, kv[m][0], kv[m][1]);
+        stage_token_pair(reinterpret_cast<uint32_t*>(sKU), LDC / 2, f0, p2, scale_bf16x8(kv[m][0], u0),
+                         scale_bf16x8(kv[m][1], u1));
     }
 #pragma unroll
     for (int m = 0; m < NV; ++m)
         stage_token_pair(reinterpret_cast<uint32_t*>(sVT), LDC / 2, 64 * m + 8 * fg, p2, vv[m][0], vv[m][1]);
-    if (tid < kWave) {
-        chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
-        sBeta[tid] = tid < valid ? a.beta[tok0 + tid] : 0.0f;
-    }
-
+    // this wave's H_c fragments have landed in LDS; the barrier publishes them
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
-    for (int e = tid; e < kC * kC; e += kThreads) {
-        const int i = e / kC, jj = e % kC;
-        sT[i * (kC + 1) + jj] = sBeta[i] * decay_between_hw(sLg, sZl, i, jj);
+#pragma unroll
+    for (int u = 0; u < NGF; ++u) {
+        const int f = wave * NGF + u;
+        load_lds16(Gf + (f * kWave + lane) * 8, sGf + f * kWave * 8);
     }
-    if (tid < kC) sZ0[tid] = decay_from_start_hw(sLg, sZl, tid);
-    __syncthreads();
+    bf16x8 hc[MT][KS];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            hc[mt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sHf + ((mt * KS + ks) * kWave + lane) * 8));
 
     // ---- decays of this sub-chunk
     const int jb = 16 * wave - 1;  // token whose state enters the sub-chunk (-1: the chunk's H_c)
     const float Dw = wave == 0 ? 1.0f : sZ0[jb];
-    // B_w = Dw H_c + sum_{i<16w} u_i k_i k_i^T with u_i = beta_i zeta_{16w-1,i}.  It is kept as
-    // B'_w = B_w / Dw = H_c + sum (u_i / Dw) k_i k_i^T and the 1/Dw goes into the column scale:
-    // zs_j = zt_j Dw = zeta_{c+j,c}.  When Dw is negligible (<= 1e-20, e.g. a zero gate) the
-    // state term Dw H_c is dropped instead: B_w = sum u_i k_i k_i^T and zs_j = zt_j.
-    const bool keepH = wave == 0 || Dw > 1e-20f;
+    // B_w = Dw H_c + sum_{i<16w} beta_i zeta_{16w-1,i} k_i k_i^T.  It is kept as
+    // B'_w = B_w / Dw = H_c + sum_{i<16w} u_i k_i k_i^T (u_i = beta_i / zeta_{c+i,c}, the
+    // staged sKU) and the 1/Dw goes into the column scale: zs_j = zt_j Dw = zeta_{c+j,c}.
+    // When Dw is negligible (<= kMinDecay, e.g. after a zero gate) the state term Dw H_c
+    // is dropped instead: B_w = sum_{i<16w} beta_i zeta_{16w-1,i} k_i k_i^T and zs_j = zt_j.
+    const bool keepH = wave == 0 || Dw > kMinDecay;
     const float zs = keepH ? sZ0[j] : decay_between_hw(sLg, sZl, jb, j);
-    const float ush = keepH && wave > 0 ? 1.0f / Dw : 1.0f;
     f32x4 zw;  // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
         const int i = 16 * wave + 4 * g + ii;
-        zw[ii] = sT[i * (kC + 1) + j];
+        zw[ii] = sBeta[i] * decay_between_hw(sLg, sZl, i, j);
     }
-    // rank-update weights (scaled) on this lane's k-indices
-    bf16x8 uwb[2];
-    float uw[2][8];
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
-            uw[u][e] = i < 16 * wave ? sT[i * (kC + 1) + jb] * ush : 0.0f;
-            uwb[u][e] = (__bf16)uw[u][e];
-        }
-    const int nu = (16 * wave + 31) / 32;  // 32-token steps holding tokens < 16w
 
     // ---- B'_w as bf16 A-fragments: hf[mt][s] covers rows 16mt.., columns 32s..
-    // The A operand of the rank update for rows 32s + 16h.. does not depend on mt: load once.
+    // Every wave runs the same straight-line code: both 32-token steps of the rank update,
+    // with the tokens i >= 16w zeroed in its A operand (rows 32s + 16h.., independent of mt,
+    // loaded once).  Element e of step u is token 32u + 4g + e (e < 4) or 32u + 16 + 4g + e - 4,
+    // so whole halves are in or out: the lower half of step u iff 32u + 16 <= 16w, the upper
+    // half iff 32u + 32 <= 16w.
     bf16x8 ka[KS][2][2];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+    for (int u = 0; u < 2; ++u) {
+        const bool in_lo = 32 * u + 16 <= 16 * wave, in_hi = 32 * u + 32 <= 16 * wave;
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh)
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-            for (int u = 0; u < 2; ++u)
-                if (u < nu) ka[ks][hh][u] = lds_frag(sKT + (32 * ks + 16 * hh + ln) * LDC + 32 * u + 4 * g);
+            for (int hh = 0; hh < 2; ++hh) {
+                const uint4 raw = __builtin_bit_cast(uint4, lds_frag(sKT + (32 * ks + 16 * hh + ln) * LDC + 32 * u + 4 * g));
+                ka[ks][hh][u] = __builtin_bit_cast(bf16x8, make_uint4(in_lo ? raw.x : 0u, in_lo ? raw.y : 0u,
+                                                                      in_hi ? raw.z : 0u, in_hi ? raw.w : 0u));
+            }
+    }
+    // Without H_c the weights are per sub-chunk: beta_i zeta_{16w-1,i} on this lane's k-indices.
+    float uw[2][8];
+    if (!keepH) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
+                uw[u][e] = i < 16 * wave ? sBeta[i] * decay_between_hw(sLg, sZl, i, jb) : 0.0f;
+            }
+    }
     // Identity operands that copy an A-fragment of H_c, read as a B operand, into the two
-    // 16x16 result tiles (rows 32s + {0..15} and 32s + {16..31}) it belongs to.
+    // 16x16 result tiles (rows 32s + {0..15} and 32s + {16..31}) it belongs to; zero when
+    // the state term is dropped.
     bf16x8 id_lo, id_hi;
+    const float one = keepH ? 1.0f : 0.0f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        id_lo[e] = (__bf16)(4 * g + e == ln ? 1.0f : 0.0f);
+        id_lo[e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
         id_lo[4 + e] = (__bf16)0.0f;
         id_hi[e] = (__bf16)0.0f;
-        id_hi[4 + e] = (__bf16)(4 * g + e == ln ? 1.0f : 0.0f);
+        id_hi[4 + e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
     }
+    // diag(B'_w) goes to sDiag[wave][r]; lanes off the diagonal write a spare slot instead
+    const int e_diag = ln - 4 * g;
+    const bool on_diag = e_diag >= 0 && e_diag < 4;
     bf16x8 hf[MT][KS];
-    f32x4 dg1[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         bf16x8 bw[2];
-        dg1[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            if (u < nu) {
+            if (keepH) {
+                bw[u] = lds_frag(sKU + (16 * mt + ln) * LDC + 32 * u + 4 * g);
+            } else {
                 const bf16x8 raw = lds_frag(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) bw[u][e] = (__bf16)((float)raw[e] * uw[u][e]);
-                dg1[mt] = mfma16(lds_frag_sq(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g), uwb[u], dg1[mt]);
             }
         }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            if (nu == 0) {
-                hf[mt][ks] = hc[mt][ks];  // B_0 = H_c
-                continue;
-            }
-            f32x4 lo = f32x4{0.0f, 0.0f, 0.0f, 0.0f}, hi = lo;
-            if (keepH) {
-                lo = mfma16(id_lo, hc[mt][ks], lo);
-                hi = mfma16(id_hi, hc[mt][ks], hi);
-            }
+            f32x4 lo = mfma16(id_lo, hc[mt][ks], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+            f32x4 hi = mfma16(id_hi, hc[mt][ks], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
-                if (u < nu) {
-                    lo = mfma16(ka[ks][0][u], bw[u], lo);
-                    hi = mfma16(ka[ks][1][u], bw[u], hi);
-                }
+                lo = mfma16(ka[ks][0][u], bw[u], lo);
+                hi = mfma16(ka[ks][1][u], bw[u], hi);
             }
             hf[mt][ks] = pack8(lo, hi);
+            // Tile rows 16mt.. of fragment (mt, mt/2) hold the diagonal block: lane (g, n)
+            // has B'[16mt + 4g + e][16mt + n], on the diagonal for n = 4g + e.
+            if (ks == mt / 2) {
+                const f32x4 acc = (mt % 2) ? hi : lo;
+                const float dv = e_diag == 0 ? acc[0] : e_diag == 1 ? acc[1] : e_diag == 2 ? acc[2] : acc[3];
+                sDiag[wave][on_diag ? 16 * mt + ln : DK + lane] = dv;
+            }
         }
     }
     // B'_w is read only as the A operand of the state products.  Those accept the
@@ -319,7 +387,9 @@ void chunk_cg_bf16_kernel(CgArgs a)
     };
 
     // ---- Jacobi start x0 = q / diag(H_t + Lambda),
-    //      diag(H_t) = zs_j diag(B'_w) + sum_{16w <= i <= j} beta_i Z[i][j] k_i^2
+    //      diag(H_t) = zs_j diag(B'_w) + sum_{16w <= i <= j} beta_i Z[i][j] k_i^2, diag(B'_w)
+    //      read back from this wave's sDiag rows (written by other lanes of the same wave;
+    //      a wave's LDS accesses complete in order)
     f32x4 x[MT], r[MT], p[MT], w[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -333,8 +403,10 @@ void chunk_cg_bf16_kernel(CgArgs a)
         const uint2 qq = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
         const f32x4 qf{bf16_bits_to_f32(qq.x & 0xffffu), bf16_bits_to_f32(qq.x >> 16),
                        bf16_bits_to_f32(qq.y & 0xffffu), bf16_bits_to_f32(qq.y >> 16)};
-        const f32x4 d = zs * ((keepH ? 1.0f : 0.0f) * hdiag[mt] + dg1[mt]) + dg2 + *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
-        x[mt] = qf / d;
+        const f32x4 d = zs * *reinterpret_cast<const f32x4*>(&sDiag[wave][16 * mt + 4 * g]) + dg2 +
+                        *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[mt][e] = qf[e] * __builtin_amdgcn_rcpf(d[e]);
         p[mt] = qf;  // holds q until the first residual is formed
     }
     matvec(x, w);
@@ -383,6 +455,8 @@ void chunk_cg_bf16_kernel(CgArgs a)
     }
 
     // ---- read-out o_j = G_c (zeta_j x_j) + sum_i beta_i Z[i][j] v_i (k_i^T x_j)
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // this wave's G_c fragments have landed
+    __syncthreads();
     if (a.qstar && j < valid) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
@@ -395,7 +469,7 @@ void chunk_cg_bf16_kernel(CgArgs a)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
             const int i = 16 * it + 4 * g + ii;
-            zo[it][ii] = (it <= wave) ? sT[i * (kC + 1) + j] : 0.0f;
+            zo[it][ii] = (it <= wave) ? sBeta[i] * decay_between_hw(sLg, sZl, i, j) : 0.0f;
         }
     bf16x8 xb[KS], xz[KS];
 #pragma unroll
@@ -403,15 +477,14 @@ void chunk_cg_bf16_kernel(CgArgs a)
         xb[ks] = pack8(x[2 * ks], x[2 * ks + 1]);
         xz[ks] = pack8(zeta * x[2 * ks], zeta * x[2 * ks + 1]);
     }
+    // every wave runs all four token tiles (zo is zero past the causal ones)
     f32x4 sacc[4];
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
         sacc[it] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        if (it <= wave) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                sacc[it] = mfma16(lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g), xb[ks], sacc[it]);
-        }
+        for (int ks = 0; ks < KS; ++ks)
+            sacc[it] = mfma16(lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g), xb[ks], sacc[it]);
     }
     f32x4 o[MTV];
 #pragma unroll
@@ -419,17 +492,15 @@ void chunk_cg_bf16_kernel(CgArgs a)
         o[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-            o[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(Gf + ((mt * KS + ks) * 64 + lane) * 8)),
+            o[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sGf + ((mt * KS + ks) * kWave + lane) * 8)),
                            xz[ks], o[mt]);
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-        if (2 * u <= wave) {
-            const bf16x8 sb = pack8(sacc[2 * u] * zo[2 * u], sacc[2 * u + 1] * zo[2 * u + 1]);
+        const bf16x8 sb = pack8(sacc[2 * u] * zo[2 * u], sacc[2 * u + 1] * zo[2 * u + 1]);
 #pragma unroll
-            for (int mt = 0; mt < MTV; ++mt)
-                o[mt] = mfma16(lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, o[mt]);
-        }
+        for (int mt = 0; mt < MTV; ++mt)
+            o[mt] = mfma16(lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, o[mt]);
     }
     if (j < valid) {
 #pragma unroll

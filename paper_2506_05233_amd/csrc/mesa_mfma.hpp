@@ -74,4 +74,23 @@ __device__ __forceinline__ void stage_token_pair(uint32_t* dst32, int ld32, int 
     }
 }
 
+// Direct global -> LDS load of one wave (gfx950 global_load_lds_dwordx4): lane l's
+// 16 bytes at src land at lds + 16 l; lds must be the same in every lane.  The data
+// is complete once the issuing wave's vector memory count has drained.  The builtin
+// exists for the device pass only: in the host pass a kernel that names it would
+// lose its launch stub, and the host never runs this code.
+__device__ __forceinline__ void load_lds16(const void* src, void* lds)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+#else
+    (void)src;
+    (void)lds;
+#endif
+}
+
+// s_waitcnt operand that waits for the vector memory count to reach 0 and leaves
+// the export and LDS/scalar counts alone (GFX9 encoding).
+constexpr int kWaitVmcnt0 = 0x0F70;
+
 }  // namespace mesa

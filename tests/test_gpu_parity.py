@@ -120,6 +120,22 @@ def test_bf16_path_edge_cases():
         assert np.all(got[0, 0, 10] == 0.0)
 
 
+def test_bf16_path_strong_decay():
+    """Gates in [0.25, 0.6]: the decay across 32-48 tokens drops below 1e-20, so the
+    later sub-chunk states of every chunk are built without the chunk state, and the
+    earlier ones carry rank-update weights up to ~1e14 (both regimes of the
+    sub-chunk states of the matrix-core path), checked over every output."""
+    x = W.forward_inputs(2, 2, 4 * 64 + 17, 128, 128, "bf16", 4.0, seed=43)
+    rng = np.random.default_rng(4301)
+    x["gamma"][...] = rng.uniform(0.25, 0.6, size=x["gamma"].shape).astype(np.float32)
+    for n_cg in (0, 15):
+        got = _gpu_forward(x, "bf16", n_cg, 64, precision=L.MESA_PREC_BF16, want_qstar=True)
+        ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], n_cg, want_qstar=True)
+        e_out, e_q = rel_l2(got["out"], ref["out"]), rel_l2(got["qstar"], ref["qstar"])
+        _say("bf16 strong decay n_cg=%d: out %.3e qstar %.3e" % (n_cg, e_out, e_q))
+        assert e_out <= TOL_BF16 and e_q <= TOL_BF16, n_cg
+
+
 def test_stress_repeated_keys_bf16_path_reported():
     """Single-pass bf16 operands are validated on the workload distributions,
     not on adversarial inputs: on the repeated-key stress input the error is
