@@ -8,9 +8,10 @@
 //   (H_t + Lambda) p_j = H_c (zeta_j p_j) + sum_{i<=j} beta_i Z[i][j] k_i (k_i^T p_j) + Lambda p_j
 //   o_j               = G_c (zeta_j x_j) + sum_{i<=j} beta_i Z[i][j] v_i (k_i^T x_j).
 //
-// Work split: a workgroup is one chunk; wave w owns the 16-token sub-chunk
-// j = 16w .. 16w+15 and runs its own CG on it with no barrier.  Each wave
-// first forms the state that enters its sub-chunk,
+// Work split: a workgroup (one per CU, looping over chunks) takes one chunk at a
+// time; wave w owns the 16-token sub-chunk j = 16w .. 16w+15 and runs its own
+// CG on it with no barrier.  Each wave first forms the state that enters its
+// sub-chunk,
 //
 //   B_w = zeta_{16w-1} H_c + sum_{i < 16w} beta_i zeta_{16w-1,i} k_i k_i^T   (B_0 = H_c),
 //
@@ -38,6 +39,12 @@
 //
 // The read-out o_j = G_c (zeta_j x_j) + sum_{i <= j} beta_i Z[i][j] v_i (k_i^T x_j)
 // runs once per chunk over the whole causal chunk.
+//
+// Memory: the chunk's keys, queries, values and H_c come in by direct global ->
+// LDS loads issued while the previous chunk's CG runs, into LDS that only the
+// state build and the Jacobi start use (so HBM traffic is spread over the whole
+// kernel instead of arriving in bursts at every chunk start); G_c is loaded the
+// same way during the chunk's own build and CG.
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
 #include "mesa_mfma.hpp"
@@ -47,18 +54,6 @@ namespace {
 
 constexpr int kC = 64;         // chunk
 constexpr int kThreads = 256;  // four waves, 16 tokens each
-
-// Same, with every element squared (fp32 square, rounded back to bf16).
-__device__ __forceinline__ bf16x8 lds_frag_sq(const uint16_t* base)
-{
-    bf16x8 f = lds_frag(base);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const float v = (float)f[e];
-        f[e] = (__bf16)(v * v);
-    }
-    return f;
-}
 
 // Gate decay with the hardware exponential (relative error ~1e-7, far below
 // the bf16 operand rounding of this path); same zero-gate rule as the shared
@@ -93,427 +88,547 @@ __device__ __forceinline__ uint4 scale_bf16x8(const uint4& v, float u)
 // Sum over the four lanes that hold one column (lanes n, n+16, n+32, n+48).
 __device__ __forceinline__ float col_sum(float v) { return row_pair_sums(v); }
 
+// LDS arena of the kernel (byte offsets).  G_c and diag(B'_w) have arrays of their
+// own: G_c's direct loads run under the state build and the Jacobi start, and
+// accesses the compiler can tell apart from them are not ordered behind them.
+// The next chunk's staging data lands on
+// the key tiles, scaled keys and queries (sKT, sKU, sQ) while the CG loop runs:
+// those are only read before it.  Thread t's 16-byte staging slot q is at raw
+// slot q * kThreads + t, so one wave's direct load fills 64 consecutive slots and
+// every thread reads back its own slots.
+template <int DK, int DV>
+struct CgSmem {
+    static constexpr int LDK = DK + 8;  // row stride (elements) of token-major tiles
+    static constexpr int LDC = kC + 8;  // row stride of feature-major tiles
+    static constexpr int NKQ = DK / 64;  // staging passes over the key features
+    static constexpr int NV = DV / 64;
+    static constexpr int kRawSlots = 2 * (2 * NKQ + NV);
+    static constexpr int oK = 0;                              // k_i[b], token-major
+    static constexpr int oVT = oK + kC * LDK * 2;             // v_i[e], feature-major
+    static constexpr int oLam = oVT + DV * LDC * 2;           // lambda
+    static constexpr int oLg = oLam + DK * 4;                 // gate log-cumsums
+    static constexpr int oBeta = oLg + kWave * 4;
+    static constexpr int oZl = oBeta + kWave * 4;             // last zero gate
+    static constexpr int oZ0 = oZl + kWave * 4;               // zeta_{c+j,c}
+    static constexpr int oHf = oZ0 + kC * 4;                  // H_c as A-fragments
+    static constexpr int oKT = oHf + DK * DK * 2;             // k_i[b], feature-major
+    static constexpr int oKU = oKT + DK * LDC * 2;            // u_i k_i[b], feature-major
+    static constexpr int oQ = oKU + DK * LDC * 2;             // q_j[b], token-major
+    static constexpr int oRaw = oKT;                          // next chunk's staging slots
+    static constexpr int kEnd = oQ + kC * LDK * 2;
+    static constexpr int kRawEnd = oRaw + kRawSlots * kThreads * 16;
+    static constexpr int kBytes = kEnd > kRawEnd ? kEnd : kRawEnd;
+    static_assert(kBytes + DV * DK * 2 + (kThreads / kWave) * (DK + kWave) * 4 <= 160 * 1024,
+                  "LDS use exceeds 160 KiB");
+};
+
 template <int DK, int DV>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void chunk_cg_bf16_kernel(CgArgs a)
+void chunk_cg_bf16_kernel(CgArgs a, int total)
 {
+    using L = CgSmem<DK, DV>;
     constexpr int MT = DK / 16;    // 16-row tiles of a per-token vector
     constexpr int KS = DK / 32;    // 32-long contraction steps over features
     constexpr int MTV = DV / 16;   // 16-row tiles of an output column
-    constexpr int LDK = DK + 8;    // row stride (elements) of token-major tiles
-    constexpr int LDC = kC + 8;    // row stride of feature-major tiles
+    constexpr int LDK = L::LDK, LDC = L::LDC, NKQ = L::NKQ, NV = L::NV;
+    constexpr int NHF = DK * DK / (8 * kWave) / 4;  // H_c fragments per wave
+    constexpr int NGF = DV * DK / (8 * kWave) / 4;  // G_c fragments per wave
+
+    __shared__ __attribute__((aligned(16))) unsigned char smem[L::kBytes];
+    uint16_t* sK = reinterpret_cast<uint16_t*>(smem + L::oK);
+    uint16_t* sVT = reinterpret_cast<uint16_t*>(smem + L::oVT);
+    __shared__ __attribute__((aligned(16))) uint16_t sGf[DV * DK];  // G_c as A-fragments
+    float* sLam = reinterpret_cast<float*>(smem + L::oLam);
+    float* sLg = reinterpret_cast<float*>(smem + L::oLg);
+    float* sBeta = reinterpret_cast<float*>(smem + L::oBeta);
+    int* sZl = reinterpret_cast<int*>(smem + L::oZl);
+    float* sZ0 = reinterpret_cast<float*>(smem + L::oZ0);
+    __shared__ __attribute__((aligned(16))) float sDiag[kThreads / kWave][DK + kWave];  // diag(B'_w), spare slots
+    uint16_t* sHf = reinterpret_cast<uint16_t*>(smem + L::oHf);
+    uint16_t* sKT = reinterpret_cast<uint16_t*>(smem + L::oKT);
+    uint16_t* sKU = reinterpret_cast<uint16_t*>(smem + L::oKU);
+    uint16_t* sQ = reinterpret_cast<uint16_t*>(smem + L::oQ);
+    uint4* sRaw = reinterpret_cast<uint4*>(smem + L::oRaw);
 
     const ForwardShape s = a.s;
-    // the grid has fewer than 2^31 blocks (checked at launch): 32-bit index arithmetic
-    const int n = int(blockIdx.x % unsigned(s.n_chunks));
-    const int64_t bh = blockIdx.x / unsigned(s.n_chunks);
-    const int h = int(unsigned(bh) % unsigned(s.heads));
-    const int64_t t0 = int64_t(n) * kC;
-    const int valid = int(min<int64_t>(kC, s.seq_len - t0));
-    const int64_t tok0 = bh * s.seq_len + t0;
-    const int tid = threadIdx.x;
-    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-    const int lane = tid % kWave;
-    const int g = lane / 16;   // lane group: rows 4g..4g+3 of each tile
-    const int ln = lane % 16;  // column (B / result layout) or row (A layout)
-    const int j = wave * 16 + ln;  // this lane's token within the chunk
-
-    __shared__ __attribute__((aligned(16))) uint16_t sK[kC * LDK];   // k_i[b], token-major
-    __shared__ __attribute__((aligned(16))) uint16_t sKT[DK * LDC];  // k_i[b], feature-major
-    __shared__ __attribute__((aligned(16))) uint16_t sVT[DV * LDC];  // v_i[e], feature-major
-    __shared__ __attribute__((aligned(16))) uint16_t sQ[kC * LDK];   // q_j[b], token-major
-    __shared__ __attribute__((aligned(16))) uint16_t sHf[DK * DK];   // H_c as A-fragments
-    __shared__ __attribute__((aligned(16))) uint16_t sGf[DV * DK];   // G_c as A-fragments
-    __shared__ __attribute__((aligned(16))) uint16_t sKU[DK * LDC];  // u_i k_i[b], feature-major
-    __shared__ float sLg[kWave], sBeta[kWave];
-    __shared__ int sZl[kWave];
-    __shared__ __attribute__((aligned(16))) float sLam[DK];
-    __shared__ float sZ0[kC];            // zeta_{c+j,c}: decay from the chunk's entering state
-    __shared__ __attribute__((aligned(16))) float sDiag[kThreads / kWave][DK + kWave];  // diag(B'_w) per wave, spare slots
-
-    // ---- stage the chunk's keys, values and queries (bf16 bits) in LDS
     const uint16_t* kp = static_cast<const uint16_t*>(a.k);
     const uint16_t* qp = static_cast<const uint16_t*>(a.q);
     const uint16_t* vp = static_cast<const uint16_t*>(a.v);
-    // Every global load of the chunk is issued before the first use of any of them,
-    // gates first (the first ones needed; vector memory returns in order).  Loads
-    // never sit behind a branch: tokens past the end of the sequence read the last
-    // valid token (valid >= 1) and are zeroed once the data is in registers.
-    const int lt = min(lane, valid - 1);
-    const float g_raw = a.gamma[tok0 + lt];
-    const float b_raw = a.beta[tok0 + lt];
-    // thread t stages tokens 2p, 2p+1 (p = t % 32) for 8 features per pass
-    constexpr int NKQ = DK / 64;  // passes over the key features (8 groups of 8 per pass)
-    constexpr int NV = DV / 64;
-    const int p2 = tid % 32, fg = tid / 32;
-    const int i0 = 2 * p2, i1 = 2 * p2 + 1;
-    const int64_t r0 = tok0 + min(i0, valid - 1), r1 = tok0 + min(i1, valid - 1);
-    uint4 kv[NKQ][2], qv[NKQ][2], vv[NV][2];
+    const int n_chunks = s.n_chunks;
+    const int heads = int(s.heads);
+
+    // Chunk c (fewer than 2^31, checked at launch) is chunk c % n_chunks of the
+    // sequence (b, h) = c / n_chunks; it is also the index of its entering state.
+    // Its loads never sit behind a branch: tokens past the end of the sequence read
+    // the last valid token (valid >= 1) and are zeroed once the data is in
+    // registers.  The gates and lambda go to registers; keys, queries and values to
+    // the thread's own staging slots; H_c, as bf16 A-fragments (fragment f of lane l
+    // at [f * 64 + l] * 8, one 1-KiB direct load per fragment), to sHf.  They are
+    // issued in kPieces pieces of at most four direct loads: a wave that issues many
+    // more at once stalls until the first ones return, so the next chunk's pieces
+    // are spread over the CG iterations of the current one.
+    constexpr int kRawSlots = L::kRawSlots;
+    constexpr int kPieces = 2 + (kRawSlots + 3) / 4;
+    auto issue_piece = [&](int c, int piece, int tid_in, float& g_out, float& b_out, float& lam_out) {
+        int tid = tid_in;
+        asm volatile("" : "+v"(tid));  // recompute the addresses here, not hoisted
+        const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+        const int lane = tid % kWave, fg = tid / 32;
+        const int i0 = 2 * (tid % 32), i1 = i0 + 1;
+        const int nn = c % n_chunks;
+        const int bh_ = c / n_chunks;
+        const int64_t t0_ = int64_t(nn) * kC;
+        const int valid_ = int(min<int64_t>(kC, s.seq_len - t0_));
+        const int64_t tok0_ = int64_t(bh_) * s.seq_len + t0_;
+        if (piece < 2) {
+            if (piece == 0) {
+                const int lt = min(lane, valid_ - 1);
+                g_out = a.gamma[tok0_ + lt];
+                b_out = a.beta[tok0_ + lt];
+                lam_out = a.lambda[(bh_ % heads) * DK + min(tid, DK - 1)];
+            }
+            const uint16_t* Hf = static_cast<const uint16_t*>(a.Hs) + int64_t(c) * DK * DK;
 #pragma unroll
-    for (int m = 0; m < NKQ; ++m) {
-        const int f0 = 64 * m + 8 * fg;
-        kv[m][0] = *reinterpret_cast<const uint4*>(kp + r0 * DK + f0);
-        qv[m][0] = *reinterpret_cast<const uint4*>(qp + r0 * DK + f0);
-        kv[m][1] = *reinterpret_cast<const uint4*>(kp + r1 * DK + f0);
-        qv[m][1] = *reinterpret_cast<const uint4*>(qp + r1 * DK + f0);
-    }
+            for (int u = piece * (NHF / 2); u < (piece + 1) * (NHF / 2); ++u) {
+                const int f = wave * NHF + u;
+                load_lds16(Hf + (f * kWave + lane) * 8, sHf + f * kWave * 8);
+            }
+            return;
+        }
+        // staging slots 4 (piece - 2) .. +3: per key/query pass m slots 4m .. 4m+3 =
+        // (k, token 2p), (k, 2p+1), (q, 2p), (q, 2p+1); then per value pass two slots
+        const int64_t r0 = tok0_ + min(i0, valid_ - 1), r1 = tok0_ + min(i1, valid_ - 1);
+        uint4* slot = sRaw + wave * kWave;  // this wave's threads' slots of staging slot 0
 #pragma unroll
-    for (int m = 0; m < NV; ++m) {
-        const int f0 = 64 * m + 8 * fg;
-        vv[m][0] = *reinterpret_cast<const uint4*>(vp + r0 * DV + f0);
-        vv[m][1] = *reinterpret_cast<const uint4*>(vp + r1 * DV + f0);
-    }
-    // Chunk states as bf16 A-fragments, fragment f of lane l at [f * 64 + l] * 8: one
-    // fragment is 1 KiB, so each is one direct global -> LDS load of the whole wave
-    // (lane l's 16 bytes land at byte 16 l of the fragment).  Every wave needs all of
-    // H_c and G_c; they cross the vector caches once per workgroup this way.  H_c is
-    // needed first; G_c only by the read-out, so its loads go out after the barrier.
-    const uint16_t* Hf = static_cast<const uint16_t*>(a.Hs) + (bh * s.n_chunks + n) * int64_t(DK) * DK;
-    const uint16_t* Gf = static_cast<const uint16_t*>(a.Gs) + (bh * s.n_chunks + n) * int64_t(DV) * DK;
-    constexpr int NHF = DK * DK / (8 * kWave) / 4;  // H_c fragments per wave
-    constexpr int NGF = DV * DK / (8 * kWave) / 4;  // G_c fragments per wave
+        for (int q = 0; q < kRawSlots; ++q) {
+            if (q / 4 != piece - 2) continue;
+            const bool kq = q < 4 * NKQ;
+            const int m = kq ? q / 4 : (q - 4 * NKQ) / 2;
+            const int f0 = 64 * m + 8 * fg;
+            const int64_t row = (kq ? q % 2 : (q - 4 * NKQ) % 2) ? r1 : r0;
+            const uint16_t* src = kq ? ((q % 4) < 2 ? kp + row * DK + f0 : qp + row * DK + f0) : vp + row * DV + f0;
+            load_lds16(src, slot + q * kThreads);
+        }
+    };
+    auto issue_all = [&](int c, int tid_in, float& g_out, float& b_out, float& lam_out) {
 #pragma unroll
-    for (int u = 0; u < NHF; ++u) {
-        const int f = wave * NHF + u;
-        load_lds16(Hf + (f * kWave + lane) * 8, sHf + f * kWave * 8);
-    }
-    // gates and write strengths of the chunk, one token per lane, in every wave;
-    // absent tokens have gate 1 and strength 0
-    const float gl = lane < valid ? g_raw : 1.0f;
-    const float bl = lane < valid ? b_raw : 0.0f;
-    if (valid < kC) {
-        const bool k0 = i0 < valid, k1 = i1 < valid;
+        for (int piece = 0; piece < kPieces; ++piece) issue_piece(c, piece, tid_in, g_out, b_out, lam_out);
+    };
+
+    int cc = blockIdx.x;
+    float g_cur = 1.0f, b_cur = 0.0f, lam_cur = 0.0f;
+    issue_all(cc, threadIdx.x, g_cur, b_cur, lam_cur);
+    for (;;) {
+        // The thread's index values are re-derived for every chunk from a copy the
+        // compiler cannot see through, so the many per-lane LDS addresses below are
+        // recomputed where they are used rather than hoisted out of the chunk loop
+        // into registers held for the whole kernel.
+        int tid = threadIdx.x;
+        asm volatile("" : "+v"(tid));
+        int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+        asm volatile("" : "+s"(wave));
+        const int lane = tid % kWave;
+        const int g = lane / 16;   // lane group: rows 4g..4g+3 of each tile
+        const int ln = lane % 16;  // column (B / result layout) or row (A layout)
+        const int j = wave * 16 + ln;  // this lane's token within the chunk
+        // thread t stages tokens 2p, 2p+1 (p = t % 32) for 8 features per pass
+        const int p2 = tid % 32, fg = tid / 32;
+        const int i0 = 2 * p2, i1 = 2 * p2 + 1;
+        const int cn = cc + int(gridDim.x);
+        const bool more = cn < total;
+        const int n = cc % n_chunks;
+        const int bh = cc / n_chunks;
+        const int64_t t0 = int64_t(n) * kC;
+        const int valid = int(min<int64_t>(kC, s.seq_len - t0));
+        const int64_t tok0 = int64_t(bh) * s.seq_len + t0;
+
+        // ---- this thread's staging data, its gates and this wave's H_c fragments have
+        // landed; the barrier publishes H_c and ends the previous chunk's read-out
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        uint4 kv[NKQ][2], qv[NKQ][2], vv[NV][2];
 #pragma unroll
         for (int m = 0; m < NKQ; ++m) {
-            kv[m][0] = keep_if(k0, kv[m][0]);
-            qv[m][0] = keep_if(k0, qv[m][0]);
-            kv[m][1] = keep_if(k1, kv[m][1]);
-            qv[m][1] = keep_if(k1, qv[m][1]);
+            kv[m][0] = sRaw[(4 * m + 0) * kThreads + tid];
+            kv[m][1] = sRaw[(4 * m + 1) * kThreads + tid];
+            qv[m][0] = sRaw[(4 * m + 2) * kThreads + tid];
+            qv[m][1] = sRaw[(4 * m + 3) * kThreads + tid];
         }
 #pragma unroll
         for (int m = 0; m < NV; ++m) {
-            vv[m][0] = keep_if(k0, vv[m][0]);
-            vv[m][1] = keep_if(k1, vv[m][1]);
+            vv[m][0] = sRaw[(4 * NKQ + 2 * m + 0) * kThreads + tid];
+            vv[m][1] = sRaw[(4 * NKQ + 2 * m + 1) * kThreads + tid];
         }
-    }
-    const float* lam = a.lambda + int64_t(h) * DK;
-    if (tid < DK) sLam[tid] = lam[tid];
-    // Gate log-cumsums of the chunk in registers (lane = token; the same rules as
-    // chunk_log_decays: a zero gate resets memory through zl instead of log 0).
-    const float lgl = wave_scan_add(gl > 0.0f ? logf(gl) : 0.0f);
-    const int zll = wave_scan_max((lane < valid && !(gl > 0.0f)) ? lane : -1);
-    const float zeta_l = zll >= 0 ? 0.0f : __expf(lgl);  // zeta_{c+l,c}
-    if (wave == 0) {
-        sLg[lane] = lgl;
-        sZl[lane] = zll;
-        sZ0[lane] = zeta_l;
-        sBeta[lane] = bl;
-    }
-    // Rank-update weight of token i relative to the chunk's entering state,
-    // u_i = beta_i / zeta_{c+i,c}; 0 where zeta_{c+i,c} <= kMinDecay (those tokens
-    // only enter sub-chunk states built without H_c, below).
-    const float u_l = zeta_l > kMinDecay ? bl * __expf(-lgl) : 0.0f;
-    const float u0 = __shfl(u_l, i0), u1 = __shfl(u_l, i1);
+        __syncthreads();
+        // gates and write strengths of the chunk, one token per lane, in every wave;
+        // absent tokens have gate 1 and strength 0
+        const float gl = lane < valid ? g_cur : 1.0f;
+        const float bl = lane < valid ? b_cur : 0.0f;
+        if (valid < kC) {
+            const bool k0 = i0 < valid, k1 = i1 < valid;
 #pragma unroll
-    for (int m = 0; m < NKQ; ++m) {
-        const int f0 = 64 * m + 8 * fg;
-        *reinterpret_cast<uint4*>(sK + i0 * LDK + f0) = kv[m][0];
-        *reinterpret_cast<uint4*>(sK + i1 * LDK + f0) = kv[m][1];
-        *reinterpret_cast<uint4*>(sQ + i0 * LDK + f0) = qv[m][0];
-        *reinterpret_cast<uint4*>(sQ + i1 * LDK + f0) = qv[m][1];
-        stage_token_pair(reinterpret_cast<uint32_t*>(sKT), LDC / 2, f0, p2, kv[m][0], kv[m][1]);
-        stage_token_pair(reinterpret_cast<uint32_t*>(sKU), LDC / 2, f0, p2, scale_bf16x8(kv[m][0], u0),
-                         scale_bf16x8(kv[m][1], u1));
-    }
+            for (int m = 0; m < NKQ; ++m) {
+                kv[m][0] = keep_if(k0, kv[m][0]);
+                qv[m][0] = keep_if(k0, qv[m][0]);
+                kv[m][1] = keep_if(k1, kv[m][1]);
+                qv[m][1] = keep_if(k1, qv[m][1]);
+            }
 #pragma unroll
-    for (int m = 0; m < NV; ++m)
-        stage_token_pair(reinterpret_cast<uint32_t*>(sVT), LDC / 2, 64 * m + 8 * fg, p2, vv[m][0], vv[m][1]);
-    // this wave's H_c fragments have landed in LDS; the barrier publishes them
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    __syncthreads();
+            for (int m = 0; m < NV; ++m) {
+                vv[m][0] = keep_if(k0, vv[m][0]);
+                vv[m][1] = keep_if(k1, vv[m][1]);
+            }
+        }
+        if (tid < DK) sLam[tid] = lam_cur;
+        // Gate log-cumsums of the chunk in registers (lane = token; the same rules as
+        // chunk_log_decays: a zero gate resets memory through zl instead of log 0).
+        const float lgl = wave_scan_add(gl > 0.0f ? logf(gl) : 0.0f);
+        const int zll = wave_scan_max((lane < valid && !(gl > 0.0f)) ? lane : -1);
+        const float zeta_l = zll >= 0 ? 0.0f : __expf(lgl);  // zeta_{c+l,c}
+        if (wave == 0) {
+            sLg[lane] = lgl;
+            sZl[lane] = zll;
+            sZ0[lane] = zeta_l;
+            sBeta[lane] = bl;
+        }
+        // Rank-update weight of token i relative to the chunk's entering state,
+        // u_i = beta_i / zeta_{c+i,c}; 0 where zeta_{c+i,c} <= kMinDecay (those tokens
+        // only enter sub-chunk states built without H_c, below).
+        const float u_l = zeta_l > kMinDecay ? bl * __expf(-lgl) : 0.0f;
+        const float u0 = __shfl(u_l, i0), u1 = __shfl(u_l, i1);
 #pragma unroll
-    for (int u = 0; u < NGF; ++u) {
-        const int f = wave * NGF + u;
-        load_lds16(Gf + (f * kWave + lane) * 8, sGf + f * kWave * 8);
-    }
-    bf16x8 hc[MT][KS];
+        for (int m = 0; m < NKQ; ++m) {
+            const int f0 = 64 * m + 8 * fg;
+            *reinterpret_cast<uint4*>(sK + i0 * LDK + f0) = kv[m][0];
+            *reinterpret_cast<uint4*>(sK + i1 * LDK + f0) = kv[m][1];
+            *reinterpret_cast<uint4*>(sQ + i0 * LDK + f0) = qv[m][0];
+            *reinterpret_cast<uint4*>(sQ + i1 * LDK + f0) = qv[m][1];
+            stage_token_pair(reinterpret_cast<uint32_t*>(sKT), LDC / 2, f0, p2, kv[m][0], kv[m][1]);
+            stage_token_pair(reinterpret_cast<uint32_t*>(sKU), LDC / 2, f0, p2, scale_bf16x8(kv[m][0], u0),
+                             scale_bf16x8(kv[m][1], u1));
+        }
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            hc[mt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sHf + ((mt * KS + ks) * kWave + lane) * 8));
+        for (int m = 0; m < NV; ++m)
+            stage_token_pair(reinterpret_cast<uint32_t*>(sVT), LDC / 2, 64 * m + 8 * fg, p2, vv[m][0], vv[m][1]);
+        __syncthreads();
 
-    // ---- decays of this sub-chunk
-    const int jb = 16 * wave - 1;  // token whose state enters the sub-chunk (-1: the chunk's H_c)
-    const float Dw = wave == 0 ? 1.0f : sZ0[jb];
-    // B_w = Dw H_c + sum_{i<16w} beta_i zeta_{16w-1,i} k_i k_i^T.  It is kept as
-    // B'_w = B_w / Dw = H_c + sum_{i<16w} u_i k_i k_i^T (u_i = beta_i / zeta_{c+i,c}, the
-    // staged sKU) and the 1/Dw goes into the column scale: zs_j = zt_j Dw = zeta_{c+j,c}.
-    // When Dw is negligible (<= kMinDecay, e.g. after a zero gate) the state term Dw H_c
-    // is dropped instead: B_w = sum_{i<16w} beta_i zeta_{16w-1,i} k_i k_i^T and zs_j = zt_j.
-    const bool keepH = wave == 0 || Dw > kMinDecay;
-    const float zs = keepH ? sZ0[j] : decay_between_hw(sLg, sZl, jb, j);
-    f32x4 zw;  // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-        const int i = 16 * wave + 4 * g + ii;
-        zw[ii] = sBeta[i] * decay_between_hw(sLg, sZl, i, j);
-    }
-
-    // ---- B'_w as bf16 A-fragments: hf[mt][s] covers rows 16mt.., columns 32s..
-    // Every wave runs the same straight-line code: both 32-token steps of the rank update,
-    // with the tokens i >= 16w zeroed in its A operand (rows 32s + 16h.., independent of mt,
-    // loaded once).  Element e of step u is token 32u + 4g + e (e < 4) or 32u + 16 + 4g + e - 4,
-    // so whole halves are in or out: the lower half of step u iff 32u + 16 <= 16w, the upper
-    // half iff 32u + 32 <= 16w.
-    bf16x8 ka[KS][2][2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const bool in_lo = 32 * u + 16 <= 16 * wave, in_hi = 32 * u + 32 <= 16 * wave;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
-                const uint4 raw = __builtin_bit_cast(uint4, lds_frag(sKT + (32 * ks + 16 * hh + ln) * LDC + 32 * u + 4 * g));
-                ka[ks][hh][u] = __builtin_bit_cast(bf16x8, make_uint4(in_lo ? raw.x : 0u, in_lo ? raw.y : 0u,
-                                                                      in_hi ? raw.z : 0u, in_hi ? raw.w : 0u));
-            }
-    }
-    // Without H_c the weights are per sub-chunk: beta_i zeta_{16w-1,i} on this lane's k-indices.
-    float uw[2][8];
-    if (!keepH) {
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
-                uw[u][e] = i < 16 * wave ? sBeta[i] * decay_between_hw(sLg, sZl, i, jb) : 0.0f;
-            }
-    }
-    // Identity operands that copy an A-fragment of H_c, read as a B operand, into the two
-    // 16x16 result tiles (rows 32s + {0..15} and 32s + {16..31}) it belongs to; zero when
-    // the state term is dropped.
-    bf16x8 id_lo, id_hi;
-    const float one = keepH ? 1.0f : 0.0f;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        id_lo[e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
-        id_lo[4 + e] = (__bf16)0.0f;
-        id_hi[e] = (__bf16)0.0f;
-        id_hi[4 + e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
-    }
-    // diag(B'_w) goes to sDiag[wave][r]; lanes off the diagonal write a spare slot instead
-    const int e_diag = ln - 4 * g;
-    const bool on_diag = e_diag >= 0 && e_diag < 4;
-    bf16x8 hf[MT][KS];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        bf16x8 bw[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            if (keepH) {
-                bw[u] = lds_frag(sKU + (16 * mt + ln) * LDC + 32 * u + 4 * g);
-            } else {
-                const bf16x8 raw = lds_frag(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) bw[u][e] = (__bf16)((float)raw[e] * uw[u][e]);
-            }
-        }
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            f32x4 lo = mfma16(id_lo, hc[mt][ks], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
-            f32x4 hi = mfma16(id_hi, hc[mt][ks], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                lo = mfma16(ka[ks][0][u], bw[u], lo);
-                hi = mfma16(ka[ks][1][u], bw[u], hi);
-            }
-            hf[mt][ks] = pack8(lo, hi);
-            // Tile rows 16mt.. of fragment (mt, mt/2) hold the diagonal block: lane (g, n)
-            // has B'[16mt + 4g + e][16mt + n], on the diagonal for n = 4g + e.
-            if (ks == mt / 2) {
-                const f32x4 acc = (mt % 2) ? hi : lo;
-                const float dv = e_diag == 0 ? acc[0] : e_diag == 1 ? acc[1] : e_diag == 2 ? acc[2] : acc[3];
-                sDiag[wave][on_diag ? 16 * mt + ln : DK + lane] = dv;
-            }
-        }
-    }
-    // B'_w is read only as the A operand of the state products.  Those accept the
-    // accumulation registers directly, so keep it there: the loop's fp32 vectors
-    // then have the ordinary vector registers to themselves.
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) asm volatile("" : "=a"(hf[mt][ks]) : "0"(hf[mt][ks]));
-    // ---- the sub-chunk's keys as A-fragments: rows of S (kf2), columns of W (kf3)
-    bf16x8 kf2[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kf2[ks] = lds_frag(sK + (16 * wave + ln) * LDK + 32 * ks + 4 * g);
-    // kf3: one 32-long contraction per row tile adds both remaining terms of the
-    // product: its lower half holds the 16 sub-chunk tokens (K_w^T, met by S'),
-    // its upper half diag(lambda) of the tile's rows (met by the tile's own rows
-    // of the vector), so W += K_w^T S' + Lambda vec is one v_mfma_f32_16x16x32_bf16.
-    bf16x8 kf3[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const uint2 kk = *reinterpret_cast<const uint2*>(sKT + (16 * mt + ln) * LDC + 16 * wave + 4 * g);
-        kf3[mt] = __builtin_bit_cast(bf16x8, make_uint4(kk.x, kk.y, 0u, 0u));
-        const float lrow = sLam[16 * mt + ln];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) kf3[mt][4 + e] = (__bf16)(4 * g + e == ln ? lrow : 0.0f);
-    }
-    const f32x4 zero4 = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    const bf16x8 zwb = pack8(zw, zero4);
-
-    // W = A_j vec for this wave's 16 columns (A_j = H_t + Lambda of token j):
-    // W = zs_j (B'_w vec) + K_w^T S' + Lambda vec, the column scale applied to the
-    // state products' accumulators.
-    auto matvec = [&](const f32x4 (&vec)[MT], f32x4 (&w)[MT]) {
-        bf16x8 pb[KS];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) pb[ks] = pack8(vec[2 * ks], vec[2 * ks + 1]);
-        f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) sacc = mfma16(kf2[ks], pb[ks], sacc);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            w[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) w[mt] = mfma16(hf[mt][ks], pb[ks], w[mt]);
-        }
-        const f32x4 sz = sacc * zw;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(kf3[mt], pack8(sz, vec[mt]), zs * w[mt]);
-    };
-
-    // ---- Jacobi start x0 = q / diag(H_t + Lambda),
-    //      diag(H_t) = zs_j diag(B'_w) + sum_{16w <= i <= j} beta_i Z[i][j] k_i^2, diag(B'_w)
-    //      read back from this wave's sDiag rows (written by other lanes of the same wave;
-    //      a wave's LDS accesses complete in order)
-    f32x4 x[MT], r[MT], p[MT], w[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        bf16x8 ksq = kf3[mt];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float v = (float)ksq[e];
-            ksq[e] = (__bf16)(v * v);
-        }
-        const f32x4 dg2 = mfma16(ksq, zwb, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
-        const uint2 qq = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
-        const f32x4 qf{bf16_bits_to_f32(qq.x & 0xffffu), bf16_bits_to_f32(qq.x >> 16),
-                       bf16_bits_to_f32(qq.y & 0xffffu), bf16_bits_to_f32(qq.y >> 16)};
-        const f32x4 d = zs * *reinterpret_cast<const f32x4*>(&sDiag[wave][16 * mt + 4 * g]) + dg2 +
-                        *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x[mt][e] = qf[e] * __builtin_amdgcn_rcpf(d[e]);
-        p[mt] = qf;  // holds q until the first residual is formed
-    }
-    matvec(x, w);
-    float part = 0.0f;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        r[mt] = p[mt] - w[mt];
-        p[mt] = r[mt];
-        part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
-    }
-    float delta = col_sum(part);
-    bool active = delta > 0.0f;
-
-    for (int it = 0; it < a.n_cg; ++it) {
-        if (!__any(active)) break;
-        matvec(p, w);
-        part = 0.0f;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            part += p[mt][0] * w[mt][0] + p[mt][1] * w[mt][1] + p[mt][2] * w[mt][2] + p[mt][3] * w[mt][3];
-        const float pw = col_sum(part);
-        if (!(pw > 0.0f)) active = false;
-        if (active) {
-            const float alpha = delta / pw;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                x[mt] += alpha * p[mt];
-                r[mt] -= alpha * w[mt];
-            }
-        }
-        part = 0.0f;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
-        const float dn = col_sum(part);
-        if (active) {
-            if (dn == 0.0f) {
-                active = false;
-            } else {
-                const float beta_cg = dn / delta;
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) p[mt] = r[mt] + beta_cg * p[mt];
-                delta = dn;
-            }
-        }
-    }
-
-    // ---- read-out o_j = G_c (zeta_j x_j) + sum_i beta_i Z[i][j] v_i (k_i^T x_j)
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // this wave's G_c fragments have landed
-    __syncthreads();
-    if (a.qstar && j < valid) {
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            *reinterpret_cast<f32x4*>(a.qstar + (tok0 + j) * DK + 16 * mt + 4 * g) = x[mt];
-    }
-    const float zeta = sZ0[j];
-    f32x4 zo[4];  // beta_i Z[i][j] over the causal tiles it <= wave
-#pragma unroll
-    for (int it = 0; it < 4; ++it)
+        // ---- decays of this sub-chunk
+        const int jb = 16 * wave - 1;  // token whose state enters the sub-chunk (-1: the chunk's H_c)
+        const float Dw = wave == 0 ? 1.0f : sZ0[jb];
+        // B_w = Dw H_c + sum_{i<16w} beta_i zeta_{16w-1,i} k_i k_i^T.  It is kept as
+        // B'_w = B_w / Dw = H_c + sum_{i<16w} u_i k_i k_i^T (u_i = beta_i / zeta_{c+i,c}, the
+        // staged sKU) and the 1/Dw goes into the column scale: zs_j = zt_j Dw = zeta_{c+j,c}.
+        // When Dw is negligible (<= kMinDecay, e.g. after a zero gate) the state term Dw H_c
+        // is dropped instead: B_w = sum_{i<16w} beta_i zeta_{16w-1,i} k_i k_i^T and zs_j = zt_j.
+        const bool keepH = wave == 0 || Dw > kMinDecay;
+        const float zs = keepH ? sZ0[j] : decay_between_hw(sLg, sZl, jb, j);
+        f32x4 zw;  // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
-            const int i = 16 * it + 4 * g + ii;
-            zo[it][ii] = (it <= wave) ? sBeta[i] * decay_between_hw(sLg, sZl, i, j) : 0.0f;
+            const int i = 16 * wave + 4 * g + ii;
+            zw[ii] = sBeta[i] * decay_between_hw(sLg, sZl, i, j);
         }
-    bf16x8 xb[KS], xz[KS];
+
+        // ---- B'_w as bf16 A-fragments: hf[mt][s] covers rows 16mt.., columns 32s..
+        // Every wave runs the same straight-line code: both 32-token steps of the rank update,
+        // with the tokens i >= 16w zeroed in its A operand (rows 32s + 16h.., independent of mt,
+        // loaded once).  Element e of step u is token 32u + 4g + e (e < 4) or 32u + 16 + 4g + e - 4,
+        // so whole halves are in or out: the lower half of step u iff 32u + 16 <= 16w, the upper
+        // half iff 32u + 32 <= 16w.
+        bf16x8 ka[KS][2][2];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-        xb[ks] = pack8(x[2 * ks], x[2 * ks + 1]);
-        xz[ks] = pack8(zeta * x[2 * ks], zeta * x[2 * ks + 1]);
+        for (int u = 0; u < 2; ++u) {
+            const bool in_lo = 32 * u + 16 <= 16 * wave, in_hi = 32 * u + 32 <= 16 * wave;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh) {
+                    const uint4 raw = __builtin_bit_cast(uint4, lds_frag(sKT + (32 * ks + 16 * hh + ln) * LDC + 32 * u + 4 * g));
+                    ka[ks][hh][u] = __builtin_bit_cast(bf16x8, make_uint4(in_lo ? raw.x : 0u, in_lo ? raw.y : 0u,
+                                                                          in_hi ? raw.z : 0u, in_hi ? raw.w : 0u));
+                }
+        }
+        // Without H_c the weights are per sub-chunk: beta_i zeta_{16w-1,i} on this lane's k-indices.
+        float uw[2][8];
+        if (!keepH) {
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
+                    uw[u][e] = i < 16 * wave ? sBeta[i] * decay_between_hw(sLg, sZl, i, jb) : 0.0f;
+                }
+        }
+        // Identity operands that copy an A-fragment of H_c, read as a B operand, into the two
+        // 16x16 result tiles (rows 32s + {0..15} and 32s + {16..31}) it belongs to; zero when
+        // the state term is dropped.
+        bf16x8 id_lo, id_hi;
+        const float one = keepH ? 1.0f : 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            id_lo[e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
+            id_lo[4 + e] = (__bf16)0.0f;
+            id_hi[e] = (__bf16)0.0f;
+            id_hi[4 + e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
+        }
+        // diag(B'_w) goes to sDiag[wave][r]; lanes off the diagonal write a spare slot instead
+        const int e_diag = ln - 4 * g;
+        const bool on_diag = e_diag >= 0 && e_diag < 4;
+        bf16x8 hf[MT][KS];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            bf16x8 bw[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                if (keepH) {
+                    bw[u] = lds_frag(sKU + (16 * mt + ln) * LDC + 32 * u + 4 * g);
+                } else {
+                    const bf16x8 raw = lds_frag(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) bw[u][e] = (__bf16)((float)raw[e] * uw[u][e]);
+                }
+            }
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                // H_c fragment (mt, ks) straight from LDS, where it is used
+                const bf16x8 hcf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sHf + ((mt * KS + ks) * kWave + lane) * 8));
+                f32x4 lo = mfma16(id_lo, hcf, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+                f32x4 hi = mfma16(id_hi, hcf, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    lo = mfma16(ka[ks][0][u], bw[u], lo);
+                    hi = mfma16(ka[ks][1][u], bw[u], hi);
+                }
+                hf[mt][ks] = pack8(lo, hi);
+                // B'_w is read only as the A operand of the state products.  Those accept the
+                // accumulation registers directly, so it goes there as it is formed: the loop's
+                // fp32 vectors then have the ordinary vector registers to themselves.
+                asm volatile("" : "=a"(hf[mt][ks]) : "0"(hf[mt][ks]));
+                // Tile rows 16mt.. of fragment (mt, mt/2) hold the diagonal block: lane (g, n)
+                // has B'[16mt + 4g + e][16mt + n], on the diagonal for n = 4g + e.
+                if (ks == mt / 2) {
+                    const f32x4 acc = (mt % 2) ? hi : lo;
+                    const float dv = e_diag == 0 ? acc[0] : e_diag == 1 ? acc[1] : e_diag == 2 ? acc[2] : acc[3];
+                    sDiag[wave][on_diag ? 16 * mt + ln : DK + lane] = dv;
+                }
+            }
+        }
+        // ---- the sub-chunk's keys as A-fragments: rows of S (kf2), columns of W (kf3)
+        bf16x8 kf2[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kf2[ks] = lds_frag(sK + (16 * wave + ln) * LDK + 32 * ks + 4 * g);
+        // kf3: one 32-long contraction per row tile adds both remaining terms of the
+        // product: its lower half holds the 16 sub-chunk tokens (K_w^T, met by S'),
+        // its upper half diag(lambda) of the tile's rows (met by the tile's own rows
+        // of the vector), so W += K_w^T S' + Lambda vec is one v_mfma_f32_16x16x32_bf16.
+        bf16x8 kf3[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const uint2 kk = *reinterpret_cast<const uint2*>(sKT + (16 * mt + ln) * LDC + 16 * wave + 4 * g);
+            kf3[mt] = __builtin_bit_cast(bf16x8, make_uint4(kk.x, kk.y, 0u, 0u));
+            const float lrow = sLam[16 * mt + ln];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) kf3[mt][4 + e] = (__bf16)(4 * g + e == ln ? lrow : 0.0f);
+        }
+        const f32x4 zero4 = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        const bf16x8 zwb = pack8(zw, zero4);
+
+        // W = A_j vec for this wave's 16 columns (A_j = H_t + Lambda of token j):
+        // W = zs_j (B'_w vec) + K_w^T S' + Lambda vec, the column scale applied to the
+        // state products' accumulators.
+        auto matvec = [&](const f32x4 (&vec)[MT], f32x4 (&w)[MT]) {
+            bf16x8 pb[KS];
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) pb[ks] = pack8(vec[2 * ks], vec[2 * ks + 1]);
+            f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) sacc = mfma16(kf2[ks], pb[ks], sacc);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                w[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) w[mt] = mfma16(hf[mt][ks], pb[ks], w[mt]);
+            }
+            const f32x4 sz = sacc * zw;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(kf3[mt], pack8(sz, vec[mt]), zs * w[mt]);
+        };
+
+        // ---- Jacobi start x0 = q / diag(H_t + Lambda),
+        //      diag(H_t) = zs_j diag(B'_w) + sum_{16w <= i <= j} beta_i Z[i][j] k_i^2, diag(B'_w)
+        //      read back from this wave's sDiag rows (written by other lanes of the same wave;
+        //      a wave's LDS accesses complete in order)
+        f32x4 x[MT], r[MT], p[MT], w[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            bf16x8 ksq = kf3[mt];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float v = (float)ksq[e];
+                ksq[e] = (__bf16)(v * v);
+            }
+            const f32x4 dg2 = mfma16(ksq, zwb, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+            const uint2 qq = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
+            const f32x4 qf{bf16_bits_to_f32(qq.x & 0xffffu), bf16_bits_to_f32(qq.x >> 16),
+                           bf16_bits_to_f32(qq.y & 0xffffu), bf16_bits_to_f32(qq.y >> 16)};
+            const f32x4 d = zs * *reinterpret_cast<const f32x4*>(&sDiag[wave][16 * mt + 4 * g]) + dg2 +
+                            *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[mt][e] = qf[e] * __builtin_amdgcn_rcpf(d[e]);
+            p[mt] = qf;  // holds q until the first residual is formed
+        }
+        matvec(x, w);
+        float part = 0.0f;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            r[mt] = p[mt] - w[mt];
+            p[mt] = r[mt];
+            part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
+        }
+        float delta = col_sum(part);
+        bool active = delta > 0.0f;
+
+        // ---- every wave is done with sHf, sKT, sKU and sQ: the next chunk's loads may land
+        // there while this chunk's CG runs (the barrier also waits for this wave's memory
+        // operations, so nothing is issued before it)
+        if (more) __syncthreads();
+        // G_c is needed only by the read-out: its loads run under the CG loop (no LDS
+        // access of this chunk's build or Jacobi start is ordered behind them)
+        {
+            const uint16_t* Gf = static_cast<const uint16_t*>(a.Gs) + int64_t(cc) * DV * DK;
+#pragma unroll
+            for (int u = 0; u < NGF; ++u) {
+                const int f = wave * NGF + u;
+                load_lds16(Gf + (f * kWave + lane) * 8, sGf + f * kWave * 8);
+            }
+        }
+        float g_nx = 1.0f, b_nx = 0.0f, lam_nx = 0.0f;
+        int pieces = 0;  // pieces of the next chunk's loads issued so far
+
+        for (int it = 0; it < a.n_cg; ++it) {
+            if (!__any(active)) break;
+            if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
+            matvec(p, w);
+            part = 0.0f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                part += p[mt][0] * w[mt][0] + p[mt][1] * w[mt][1] + p[mt][2] * w[mt][2] + p[mt][3] * w[mt][3];
+            const float pw = col_sum(part);
+            if (!(pw > 0.0f)) active = false;
+            if (active) {
+                const float alpha = delta / pw;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    x[mt] += alpha * p[mt];
+                    r[mt] -= alpha * w[mt];
+                }
+            }
+            part = 0.0f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
+            const float dn = col_sum(part);
+            if (active) {
+                if (dn == 0.0f) {
+                    active = false;
+                } else {
+                    const float beta_cg = dn / delta;
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) p[mt] = r[mt] + beta_cg * p[mt];
+                    delta = dn;
+                }
+            }
+        }
+
+        if (more)
+            while (pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
+
+        // ---- read-out o_j = G_c (zeta_j x_j) + sum_i beta_i Z[i][j] v_i (k_i^T x_j)
+        // this wave's G_c fragments (and the next chunk's loads) have landed; the barrier
+        // publishes G_c to every wave
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        if (a.qstar && j < valid) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                *reinterpret_cast<f32x4*>(a.qstar + (tok0 + j) * DK + 16 * mt + 4 * g) = x[mt];
+        }
+        const float zeta = sZ0[j];
+        f32x4 zo[4];  // beta_i Z[i][j] over the causal tiles it <= wave
+#pragma unroll
+        for (int it = 0; it < 4; ++it)
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) {
+                const int i = 16 * it + 4 * g + ii;
+                zo[it][ii] = (it <= wave) ? sBeta[i] * decay_between_hw(sLg, sZl, i, j) : 0.0f;
+            }
+        bf16x8 xb[KS], xz[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            xb[ks] = pack8(x[2 * ks], x[2 * ks + 1]);
+            xz[ks] = pack8(zeta * x[2 * ks], zeta * x[2 * ks + 1]);
+        }
+        // every wave runs all four token tiles (zo is zero past the causal ones)
+        f32x4 sacc[4];
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+            sacc[it] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                sacc[it] = mfma16(lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g), xb[ks], sacc[it]);
+        }
+        f32x4 o[MTV];
+#pragma unroll
+        for (int mt = 0; mt < MTV; ++mt) {
+            o[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                o[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sGf + ((mt * KS + ks) * kWave + lane) * 8)),
+                               xz[ks], o[mt]);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const bf16x8 sb = pack8(sacc[2 * u] * zo[2 * u], sacc[2 * u + 1] * zo[2 * u + 1]);
+#pragma unroll
+            for (int mt = 0; mt < MTV; ++mt)
+                o[mt] = mfma16(lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, o[mt]);
+        }
+
+        if (j < valid) {
+#pragma unroll
+            for (int mt = 0; mt < MTV; ++mt)
+                *reinterpret_cast<f32x4*>(a.out + (tok0 + j) * DV + 16 * mt + 4 * g) = o[mt];
+        }
+
+        if (!more) break;
+        cc = cn;
+        g_cur = g_nx;
+        b_cur = b_nx;
+        lam_cur = lam_nx;
     }
-    // every wave runs all four token tiles (zo is zero past the causal ones)
-    f32x4 sacc[4];
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-        sacc[it] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            sacc[it] = mfma16(lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g), xb[ks], sacc[it]);
-    }
-    f32x4 o[MTV];
-#pragma unroll
-    for (int mt = 0; mt < MTV; ++mt) {
-        o[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            o[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sGf + ((mt * KS + ks) * kWave + lane) * 8)),
-                           xz[ks], o[mt]);
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const bf16x8 sb = pack8(sacc[2 * u] * zo[2 * u], sacc[2 * u + 1] * zo[2 * u + 1]);
-#pragma unroll
-        for (int mt = 0; mt < MTV; ++mt)
-            o[mt] = mfma16(lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, o[mt]);
-    }
-    if (j < valid) {
-#pragma unroll
-        for (int mt = 0; mt < MTV; ++mt)
-            *reinterpret_cast<f32x4*>(a.out + (tok0 + j) * DV + 16 * mt + 4 * g) = o[mt];
-    }
+}
+
+// Compute units of the current device (one workgroup of the kernel fills a CU's LDS).
+int device_cus()
+{
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 1;
+    if (dev < 64 && cached[dev] > 0) return cached[dev];
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 1;
+    if (dev < 64) cached[dev] = n;
+    return n;
 }
 
 template <int DK, int DV>
 hipError_t launch_shape(const CgArgs& a, hipStream_t stream)
 {
-    const unsigned blocks = unsigned(a.s.batch * a.s.heads * a.s.n_chunks);
-    hipLaunchKernelGGL((chunk_cg_bf16_kernel<DK, DV>), dim3(blocks), dim3(kThreads), 0, stream, a);
+    const int64_t total = a.s.batch * a.s.heads * a.s.n_chunks;
+    if (total <= 0) return hipSuccess;
+    if (total > INT32_MAX) return hipErrorInvalidValue;
+    const int64_t cus = device_cus();
+    const unsigned blocks = unsigned(total < cus ? total : cus);
+    hipLaunchKernelGGL((chunk_cg_bf16_kernel<DK, DV>), dim3(blocks), dim3(kThreads), 0, stream, a, int(total));
     return hipGetLastError();
 }
 
