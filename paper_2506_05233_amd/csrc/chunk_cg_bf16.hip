@@ -65,6 +65,19 @@ __device__ __forceinline__ float decay_between_hw(const float* lg, const int* zl
 }
 
 
+// beta_i prod_{s=i+1..j} gamma_s for the four tokens i = i4 .. i4+3 (i4 a multiple
+// of 4) and token j, from the chunk's gate log-cumsums and strengths: 0 for i > j or
+// when a zero gate lies in (i, j] (zl_j > i).  lgj = lg[j], zlj = zl[j].
+__device__ __forceinline__ f32x4 decay_weights4(const float* lg, const float* beta, float lgj, int zlj, int i4, int j)
+{
+    const f32x4 lgi = *reinterpret_cast<const f32x4*>(lg + i4);
+    const f32x4 bi = *reinterpret_cast<const f32x4*>(beta + i4);
+    f32x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = (i4 + e <= j && zlj <= i4 + e) ? bi[e] * __expf(lgj - lgi[e]) : 0.0f;
+    return r;
+}
+
 // v if c, else zero (per component, so the operands stay in registers)
 __device__ __forceinline__ uint4 keep_if(bool c, const uint4& v)
 {
@@ -321,12 +334,10 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         // is dropped instead: B_w = sum_{i<16w} beta_i zeta_{16w-1,i} k_i k_i^T and zs_j = zt_j.
         const bool keepH = wave == 0 || Dw > kMinDecay;
         const float zs = keepH ? sZ0[j] : decay_between_hw(sLg, sZl, jb, j);
-        f32x4 zw;  // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
-#pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-            const int i = 16 * wave + 4 * g + ii;
-            zw[ii] = sBeta[i] * decay_between_hw(sLg, sZl, i, j);
-        }
+        const float lgj = sLg[j];
+        const int zlj = sZl[j];
+        // beta_i Z[i][j] for the sub-chunk rows i = 16w + 4g + ii met in S
+        const f32x4 zw = decay_weights4(sLg, sBeta, lgj, zlj, 16 * wave + 4 * g, j);
 
         // ---- B'_w as bf16 A-fragments: hf[mt][s] covers rows 16mt.., columns 32s..
         // Every wave runs the same straight-line code: both 32-token steps of the rank update,
@@ -348,15 +359,15 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
                 }
         }
         // Without H_c the weights are per sub-chunk: beta_i zeta_{16w-1,i} on this lane's k-indices.
-        float uw[2][8];
-        if (!keepH) {
+        // (tokens i > jb, i.e. i >= 16w, get 0)
+        f32x4 uw[2][2];
+        if (!keepH) {  // never for wave 0, so jb >= 0
+            const float lgb = sLg[jb];
+            const int zlb = sZl[jb];
 #pragma unroll
             for (int u = 0; u < 2; ++u)
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int i = 32 * u + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
-                    uw[u][e] = i < 16 * wave ? sBeta[i] * decay_between_hw(sLg, sZl, i, jb) : 0.0f;
-                }
+                for (int hh = 0; hh < 2; ++hh) uw[u][hh] = decay_weights4(sLg, sBeta, lgb, zlb, 32 * u + 16 * hh + 4 * g, jb);
         }
         // Identity operands that copy an A-fragment of H_c, read as a B operand, into the two
         // 16x16 result tiles (rows 32s + {0..15} and 32s + {16..31}) it belongs to; zero when
@@ -374,25 +385,32 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         const int e_diag = ln - 4 * g;
         const bool on_diag = e_diag >= 0 && e_diag < 4;
         bf16x8 hf[MT][KS];
+        // operands of row tile mt: H_c fragments (mt, 0..KS-1) and the scaled keys; the
+        // next tile's are read from LDS while this tile's products run
+        auto load_tile = [&](int mt, bf16x8 (&hcs)[KS], bf16x8 (&bw)[2]) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                hcs[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sHf + ((mt * KS + ks) * kWave + lane) * 8));
+#pragma unroll
+            for (int u = 0; u < 2; ++u) bw[u] = lds_frag((keepH ? sKU : sKT) + (16 * mt + ln) * LDC + 32 * u + 4 * g);
+        };
+        bf16x8 hcA[KS], hcB[KS], bwA[2], bwB[2];
+        load_tile(0, hcA, bwA);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            bf16x8 bw[2];
+            bf16x8 (&hcs)[KS] = (mt % 2) ? hcB : hcA;
+            bf16x8 (&bw)[2] = (mt % 2) ? bwB : bwA;
+            if (mt + 1 < MT) load_tile(mt + 1, (mt % 2) ? hcA : hcB, (mt % 2) ? bwA : bwB);
+            if (!keepH) {
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                if (keepH) {
-                    bw[u] = lds_frag(sKU + (16 * mt + ln) * LDC + 32 * u + 4 * g);
-                } else {
-                    const bf16x8 raw = lds_frag(sKT + (16 * mt + ln) * LDC + 32 * u + 4 * g);
+                for (int u = 0; u < 2; ++u)
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) bw[u][e] = (__bf16)((float)raw[e] * uw[u][e]);
-                }
+                    for (int e = 0; e < 8; ++e) bw[u][e] = (__bf16)((float)bw[u][e] * uw[u][e / 4][e % 4]);
             }
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                // H_c fragment (mt, ks) straight from LDS, where it is used
-                const bf16x8 hcf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sHf + ((mt * KS + ks) * kWave + lane) * 8));
-                f32x4 lo = mfma16(id_lo, hcf, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
-                f32x4 hi = mfma16(id_hi, hcf, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+                f32x4 lo = mfma16(id_lo, hcs[ks], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+                f32x4 hi = mfma16(id_hi, hcs[ks], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
 #pragma unroll
                 for (int u = 0; u < 2; ++u) {
                     lo = mfma16(ka[ks][0][u], bw[u], lo);
@@ -401,8 +419,9 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
                 hf[mt][ks] = pack8(lo, hi);
                 // B'_w is read only as the A operand of the state products.  Those accept the
                 // accumulation registers directly, so it goes there as it is formed: the loop's
-                // fp32 vectors then have the ordinary vector registers to themselves.
-                asm volatile("" : "=a"(hf[mt][ks]) : "0"(hf[mt][ks]));
+                // fp32 vectors then have the ordinary vector registers to themselves.  (Not
+                // volatile: the move is not a scheduling barrier.)
+                asm("" : "=a"(hf[mt][ks]) : "0"(hf[mt][ks]));
                 // Tile rows 16mt.. of fragment (mt, mt/2) hold the diagonal block: lane (g, n)
                 // has B'[16mt + 4g + e][16mt + n], on the diagonal for n = 4g + e.
                 if (ks == mt / 2) {
@@ -553,14 +572,9 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
                 *reinterpret_cast<f32x4*>(a.qstar + (tok0 + j) * DK + 16 * mt + 4 * g) = x[mt];
         }
         const float zeta = sZ0[j];
-        f32x4 zo[4];  // beta_i Z[i][j] over the causal tiles it <= wave
+        f32x4 zo[4];  // beta_i Z[i][j] over the four token tiles (0 past the causal ones)
 #pragma unroll
-        for (int it = 0; it < 4; ++it)
-#pragma unroll
-            for (int ii = 0; ii < 4; ++ii) {
-                const int i = 16 * it + 4 * g + ii;
-                zo[it][ii] = (it <= wave) ? sBeta[i] * decay_between_hw(sLg, sZl, i, j) : 0.0f;
-            }
+        for (int it = 0; it < 4; ++it) zo[it] = decay_weights4(sLg, sBeta, lgj, zlj, 16 * it + 4 * g, j);
         bf16x8 xb[KS], xz[KS];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
