@@ -10,6 +10,8 @@
 // chunk with coalesced stores.  The tile stays in registers between chunks.
 // HBM traffic per token-head: the states, 4 (d_k + d_v) d_k / C bytes, plus the
 // chunk's k and v, read once per tile.
+#include <type_traits>
+
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
 #include "mesa_mfma.hpp"
@@ -410,6 +412,214 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
     }
 }
 
+// Wide variant (bf16 k and v, chunk 64, d_k and d_v in {64, 128}), used for the
+// bf16 fragment chunk states and for the states-only call.  One workgroup owns a
+// whole part of the state of one (batch, head) sequence -- part 0 is H (d_k x d_k),
+// part 1 is G^T (d_k x d_v), both as [key feature R][column c] -- in registers,
+// and walks its chunks in order:
+//
+//   X_{next} = D X + K^T (w ⊙ Y),   Y = K (part 0) or V (part 1), w_i = beta_i zeta_{end,i},
+//
+// with w ⊙ Y split into bf16 high and low parts (two products, ~16-bit weights).
+// Wave w owns key rows 32 (w % NS) .. +31 (NS = d_k / 32) and a 1/CS share of the
+// columns (CS = 4 / NS); its 16x16 result tiles pair up into complete bf16
+// A-fragments of the fragment layout (rows 32s.. of X^T are fragment row block s),
+// so every chunk state is written with whole 1-KiB wave stores.  Staging is
+// double-buffered in LDS (one barrier per chunk) and the inputs of chunk n + 2 are
+// loaded while chunk n is consumed.
+template <int DK, int DV>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void chunk_state_wide_kernel(StateArgs a)
+{
+    constexpr int C = 64;
+    constexpr int LDT = C + 8;           // row stride of the [feature][token] tiles
+    constexpr int NS = DK / 32;          // 32-row blocks of the key features
+    constexpr int CS = kThreads / kWave / NS;  // column shares per row block
+    const ForwardShape s = a.s;
+    const int blk = xcd_major_block(blockIdx.x, gridDim.x);  // H and G^T of one sequence share an L2
+    const int part = blk % 2;
+    const int64_t bh = blk / 2;
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int lane = tid % kWave;
+    const int g = lane / 16, ln = lane % 16;
+    const int p = tid % 32, fg = tid / 32;  // staging: tokens 2p, 2p+1, 8 features of group fg
+
+    __shared__ __attribute__((aligned(16))) uint16_t sA[2][DK * LDT];                           // k_i[R], [R][i]
+    __shared__ __attribute__((aligned(16))) uint16_t sBh[2][(DK > DV ? DK : DV) * LDT];         // hi(w_i y_i[c]), [c][i]
+    __shared__ __attribute__((aligned(16))) uint16_t sBl[2][(DK > DV ? DK : DV) * LDT];         // lo(w_i y_i[c])
+
+    auto run = [&](auto nc_tag) {
+        constexpr int NC = decltype(nc_tag)::value;  // columns of this part
+        constexpr int NCT = NC / 16 / CS;            // 16-column tiles of this wave
+        constexpr int NKQ = DK / 64, NY = NC / 64;   // staging passes (64 features each)
+        const int sblk = wave % NS, cs = wave / NS;
+        const int ct0 = cs * NCT;
+        const uint16_t* kp = static_cast<const uint16_t*>(a.k);
+        const uint16_t* yp = static_cast<const uint16_t*>(part ? a.v : a.k);
+
+        struct Regs {
+            uint4 k[NKQ][2];  // k of tokens 2p, 2p+1, features 64m + 8fg ..
+            uint4 y[NY][2];   // y of the same tokens (v; unused for H, whose y is k)
+            float gam, bet;
+            int valid;
+        };
+        auto load = [&](int n, Regs& R) {
+            const int64_t t0 = int64_t(n) * C;
+            const int valid = int(min<int64_t>(C, s.seq_len - t0));
+            const int64_t tok0 = bh * s.seq_len + t0;
+            R.valid = valid;
+            const int lt = min(lane, valid - 1);
+            R.gam = a.gamma[tok0 + lt];
+            R.bet = a.beta[tok0 + lt];
+            const int64_t r0 = tok0 + min(2 * p, valid - 1), r1 = tok0 + min(2 * p + 1, valid - 1);
+#pragma unroll
+            for (int m = 0; m < NKQ; ++m) {
+                R.k[m][0] = *reinterpret_cast<const uint4*>(kp + r0 * DK + 64 * m + 8 * fg);
+                R.k[m][1] = *reinterpret_cast<const uint4*>(kp + r1 * DK + 64 * m + 8 * fg);
+            }
+            if (part) {
+#pragma unroll
+                for (int m = 0; m < NY; ++m) {
+                    R.y[m][0] = *reinterpret_cast<const uint4*>(yp + r0 * DV + 64 * m + 8 * fg);
+                    R.y[m][1] = *reinterpret_cast<const uint4*>(yp + r1 * DV + 64 * m + 8 * fg);
+                }
+            }
+        };
+        // gate scan of a chunk and its staging into buffer b; returns the chunk decay D
+        auto stage = [&](const Regs& R, int b) -> float {
+            const bool live = lane < R.valid;
+            const float gl = live ? R.gam : 1.0f;
+            const float lg = wave_scan_add(gl > 0.0f ? logf(gl) : 0.0f);
+            const int zl = wave_scan_max((live && !(gl > 0.0f)) ? lane : -1);
+            const float lgE = lane_value(lg, C - 1);
+            const int zlE = lane_value(zl, C - 1);
+            const float wl = live ? R.bet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
+            const float w0 = __shfl(wl, 2 * p), w1 = __shfl(wl, 2 * p + 1);
+            const bool k0 = 2 * p < R.valid, k1 = 2 * p + 1 < R.valid;
+#pragma unroll
+            for (int m = 0; m < NKQ; ++m) {
+                const uint4 ka = k0 ? R.k[m][0] : make_uint4(0, 0, 0, 0);
+                const uint4 kb = k1 ? R.k[m][1] : make_uint4(0, 0, 0, 0);
+                stage_token_pair(reinterpret_cast<uint32_t*>(sA[b]), LDT / 2, 64 * m + 8 * fg, p, ka, kb);
+            }
+#pragma unroll
+            for (int m = 0; m < NY; ++m) {
+                const uint4 ya = part ? R.y[m][0] : R.k[m][0];
+                const uint4 yb = part ? R.y[m][1] : R.k[m][1];
+                const uint32_t a4[4] = {ya.x, ya.y, ya.z, ya.w};
+                const uint32_t b4[4] = {yb.x, yb.y, yb.z, yb.w};
+                uint32_t* hi32 = reinterpret_cast<uint32_t*>(sBh[b]);
+                uint32_t* lo32 = reinterpret_cast<uint32_t*>(sBl[b]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const uint32_t ba = (q & 1) ? (a4[q / 2] >> 16) : (a4[q / 2] & 0xffffu);
+                    const uint32_t bb = (q & 1) ? (b4[q / 2] >> 16) : (b4[q / 2] & 0xffffu);
+                    const float va = w0 * bf16_bits_to_f32(ba), vb = w1 * bf16_bits_to_f32(bb);
+                    const __bf16 ha = (__bf16)va, hb = (__bf16)vb;
+                    const __bf16 la = (__bf16)(va - (float)ha), lb = (__bf16)(vb - (float)hb);
+                    const int c = 64 * m + 8 * fg + q;
+                    hi32[c * (LDT / 2) + p] = uint32_t(bf16_bits(ha)) | (uint32_t(bf16_bits(hb)) << 16);
+                    lo32[c * (LDT / 2) + p] = uint32_t(bf16_bits(la)) | (uint32_t(bf16_bits(lb)) << 16);
+                }
+            }
+            return zlE >= 0 ? 0.0f : expf(lgE);
+        };
+
+        f32x4 acc[2][NCT];
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) acc[rt][ct] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        const bool frag_out = a.store_chunks && a.frag;
+        uint16_t* frag_base = static_cast<uint16_t*>(part ? a.Gs : a.Hs);
+        constexpr int kStateElems = NC * DK;  // bf16 per chunk state of this part
+
+        // chunk n: its state is stored, then acc = D acc + K^T (w ⊙ Y) from buffer n % 2;
+        // chunk n + 1 is staged (from Rn1) into the other buffer and chunk n + 2 loaded
+        auto consume = [&](int n, float D, Regs& Rn1, Regs& Rfree, float& Dnext) {
+            if (frag_out) {
+                uint16_t* base = frag_base + (bh * s.n_chunks + n) * int64_t(kStateElems);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    uint4 pk;
+                    pk.x = uint32_t(bf16_bits((__bf16)acc[0][ct][0])) | (uint32_t(bf16_bits((__bf16)acc[0][ct][1])) << 16);
+                    pk.y = uint32_t(bf16_bits((__bf16)acc[0][ct][2])) | (uint32_t(bf16_bits((__bf16)acc[0][ct][3])) << 16);
+                    pk.z = uint32_t(bf16_bits((__bf16)acc[1][ct][0])) | (uint32_t(bf16_bits((__bf16)acc[1][ct][1])) << 16);
+                    pk.w = uint32_t(bf16_bits((__bf16)acc[1][ct][2])) | (uint32_t(bf16_bits((__bf16)acc[1][ct][3])) << 16);
+                    *reinterpret_cast<uint4*>(base + (((ct0 + ct) * NS + sblk) * kWave + lane) * 8) = pk;
+                }
+            }
+            const int b = n % 2;
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) acc[rt][ct] *= D;
+#pragma unroll
+            for (int u = 0; u < C / 32; ++u) {
+                bf16x8 af[2];
+#pragma unroll
+                for (int rt = 0; rt < 2; ++rt) af[rt] = lds_frag(sA[b] + (32 * sblk + 16 * rt + ln) * LDT + 32 * u + 4 * g);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const int c = 16 * (ct0 + ct) + ln;
+                    const bf16x8 bh_ = lds_frag(sBh[b] + c * LDT + 32 * u + 4 * g);
+                    const bf16x8 bl_ = lds_frag(sBl[b] + c * LDT + 32 * u + 4 * g);
+#pragma unroll
+                    for (int rt = 0; rt < 2; ++rt) {
+                        acc[rt][ct] = mfma16(af[rt], bh_, acc[rt][ct]);
+                        acc[rt][ct] = mfma16(af[rt], bl_, acc[rt][ct]);
+                    }
+                }
+            }
+            if (n + 1 < s.n_chunks) Dnext = stage(Rn1, (n + 1) % 2);
+            if (n + 2 < s.n_chunks) load(n + 2, Rfree);
+            __syncthreads();
+        };
+
+        Regs R0, R1;
+        load(0, R0);
+        if (s.n_chunks > 1) load(1, R1);
+        float D0 = stage(R0, 0), D1 = 1.0f;
+        __syncthreads();
+        for (int n = 0; n < s.n_chunks; n += 2) {
+            consume(n, D0, R1, R0, D1);       // stages chunk n+1 (R1), loads n+2 into R0
+            if (n + 1 < s.n_chunks) consume(n + 1, D1, R0, R1, D0);  // stages n+2 (R0), loads n+3 into R1
+        }
+        // final states, fp32: tile value (R, c) is H[R][c] or G[c][R]
+        float* fin = part ? a.final_G : a.final_H;
+        if (fin) {
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) {
+                const int R = 32 * sblk + 16 * rt + 4 * g;
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const int c = 16 * (ct0 + ct) + ln;
+#pragma unroll
+                    for (int ii = 0; ii < 4; ++ii) {
+                        if (part)
+                            fin[(bh * DV + c) * int64_t(DK) + R + ii] = acc[rt][ct][ii];
+                        else
+                            fin[(bh * DK + R + ii) * int64_t(DK) + c] = acc[rt][ct][ii];
+                    }
+                }
+            }
+        }
+    };
+    if (part == 0)
+        run(std::integral_constant<int, DK>{});
+    else
+        run(std::integral_constant<int, DV>{});
+}
+
+template <int DK, int DV>
+hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
+{
+    const unsigned blocks = unsigned(a.s.batch * a.s.heads * 2);
+    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV>), dim3(blocks), dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
 __global__ __launch_bounds__(kThreads) void fill_zero_kernel(float* dst, int64_t n)
 {
     const int64_t stride = int64_t(gridDim.x) * kThreads;
@@ -435,11 +645,10 @@ bool chunk_state_frag_supported(const ForwardShape& s)
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream)
 {
     const int64_t bh = a.s.batch * a.s.heads;
-    if (a.frag) {
-        if (!chunk_state_frag_supported(a.s)) return hipErrorInvalidValue;
-        const unsigned blocks = unsigned(bh * (a.s.d_k / 64) * ((a.s.d_k + a.s.d_v) / 32));
-        hipLaunchKernelGGL(chunk_state_frag_kernel, dim3(blocks), dim3(kThreads), 0, stream, a);
-        return hipGetLastError();
+    if (a.frag && !chunk_state_frag_supported(a.s)) return hipErrorInvalidValue;
+    if (chunk_state_frag_supported(a.s) && (a.frag || !a.store_chunks)) {
+        if (a.s.d_k == 64) return a.s.d_v == 64 ? launch_wide<64, 64>(a, stream) : launch_wide<64, 128>(a, stream);
+        return a.s.d_v == 64 ? launch_wide<128, 64>(a, stream) : launch_wide<128, 128>(a, stream);
     }
     if (a.s.bf16 && a.s.chunk == 64) {
         const unsigned blocks = unsigned(bh * ((a.s.d_k + a.s.d_v) / 64) * (a.s.d_k / 32));
