@@ -49,11 +49,12 @@ def cg_kernel_flops(B, H, T, dk, dv, C, n_cg):
     return B * H * T * per_th
 
 
-def state_kernel_bytes(B, H, T, dk, dv, C, in_bytes):
-    """Algorithmic HBM bytes of the chunk-state launch: the fp32 states entering
-    every chunk written once, plus k and v read once (gates ignored)."""
+def state_kernel_bytes(B, H, T, dk, dv, C, in_bytes, state_bytes):
+    """Algorithmic HBM bytes of the chunk-state launch: the states entering every
+    chunk written once (state_bytes per element: 2 for the bf16 fragments of the
+    bf16 path, 4 for fp32 states), plus k and v read once (gates ignored)."""
     nc = (T + C - 1) // C
-    return B * H * nc * dk * (dk + dv) * 4 + B * H * T * (dk + dv) * in_bytes
+    return B * H * nc * dk * (dk + dv) * state_bytes + B * H * T * (dk + dv) * in_bytes
 
 
 def traffic_entry(kernel_src_hash):
@@ -114,10 +115,12 @@ def run_forward(args, torch, L, W):
     if not bool(torch.isfinite(out).all()):
         raise RuntimeError("non-finite output")
     B, H, T, dk, dv = w.batch, w.heads, w.seq_len, w.d_k, w.d_v
+    bf16_states = args.precision == L.MESA_PREC_BF16 or (
+        args.precision == L.MESA_PREC_AUTO and L.bf16_path_available(dk, dv, w.chunk, T))
     return {
         "w": w, "wall": wall, "state_ms": state_ms, "cg_ms": cg_ms,
         "flops": cg_kernel_flops(B, H, T, dk, dv, w.chunk, w.n_cg),
-        "state_bytes": state_kernel_bytes(B, H, T, dk, dv, w.chunk, 2),
+        "state_bytes": state_kernel_bytes(B, H, T, dk, dv, w.chunk, 2, 2 if bf16_states else 4),
         "x": x,
     }
 

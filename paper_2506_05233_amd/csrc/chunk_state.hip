@@ -421,20 +421,22 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
 //   X_{next} = D X + K^T (w ⊙ Y),   Y = K (part 0) or V (part 1), w_i = beta_i zeta_{end,i},
 //
 // with w ⊙ Y split into bf16 high and low parts (two products, ~16-bit weights).
-// Wave w owns key rows 32 (w % NS) .. +31 (NS = d_k / 32) and a 1/CS share of the
-// columns (CS = 4 / NS); its 16x16 result tiles pair up into complete bf16
+// Eight waves (two per SIMD, so one hides the other's latencies); wave w owns key
+// rows 32 (w % NS) .. +31 (NS = d_k / 32) and a 1/CS share of the columns (CS = 8 / NS); its 16x16 result tiles pair up into complete bf16
 // A-fragments of the fragment layout (rows 32s.. of X^T are fragment row block s),
 // so every chunk state is written with whole 1-KiB wave stores.  Staging is
 // double-buffered in LDS (one barrier per chunk) and the inputs of chunk n + 2 are
 // loaded while chunk n is consumed.
+constexpr int kWideThreads = 512;  // eight waves: two per SIMD
+
 template <int DK, int DV>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void chunk_state_wide_kernel(StateArgs a)
+__global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArgs a)
 {
     constexpr int C = 64;
     constexpr int LDT = C + 8;           // row stride of the [feature][token] tiles
     constexpr int NS = DK / 32;          // 32-row blocks of the key features
-    constexpr int CS = kThreads / kWave / NS;  // column shares per row block
+    constexpr int CS = kWideThreads / kWave / NS;  // column shares per row block
+    constexpr int FPP = 8 * kWideThreads / 32;     // features staged per pass (8 per thread group)
     const ForwardShape s = a.s;
     const int blk = xcd_major_block(blockIdx.x, gridDim.x);  // H and G^T of one sequence share an L2
     const int part = blk % 2;
@@ -443,7 +445,7 @@ void chunk_state_wide_kernel(StateArgs a)
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int lane = tid % kWave;
     const int g = lane / 16, ln = lane % 16;
-    const int p = tid % 32, fg = tid / 32;  // staging: tokens 2p, 2p+1, 8 features of group fg
+    const int p = tid % 32, fg = tid / 32;  // staging: tokens 2p, 2p+1, features 8 fg + FPP m ..
 
     __shared__ __attribute__((aligned(16))) uint16_t sA[2][DK * LDT];                           // k_i[R], [R][i]
     __shared__ __attribute__((aligned(16))) uint16_t sBh[2][(DK > DV ? DK : DV) * LDT];         // hi(w_i y_i[c]), [c][i]
@@ -452,7 +454,7 @@ void chunk_state_wide_kernel(StateArgs a)
     auto run = [&](auto nc_tag) {
         constexpr int NC = decltype(nc_tag)::value;  // columns of this part
         constexpr int NCT = NC / 16 / CS;            // 16-column tiles of this wave
-        constexpr int NKQ = DK / 64, NY = NC / 64;   // staging passes (64 features each)
+        constexpr int NKQ = (DK + FPP - 1) / FPP, NY = (NC + FPP - 1) / FPP;  // staging passes
         const int sblk = wave % NS, cs = wave / NS;
         const int ct0 = cs * NCT;
         const uint16_t* kp = static_cast<const uint16_t*>(a.k);
@@ -473,16 +475,19 @@ void chunk_state_wide_kernel(StateArgs a)
             R.gam = a.gamma[tok0 + lt];
             R.bet = a.beta[tok0 + lt];
             const int64_t r0 = tok0 + min(2 * p, valid - 1), r1 = tok0 + min(2 * p + 1, valid - 1);
+            // feature offsets beyond the row wrap into it (those threads stage nothing)
 #pragma unroll
             for (int m = 0; m < NKQ; ++m) {
-                R.k[m][0] = *reinterpret_cast<const uint4*>(kp + r0 * DK + 64 * m + 8 * fg);
-                R.k[m][1] = *reinterpret_cast<const uint4*>(kp + r1 * DK + 64 * m + 8 * fg);
+                const int f0 = (FPP * m + 8 * fg) % DK;
+                R.k[m][0] = *reinterpret_cast<const uint4*>(kp + r0 * DK + f0);
+                R.k[m][1] = *reinterpret_cast<const uint4*>(kp + r1 * DK + f0);
             }
             if (part) {
 #pragma unroll
                 for (int m = 0; m < NY; ++m) {
-                    R.y[m][0] = *reinterpret_cast<const uint4*>(yp + r0 * DV + 64 * m + 8 * fg);
-                    R.y[m][1] = *reinterpret_cast<const uint4*>(yp + r1 * DV + 64 * m + 8 * fg);
+                    const int f0 = (FPP * m + 8 * fg) % NC;
+                    R.y[m][0] = *reinterpret_cast<const uint4*>(yp + r0 * DV + f0);
+                    R.y[m][1] = *reinterpret_cast<const uint4*>(yp + r1 * DV + f0);
                 }
             }
         };
@@ -499,12 +504,14 @@ void chunk_state_wide_kernel(StateArgs a)
             const bool k0 = 2 * p < R.valid, k1 = 2 * p + 1 < R.valid;
 #pragma unroll
             for (int m = 0; m < NKQ; ++m) {
+                if (FPP * m + 8 * fg >= DK) continue;
                 const uint4 ka = k0 ? R.k[m][0] : make_uint4(0, 0, 0, 0);
                 const uint4 kb = k1 ? R.k[m][1] : make_uint4(0, 0, 0, 0);
-                stage_token_pair(reinterpret_cast<uint32_t*>(sA[b]), LDT / 2, 64 * m + 8 * fg, p, ka, kb);
+                stage_token_pair(reinterpret_cast<uint32_t*>(sA[b]), LDT / 2, FPP * m + 8 * fg, p, ka, kb);
             }
 #pragma unroll
             for (int m = 0; m < NY; ++m) {
+                if (FPP * m + 8 * fg >= NC) continue;
                 const uint4 ya = part ? R.y[m][0] : R.k[m][0];
                 const uint4 yb = part ? R.y[m][1] : R.k[m][1];
                 const uint32_t a4[4] = {ya.x, ya.y, ya.z, ya.w};
@@ -518,7 +525,7 @@ void chunk_state_wide_kernel(StateArgs a)
                     const float va = w0 * bf16_bits_to_f32(ba), vb = w1 * bf16_bits_to_f32(bb);
                     const __bf16 ha = (__bf16)va, hb = (__bf16)vb;
                     const __bf16 la = (__bf16)(va - (float)ha), lb = (__bf16)(vb - (float)hb);
-                    const int c = 64 * m + 8 * fg + q;
+                    const int c = FPP * m + 8 * fg + q;
                     hi32[c * (LDT / 2) + p] = uint32_t(bf16_bits(ha)) | (uint32_t(bf16_bits(hb)) << 16);
                     lo32[c * (LDT / 2) + p] = uint32_t(bf16_bits(la)) | (uint32_t(bf16_bits(lb)) << 16);
                 }
@@ -616,7 +623,7 @@ template <int DK, int DV>
 hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
 {
     const unsigned blocks = unsigned(a.s.batch * a.s.heads * 2);
-    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV>), dim3(blocks), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV>), dim3(blocks), dim3(kWideThreads), 0, stream, a);
     return hipGetLastError();
 }
 
