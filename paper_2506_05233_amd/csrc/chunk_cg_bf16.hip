@@ -88,6 +88,9 @@ __device__ __forceinline__ uint4 keep_if(bool c, const uint4& v)
 // their reciprocal (see the sub-chunk states below).
 constexpr float kMinDecay = 1e-20f;
 
+// Smallest normal fp32 number (2^-126): CG scalars below it stop a column (see the loop).
+constexpr float kMinNormal = 1.17549435e-38f;
+
 // 8 bf16 (bits in v) times u, rounded back to bf16.
 __device__ __forceinline__ uint4 scale_bf16x8(const uint4& v, float u)
 {
@@ -449,62 +452,90 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
             for (int e = 0; e < 4; ++e) kf3[mt][4 + e] = (__bf16)(4 * g + e == ln ? lrow : 0.0f);
         }
         const f32x4 zero4 = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        const bf16x8 zwb = pack8(zw, zero4);
+        int qsh = 0;  // log2 of the power-of-two scale of q_j (below)
 
-        // W = A_j vec for this wave's 16 columns (A_j = H_t + Lambda of token j):
-        // W = zs_j (B'_w vec) + K_w^T S' + Lambda vec, the column scale applied to the
-        // state products' accumulators.
-        auto matvec = [&](const f32x4 (&vec)[MT], f32x4 (&w)[MT]) {
-            bf16x8 pb[KS];
+        // W = A_j vec for this wave's 16 columns (A_j = H_t + Lambda of token j), from the
+        // bf16 operand vb of vec: W = zs_j (B'_w vec) + K_w^T S' + Lambda vec, the column
+        // scale applied to the state products' accumulators.  The state products run
+        // feature-step-major, so the first ones need only vb[0].
+        auto matvec = [&](const bf16x8 (&vb)[KS], f32x4 (&w)[MT]) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) pb[ks] = pack8(vec[2 * ks], vec[2 * ks + 1]);
-            f32x4 sacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int mt = 0; mt < MT; ++mt) w[mt] = zero4;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) sacc = mfma16(kf2[ks], pb[ks], sacc);
+            for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(hf[mt][ks], vb[ks], w[mt]);
+            f32x4 sacc = zero4;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) sacc = mfma16(kf2[ks], vb[ks], sacc);
+            const uint2 sb = pack4(sacc * zw);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                w[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) w[mt] = mfma16(hf[mt][ks], pb[ks], w[mt]);
+                const uint4 v = __builtin_bit_cast(uint4, vb[mt / 2]);
+                const uint4 op = (mt % 2) ? make_uint4(sb.x, sb.y, v.z, v.w) : make_uint4(sb.x, sb.y, v.x, v.y);
+                w[mt] *= zs;
+                w[mt] = mfma16(kf3[mt], __builtin_bit_cast(bf16x8, op), w[mt]);
             }
-            const f32x4 sz = sacc * zw;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(kf3[mt], pack8(sz, vec[mt]), zs * w[mt]);
         };
 
         // ---- Jacobi start x0 = q / diag(H_t + Lambda),
         //      diag(H_t) = zs_j diag(B'_w) + sum_{16w <= i <= j} beta_i Z[i][j] k_i^2, diag(B'_w)
         //      read back from this wave's sDiag rows (written by other lanes of the same wave;
-        //      a wave's LDS accesses complete in order)
+        //      a wave's LDS accesses complete in order).
+        // Each column's system is solved for q_j scaled by a power of two that brings |q_j|^2
+        // into [1/4, 2): CG iterates are homogeneous in q and a power-of-two scale is exact, so
+        // this changes no rounding, and it keeps the CG scalars in the range where the
+        // hardware reciprocal is exact to an ulp.
         f32x4 x[MT], r[MT], p[MT], w[MT];
+        {
+            const bf16x8 zwb = pack8(zw, zero4);
+            f32x4 qf[MT];
+            float qq = 0.0f;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            bf16x8 ksq = kf3[mt];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float v = (float)ksq[e];
-                ksq[e] = (__bf16)(v * v);
+            for (int mt = 0; mt < MT; ++mt) {
+                const uint2 qv2 = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
+                qf[mt] = f32x4{bf16_bits_to_f32(qv2.x & 0xffffu), bf16_bits_to_f32(qv2.x >> 16),
+                               bf16_bits_to_f32(qv2.y & 0xffffu), bf16_bits_to_f32(qv2.y >> 16)};
+                qq += qf[mt][0] * qf[mt][0] + qf[mt][1] * qf[mt][1] + qf[mt][2] * qf[mt][2] + qf[mt][3] * qf[mt][3];
             }
-            const f32x4 dg2 = mfma16(ksq, zwb, f32x4{0.0f, 0.0f, 0.0f, 0.0f});
-            const uint2 qq = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
-            const f32x4 qf{bf16_bits_to_f32(qq.x & 0xffffu), bf16_bits_to_f32(qq.x >> 16),
-                           bf16_bits_to_f32(qq.y & 0xffffu), bf16_bits_to_f32(qq.y >> 16)};
-            const f32x4 d = zs * *reinterpret_cast<const f32x4*>(&sDiag[wave][16 * mt + 4 * g]) + dg2 +
-                            *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
+            qsh = __builtin_amdgcn_frexp_expf(col_sum(qq)) >> 1;  // |q|^2 = m 2^e, m in [1/2, 1)
+            const float qs = __builtin_ldexpf(1.0f, -qsh);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) x[mt][e] = qf[e] * __builtin_amdgcn_rcpf(d[e]);
-            p[mt] = qf;  // holds q until the first residual is formed
+            for (int mt = 0; mt < MT; ++mt) {
+                bf16x8 ksq = kf3[mt];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float v = (float)ksq[e];
+                    ksq[e] = (__bf16)(v * v);
+                }
+                const f32x4 dg2 = mfma16(ksq, zwb, zero4);
+                const f32x4 d = zs * *reinterpret_cast<const f32x4*>(&sDiag[wave][16 * mt + 4 * g]) + dg2 +
+                                *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
+                qf[mt] = qs * qf[mt];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) x[mt][e] = qf[mt][e] * __builtin_amdgcn_rcpf(d[e]);
+            }
+            // kf2 and kf3 are read only as A operands from here on: like B'_w they move to
+            // the accumulation registers, leaving the ordinary ones to the CG vectors.
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) asm("" : "=a"(kf2[ks]) : "0"(kf2[ks]));
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) asm("" : "=a"(kf3[mt]) : "0"(kf3[mt]));
+            bf16x8 xb[KS];
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) xb[ks] = pack8(x[2 * ks], x[2 * ks + 1]);
+            matvec(xb, w);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) r[mt] = qf[mt] - w[mt];
         }
-        matvec(x, w);
         float part = 0.0f;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            r[mt] = p[mt] - w[mt];
             p[mt] = r[mt];
             part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
         }
         float delta = col_sum(part);
-        bool active = delta > 0.0f;
+        bool active = delta >= kMinNormal;
 
         // ---- every wave is done with sHf, sKT, sKU and sQ: the next chunk's loads may land
         // there while this chunk's CG runs (the barrier also waits for this wave's memory
@@ -523,39 +554,52 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         float g_nx = 1.0f, b_nx = 0.0f, lam_nx = 0.0f;
         int pieces = 0;  // pieces of the next chunk's loads issued so far
 
+        // One CG step (App. C, Alg. 1 with tolerance 0), branch-free: a stopped column takes
+        // alpha = 0 and keeps x.  A column stops when p^T A p is not a positive normal number
+        // (alpha would need the reciprocal of a subnormal) or when the new squared residual
+        // falls below the smallest normal number (relative to |q|^2, which the scaling above
+        // keeps in [1/4, 2)); Alg. 1 stops at exactly zero.
         for (int it = 0; it < a.n_cg; ++it) {
             if (!__any(active)) break;
             if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
-            matvec(p, w);
-            part = 0.0f;
+            {
+                bf16x8 pb[KS];
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                part += p[mt][0] * w[mt][0] + p[mt][1] * w[mt][1] + p[mt][2] * w[mt][2] + p[mt][3] * w[mt][3];
-            const float pw = col_sum(part);
-            if (!(pw > 0.0f)) active = false;
-            if (active) {
-                const float alpha = delta / pw;
+                for (int ks = 0; ks < KS; ++ks) pb[ks] = pack8(p[2 * ks], p[2 * ks + 1]);
+                matvec(pb, w);
+            }
+            // column dot products in four independent partial sums (one per element of a
+            // tile), so consecutive fused multiply-adds do not wait on each other
+            f32x4 acc = zero4;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc += p[mt] * w[mt];
+            const float pw = col_sum((acc[0] + acc[1]) + (acc[2] + acc[3]));
+            const bool act1 = active && pw >= kMinNormal;
+            if (act1) {
+                const float alpha = delta * __builtin_amdgcn_rcpf(pw);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    x[mt] += alpha * p[mt];
                     r[mt] -= alpha * w[mt];
+                    x[mt] += alpha * p[mt];
                 }
             }
-            part = 0.0f;
+            acc = zero4;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
-            const float dn = col_sum(part);
-            if (active) {
-                if (dn == 0.0f) {
-                    active = false;
-                } else {
-                    const float beta_cg = dn / delta;
+            for (int mt = 0; mt < MT; ++mt) acc += r[mt] * r[mt];
+            const float dn = col_sum((acc[0] + acc[1]) + (acc[2] + acc[3]));
+            const bool act2 = act1 && dn >= kMinNormal;
+            if (act2) {
+                const float bcg = dn * __builtin_amdgcn_rcpf(delta);
 #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) p[mt] = r[mt] + beta_cg * p[mt];
-                    delta = dn;
-                }
+                for (int mt = 0; mt < MT; ++mt) p[mt] = r[mt] + bcg * p[mt];
             }
+            delta = act2 ? dn : delta;
+            active = act2;
+        }
+        {
+            const float us = __builtin_ldexpf(1.0f, qsh);  // undoes the power-of-two scale of q
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) x[mt] = us * x[mt];
         }
 
         if (more)

@@ -37,6 +37,14 @@ __device__ __forceinline__ bf16x8 pack8(const f32x4& lo, const f32x4& hi)
     return r;
 }
 
+// Four fp32 rounded to bf16, as two 32-bit words (half of an 8-wide operand).
+__device__ __forceinline__ uint2 pack4(const f32x4& v)
+{
+    const bf16x8 r = pack8(v, v);
+    const uint4 u = __builtin_bit_cast(uint4, r);
+    return make_uint2(u.x, u.y);
+}
+
 // 8 bf16 from LDS: base[0..3] and base[16..19] (the k-index map above).
 __device__ __forceinline__ bf16x8 lds_frag(const uint16_t* base)
 {

@@ -136,6 +136,23 @@ def test_bf16_path_strong_decay():
         assert e_out <= TOL_BF16 and e_q <= TOL_BF16, n_cg
 
 
+def test_bf16_path_query_scale_is_exact():
+    """o is positively homogeneous in q (App. C: every CG iterate scales with the
+    right-hand side).  The matrix-core path solves each column for q scaled by a power
+    of two, so scaling q by 2^k, from 2^-60 to 2^60, must scale out by exactly 2^k, bit
+    for bit, and stay within the bf16 tolerance of the oracle."""
+    x = W.forward_inputs(1, 2, 128 + 40, 128, 128, "bf16", 4.0, seed=47)
+    base = _gpu_forward(x, "bf16", 15, 64, precision=L.MESA_PREC_BF16)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 15)["out"]
+    assert rel_l2(base, ref) <= TOL_BF16
+    for k in (-60, -20, 7, 60):
+        y = dict(x)
+        y["q"] = (x["q"].astype(np.float64) * 2.0 ** k).astype(np.float32)
+        got = _gpu_forward(y, "bf16", 15, 64, precision=L.MESA_PREC_BF16)
+        _say("q scaled by 2^%d: max |got/2^k - base| = %.3e" % (k, np.abs(got * 2.0 ** -k - base).max()))
+        assert np.array_equal(got, (base.astype(np.float64) * 2.0 ** k).astype(np.float32)), k
+
+
 def test_stress_repeated_keys_bf16_path_reported():
     """Single-pass bf16 operands are validated on the workload distributions,
     not on adversarial inputs: on the repeated-key stress input the error is
