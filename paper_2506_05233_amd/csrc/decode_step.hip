@@ -5,20 +5,19 @@
 // is bound by HBM, since each pair reads and writes its two fp32 states
 // (8 (d_k + d_v) d_k bytes), so the kernel is built for many pairs in flight
 // per compute unit: about 160 registers per thread let three workgroups share
-// a SIMD, and pairs in different phases (state traffic, CG) overlap.
+// a SIMD, and pairs in different phases (state traffic, CG) overlap.  Every
+// state access of a wave is one row segment of 256 contiguous bytes.
 //   1. H <- gamma H + beta k k^T.  Thread R keeps row R of H in registers.  H is
-//      symmetric, so row R is read as column R, H[c][R] for c = 0..d_k-1: the
-//      threads of a wave read and write 64 consecutive floats of one row of H
-//      per access (256 contiguous bytes); the updated values are written back in
-//      place.
+//      symmetric, so row R is read as column R, H[c][R] for c = 0..d_k-1; the
+//      updated values are written back in place.
 //   2. Alg. 1 with tolerance 0 on (H + Lambda) x = q: thread R owns element R of
 //      x, r, p, w; each product is a register-resident row times p, with p
 //      broadcast through LDS; the CG scalars are wave reductions combined across
 //      the waves through LDS (every wave adds the partial sums in the same order,
 //      so all waves take the same branches).
-//   3. G <- gamma G + beta v k^T and o = G x: thread e streams row e of G through
-//      registers (rows e, e + d_k, ... when d_v > d_k), writes it back and forms
-//      o_e on the way.
+//   3. G <- gamma G + beta v k^T and o = G x: thread c keeps column c of G,
+//      writes it back, and the row sums of G diag(x) are reduced across lanes
+//      and waves.
 // All arithmetic is fp32.
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
@@ -44,6 +43,8 @@ void decode_step_kernel(DecodeArgs a)
     __shared__ __attribute__((aligned(16))) float sk[DK];
     __shared__ __attribute__((aligned(16))) float sp[DK];
     __shared__ float sred[2][NW];
+    __shared__ __attribute__((aligned(16))) float sv[DV];
+    __shared__ float so[NW][DV];
 
     const Tin* qp = static_cast<const Tin*>(a.q) + pair * DK;
     const Tin* kp = static_cast<const Tin*>(a.k) + pair * DK;
@@ -51,6 +52,7 @@ void decode_step_kernel(DecodeArgs a)
     const float gam = a.gamma[pair], bet = a.beta[pair];
     const float kR = to_f32(kp[tid]), qR = to_f32(qp[tid]), lR = a.lambda[int64_t(h) * DK + tid];
     sk[tid] = kR;
+    for (int e = tid; e < DV; e += DK) sv[e] = to_f32(vp[e]);
 
     // ---- 1. state update of H, row tid held as hc[c] = H[c][tid].  The pair's H is
     // addressed through a buffer resource: the column offset c d_k is a scalar, so the
@@ -122,29 +124,61 @@ void decode_step_kernel(DecodeArgs a)
         }
     }
 
-    // ---- 3. G update and read-out, rows e = tid, tid + d_k, ... of G
-    sp[tid] = x;  // sp's last readers (the last product) passed a dot product's barrier
-    __syncthreads();
+    // ---- 3. G update and read-out.  Thread c owns column c of G: G[e][c] for every row e
+    // is read and written as one 256-byte wave access per row (like H), and the row sums
+    // o_e = sum_c G[e][c] x_c are formed by a transposing reduction across the lanes
+    // (blocks of 32 rows: two lane-half swaps leave 8 rows per lane summed over 4 lanes,
+    // a 16-lane reduction completes each), then across the waves through LDS.
     float* Gp = a.G + pair * int64_t(DV) * DK;
+    const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc(Gp, 0, DV * DK * 4, kBufferRsrcWord3);
+    float gc[DV];
 #pragma unroll
-    for (int e = tid; e < DV; e += DK) {
-        float* grow = Gp + int64_t(e) * DK;
-        const float bv = bet * to_f32(vp[e]);
-        f32x4 o4 = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int e = 0; e < DV; ++e) gc[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(gr, tid * 4, e * DK * 4, 0));
+    const float bk = bet * kR;
 #pragma unroll
-        for (int c4 = 0; c4 < DK; c4 += 4) {
-            const f32x4 gv = *reinterpret_cast<const f32x4*>(grow + c4);
-            const f32x4 kc = *reinterpret_cast<const f32x4*>(sk + c4);
-            const f32x4 xc = *reinterpret_cast<const f32x4*>(sp + c4);
-            f32x4 gn;
+    for (int e4 = 0; e4 < DV; e4 += 4) {
+        const f32x4 ve = *reinterpret_cast<const f32x4*>(sv + e4);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                gn[q] = gam * gv[q] + bv * kc[q];
-                o4[q] += gn[q] * xc[q];
-            }
-            *reinterpret_cast<f32x4*>(grow + c4) = gn;
+        for (int q = 0; q < 4; ++q) {
+            gc[e4 + q] = gam * gc[e4 + q] + bk * ve[q];
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(gc[e4 + q]), gr, tid * 4, (e4 + q) * DK * 4, 0);
+            gc[e4 + q] *= x;
         }
-        a.out[pair * DV + e] = (o4[0] + o4[1]) + (o4[2] + o4[3]);
+    }
+#pragma unroll
+    for (int b = 0; b < DV; b += 32) {
+        float s16[16], s8[8];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(gc[b + i]), __float_as_uint(gc[b + 16 + i]), false, false);
+            s16[i] = __uint_as_float(t[0]) + __uint_as_float(t[1]);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(s16[i]), __float_as_uint(s16[8 + i]), false, false);
+            s8[i] = __uint_as_float(t[0]) + __uint_as_float(t[1]);
+        }
+        // lanes of 16-lane row rr hold rows b + 8 rr + i; sum over the row's 16 lanes
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float v = s8[i];
+            v += dpp_f32<kDppQuadSwap1>(v, v);
+            v += dpp_f32<kDppQuadSwap2>(v, v);
+            v += dpp_f32<kDppRowRor4>(v, v);
+            v += dpp_f32<kDppRowRor8>(v, v);
+            s8[i] = v;
+        }
+        if (lane % 16 == 0) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) so[wv][b + 8 * (lane / 16) + i] = s8[i];
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < DV; e += DK) {
+        float o = so[0][e];
+#pragma unroll
+        for (int u = 1; u < NW; ++u) o += so[u][e];
+        a.out[pair * DV + e] = o;
     }
 }
 
