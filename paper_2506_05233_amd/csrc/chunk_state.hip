@@ -418,18 +418,23 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
 // part 1 is G^T (d_k x d_v), both as [key feature R][column c] -- in registers,
 // and walks its chunks in order:
 //
-//   X_{next} = D X + K^T (w ⊙ Y),   Y = K (part 0) or V (part 1), w_i = beta_i zeta_{end,i},
+//   X_{next} = D X + K^T (w ⊙ Y),   Y = K (part 0) or V (part 1), w_i = beta_i zeta_{end,i}.
 //
-// with w ⊙ Y split into bf16 high and low parts (two products, ~16-bit weights).
+// When fp32 states leave the kernel (the final states), w ⊙ Y is split into bf16
+// high and low parts (two products, ~16-bit weights, states fp32-accurate); when
+// only the bf16 chunk states are produced, the high part alone is used: its
+// rounding (2^-9 per term, averaged over the chunk's 64 terms) stays well below the
+// bf16 rounding of the stored states.
 // Eight waves (two per SIMD, so one hides the other's latencies); wave w owns key
 // rows 32 (w % NS) .. +31 (NS = d_k / 32) and a 1/CS share of the columns (CS = 8 / NS); its 16x16 result tiles pair up into complete bf16
 // A-fragments of the fragment layout (rows 32s.. of X^T are fragment row block s),
 // so every chunk state is written with whole 1-KiB wave stores.  Staging is
 // double-buffered in LDS (one barrier per chunk) and the inputs of chunk n + 2 are
-// loaded while chunk n is consumed.
+// loaded while chunk n is consumed; the staging of chunk n + 1 is interleaved with
+// the products of chunk n.
 constexpr int kWideThreads = 512;  // eight waves: two per SIMD
 
-template <int DK, int DV>
+template <int DK, int DV, bool STORE, bool SPLIT>
 __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArgs a)
 {
     constexpr int C = 64;
@@ -491,8 +496,15 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                 }
             }
         };
-        // gate scan of a chunk and its staging into buffer b; returns the chunk decay D
-        auto stage = [&](const Regs& R, int b) -> float {
+        // Staging of a chunk into buffer b, in three pieces that the chunk loop interleaves
+        // with the previous chunk's products: the gate scan (write weights w_i = beta_i
+        // zeta_{end,i} of this thread's two tokens, and the chunk decay D), the key tile, and
+        // the weighted y tile split into bf16 high and low parts (features q0 .. q1-1 of this
+        // thread's group).
+        struct Gate {
+            float w0, w1, D;
+        };
+        auto gates = [&](const Regs& R) -> Gate {
             const bool live = lane < R.valid;
             const float gl = live ? R.gam : 1.0f;
             const float lg = wave_scan_add(gl > 0.0f ? logf(gl) : 0.0f);
@@ -500,7 +512,9 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
             const float lgE = lane_value(lg, C - 1);
             const int zlE = lane_value(zl, C - 1);
             const float wl = live ? R.bet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
-            const float w0 = __shfl(wl, 2 * p), w1 = __shfl(wl, 2 * p + 1);
+            return Gate{__shfl(wl, 2 * p), __shfl(wl, 2 * p + 1), zlE >= 0 ? 0.0f : expf(lgE)};
+        };
+        auto stage_k = [&](const Regs& R, int b) {
             const bool k0 = 2 * p < R.valid, k1 = 2 * p + 1 < R.valid;
 #pragma unroll
             for (int m = 0; m < NKQ; ++m) {
@@ -509,6 +523,8 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                 const uint4 kb = k1 ? R.k[m][1] : make_uint4(0, 0, 0, 0);
                 stage_token_pair(reinterpret_cast<uint32_t*>(sA[b]), LDT / 2, FPP * m + 8 * fg, p, ka, kb);
             }
+        };
+        auto stage_y = [&](const Regs& R, int b, const Gate& gt, int q0, int q1) {
 #pragma unroll
             for (int m = 0; m < NY; ++m) {
                 if (FPP * m + 8 * fg >= NC) continue;
@@ -519,18 +535,16 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                 uint32_t* hi32 = reinterpret_cast<uint32_t*>(sBh[b]);
                 uint32_t* lo32 = reinterpret_cast<uint32_t*>(sBl[b]);
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const uint32_t ba = (q & 1) ? (a4[q / 2] >> 16) : (a4[q / 2] & 0xffffu);
-                    const uint32_t bb = (q & 1) ? (b4[q / 2] >> 16) : (b4[q / 2] & 0xffffu);
-                    const float va = w0 * bf16_bits_to_f32(ba), vb = w1 * bf16_bits_to_f32(bb);
-                    const __bf16 ha = (__bf16)va, hb = (__bf16)vb;
-                    const __bf16 la = (__bf16)(va - (float)ha), lb = (__bf16)(vb - (float)hb);
+                for (int q = q0; q < q1; ++q) {
+                    // feature q of tokens 2p and 2p+1: bf16 bits widened by a shift or a mask
+                    const float va = gt.w0 * __uint_as_float((q & 1) ? (a4[q / 2] & 0xffff0000u) : (a4[q / 2] << 16));
+                    const float vb = gt.w1 * __uint_as_float((q & 1) ? (b4[q / 2] & 0xffff0000u) : (b4[q / 2] << 16));
+                    const uint32_t h2 = pack_bf16x2(va, vb);
                     const int c = FPP * m + 8 * fg + q;
-                    hi32[c * (LDT / 2) + p] = uint32_t(bf16_bits(ha)) | (uint32_t(bf16_bits(hb)) << 16);
-                    lo32[c * (LDT / 2) + p] = uint32_t(bf16_bits(la)) | (uint32_t(bf16_bits(lb)) << 16);
+                    hi32[c * (LDT / 2) + p] = h2;
+                    if (SPLIT) lo32[c * (LDT / 2) + p] = pack_bf16x2(va - __uint_as_float(h2 << 16), vb - __uint_as_float(h2 & 0xffff0000u));
                 }
             }
-            return zlE >= 0 ? 0.0f : expf(lgE);
         };
 
         f32x4 acc[2][NCT];
@@ -538,7 +552,7 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
         for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) acc[rt][ct] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        const bool frag_out = a.store_chunks && a.frag;
+        constexpr bool frag_out = STORE;
         uint16_t* frag_base = static_cast<uint16_t*>(part ? a.Gs : a.Hs);
         constexpr int kStateElems = NC * DK;  // bf16 per chunk state of this part
 
@@ -562,32 +576,55 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
             for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) acc[rt][ct] *= D;
+            // every operand of this chunk's products is read from LDS first; the products then
+            // run in three batches with the staging pieces of the next chunk (into the other
+            // buffer) between them, and scheduling barriers keep that order
+            bf16x8 af[C / 32][2], bfh[C / 32][NCT], bfl[C / 32][NCT];
 #pragma unroll
             for (int u = 0; u < C / 32; ++u) {
-                bf16x8 af[2];
 #pragma unroll
-                for (int rt = 0; rt < 2; ++rt) af[rt] = lds_frag(sA[b] + (32 * sblk + 16 * rt + ln) * LDT + 32 * u + 4 * g);
+                for (int rt = 0; rt < 2; ++rt) af[u][rt] = lds_frag(sA[b] + (32 * sblk + 16 * rt + ln) * LDT + 32 * u + 4 * g);
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     const int c = 16 * (ct0 + ct) + ln;
-                    const bf16x8 bh_ = lds_frag(sBh[b] + c * LDT + 32 * u + 4 * g);
-                    const bf16x8 bl_ = lds_frag(sBl[b] + c * LDT + 32 * u + 4 * g);
-#pragma unroll
-                    for (int rt = 0; rt < 2; ++rt) {
-                        acc[rt][ct] = mfma16(af[rt], bh_, acc[rt][ct]);
-                        acc[rt][ct] = mfma16(af[rt], bl_, acc[rt][ct]);
-                    }
+                    bfh[u][ct] = lds_frag(sBh[b] + c * LDT + 32 * u + 4 * g);
+                    if (SPLIT) bfl[u][ct] = lds_frag(sBl[b] + c * LDT + 32 * u + 4 * g);
                 }
             }
-            if (n + 1 < s.n_chunks) Dnext = stage(Rn1, (n + 1) % 2);
-            if (n + 2 < s.n_chunks) load(n + 2, Rfree);
+            auto products = [&](int u, int ct_lo, int ct_hi) {
+#pragma unroll
+                for (int ct = ct_lo; ct < ct_hi; ++ct)
+#pragma unroll
+                    for (int rt = 0; rt < 2; ++rt) {
+                        acc[rt][ct] = mfma16(af[u][rt], bfh[u][ct], acc[rt][ct]);
+                        if (SPLIT) acc[rt][ct] = mfma16(af[u][rt], bfl[u][ct], acc[rt][ct]);
+                    }
+            };
+            const int bn = (n + 1) % 2;  // a chunk past the end stages into a buffer nobody reads
+            products(0, 0, NCT);
+            const Gate gt = gates(Rn1);
+            __builtin_amdgcn_sched_barrier(0);
+            products(1, 0, NCT / 2);
+            stage_k(Rn1, bn);
+            stage_y(Rn1, bn, gt, 0, 4);
+            __builtin_amdgcn_sched_barrier(0);
+            products(1, NCT / 2, NCT);
+            stage_y(Rn1, bn, gt, 4, 8);
+            Dnext = gt.D;
+            load(min(n + 2, s.n_chunks - 1), Rfree);  // unconditional, so memory waits count statically
             __syncthreads();
         };
 
         Regs R0, R1;
         load(0, R0);
-        if (s.n_chunks > 1) load(1, R1);
-        float D0 = stage(R0, 0), D1 = 1.0f;
+        load(min(1, s.n_chunks - 1), R1);
+        float D0, D1 = 1.0f;
+        {
+            const Gate gt = gates(R0);
+            stage_k(R0, 0);
+            stage_y(R0, 0, gt, 0, 8);
+            D0 = gt.D;
+        }
         __syncthreads();
         for (int n = 0; n < s.n_chunks; n += 2) {
             consume(n, D0, R1, R0, D1);       // stages chunk n+1 (R1), loads n+2 into R0
@@ -623,7 +660,13 @@ template <int DK, int DV>
 hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
 {
     const unsigned blocks = unsigned(a.s.batch * a.s.heads * 2);
-    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV>), dim3(blocks), dim3(kWideThreads), 0, stream, a);
+    const bool fin = a.final_H != nullptr || a.final_G != nullptr;
+    if (a.store_chunks && a.frag && !fin)
+        hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, true, false>), dim3(blocks), dim3(kWideThreads), 0, stream, a);
+    else if (a.store_chunks && a.frag)
+        hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, true, true>), dim3(blocks), dim3(kWideThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, false, true>), dim3(blocks), dim3(kWideThreads), 0, stream, a);
     return hipGetLastError();
 }
 

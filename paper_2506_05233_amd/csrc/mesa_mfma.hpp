@@ -37,6 +37,15 @@ __device__ __forceinline__ bf16x8 pack8(const f32x4& lo, const f32x4& hi)
     return r;
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 rounded to bf16 (nearest even), packed as a | b << 16 (one conversion).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
+{
+    const bf16x2 r = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(uint32_t, r);
+}
+
 // Four fp32 rounded to bf16, as two 32-bit words (half of an 8-wide operand).
 __device__ __forceinline__ uint2 pack4(const f32x4& v)
 {
