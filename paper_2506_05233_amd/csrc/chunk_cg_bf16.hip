@@ -180,11 +180,13 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
     // registers.  The gates and lambda go to registers; keys, queries and values to
     // the thread's own staging slots; H_c, as bf16 A-fragments (fragment f of lane l
     // at [f * 64 + l] * 8, one 1-KiB direct load per fragment), to sHf.  They are
-    // issued in kPieces pieces of at most four direct loads: a wave that issues many
-    // more at once stalls until the first ones return, so the next chunk's pieces
-    // are spread over the CG iterations of the current one.
+    // issued in kPieces pieces (H_c in pieces of two direct loads, the staging slots
+    // in pieces of four): a wave that issues many more at once stalls until the
+    // first ones return, so the next chunk's pieces are spread over the CG
+    // iterations of the current one, one per iteration.
     constexpr int kRawSlots = L::kRawSlots;
-    constexpr int kPieces = 2 + (kRawSlots + 3) / 4;
+    constexpr int kHcPieces = NHF < 4 ? NHF : 4, kRawPer = 4;
+    constexpr int kPieces = kHcPieces + (kRawSlots + kRawPer - 1) / kRawPer;
     auto issue_piece = [&](int c, int piece, int tid_in, float& g_out, float& b_out, float& lam_out) {
         int tid = tid_in;
         asm volatile("" : "+v"(tid));  // recompute the addresses here, not hoisted
@@ -196,7 +198,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         const int64_t t0_ = int64_t(nn) * kC;
         const int valid_ = int(min<int64_t>(kC, s.seq_len - t0_));
         const int64_t tok0_ = int64_t(bh_) * s.seq_len + t0_;
-        if (piece < 2) {
+        if (piece < kHcPieces) {
             if (piece == 0) {
                 const int lt = min(lane, valid_ - 1);
                 g_out = a.gamma[tok0_ + lt];
@@ -205,7 +207,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
             }
             const uint16_t* Hf = static_cast<const uint16_t*>(a.Hs) + int64_t(c) * DK * DK;
 #pragma unroll
-            for (int u = piece * (NHF / 2); u < (piece + 1) * (NHF / 2); ++u) {
+            for (int u = piece * (NHF / kHcPieces); u < (piece + 1) * (NHF / kHcPieces); ++u) {
                 const int f = wave * NHF + u;
                 load_lds16(Hf + (f * kWave + lane) * 8, sHf + f * kWave * 8);
             }
@@ -217,7 +219,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         uint4* slot = sRaw + wave * kWave;  // this wave's threads' slots of staging slot 0
 #pragma unroll
         for (int q = 0; q < kRawSlots; ++q) {
-            if (q / 4 != piece - 2) continue;
+            if (q / kRawPer != piece - kHcPieces) continue;
             const bool kq = q < 4 * NKQ;
             const int m = kq ? q / 4 : (q - 4 * NKQ) / 2;
             const int f0 = 64 * m + 8 * fg;
