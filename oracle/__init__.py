@@ -57,13 +57,15 @@ def _load():
             lib = ctypes.CDLL(_LIB_PATH)
             P = ctypes.POINTER(ctypes.c_double)
             i64, ci = ctypes.c_int64, ctypes.c_int
+            I32 = ctypes.POINTER(ctypes.c_int32)
+            dbl = ctypes.c_double
             lib.oracle_forward.argtypes = [P, P, P, P, P, P, i64, i64, i64, i64, i64, ci, ci, ci,
-                                           P, P, P, P, ci]
+                                           dbl, P, P, P, P, I32, ci]
             lib.oracle_forward.restype = ci
             lib.oracle_decode_step.argtypes = [P, P, P, P, P, P, P, P, i64, i64, i64, i64, ci, ci,
-                                               ci, P, P, ci]
+                                               ci, dbl, P, P, I32, ci]
             lib.oracle_decode_step.restype = ci
-            lib.oracle_cg.argtypes = [P, P, i64, ci, ci, P, P]
+            lib.oracle_cg.argtypes = [P, P, i64, ci, ci, dbl, P, P]
             lib.oracle_cg.restype = ci
             lib.oracle_cholesky_solve.argtypes = [P, P, i64, P, P]
             lib.oracle_cholesky_solve.restype = ci
@@ -81,6 +83,19 @@ def _ptr(a):
     return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
 
 
+def _iptr(a):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _eps(eps):
+    eps = float(eps)
+    if not eps >= 0.0 or eps == float("inf"):
+        raise ValueError("eps must be finite and >= 0")
+    return eps
+
+
 def default_threads() -> int:
     try:
         return max(1, len(os.sched_getaffinity(0)))
@@ -89,15 +104,16 @@ def default_threads() -> int:
 
 
 def forward(q, k, v, gamma, beta, lam, n_cg, solver="cg", init="jacobi", want_qstar=False,
-            want_states=False, threads=None):
+            want_states=False, threads=None, eps=0.0, want_steps=False):
     """Sequential Mesa forward over [B, H, T, d] inputs.
 
-    solver: "cg" (Alg. 1, fixed n_cg loop iterations, tolerance 0) or
-            "cholesky" (exact solve; n_cg ignored).
+    solver: "cg" (Alg. 1, at most n_cg loop iterations, relative tolerance eps;
+            eps = 0 is the fixed-step solve) or "cholesky" (exact; n_cg ignored).
     init:   "jacobi" (x0 = q / diag(H_t + Lambda), the paper's choice) or
             "query" (x0 = q; only to check the GLA remark with n_cg = 0).
     Returns a dict with "out" [B,H,T,dv] and, if asked, "qstar" [B,H,T,dk],
-    "H" [B,H,dk,dk], "G" [B,H,dv,dk] (final states).
+    "H" [B,H,dk,dk], "G" [B,H,dv,dk] (final states), "steps" [B,H,T] int32
+    (CG iterations per token).
     """
     lib = _load()
     q, k, v, gamma, beta, lam = map(_f64, (q, k, v, gamma, beta, lam))
@@ -109,11 +125,12 @@ def forward(q, k, v, gamma, beta, lam, n_cg, solver="cg", init="jacobi", want_qs
     qstar = np.zeros((B, Hh, T, dk)) if want_qstar else None
     fH = np.zeros((B, Hh, dk, dk)) if want_states else None
     fG = np.zeros((B, Hh, dv, dk)) if want_states else None
+    steps = np.zeros((B, Hh, T), dtype=np.int32) if want_steps else None
     s = {"cg": SOLVE_CG, "cholesky": SOLVE_CHOLESKY}[solver]
     i = {"jacobi": INIT_JACOBI, "query": INIT_QUERY}[init]
     rc = lib.oracle_forward(_ptr(q), _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam),
-                            B, Hh, T, dk, dv, int(n_cg), s, i, _ptr(out), _ptr(qstar), _ptr(fH),
-                            _ptr(fG), int(threads or default_threads()))
+                            B, Hh, T, dk, dv, int(n_cg), s, i, _eps(eps), _ptr(out), _ptr(qstar),
+                            _ptr(fH), _ptr(fG), _iptr(steps), int(threads or default_threads()))
     if rc != 0:
         raise FloatingPointError("oracle: a system H_t + Lambda was not positive definite")
     res = {"out": out}
@@ -122,12 +139,16 @@ def forward(q, k, v, gamma, beta, lam, n_cg, solver="cg", init="jacobi", want_qs
     if want_states:
         res["H"] = fH
         res["G"] = fG
+    if want_steps:
+        res["steps"] = steps
     return res
 
 
 def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, solver="cg", init="jacobi",
-                want_qstar=False, threads=None):
-    """One recurrent step on [N, H, ...] states.  Returns (out, H_new, G_new[, qstar])."""
+                want_qstar=False, threads=None, eps=0.0, steps_out=None):
+    """One recurrent step on [N, H, ...] states.  Returns (out, H_new, G_new[, qstar]).
+    eps: CG relative tolerance (0: fixed steps); steps_out: optional int32 [N, H]
+    array that receives the CG iterations of every (sequence, head)."""
     lib = _load()
     H = _f64(state_H).copy()
     G = _f64(state_G).copy()
@@ -139,9 +160,12 @@ def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, solver="cg", 
     qstar = np.zeros((N, Hh, dk)) if want_qstar else None
     s = {"cg": SOLVE_CG, "cholesky": SOLVE_CHOLESKY}[solver]
     i = {"jacobi": INIT_JACOBI, "query": INIT_QUERY}[init]
+    if steps_out is not None:
+        assert steps_out.shape == (N, Hh) and steps_out.dtype == np.int32 and steps_out.flags.c_contiguous
     rc = lib.oracle_decode_step(_ptr(H), _ptr(G), _ptr(q), _ptr(k), _ptr(v), _ptr(gamma),
-                                _ptr(beta), _ptr(lam), N, Hh, dk, dv, int(n_cg), s, i, _ptr(out),
-                                _ptr(qstar), int(threads or default_threads()))
+                                _ptr(beta), _ptr(lam), N, Hh, dk, dv, int(n_cg), s, i, _eps(eps),
+                                _ptr(out), _ptr(qstar), _iptr(steps_out),
+                                int(threads or default_threads()))
     if rc != 0:
         raise FloatingPointError("oracle: a system H_t + Lambda was not positive definite")
     if want_qstar:
@@ -149,17 +173,18 @@ def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, solver="cg", 
     return out, H, G
 
 
-def cg_solve(A, b, n_cg, init="jacobi"):
-    """Alg. 1 with tolerance 0 on one SPD system; returns x."""
+def cg_solve(A, b, n_cg, init="jacobi", eps=0.0, return_steps=False):
+    """Alg. 1 on one SPD system (at most n_cg iterations, relative tolerance eps);
+    returns x, or (x, iterations) with return_steps."""
     lib = _load()
     A = _f64(A)
     b = _f64(b)
     n = b.shape[0]
     x = np.zeros(n)
     work = np.zeros(3 * n)
-    lib.oracle_cg(_ptr(A), _ptr(b), n, int(n_cg), {"jacobi": INIT_JACOBI, "query": INIT_QUERY}[init],
-                  _ptr(x), _ptr(work))
-    return x
+    it = lib.oracle_cg(_ptr(A), _ptr(b), n, int(n_cg), {"jacobi": INIT_JACOBI, "query": INIT_QUERY}[init],
+                       _eps(eps), _ptr(x), _ptr(work))
+    return (x, it) if return_steps else x
 
 
 def cholesky_solve(A, b):

@@ -23,9 +23,11 @@
  * Readings adopted where the paper is ambiguous (all listed in the design doc):
  *   - the Jacobi diagonal is that of the system being solved, H_t + Lambda;
  *   - n_cg counts loop iterations, so a solve does n_cg + 1 products;
- *   - with tolerance zero the loop stops when the new squared residual is
- *     exactly zero; it also stops, keeping x, when the squared residual is zero
- *     before a step or when p^T A p <= 0 (guards for q = 0 and breakdown);
+ *   - the loop stops, after updating x, when the new residual meets Alg. 1's
+ *     relative test |r_{k+1}| <= eps |r_0| (squared: delta_new <= eps^2 delta_0;
+ *     with eps = 0 that is a residual of exactly zero); it also stops, keeping
+ *     x, when the squared residual is zero before a step or when p^T A p <= 0
+ *     (guards for q = 0 and breakdown);
  *   - beta enters once: H += beta k k^T, G += beta v k^T;
  *   - decode updates the state with the new token first, then solves.
  *
@@ -40,12 +42,14 @@
 enum { ORACLE_SOLVE_CG = 0, ORACLE_SOLVE_CHOLESKY = 1 };
 enum { ORACLE_INIT_JACOBI = 0, ORACLE_INIT_QUERY = 1 };
 
-/* Fixed-step CG on the SPD system A x = b (App. C, Alg. 1, epsilon = 0).
+/* CG on the SPD system A x = b (App. C, Alg. 1): at most n_cg loop iterations,
+ * relative tolerance eps >= 0 (eps = 0: the fixed-step solve).
  * init = ORACLE_INIT_JACOBI: x0 = b / diag(A)  (the paper's choice);
  * init = ORACLE_INIT_QUERY : x0 = b            (the "zero CG steps gives GLA"
  *                                               remark of Sec. 4; tests only).
- * work must hold 3n doubles.  Returns the number of loop iterations done. */
-int oracle_cg(const double* A, const double* b, int64_t n, int n_cg, int init,
+ * work must hold 3n doubles.  Returns the number of loop iterations that
+ * updated x. */
+int oracle_cg(const double* A, const double* b, int64_t n, int n_cg, int init, double eps,
               double* x, double* work)
 {
     double* r = work;
@@ -61,6 +65,7 @@ int oracle_cg(const double* A, const double* b, int64_t n, int n_cg, int init,
         p[i] = r[i];
         delta += r[i] * r[i];
     }
+    const double delta0 = delta;  /* |r_0|^2, the reference of the relative test */
     int it = 0;
     for (; it < n_cg; ++it) {
         if (delta == 0.0) break;
@@ -79,7 +84,7 @@ int oracle_cg(const double* A, const double* b, int64_t n, int n_cg, int init,
             r[i] -= alpha * w[i];
             delta_new += r[i] * r[i];
         }
-        if (delta_new == 0.0) { ++it; break; }
+        if (delta_new <= eps * eps * delta0) { ++it; break; }
         double beta_cg = delta_new / delta;
         for (int64_t i = 0; i < n; ++i) p[i] = r[i] + beta_cg * p[i];
         delta = delta_new;
@@ -125,8 +130,8 @@ int oracle_cholesky_solve(const double* A, const double* b, int64_t n, double* x
  * holds max(3*dk, dk*dk), xq holds dk (returns q*).  Returns 0 or -1. */
 static int mesa_token(double* H, double* G, const double* q, const double* k, const double* v,
                       double gamma, double beta, const double* lambda, int64_t dk, int64_t dv,
-                      int n_cg, int solver, int init, double* o, double* xq,
-                      double* A_work, double* solve_work)
+                      int n_cg, int solver, int init, double eps, double* o, double* xq,
+                      int32_t* steps, double* A_work, double* solve_work)
 {
     for (int64_t a = 0; a < dk; ++a)
         for (int64_t b = 0; b < dk; ++b)
@@ -140,7 +145,8 @@ static int mesa_token(double* H, double* G, const double* q, const double* k, co
     if (solver == ORACLE_SOLVE_CHOLESKY) {
         if (oracle_cholesky_solve(A_work, q, dk, xq, solve_work) != 0) return -1;
     } else {
-        oracle_cg(A_work, q, dk, n_cg, init, xq, solve_work);
+        const int it = oracle_cg(A_work, q, dk, n_cg, init, eps, xq, solve_work);
+        if (steps) *steps = it;
     }
     for (int64_t a = 0; a < dv; ++a) {
         double s = 0.0;
@@ -154,6 +160,8 @@ typedef struct {
     const double *q, *k, *v, *gamma, *beta, *lambda;
     int64_t B, Hh, T, dk, dv;
     int n_cg, solver, init;
+    double eps;
+    int32_t* steps;
     double *out, *qstar, *final_H, *final_G;
     double *state_H, *state_G;   /* decode: in/out states; forward: NULL */
     int n_threads, tid;
@@ -178,7 +186,8 @@ static void* forward_worker(void* arg)
             const int64_t tok = bh * T + t;
             if (mesa_token(H, G, j->q + tok * dk, j->k + tok * dk, j->v + tok * dv,
                            j->gamma[tok], j->beta[tok], j->lambda + h * dk, dk, dv,
-                           j->n_cg, j->solver, j->init, j->out + tok * dv, xq, A, sw) != 0)
+                           j->n_cg, j->solver, j->init, j->eps, j->out + tok * dv, xq,
+                           j->steps ? j->steps + tok : NULL, A, sw) != 0)
                 j->status = -1;
             if (j->qstar) memcpy(j->qstar + tok * dk, xq, (size_t)dk * sizeof(double));
         }
@@ -202,7 +211,8 @@ static void* decode_worker(void* arg)
         if (mesa_token(j->state_H + bh * dk * dk, j->state_G + bh * dv * dk,
                        j->q + bh * dk, j->k + bh * dk, j->v + bh * dv,
                        j->gamma[bh], j->beta[bh], j->lambda + h * dk, dk, dv,
-                       j->n_cg, j->solver, j->init, j->out + bh * dv, xq, A, sw) != 0)
+                       j->n_cg, j->solver, j->init, j->eps, j->out + bh * dv, xq,
+                       j->steps ? j->steps + bh : NULL, A, sw) != 0)
             j->status = -1;
         if (j->qstar) memcpy(j->qstar + bh * dk, xq, (size_t)dk * sizeof(double));
     }
@@ -235,13 +245,14 @@ static int run_jobs(oracle_job* proto, void* (*fn)(void*), int n_threads)
 }
 
 /* Whole-sequence forward.  q,k [B,Hh,T,dk]; v [B,Hh,T,dv]; gamma,beta [B,Hh,T];
- * lambda [Hh,dk]; out [B,Hh,T,dv]; optional (may be NULL): qstar [B,Hh,T,dk],
- * final_H [B,Hh,dk,dk], final_G [B,Hh,dv,dk].  Returns 0, or -1 if a Cholesky
+ * lambda [Hh,dk]; CG tolerance eps (0: fixed steps); out [B,Hh,T,dv]; optional
+ * (may be NULL): qstar [B,Hh,T,dk], final_H [B,Hh,dk,dk], final_G [B,Hh,dv,dk],
+ * steps [B,Hh,T] (CG iterations per token).  Returns 0, or -1 if a Cholesky
  * solve met a non-positive pivot. */
 int oracle_forward(const double* q, const double* k, const double* v, const double* gamma,
                    const double* beta, const double* lambda, int64_t B, int64_t Hh, int64_t T,
-                   int64_t dk, int64_t dv, int n_cg, int solver, int init, double* out,
-                   double* qstar, double* final_H, double* final_G, int n_threads)
+                   int64_t dk, int64_t dv, int n_cg, int solver, int init, double eps, double* out,
+                   double* qstar, double* final_H, double* final_G, int32_t* steps, int n_threads)
 {
     oracle_job proto;
     memset(&proto, 0, sizeof(proto));
@@ -249,16 +260,19 @@ int oracle_forward(const double* q, const double* k, const double* v, const doub
     proto.lambda = lambda; proto.B = B; proto.Hh = Hh; proto.T = T; proto.dk = dk; proto.dv = dv;
     proto.n_cg = n_cg; proto.solver = solver; proto.init = init; proto.out = out;
     proto.qstar = qstar; proto.final_H = final_H; proto.final_G = final_G;
+    proto.eps = eps; proto.steps = steps;
     return run_jobs(&proto, forward_worker, n_threads);
 }
 
 /* One recurrent decode step from the given states (updated in place).
  * state_H [N,Hh,dk,dk]; state_G [N,Hh,dv,dk]; q,k [N,Hh,dk]; v [N,Hh,dv];
- * gamma,beta [N,Hh]; lambda [Hh,dk]; out [N,Hh,dv]; qstar [N,Hh,dk] or NULL. */
+ * gamma,beta [N,Hh]; lambda [Hh,dk]; CG tolerance eps; out [N,Hh,dv];
+ * qstar [N,Hh,dk] and steps [N,Hh] may be NULL. */
 int oracle_decode_step(double* state_H, double* state_G, const double* q, const double* k,
                        const double* v, const double* gamma, const double* beta,
                        const double* lambda, int64_t N, int64_t Hh, int64_t dk, int64_t dv,
-                       int n_cg, int solver, int init, double* out, double* qstar, int n_threads)
+                       int n_cg, int solver, int init, double eps, double* out, double* qstar,
+                       int32_t* steps, int n_threads)
 {
     oracle_job proto;
     memset(&proto, 0, sizeof(proto));
@@ -266,5 +280,6 @@ int oracle_decode_step(double* state_H, double* state_G, const double* q, const 
     proto.lambda = lambda; proto.B = N; proto.Hh = Hh; proto.T = 1; proto.dk = dk; proto.dv = dv;
     proto.n_cg = n_cg; proto.solver = solver; proto.init = init; proto.out = out;
     proto.qstar = qstar; proto.state_H = state_H; proto.state_G = state_G;
+    proto.eps = eps; proto.steps = steps;
     return run_jobs(&proto, decode_worker, n_threads);
 }

@@ -226,6 +226,68 @@ def test_cg_iterate_is_krylov_galerkin_projection(k):
     assert _rel(got, want) < 1e-9
 
 
+# --------------------------------------- dynamic stopping (App. C, Alg. 1, eps > 0)
+def _galerkin_iterate(A, b, k):
+    """x_k of CG without the CG recurrences: the Galerkin projection onto
+    x0 + K_k(A, r0), x0 = b / diag(A)."""
+    x0 = b / np.diag(A)
+    if k == 0:
+        return x0
+    r0 = b - A @ x0
+    Kr = np.stack([np.linalg.matrix_power(A, i) @ r0 for i in range(k)], axis=1)
+    V, _ = np.linalg.qr(Kr)
+    return x0 + V @ np.linalg.solve(V.T @ A @ V, V.T @ r0)
+
+
+@pytest.mark.parametrize("eps", [1e-1, 1e-2, 1e-4, 1e-7])
+def test_tolerance_stops_at_first_iterate_meeting_relative_residual(eps):
+    """Alg. 1 stops after the first iteration k whose residual meets
+    |b - A x_k| <= eps |b - A x_0|, and returns that x_k.  The residuals here are
+    the true ones of the Galerkin iterates (no CG recurrence involved); cases
+    within 1e-6 of the threshold are skipped as ambiguous in floating point."""
+    rng = np.random.default_rng(int(-math.log10(eps) * 7))
+    checked = 0
+    for trial in range(20):
+        A = _spd(10, 40.0, rng) + np.diag(rng.uniform(0.1, 1.0, 10))
+        b = rng.standard_normal(10)
+        n_max = 10
+        x0 = b / np.diag(A)
+        rn0 = np.linalg.norm(b - A @ x0)
+        ratios = [np.linalg.norm(b - A @ _galerkin_iterate(A, b, k)) / rn0 for k in range(1, n_max + 1)]
+        want = next((k for k, rr in enumerate(ratios, 1) if rr <= eps), n_max)
+        if any(abs(rr / eps - 1.0) < 1e-6 for rr in ratios[:want]):
+            continue
+        x, steps = oracle.cg_solve(A, b, n_max, eps=eps, return_steps=True)
+        assert steps == want, (trial, steps, want, ratios)
+        assert _rel(x, _galerkin_iterate(A, b, steps)) < 1e-8
+        checked += 1
+    assert checked >= 15
+
+
+def test_tolerance_zero_is_fixed_steps_and_steps_shrink_with_eps():
+    x = _inputs(B=1, H=2, T=40, dk=6, dv=5, seed=11)
+    fixed = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 6, want_steps=True)
+    zero = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 6, eps=0.0, want_steps=True)
+    assert np.array_equal(fixed["out"], zero["out"])
+    assert np.all(fixed["steps"] <= 6) and np.mean(fixed["steps"] == 6) > 0.5
+    prev = fixed["steps"]
+    for eps in (1e-6, 1e-3, 1e-1):
+        r = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 6, eps=eps, want_steps=True)
+        assert np.all(r["steps"] <= prev) and np.all(r["steps"] >= 1)
+        prev = r["steps"]
+    # decode reports the same counts as the forward for the same tokens
+    B, H, T, dk = x["q"].shape
+    dv = x["v"].shape[-1]
+    sH, sG = np.zeros((1, H, dk, dk)), np.zeros((1, H, dv, dk))
+    fw = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 6, eps=1e-3, want_steps=True)
+    st = np.zeros((1, H), dtype=np.int32)
+    for t in range(T):
+        o, sH, sG = oracle.decode_step(sH, sG, x["q"][:, :, t], x["k"][:, :, t], x["v"][:, :, t], x["gamma"][:, :, t],
+                                       x["beta"][:, :, t], x["lam"], 6, eps=1e-3, steps_out=st)
+        assert np.array_equal(st, fw["steps"][:, :, t])
+        assert _rel(o, fw["out"][:, :, t]) < 1e-12
+
+
 def test_cg_error_within_textbook_bound():
     """||x_k - x*||_A <= 2 ((sqrt(kappa) - 1) / (sqrt(kappa) + 1))^k ||x_0 - x*||_A."""
     rng = np.random.default_rng(7)
