@@ -11,10 +11,13 @@
  *     q*_t ~= (H_t + Lambda)^{-1} q_t                 (fixed-step CG, App. C, Alg. 1)
  *     o_t  = G_t q*_t                                 (Eq. mesa-layer-final)
  *
- * The solve is Alg. 1 with tolerance zero: x0 = q_t / diag(H_t + Lambda), one
- * product for the first residual, then n_cg iterations (n_cg + 1 products).
- * An iteration stops a column, keeping its x, when its squared residual is
- * exactly zero or when p^T A p <= 0.
+ * The solve is Alg. 1: x0 = q_t / diag(H_t + Lambda), one product for the
+ * first residual, then at most n_cg iterations (n_cg + 1 products).  An
+ * iteration that updates x stops its column when the new residual meets Alg.
+ * 1's relative test |r_k| <= eps |r_0|; the plain entry points use eps = 0,
+ * the fixed-step solve, which stops early only at a residual of exactly zero
+ * (on the matrix-core path: below the smallest normal fp32 number, relative to
+ * |q_t|^2).  A column also stops, keeping its x, when p^T A p <= 0.
  *
  * The forward pass is evaluated chunkwise (Sec. 3, Eq. gla_matrix; App. D,
  * Eq. gla and Eq. q_star_parallel): states are materialised only at chunk
@@ -70,7 +73,7 @@ extern "C" {
 #define MESA_ERR_NULL 1          /* a required pointer is NULL                         */
 #define MESA_ERR_SHAPE 2         /* a size is negative or the sizes are inconsistent  */
 #define MESA_ERR_UNSUPPORTED 3   /* d_k, d_v, chunk, dtype or precision not supported */
-#define MESA_ERR_ARG 4           /* n_cg out of range, misaligned, or overlapping      */
+#define MESA_ERR_ARG 4           /* n_cg or eps out of range, misaligned, overlapping  */
 #define MESA_ERR_WORKSPACE 5     /* workspace too small                                */
 #define MESA_ERR_HIP 6           /* the HIP runtime refused a launch                   */
 
@@ -164,6 +167,30 @@ int mesa_decode_step(float* state_H, float* state_G, const void* q, const void* 
                      const float* gamma, const float* beta, const float* lambda, int64_t batch,
                      int64_t heads, int64_t d_k, int64_t d_v, int dtype, int n_cg, float* out,
                      void* stream);
+
+/* Dynamic stopping (App. C, Alg. 1 with a tolerance; Sec. 4: the layer spends
+ * as many CG iterations on a token as its system needs).  Each token's solve
+ * stops after the first iteration whose residual satisfies |r_k| <= eps |r_0|
+ * (r_0 the residual of the Jacobi start), or after max_cg iterations.
+ *   eps        relative tolerance, finite and >= 0 (MESA_ERR_ARG otherwise);
+ *              eps = 0 gives exactly the fixed-step results
+ *   max_cg     iteration limit, 0 <= max_cg <= MESA_MAX_NCG
+ *   steps_out  int32, may be NULL: the iterations each token used (4-byte
+ *              aligned; must not overlap any other array)
+ *
+ * mesa_forward_tol: mesa_forward_ex with out required, no final states;
+ *   steps_out [batch, heads, seq_len].  Two kernel launches. */
+int mesa_forward_tol(const void* q, const void* k, const void* v, const float* gamma,
+                     const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                     int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps,
+                     int chunk, int precision, float* out, float* qstar_out, int32_t* steps_out,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* mesa_decode_step_tol: mesa_decode_step with a tolerance; steps_out [batch, heads]. */
+int mesa_decode_step_tol(float* state_H, float* state_G, const void* q, const void* k, const void* v,
+                         const float* gamma, const float* beta, const float* lambda, int64_t batch,
+                         int64_t heads, int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps,
+                         float* out, int32_t* steps_out, void* stream);
 
 /* Static text for a status code (never NULL). */
 const char* mesa_status_string(int status);

@@ -1,7 +1,7 @@
 // Chunked conjugate gradients + read-out on the gfx950 matrix cores (bf16
 // operands, fp32 accumulation), for bf16 q, k, v and chunk C = 64.
 //
-// Same mathematics as the fp32 path (App. C, Alg. 1 with tolerance 0; App. D,
+// Same mathematics as the fp32 path (App. C, Alg. 1 with its relative tolerance; App. D,
 // Eq. q_star_parallel and Eq. gla): for the chunk starting after token c,
 // with zeta_j = zeta_{c+j,c} and Z[i][j] = zeta_{c+j,c+i},
 //
@@ -537,7 +537,9 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
             part += r[mt][0] * r[mt][0] + r[mt][1] * r[mt][1] + r[mt][2] * r[mt][2] + r[mt][3] * r[mt][3];
         }
         float delta = col_sum(part);
+        const float thr = a.eps2 * delta;  // Alg. 1: the column stops once |r|^2 <= eps^2 |r_0|^2
         bool active = delta >= kMinNormal;
+        int steps = 0;  // iterations that updated x
 
         // ---- every wave is done with sHf, sKT, sKU and sQ: the next chunk's loads may land
         // there while this chunk's CG runs (the barrier also waits for this wave's memory
@@ -556,11 +558,12 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         float g_nx = 1.0f, b_nx = 0.0f, lam_nx = 0.0f;
         int pieces = 0;  // pieces of the next chunk's loads issued so far
 
-        // One CG step (App. C, Alg. 1 with tolerance 0), branch-free: a stopped column takes
-        // alpha = 0 and keeps x.  A column stops when p^T A p is not a positive normal number
-        // (alpha would need the reciprocal of a subnormal) or when the new squared residual
-        // falls below the smallest normal number (relative to |q|^2, which the scaling above
-        // keeps in [1/4, 2)); Alg. 1 stops at exactly zero.
+        // One CG step (App. C, Alg. 1), branch-free: a stopped column takes alpha = 0 and
+        // keeps x.  A column stops, after its x update, when the new squared residual meets
+        // Alg. 1's relative test (<= eps^2 |r_0|^2; with eps = 0 Alg. 1 stops at exactly zero)
+        // or falls below the smallest normal number (relative to |q|^2, which the scaling
+        // above keeps in [1/4, 2)); it stops without an update when p^T A p is not a
+        // positive normal number (alpha would need the reciprocal of a subnormal).
         for (int it = 0; it < a.n_cg; ++it) {
             if (!__any(active)) break;
             if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
@@ -577,6 +580,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
             for (int mt = 0; mt < MT; ++mt) acc += p[mt] * w[mt];
             const float pw = col_sum((acc[0] + acc[1]) + (acc[2] + acc[3]));
             const bool act1 = active && pw >= kMinNormal;
+            steps += act1 ? 1 : 0;
             if (act1) {
                 const float alpha = delta * __builtin_amdgcn_rcpf(pw);
 #pragma unroll
@@ -589,7 +593,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) acc += r[mt] * r[mt];
             const float dn = col_sum((acc[0] + acc[1]) + (acc[2] + acc[3]));
-            const bool act2 = act1 && dn >= kMinNormal;
+            const bool act2 = act1 && dn >= kMinNormal && dn > thr;
             if (act2) {
                 const float bcg = dn * __builtin_amdgcn_rcpf(delta);
 #pragma unroll
@@ -612,6 +616,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         // publishes G_c to every wave
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         __syncthreads();
+        if (a.steps && g == 0 && j < valid) a.steps[tok0 + j] = steps;
         if (a.qstar && j < valid) {
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)

@@ -1,7 +1,8 @@
 // Chunked conjugate gradients + read-out of the Mesa layer, fp32 products.
 //
 // One workgroup solves the C systems (H_t + Lambda) q*_t = q_t of one chunk
-// together (App. C, Alg. 1 with tolerance 0; App. D, Eq. q_star_parallel) and
+// together (App. C, Alg. 1, at most n_cg iterations and its relative tolerance;
+// App. D, Eq. q_star_parallel) and
 // then forms o_t = G_t q*_t (App. D, Eq. gla).  With c the chunk start, j the
 // in-chunk token, Z[i][j] = zeta_{c+j,c+i} (Z upper triangular, unit diagonal)
 // and zeta_j = zeta_{c+j,c}, every CG product over the chunk is
@@ -158,7 +159,9 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
         part += r[m] * r[m];
     }
     float delta = colsum(part);
+    const float thr = a.eps2 * delta;  // Alg. 1: the column stops once |r|^2 <= eps^2 |r_0|^2
     bool active = delta > 0.0f;
+    int steps = 0;  // iterations that updated x
     for (int it = 0; it < a.n_cg; ++it) {
         if (!__syncthreads_or(active)) break;
         matvec(p, w);
@@ -174,13 +177,14 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
                 x[m] += alpha * p[m];
                 r[m] -= alpha * w[m];
             }
+            ++steps;
         }
         part = 0.0f;
 #pragma unroll
         for (int m = 0; m < NE; ++m) part += r[m] * r[m];
         const float dn = colsum(part);
         if (active) {
-            if (dn == 0.0f) {
+            if (dn <= thr) {
                 active = false;
             } else {
                 const float beta_cg = dn / delta;
@@ -190,6 +194,8 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
             }
         }
     }
+
+    if (a.steps && a0 == 0 && j < valid) a.steps[tok0 + j] = steps;
 
     // Read-out o_t = G_t q*_t, chunkwise.
     __syncthreads();

@@ -10,11 +10,11 @@
 //   1. H <- gamma H + beta k k^T.  Thread R keeps row R of H in registers.  H is
 //      symmetric, so row R is read as column R, H[c][R] for c = 0..d_k-1; the
 //      updated values are written back in place.
-//   2. Alg. 1 with tolerance 0 on (H + Lambda) x = q: thread R owns element R of
-//      x, r, p, w; each product is a register-resident row times p, with p
-//      broadcast through LDS; the CG scalars are wave reductions combined across
-//      the waves through LDS (every wave adds the partial sums in the same order,
-//      so all waves take the same branches).
+//   2. Alg. 1 (at most n_cg iterations, relative tolerance eps) on (H + Lambda) x = q:
+//      thread R owns element R of x, r, p, w; each product is a register-resident
+//      row times p, with p broadcast through LDS; the CG scalars are wave
+//      reductions combined across the waves through LDS (every wave adds the
+//      partial sums in the same order, so all waves take the same branches).
 //   3. G <- gamma G + beta v k^T and o = G x: thread c keeps column c of G,
 //      writes it back, and the row sums of G diag(x) are reduced across lanes
 //      and waves.
@@ -109,6 +109,8 @@ void decode_step_kernel(DecodeArgs a)
     float r = qR - gemv(x);
     float p = r;
     float delta = dot(r, r);
+    const float thr = a.eps2 * delta;  // Alg. 1: stop once |r|^2 <= eps^2 |r_0|^2
+    int steps = 0;                     // iterations that updated x
     if (delta > 0.0f) {
         for (int it = 0; it < a.n_cg; ++it) {
             const float w = gemv(p);
@@ -117,12 +119,15 @@ void decode_step_kernel(DecodeArgs a)
             const float alpha = delta / pw;
             x += alpha * p;
             r -= alpha * w;
+            ++steps;
             const float dn = dot(r, r);
-            if (dn == 0.0f) break;
+            if (dn <= thr) break;
             p = r + (dn / delta) * p;
             delta = dn;
         }
     }
+
+    if (a.steps && tid == 0) a.steps[pair] = steps;
 
     // ---- 3. G update and read-out.  Thread c owns column c of G: G[e][c] for every row e
     // is read and written as one 256-byte wave access per row (like H), and the row sums

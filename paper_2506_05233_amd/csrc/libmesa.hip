@@ -2,6 +2,7 @@
 // The contract of every entry point is documented in include/libmesa.h.
 #include "libmesa.h"
 
+#include <math.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -51,12 +52,17 @@ struct FwdCall {
     size_t workspace_bytes;
     bool needs_q;       // the solve reads q and lambda
     bool needs_ws;      // the call uses the chunk-state workspace
+    float eps = 0.0f;            // CG relative tolerance (0: fixed steps)
+    int32_t* steps = nullptr;    // per-token CG iterations, may be NULL
 };
+
+bool eps_ok(float eps) { return isfinite(eps) && eps >= 0.0f; }
 
 int validate_forward(const FwdCall& c)
 {
     int st = check_sizes(c.batch, c.heads, c.seq_len, c.d_k, c.d_v, c.dtype, c.n_cg);
     if (st != MESA_OK) return st;
+    if (!eps_ok(c.eps)) return MESA_ERR_ARG;
     if (!chunk_ok(c.chunk)) return MESA_ERR_UNSUPPORTED;
     if (c.precision != MESA_PREC_AUTO && c.precision != MESA_PREC_F32 && c.precision != MESA_PREC_BF16)
         return MESA_ERR_UNSUPPORTED;
@@ -74,6 +80,7 @@ int validate_forward(const FwdCall& c)
                             static_cast<const void*>(c.qstar), static_cast<const void*>(c.final_H),
                             static_cast<const void*>(c.final_G), c.workspace})
         if (uintptr_t(ptr) % 16 != 0) return MESA_ERR_ARG;
+    if (uintptr_t(c.steps) % 4 != 0) return MESA_ERR_ARG;
     const size_t need = c.needs_ws ? mesa_forward_workspace_bytes(c.batch, c.heads, c.seq_len, c.d_k,
                                                                   c.d_v, c.chunk)
                                    : 0;
@@ -96,14 +103,15 @@ int validate_forward(const FwdCall& c)
     const Range outs[] = {range_of(c.out, c.out ? tokens * c.d_v * 4 : 0),
                           range_of(c.qstar, c.qstar ? tokens * c.d_k * 4 : 0),
                           range_of(c.final_H, c.final_H ? c.batch * c.heads * c.d_k * c.d_k * 4 : 0),
-                          range_of(c.final_G, c.final_G ? c.batch * c.heads * c.d_v * c.d_k * 4 : 0)};
+                          range_of(c.final_G, c.final_G ? c.batch * c.heads * c.d_v * c.d_k * 4 : 0),
+                          range_of(c.steps, c.steps ? tokens * 4 : 0)};
     for (const Range& o : outs) {
         if (o.lo == o.hi) continue;
         for (const Range& i : ins)
             if (i.lo != i.hi && overlaps(o, i)) return MESA_ERR_ARG;
     }
-    for (int x = 0; x < 4; ++x)
-        for (int y = x + 1; y < 4; ++y)
+    for (int x = 0; x < 5; ++x)
+        for (int y = x + 1; y < 5; ++y)
             if (outs[x].lo != outs[x].hi && outs[y].lo != outs[y].hi && overlaps(outs[x], outs[y]))
                 return MESA_ERR_ARG;
     return MESA_OK;
@@ -157,7 +165,8 @@ int launch_solve(const FwdCall& c, hipStream_t s)
     if (c.seq_len == 0) return MESA_OK;
     const ForwardShape shape = shape_of(c);
     const int prec = resolve_precision(c);
-    mesa::CgArgs ca{shape, c.q, c.k, c.v, c.gamma, c.beta, c.lambda, ws_H(c), ws_G(c), c.n_cg, c.out, c.qstar};
+    mesa::CgArgs ca{shape, c.q, c.k, c.v, c.gamma, c.beta, c.lambda, ws_H(c), ws_G(c), c.n_cg, c.out, c.qstar,
+                    c.eps * c.eps, c.steps};
     const hipError_t e = prec == MESA_PREC_BF16 ? mesa::launch_chunk_cg_bf16(ca, s)
                                                 : mesa::launch_chunk_cg_f32(ca, s);
     return e == hipSuccess ? MESA_OK : MESA_ERR_HIP;
@@ -167,7 +176,7 @@ int launch_solve(const FwdCall& c, hipStream_t s)
 
 extern "C" {
 
-int mesa_version(void) { return 100; }
+int mesa_version(void) { return 101; }
 
 const char* mesa_status_string(int status)
 {
@@ -176,7 +185,7 @@ const char* mesa_status_string(int status)
         case MESA_ERR_NULL: return "a required pointer is NULL";
         case MESA_ERR_SHAPE: return "a size is negative or the sizes are inconsistent";
         case MESA_ERR_UNSUPPORTED: return "d_k, d_v, chunk, dtype or precision not supported";
-        case MESA_ERR_ARG: return "n_cg out of range, a misaligned pointer, or an output overlapping an input";
+        case MESA_ERR_ARG: return "n_cg or eps out of range, a misaligned pointer, or an output overlapping an input";
         case MESA_ERR_WORKSPACE: return "workspace too small";
         case MESA_ERR_HIP: return "the HIP runtime refused a launch";
         default: return "unknown status";
@@ -253,11 +262,22 @@ int mesa_decode_step(float* state_H, float* state_G, const void* q, const void* 
                      int64_t heads, int64_t d_k, int64_t d_v, int dtype, int n_cg, float* out,
                      void* stream)
 {
-    int st = check_sizes(batch, heads, 1, d_k, d_v, dtype, n_cg);
+    return mesa_decode_step_tol(state_H, state_G, q, k, v, gamma, beta, lambda, batch, heads, d_k, d_v,
+                                dtype, n_cg, 0.0f, out, nullptr, stream);
+}
+
+int mesa_decode_step_tol(float* state_H, float* state_G, const void* q, const void* k, const void* v,
+                         const float* gamma, const float* beta, const float* lambda, int64_t batch,
+                         int64_t heads, int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps,
+                         float* out, int32_t* steps_out, void* stream)
+{
+    int st = check_sizes(batch, heads, 1, d_k, d_v, dtype, max_cg);
     if (st != MESA_OK) return st;
+    if (!eps_ok(eps)) return MESA_ERR_ARG;
     if (batch == 0 || heads == 0) return MESA_OK;
     if (!state_H || !state_G || !q || !k || !v || !gamma || !beta || !lambda || !out)
         return MESA_ERR_NULL;
+    if (uintptr_t(steps_out) % 4 != 0) return MESA_ERR_ARG;
     const int64_t pairs = batch * heads;
     if (pairs > (int64_t(1) << 31) - 1) return MESA_ERR_SHAPE;
     const int64_t in_sz = dtype == MESA_DTYPE_BF16 ? 2 : 4;
@@ -266,17 +286,40 @@ int mesa_decode_step(float* state_H, float* state_G, const void* q, const void* 
                              range_of(v, pairs * d_v * in_sz), range_of(gamma, pairs * 4),
                              range_of(beta, pairs * 4), range_of(lambda, heads * d_k * 4)};
         const Range outs[] = {range_of(state_H, pairs * d_k * d_k * 4),
-                              range_of(state_G, pairs * d_v * d_k * 4), range_of(out, pairs * d_v * 4)};
-        for (const Range& o : outs)
+                              range_of(state_G, pairs * d_v * d_k * 4), range_of(out, pairs * d_v * 4),
+                              range_of(steps_out, steps_out ? pairs * 4 : 0)};
+        for (const Range& o : outs) {
+            if (o.lo == o.hi) continue;
             for (const Range& i : ins)
                 if (overlaps(o, i)) return MESA_ERR_ARG;
-        if (overlaps(outs[0], outs[1]) || overlaps(outs[0], outs[2]) || overlaps(outs[1], outs[2]))
-            return MESA_ERR_ARG;
+        }
+        for (int x = 0; x < 4; ++x)
+            for (int y = x + 1; y < 4; ++y)
+                if (outs[x].lo != outs[x].hi && outs[y].lo != outs[y].hi && overlaps(outs[x], outs[y]))
+                    return MESA_ERR_ARG;
     }
     mesa::DecodeArgs da{batch, heads, int(d_k), int(d_v), dtype == MESA_DTYPE_BF16, state_H, state_G,
-                        q, k, v, gamma, beta, lambda, n_cg, out};
+                        q, k, v, gamma, beta, lambda, max_cg, out, eps * eps, steps_out};
     return mesa::launch_decode_step(da, static_cast<hipStream_t>(stream)) == hipSuccess ? MESA_OK
                                                                                        : MESA_ERR_HIP;
+}
+
+int mesa_forward_tol(const void* q, const void* k, const void* v, const float* gamma,
+                     const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                     int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps,
+                     int chunk, int precision, float* out, float* qstar_out, int32_t* steps_out,
+                     void* workspace, size_t workspace_bytes, void* stream)
+{
+    if (!out) return MESA_ERR_NULL;
+    FwdCall c{q, k, v, gamma, beta, lambda, batch, heads, seq_len, d_k, d_v, dtype, max_cg, chunk,
+              precision, out, qstar_out, nullptr, nullptr, workspace, workspace_bytes, true, true,
+              eps, steps_out};
+    int st = validate_forward(c);
+    if (st != MESA_OK || batch == 0 || heads == 0) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = launch_states(c, true, s);
+    if (st != MESA_OK) return st;
+    return launch_solve(c, s);
 }
 
 }  // extern "C"

@@ -55,9 +55,11 @@ struct CgArgs {
     const float* lambda;
     const void* Hs;   // chunk states, plain fp32 (fp32 path) or bf16 fragments (bf16 path)
     const void* Gs;
-    int n_cg;
+    int n_cg;        // at most n_cg CG iterations per token
     float* out;
-    float* qstar;  // may be null
+    float* qstar;    // may be null
+    float eps2;      // Alg. 1 relative tolerance, squared: stop once |r|^2 <= eps2 |r_0|^2
+    int32_t* steps;  // may be null: [B, H, T] iterations each token used
 };
 hipError_t launch_chunk_cg_f32(const CgArgs& a, hipStream_t stream);
 hipError_t launch_chunk_cg_bf16(const CgArgs& a, hipStream_t stream);
@@ -78,6 +80,8 @@ struct DecodeArgs {
     const float* lambda;
     int n_cg;
     float* out;
+    float eps2;      // Alg. 1 relative tolerance, squared (0: fixed steps)
+    int32_t* steps;  // may be null: [batch, heads] iterations each pair used
 };
 hipError_t launch_decode_step(const DecodeArgs& a, hipStream_t stream);
 

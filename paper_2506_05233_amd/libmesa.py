@@ -28,8 +28,8 @@ MESA_ERR_HIP = 6
 MESA_MAX_NCG = 1024
 
 EXPORTED = ("mesa_forward", "mesa_forward_ex", "mesa_forward_states", "mesa_forward_solve",
-            "mesa_forward_workspace_bytes", "mesa_decode_step", "mesa_status_string",
-            "mesa_version")
+            "mesa_forward_tol", "mesa_forward_workspace_bytes", "mesa_decode_step",
+            "mesa_decode_step_tol", "mesa_status_string", "mesa_version")
 
 _lib = None
 
@@ -63,6 +63,13 @@ def load():
     lib.mesa_forward_solve.restype = ci
     lib.mesa_decode_step.argtypes = [fp, fp, vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, ci, ci, fp, vp]
     lib.mesa_decode_step.restype = ci
+    cf = ctypes.c_float
+    lib.mesa_forward_tol.argtypes = [vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, cf, ci, ci,
+                                     fp, fp, vp, vp, sz, vp]
+    lib.mesa_forward_tol.restype = ci
+    lib.mesa_decode_step_tol.argtypes = [fp, fp, vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, ci, ci, cf,
+                                         fp, vp, vp]
+    lib.mesa_decode_step_tol.restype = ci
     lib.mesa_status_string.argtypes = [ci]
     lib.mesa_status_string.restype = ctypes.c_char_p
     lib.mesa_version.argtypes = []
@@ -133,10 +140,13 @@ def _stream(device):
 
 
 def forward(q, k, v, gamma, beta, lam, n_cg, chunk=64, precision=MESA_PREC_AUTO, want_qstar=False,
-            want_states=False, out=None, workspace=None):
+            want_states=False, out=None, workspace=None, eps=None, want_steps=False):
     """Mesa forward over q, k [B,H,T,d_k], v [B,H,T,d_v] (fp32 or bf16, same dtype),
     gamma, beta [B,H,T] fp32, lam [H,d_k] fp32.  Returns out [B,H,T,d_v] fp32, or a
-    dict with "out" and, if asked, "qstar" [B,H,T,d_k], "H" [B,H,d_k,d_k], "G" [B,H,d_v,d_k].
+    dict with "out" and, if asked, "qstar" [B,H,T,d_k], "H" [B,H,d_k,d_k], "G" [B,H,d_v,d_k],
+    "steps" [B,H,T] int32 (CG iterations per token).
+    eps: CG relative tolerance (Alg. 1's |r_k| <= eps |r_0|; n_cg is then the limit),
+    through mesa_forward_tol; None or 0 with want_steps False is the fixed-step solve.
     Runs on torch's current stream of q's device."""
     torch = _torch()
     lib = load()
@@ -157,6 +167,22 @@ def forward(q, k, v, gamma, beta, lam, n_cg, chunk=64, precision=MESA_PREC_AUTO,
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     qstar = torch.empty((B, H, T, dk), dtype=torch.float32, device=dev) if want_qstar else None
+    if eps is not None or want_steps:
+        if want_states:
+            raise ValueError("mesa_forward_tol returns no final states")
+        steps = torch.empty((B, H, T), dtype=torch.int32, device=dev) if want_steps else None
+        st = lib.mesa_forward_tol(_ptr(q), _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam), B, H,
+                                  T, dk, dv, code, int(n_cg), float(eps or 0.0), int(chunk),
+                                  int(precision), _ptr(out), _ptr(qstar), _ptr(steps), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(dev))
+        if st != MESA_OK:
+            raise MesaError(st, "mesa_forward_tol")
+        res = {"out": out}
+        if want_qstar:
+            res["qstar"] = qstar
+        if want_steps:
+            res["steps"] = steps
+        return res if (want_qstar or want_steps) else out
     fH = torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev) if want_states else None
     fG = torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev) if want_states else None
     st = lib.mesa_forward_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam), B, H, T,
@@ -251,10 +277,11 @@ def prefill_states(k, v, gamma, beta, chunk=64):
     return fH, fG
 
 
-def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, out=None):
+def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, out=None, eps=None, steps_out=None):
     """One recurrent step, in place on state_H [N,H,d_k,d_k] and state_G [N,H,d_v,d_k].
     q, k [N,H,d_k], v [N,H,d_v] fp32 or bf16; gamma, beta [N,H]; lam [H,d_k].
-    Returns out [N,H,d_v] fp32."""
+    eps / steps_out (int32 [N,H]): CG relative tolerance and iteration counts, through
+    mesa_decode_step_tol.  Returns out [N,H,d_v] fp32."""
     torch = _torch()
     lib = load()
     N, H, dk = q.shape
@@ -271,6 +298,16 @@ def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, out=None):
     if out is None:
         out = torch.empty((N, H, dv), dtype=torch.float32, device=dev)
     _check(out, "out", (N, H, dv), torch.float32, dev)
+    if eps is not None or steps_out is not None:
+        if steps_out is not None:
+            _check(steps_out, "steps_out", (N, H), torch.int32, dev)
+        st = lib.mesa_decode_step_tol(_ptr(state_H), _ptr(state_G), _ptr(q), _ptr(k), _ptr(v),
+                                      _ptr(gamma), _ptr(beta), _ptr(lam), N, H, dk, dv, _dtype_code(q),
+                                      int(n_cg), float(eps or 0.0), _ptr(out), _ptr(steps_out),
+                                      _stream(dev))
+        if st != MESA_OK:
+            raise MesaError(st, "mesa_decode_step_tol")
+        return out
     st = lib.mesa_decode_step(_ptr(state_H), _ptr(state_G), _ptr(q), _ptr(k), _ptr(v), _ptr(gamma),
                               _ptr(beta), _ptr(lam), N, H, dk, dv, _dtype_code(q), int(n_cg),
                               _ptr(out), _stream(dev))

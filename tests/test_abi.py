@@ -53,7 +53,7 @@ def test_status_strings(lib):
     for s in range(7):
         assert L.status_string(s)
     assert L.status_string(99) == "unknown status"
-    assert L.version() == 100
+    assert L.version() == 101
 
 
 def test_workspace_bytes(lib):
@@ -67,7 +67,7 @@ def test_workspace_bytes(lib):
 
 # fake, non-overlapping device addresses
 P = {n: 0x10000000 * (i + 1) for i, n in enumerate(
-    ["q", "k", "v", "g", "b", "lam", "out", "qs", "fh", "fg", "ws", "H", "G"])}
+    ["q", "k", "v", "g", "b", "lam", "out", "qs", "fh", "fg", "ws", "H", "G", "st"])}
 
 
 def _fwd(lib, **kw):
@@ -117,6 +117,64 @@ def test_forward_empty_batch_is_a_noop(lib):
 def test_plain_forward_requires_out(lib):
     assert lib.mesa_forward(P["q"], P["k"], P["v"], P["g"], P["b"], P["lam"], 1, 1, 64, 64, 64, 0, 3,
                             64, None, P["ws"], 1 << 30, None) == L.MESA_ERR_NULL
+
+
+def _fwd_tol(lib, **kw):
+    a = dict(q=P["q"], k=P["k"], v=P["v"], gamma=P["g"], beta=P["b"], lam=P["lam"], B=2, H=3, T=128,
+             dk=64, dv=64, dtype=0, n_cg=30, eps=1e-4, chunk=64, prec=0, out=P["out"], qstar=None,
+             steps=P["st"], ws=P["ws"], ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.mesa_forward_tol(a["q"], a["k"], a["v"], a["gamma"], a["beta"], a["lam"], a["B"],
+                                a["H"], a["T"], a["dk"], a["dv"], a["dtype"], a["n_cg"], a["eps"],
+                                a["chunk"], a["prec"], a["out"], a["qstar"], a["steps"], a["ws"],
+                                a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(eps=-1e-3), L.MESA_ERR_ARG),
+    (dict(eps=float("nan")), L.MESA_ERR_ARG),
+    (dict(eps=float("inf")), L.MESA_ERR_ARG),
+    (dict(out=None), L.MESA_ERR_NULL),
+    (dict(n_cg=L.MESA_MAX_NCG + 1), L.MESA_ERR_ARG),
+    (dict(steps=P["st"] + 2), L.MESA_ERR_ARG),        # steps not 4-byte aligned
+    (dict(steps=P["q"] + 16), L.MESA_ERR_ARG),        # steps overlaps q
+    (dict(steps=P["out"] + 64), L.MESA_ERR_ARG),      # steps overlaps out
+    (dict(dk=96), L.MESA_ERR_UNSUPPORTED),
+    (dict(ws_bytes=16), L.MESA_ERR_WORKSPACE),
+])
+def test_forward_tol_rejects_bad_arguments(lib, kw, status):
+    assert _fwd_tol(lib, **kw) == status
+
+
+def test_forward_tol_empty_batch_is_a_noop(lib):
+    assert _fwd_tol(lib, B=0) == L.MESA_OK
+
+
+def _dec_tol(lib, **kw):
+    a = dict(H=P["H"], G=P["G"], q=P["q"], k=P["k"], v=P["v"], gamma=P["g"], beta=P["b"],
+             lam=P["lam"], N=4, Hh=2, dk=128, dv=128, dtype=1, n_cg=30, eps=1e-4, out=P["out"],
+             steps=P["st"])
+    a.update(kw)
+    return lib.mesa_decode_step_tol(a["H"], a["G"], a["q"], a["k"], a["v"], a["gamma"], a["beta"],
+                                    a["lam"], a["N"], a["Hh"], a["dk"], a["dv"], a["dtype"], a["n_cg"],
+                                    a["eps"], a["out"], a["steps"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(eps=-0.5), L.MESA_ERR_ARG),
+    (dict(eps=float("nan")), L.MESA_ERR_ARG),
+    (dict(steps=P["st"] + 1), L.MESA_ERR_ARG),
+    (dict(steps=P["H"] + 4), L.MESA_ERR_ARG),         # steps overlaps the H state
+    (dict(steps=P["g"]), L.MESA_ERR_ARG),             # steps overlaps gamma
+    (dict(out=None), L.MESA_ERR_NULL),
+    (dict(n_cg=-1), L.MESA_ERR_ARG),
+])
+def test_decode_tol_rejects_bad_arguments(lib, kw, status):
+    assert _dec_tol(lib, **kw) == status
+
+
+def test_decode_tol_empty_is_a_noop(lib):
+    assert _dec_tol(lib, N=0) == L.MESA_OK
 
 
 def _dec(lib, **kw):

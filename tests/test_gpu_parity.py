@@ -312,3 +312,87 @@ def test_decode_steps_from_zero_equal_forward():
                                   d["beta"][:, :, t].contiguous(), d["lam"], 10).cpu().numpy())
     dec = np.stack(outs, axis=2)
     assert rel_l2(dec, fwd) <= 1e-4
+
+
+# --------------------------------------------- dynamic stopping (App. C, Alg. 1, eps > 0)
+def _steps_agreement(got_steps, ref_steps, what):
+    diff = np.abs(got_steps.astype(np.int64) - ref_steps.astype(np.int64))
+    _say("%s: steps equal %.4f, max |diff| %d, mean steps gpu %.2f oracle %.2f"
+         % (what, np.mean(diff == 0), diff.max(), got_steps.mean(), ref_steps.mean()))
+    return diff
+
+
+@pytest.mark.parametrize("eps", [1e-2, 1e-4])
+def test_forward_tolerance_f32_matches_oracle(eps):
+    """fp32 path: the iteration counts match the oracle's except where a residual
+    sits within rounding of the threshold (then by one step); outputs of tokens
+    with equal counts match to the fp32 tolerance, the others to O(eps)."""
+    x = W.forward_inputs(2, 2, 3 * 64 + 21, 64, 64, "f32", 3.0, seed=61)
+    d = to_device(x, "f32")
+    res = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], 40, 64,
+                    precision=L.MESA_PREC_F32, eps=eps, want_steps=True)
+    torch.cuda.synchronize()
+    out, steps = res["out"].cpu().numpy(), res["steps"].cpu().numpy()
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 40, eps=eps, want_steps=True)
+    diff = _steps_agreement(steps, ref["steps"], "f32 eps=%g" % eps)
+    assert diff.max() <= 1 and np.mean(diff == 0) >= 0.98
+    same = diff == 0
+    assert rel_l2(out[same], ref["out"][same]) <= TOL_F32
+    assert rel_l2(out, ref["out"]) <= 20 * eps + TOL_F32
+    assert steps.max() < 40  # the tolerance, not the limit, ended every solve
+
+
+@pytest.mark.parametrize("eps", [1e-2, 1e-4])
+def test_forward_tolerance_bf16_path_matches_oracle(eps):
+    """Matrix-core path: recursive residuals stay within rounding of the oracle's,
+    so counts agree to a step or two and outputs to the bf16 tolerance."""
+    x = W.forward_inputs(2, 2, 2 * 64 + 40, 128, 128, "bf16", 4.0, seed=62)
+    d = to_device(x, "bf16")
+    res = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], 40, 64,
+                    precision=L.MESA_PREC_BF16, eps=eps, want_steps=True)
+    torch.cuda.synchronize()
+    out, steps = res["out"].cpu().numpy(), res["steps"].cpu().numpy()
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 40, eps=eps, want_steps=True)
+    diff = _steps_agreement(steps, ref["steps"], "bf16 eps=%g" % eps)
+    assert diff.max() <= 3 and np.mean(diff) <= 0.5
+    e = rel_l2(out, ref["out"])
+    _say("  bf16 eps=%g out %.3e" % (eps, e))
+    assert e <= TOL_BF16
+
+
+def test_tolerance_zero_equals_fixed_steps_bitwise():
+    x = W.forward_inputs(1, 2, 150, 128, 128, "bf16", 4.0, seed=63)
+    d = to_device(x, "bf16")
+    for prec in (L.MESA_PREC_BF16, L.MESA_PREC_F32):
+        a = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], 15, 64, precision=prec)
+        b = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], 15, 64, precision=prec,
+                      eps=0.0, want_steps=True)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b["out"]), prec
+        assert int(b["steps"].max()) == 15
+
+
+def test_decode_tolerance_matches_oracle():
+    x = W.forward_inputs(3, 2, 1, 128, 128, "f32", 3.0, seed=64)
+    rng = np.random.default_rng(64)
+    H0, G0 = oracle.unrolled_states(rng.standard_normal((3, 2, 300, 128)) / 11,
+                                    rng.standard_normal((3, 2, 300, 128)),
+                                    np.full((3, 2, 300), 0.99), np.full((3, 2, 300), 0.5))
+    H0, G0 = H0.astype(np.float32), G0.astype(np.float32)
+    d = to_device({k: v[:, :, 0] for k, v in x.items() if k != "lam"}, "f32")
+    lam = torch.from_numpy(x["lam"]).cuda()
+    for eps in (0.0, 1e-3, 1e-5):
+        dH, dG = torch.from_numpy(H0).cuda(), torch.from_numpy(G0).cuda()
+        st = torch.zeros((3, 2), dtype=torch.int32, device="cuda")
+        out = L.decode_step(dH, dG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], lam, 40, eps=eps,
+                            steps_out=st)
+        rst = np.zeros((3, 2), dtype=np.int32)
+        ro, rH, rG = oracle.decode_step(H0, G0, x["q"][:, :, 0], x["k"][:, :, 0], x["v"][:, :, 0],
+                                        x["gamma"][:, :, 0], x["beta"][:, :, 0], x["lam"], 40, eps=eps,
+                                        steps_out=rst)
+        got = st.cpu().numpy()
+        _say("decode eps=%g steps gpu %s oracle %s" % (eps, got.ravel().tolist(), rst.ravel().tolist()))
+        assert np.abs(got - rst).max() <= 1
+        same = got == rst
+        assert rel_l2(out.cpu().numpy()[same], ro[same]) <= TOL_F32
+        assert rel_l2(dH.cpu().numpy(), rH) <= 1e-6 and rel_l2(dG.cpu().numpy(), rG) <= 1e-6
