@@ -10,6 +10,11 @@ dominant kernel and its algorithmic flops per launch divided by its mean event
 time give the roofline entry.  Decode (256 sequences x 16 heads, d=128,
 15 CG steps, 1024 consecutive steps) is timed after the forward steps.
 
+Two extra entries run the same forward and decode with Alg. 1's relative
+stopping test (eps = 1e-4, at most 30 iterations, the paper's dynamic
+test-time compute setting) and report tokens/s and the mean iterations used;
+they are context, not the metric.
+
 The CPU baseline is the fp64 oracle (the sequential recurrence with fixed-step
 CG) on a bounded sample of the same workload, run on the host's cores.
 
@@ -118,11 +123,36 @@ def run_forward(args, torch, L, W):
     bf16_states = args.precision == L.MESA_PREC_BF16 or (
         args.precision == L.MESA_PREC_AUTO and L.bf16_path_available(dk, dv, w.chunk, T))
     return {
-        "w": w, "wall": wall, "state_ms": state_ms, "cg_ms": cg_ms,
+        "w": w, "wall": wall, "state_ms": state_ms, "cg_ms": cg_ms, "d": d, "plan": plan,
         "flops": cg_kernel_flops(B, H, T, dk, dv, w.chunk, w.n_cg),
         "state_bytes": state_kernel_bytes(B, H, T, dk, dv, w.chunk, 2, 2 if bf16_states else 4),
         "x": x,
     }
+
+
+def run_forward_dynamic(args, torch, L, fw):
+    """The same forward with Alg. 1's relative stopping test (eps, at most
+    args.dyn_max_cg iterations): time per call and the mean iterations per token."""
+    w, d, plan = fw["w"], fw["d"], fw["plan"]
+    steps = None
+    def call():
+        return L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], args.dyn_max_cg,
+                         w.chunk, precision=args.precision, out=plan.out, workspace=plan.workspace,
+                         eps=args.eps, want_steps=True)
+    for _ in range(2):
+        steps = call()["steps"]
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"eps": args.eps, "max_cg": args.dyn_max_cg, "tokens_per_s": w.batch * w.seq_len / (ms / 1e3),
+            "ms_per_call": ms, "mean_cg_steps": float(steps.float().mean())}
 
 
 def run_decode(args, torch, L, W):
@@ -174,11 +204,29 @@ def run_decode(args, torch, L, W):
     if not bool(torch.isfinite(out).all()):
         raise RuntimeError("non-finite decode output")
     bytes_per_step = N * H * (2 * d * d * 4 * 2 + 3 * d * 2 + d * 4)
+    dyn = None
+    if args.eps > 0:  # dynamic stopping on the continuing states
+        S2 = min(S, 64)
+        st = torch.zeros((N, H), dtype=torch.int32, device=dev)
+        tot = torch.zeros((N, H), dtype=torch.int64, device=dev)
+        log("decode: timing %d steps with eps %g" % (S2, args.eps))
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(S2):
+            L.decode_step(sH, sG, q[i], k[i], v[i], gam[i], bet[i], lam, args.dyn_max_cg, out=out,
+                          eps=args.eps, steps_out=st)
+            tot += st
+        e1.record()
+        torch.cuda.synchronize()
+        ms2 = e0.elapsed_time(e1)
+        dyn = {"eps": args.eps, "max_cg": args.dyn_max_cg, "steps": S2,
+               "tokens_per_s": N * S2 / (ms2 / 1e3), "mean_cg_steps": float(tot.float().mean()) / S2}
     return {
         "workload": w.name, "steps": S, "tokens_per_s": N * S / (ms / 1e3),
         "ms_per_step": ms / S,
         "hbm_GBps": bytes_per_step * S / (ms / 1e3) / 1e9,
         "hbm_frac": bytes_per_step * S / (ms / 1e3) / 1e9 / PEAKS["hbm_gbps"],
+        "dynamic_stopping": dyn,
     }
 
 
@@ -221,6 +269,9 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=1024)
     ap.add_argument("--cpu-sequences", type=int, default=128)
     ap.add_argument("--skip-decode", action="store_true")
+    ap.add_argument("--eps", type=float, default=1e-4,
+                    help="relative CG tolerance of the extra dynamic-stopping runs (0: skip them)")
+    ap.add_argument("--dyn-max-cg", type=int, default=30, help="iteration limit of those runs")
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB once with a plain device copy "
@@ -249,6 +300,7 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    dyn = run_forward_dynamic(args, torch, L, fw) if args.eps > 0 else None
     dec = None if args.skip_decode else run_decode(args, torch, L, W)
     cpu = None if args.skip_cpu else cpu_baseline(args, fw["x"], w)
 
@@ -287,6 +339,7 @@ def main():
         "kernels_ms": {"chunk_state": fw["state_ms"], "chunk_cg": fw["cg_ms"]},
         "state_kernel_hbm": {"GBps": fw["state_bytes"] / (fw["state_ms"] / 1e3) / 1e9,
                              "frac": fw["state_bytes"] / (fw["state_ms"] / 1e3) / 1e9 / PEAKS["hbm_gbps"]},
+        "forward_dynamic_stopping": dyn,
         "decode": dec,
         "cpu_baseline": cpu,
     }
