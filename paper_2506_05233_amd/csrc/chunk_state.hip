@@ -563,11 +563,8 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                 uint16_t* base = frag_base + (bh * s.n_chunks + n) * int64_t(kStateElems);
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
-                    uint4 pk;
-                    pk.x = uint32_t(bf16_bits((__bf16)acc[0][ct][0])) | (uint32_t(bf16_bits((__bf16)acc[0][ct][1])) << 16);
-                    pk.y = uint32_t(bf16_bits((__bf16)acc[0][ct][2])) | (uint32_t(bf16_bits((__bf16)acc[0][ct][3])) << 16);
-                    pk.z = uint32_t(bf16_bits((__bf16)acc[1][ct][0])) | (uint32_t(bf16_bits((__bf16)acc[1][ct][1])) << 16);
-                    pk.w = uint32_t(bf16_bits((__bf16)acc[1][ct][2])) | (uint32_t(bf16_bits((__bf16)acc[1][ct][3])) << 16);
+                    const uint4 pk = make_uint4(pack_bf16x2(acc[0][ct][0], acc[0][ct][1]), pack_bf16x2(acc[0][ct][2], acc[0][ct][3]),
+                                                pack_bf16x2(acc[1][ct][0], acc[1][ct][1]), pack_bf16x2(acc[1][ct][2], acc[1][ct][3]));
                     *reinterpret_cast<uint4*>(base + (((ct0 + ct) * NS + sblk) * kWave + lane) * 8) = pk;
                 }
             }
