@@ -118,7 +118,11 @@ int mesa_forward(const void* q, const void* k, const void* v, const float* gamma
  * final_H and final_G are the recurrent state that mesa_decode_step continues
  * from (prefill -> decode).  If out is NULL only the state scan runs: then
  * qstar_out must be NULL, final_H and final_G must be given, and workspace may
- * be NULL with workspace_bytes 0. */
+ * be NULL with workspace_bytes 0.  A workspace given to such a call must hold
+ * mesa_forward_workspace_bytes(...) (MESA_ERR_WORKSPACE otherwise) and overlap
+ * no input or output (MESA_ERR_ARG); the scan then uses it as scratch, which
+ * lets it split the walk over the chunks into segments that run side by side
+ * when there are few sequences (see mesa_forward_states). */
 int mesa_forward_ex(const void* q, const void* k, const void* v, const float* gamma,
                     const float* beta, const float* lambda, int64_t batch, int64_t heads,
                     int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
@@ -134,7 +138,12 @@ int mesa_forward_ex(const void* q, const void* k, const void* v, const float* ga
  * final_G.  `precision` must be the one the following mesa_forward_solve
  * uses: it selects the workspace layout (fp32 states for MESA_PREC_F32,
  * bf16 states laid out as matrix-core operands for MESA_PREC_BF16).
- * One kernel launch. */
+ * One kernel launch, or two on the bf16 path when batch x heads is too small
+ * to occupy the GPU (at most 64 sequences): the chunks are then cut into
+ * segments whose totals a first launch computes from a zero state, and the
+ * second walks every segment from the state entering it (the chunk recurrence
+ * of App. D applied to whole segments), with the unused half of the workspace
+ * as scratch for the totals. */
 int mesa_forward_states(const void* k, const void* v, const float* gamma, const float* beta,
                         int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v,
                         int dtype, int chunk, int precision, float* final_H, float* final_G,

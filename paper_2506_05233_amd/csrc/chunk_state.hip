@@ -252,166 +252,6 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
     }
 }
 
-// Fragment-layout variant (bf16 k and v, chunk 64), feeding the bf16 CG
-// kernel.  Here the state is tiled as [H | G^T] (rows = key features,
-// d_k x (d_k + d_v)): A operand = the chunk's keys, B operand = w ⊙ k (columns
-// of H) or w ⊙ v (columns of G^T), in the same hi/lo two-pass form.  After each
-// chunk a lane writes its four fp32 accumulator values, rounded to bf16, into
-// the A-fragment slots that hold them: the value at row R, column c of a 16x16
-// tile is X[c][R] of H (symmetric) or of G, i.e. fragment (c/16, R/32), lane
-// (g, c%16), element 4 (R/16 % 2) + (R%4), with g = (R%16)/4.
-__global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
-{
-    constexpr int C = 64;
-    constexpr int KST = C / 32;
-    constexpr int LDT = C + 8;
-    const ForwardShape s = a.s;
-    const int dk = s.d_k, dv = s.d_v;
-    const int nrt = dk / 64, nct = (dk + dv) / 32;
-    const int blk = xcd_major_block(blockIdx.x, gridDim.x);
-    const int ct = blk % nct;
-    const int rt = (blk / nct) % nrt;
-    const int64_t bh = blk / (nct * nrt);
-    const int row0 = rt * 64;                 // key-feature rows of the tile
-    const bool isG = ct * 32 >= dk;           // columns of G^T (value features)
-    const int colX = isG ? ct * 32 - dk : ct * 32;
-    const int nX = isG ? dv : dk;             // width of the column source
-    const uint16_t* kp = static_cast<const uint16_t*>(a.k);
-    const uint16_t* xp = static_cast<const uint16_t*>(isG ? a.v : a.k);
-    const int tid = threadIdx.x;
-    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-    const int lane = tid % kWave;
-    const int g = lane / 16, ln = lane % 16;
-
-    __shared__ __attribute__((aligned(16))) uint16_t sA[64 * LDT];   // k_i[row], as [row][i]
-    __shared__ __attribute__((aligned(16))) uint16_t sBh[32 * LDT];  // hi(w_i x_i[c]), as [c][i]
-    __shared__ __attribute__((aligned(16))) uint16_t sBl[32 * LDT];
-    __shared__ float sW[kWave];  // w_i = beta_i zeta_{chunk end, i} of the chunk being staged
-
-    // inputs of one chunk, held in registers: prefetched two chunks ahead
-    struct ChunkRegs {
-        uint4 ra[2];  // A rows of tokens 2p, 2p+1
-        uint4 rb[2];  // B columns of tokens 2p, 2p+1
-        float gam, bet;
-        int valid;
-    };
-    auto load_chunk = [&](int n, ChunkRegs& R) {
-        const int64_t t0 = int64_t(n) * C;
-        const int valid = int(min<int64_t>(C, s.seq_len - t0));
-        const int64_t tok0 = bh * s.seq_len + t0;
-        R.valid = valid;
-        // thread t: tokens 2p, 2p+1 with p = t % 32; A rows f8 = 8 (t / 32), B columns f8 = 8 (t / 32 % 4)
-        {
-            const int p = tid % 32, f8 = 8 * (tid / 32);
-#pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
-                const int i = 2 * p + h2;
-                R.ra[h2] = i < valid ? *reinterpret_cast<const uint4*>(kp + (tok0 + i) * dk + row0 + f8) : make_uint4(0, 0, 0, 0);
-            }
-        }
-        {
-            const int p = tid % 32, f8 = 8 * ((tid / 32) % 4);
-#pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
-                const int i = 2 * p + h2;
-                R.rb[h2] = i < valid ? *reinterpret_cast<const uint4*>(xp + (tok0 + i) * nX + colX + f8) : make_uint4(0, 0, 0, 0);
-            }
-        }
-        R.gam = lane < valid ? a.gamma[tok0 + lane] : 1.0f;
-        R.bet = lane < valid ? a.beta[tok0 + lane] : 0.0f;
-    };
-
-    // fragment slot of this lane's tile values
-    const int MTX = (isG ? dv : dk) / 16, KS = dk / 32;
-    const int h = (row0 / 16 + wave) % 2;          // which half of the 32-long contraction
-    const int sidx = (row0 + 16 * wave) / 32;      // contraction step of these rows
-    uint16_t* frag_base = static_cast<uint16_t*>(isG ? a.Gs : a.Hs);
-
-    f32x4 acc[2] = {f32x4{0.0f, 0.0f, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}};
-    auto step = [&](int n, ChunkRegs& R) {
-        const float lg = wave_scan_add((lane < R.valid && R.gam > 0.0f) ? logf(R.gam) : 0.0f);
-        const int zl = wave_scan_max((lane < R.valid && !(R.gam > 0.0f)) ? lane : -1);
-        const float lgE = lane_value(lg, C - 1);
-        const int zlE = lane_value(zl, C - 1);
-        const float wl = lane < R.valid ? R.bet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
-        const float D = zlE >= 0 ? 0.0f : expf(lgE);
-
-        if (wave == 0) sW[lane] = wl;  // all waves computed the same weights
-        __syncthreads();
-        stage_token_pair(reinterpret_cast<uint32_t*>(sA), LDT / 2, 8 * (tid / 32), tid % 32, R.ra[0], R.ra[1]);
-        {
-            // B = hi/lo split of w_i x_i[c] for tokens 2p, 2p+1 (threads t < 128)
-            const int p = tid % 32, f8 = 8 * ((tid / 32) % 4);
-            const float w0 = sW[2 * p], w1 = sW[2 * p + 1];
-            if (tid < 128) {
-                const uint32_t a4[4] = {R.rb[0].x, R.rb[0].y, R.rb[0].z, R.rb[0].w};
-                const uint32_t b4[4] = {R.rb[1].x, R.rb[1].y, R.rb[1].z, R.rb[1].w};
-                uint32_t* hi32 = reinterpret_cast<uint32_t*>(sBh);
-                uint32_t* lo32 = reinterpret_cast<uint32_t*>(sBl);
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const uint32_t ba = (q & 1) ? (a4[q / 2] >> 16) : (a4[q / 2] & 0xffffu);
-                    const uint32_t bb = (q & 1) ? (b4[q / 2] >> 16) : (b4[q / 2] & 0xffffu);
-                    const float va = w0 * bf16_bits_to_f32(ba), vb = w1 * bf16_bits_to_f32(bb);
-                    const __bf16 ha = (__bf16)va, hb = (__bf16)vb;
-                    const __bf16 la = (__bf16)(va - (float)ha), lb = (__bf16)(vb - (float)hb);
-                    hi32[(f8 + q) * (LDT / 2) + p] = uint32_t(bf16_bits(ha)) | (uint32_t(bf16_bits(hb)) << 16);
-                    lo32[(f8 + q) * (LDT / 2) + p] = uint32_t(bf16_bits(la)) | (uint32_t(bf16_bits(lb)) << 16);
-                }
-            }
-        }
-        __syncthreads();
-        if (n + 2 < s.n_chunks) load_chunk(n + 2, R);
-
-        if (a.store_chunks) {
-            uint16_t* base = frag_base + (bh * s.n_chunks + n) * int64_t(MTX) * KS * 512;
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt) {
-                const int t = (colX + 16 * nt) / 16;
-                uint16_t* dst = base + ((t * KS + sidx) * 64 + lane) * 8 + 4 * h;
-                uint2 pk;
-                pk.x = uint32_t(bf16_bits((__bf16)acc[nt][0])) | (uint32_t(bf16_bits((__bf16)acc[nt][1])) << 16);
-                pk.y = uint32_t(bf16_bits((__bf16)acc[nt][2])) | (uint32_t(bf16_bits((__bf16)acc[nt][3])) << 16);
-                *reinterpret_cast<uint2*>(dst) = pk;
-            }
-        }
-        acc[0] *= D;
-        acc[1] *= D;
-#pragma unroll
-        for (int u = 0; u < KST; ++u) {
-            const bf16x8 af = lds_frag(sA + (16 * wave + ln) * LDT + 32 * u + 4 * g);
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt) {
-                acc[nt] = mfma16(af, lds_frag(sBh + (16 * nt + ln) * LDT + 32 * u + 4 * g), acc[nt]);
-                acc[nt] = mfma16(af, lds_frag(sBl + (16 * nt + ln) * LDT + 32 * u + 4 * g), acc[nt]);
-            }
-        }
-        };
-    ChunkRegs R0, R1;
-    load_chunk(0, R0);
-    if (s.n_chunks > 1) load_chunk(1, R1);
-    for (int n = 0; n < s.n_chunks; n += 2) {
-        step(n, R0);
-        if (n + 1 < s.n_chunks) step(n + 1, R1);
-    }
-    // final states, plain fp32: tile value (R, c) is H[R][c] or G[c][R]
-    float* fin = isG ? a.final_G : a.final_H;
-    if (fin) {
-        const int R = row0 + 16 * wave + 4 * g;
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-            const int c = colX + 16 * nt + ln;
-#pragma unroll
-            for (int ii = 0; ii < 4; ++ii) {
-                if (isG)
-                    fin[(bh * dv + c) * int64_t(dk) + R + ii] = acc[nt][ii];
-                else
-                    fin[(bh * dk + R + ii) * int64_t(dk) + c] = acc[nt][ii];
-            }
-        }
-    }
-}
-
 // Wide variant (bf16 k and v, chunk 64, d_k and d_v in {64, 128}), used for the
 // bf16 fragment chunk states and for the states-only call.  One workgroup owns a
 // whole part of the state of one (batch, head) sequence -- part 0 is H (d_k x d_k),
@@ -426,16 +266,36 @@ __global__ __launch_bounds__(kThreads) void chunk_state_frag_kernel(StateArgs a)
 // rounding (2^-9 per term, averaged over the chunk's 64 terms) stays well below the
 // bf16 rounding of the stored states.
 // Eight waves (two per SIMD, so one hides the other's latencies); wave w owns key
-// rows 32 (w % NS) .. +31 (NS = d_k / 32) and a 1/CS share of the columns (CS = 8 / NS); its 16x16 result tiles pair up into complete bf16
-// A-fragments of the fragment layout (rows 32s.. of X^T are fragment row block s),
-// so every chunk state is written with whole 1-KiB wave stores.  Staging is
-// double-buffered in LDS (one barrier per chunk) and the inputs of chunk n + 2 are
-// loaded while chunk n is consumed; the staging of chunk n + 1 is interleaved with
-// the products of chunk n.
+// rows 32 (w % NS) .. +31 (NS = d_k / 32) and a 1/CS share of the columns
+// (CS = 8 / NS); its 16x16 result tiles pair up into complete bf16 A-fragments of
+// the fragment layout (rows 32s.. of X^T are fragment row block s), so every chunk
+// state is written with whole 1-KiB wave stores.  Staging is double-buffered in LDS
+// (one barrier per chunk); the inputs of chunk n + 3 are loaded into registers while
+// chunk n is consumed (a chunk's work is shorter than a memory round trip under
+// load), and the staging of chunk n + 1 is interleaved with the products of chunk n.
+//
+// Few sequences (batch x heads below the compute units) leave most of the chip idle
+// during this chained walk, so there the chunks are cut into segments and the scan
+// runs in two launches.  The first computes each segment's total from a zero state,
+// T_s = sum over its chunks of the decayed updates, and the decay across it, D_s
+// (the product of its chunk decays).  The second starts every segment from the
+// state entering it, E_0 = 0 and E_{s+1} = D_s E_s + T_s -- the same chunk recurrence
+// applied to whole segments -- and walks the segment's chunks as above.
 constexpr int kWideThreads = 512;  // eight waves: two per SIMD
 
+// Segments of one launch of the wide scan.
+struct SegPlan {
+    int len;      // chunks per segment (the last may be shorter)
+    int total;    // segments of a sequence
+    int first;    // first segment this launch walks
+    int count;    // segments this launch walks, per (sequence, part)
+    bool totals;  // write T_s and D_s (first launch) instead of chunk and final states
+    float* tot;   // [B*H, total - 1, d_k (d_k + d_v)]: T_s of H as [R][c], then of G as [c][R]
+    float* dec;   // [B*H, total]: D_s
+};
+
 template <int DK, int DV, bool STORE, bool SPLIT>
-__global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArgs a)
+__global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArgs a, SegPlan sg)
 {
     constexpr int C = 64;
     constexpr int LDT = C + 8;           // row stride of the [feature][token] tiles
@@ -443,9 +303,11 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
     constexpr int CS = kWideThreads / kWave / NS;  // column shares per row block
     constexpr int FPP = 8 * kWideThreads / 32;     // features staged per pass (8 per thread group)
     const ForwardShape s = a.s;
-    const int blk = xcd_major_block(blockIdx.x, gridDim.x);  // H and G^T of one sequence share an L2
+    const int blk = xcd_major_block(blockIdx.x, gridDim.x);  // H and G^T of one segment share an L2
     const int part = blk % 2;
-    const int64_t bh = blk / 2;
+    const int seg = sg.first + (blk / 2) % sg.count;
+    const int64_t bh = blk / 2 / sg.count;
+    const int nbeg = seg * sg.len, nend = min(nbeg + sg.len, s.n_chunks);  // this segment's chunks
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int lane = tid % kWave;
@@ -557,7 +419,8 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
         constexpr int kStateElems = NC * DK;  // bf16 per chunk state of this part
 
         // chunk n: its state is stored, then acc = D acc + K^T (w ⊙ Y) from buffer n % 2;
-        // chunk n + 1 is staged (from Rn1) into the other buffer and chunk n + 2 loaded
+        // chunk n + 1 is staged (from Rn1) into the other buffer and chunk n + 3 loaded
+        float dprod = 1.0f;  // decay across the chunks walked so far
         auto consume = [&](int n, float D, Regs& Rn1, Regs& Rfree, float& Dnext) {
             if (frag_out) {
                 uint16_t* base = frag_base + (bh * s.n_chunks + n) * int64_t(kStateElems);
@@ -568,7 +431,8 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                     *reinterpret_cast<uint4*>(base + (((ct0 + ct) * NS + sblk) * kWave + lane) * 8) = pk;
                 }
             }
-            const int b = n % 2;
+            const int b = (n - nbeg) % 2;
+            dprod *= D;
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
@@ -597,7 +461,7 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                         if (SPLIT) acc[rt][ct] = mfma16(af[u][rt], bfl[u][ct], acc[rt][ct]);
                     }
             };
-            const int bn = (n + 1) % 2;  // a chunk past the end stages into a buffer nobody reads
+            const int bn = (n - nbeg + 1) % 2;  // a chunk past the end stages into a buffer nobody reads
             products(0, 0, NCT);
             const Gate gt = gates(Rn1);
             __builtin_amdgcn_sched_barrier(0);
@@ -608,14 +472,50 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
             products(1, NCT / 2, NCT);
             stage_y(Rn1, bn, gt, 4, 8);
             Dnext = gt.D;
-            load(min(n + 2, s.n_chunks - 1), Rfree);  // unconditional, so memory waits count statically
+            load(min(n + 3, nend - 1), Rfree);  // unconditional, so memory waits count statically
             __syncthreads();
         };
 
-        Regs R0, R1;
-        load(0, R0);
-        load(min(1, s.n_chunks - 1), R1);
-        float D0, D1 = 1.0f;
+        // element offset of this thread's tile value (rt, ct, ii) -- row R, column c of the
+        // part -- in a [R][c] (H) or [c][R] (G) fp32 state
+        auto tile_off = [&](int rt, int ct, int ii) -> int {
+            const int R = 32 * sblk + 16 * rt + 4 * g + ii, c = 16 * (ct0 + ct) + ln;
+            return part ? c * DK + R : R * DK + c;
+        };
+        constexpr int64_t kSegElems = int64_t(DK) * (DK + DV);  // one segment total, H then G
+        auto seg_total = [&](int t) -> float* { return sg.tot + (bh * (sg.total - 1) + t) * kSegElems + (part ? DK * DK : 0); };
+        // inputs of the first three chunks (the walk keeps three chunks in flight)
+        Regs R0, R1, R2;
+        load(nbeg, R0);
+        load(min(nbeg + 1, nend - 1), R1);
+        load(min(nbeg + 2, nend - 1), R2);
+
+        // the state entering this segment, E_seg = sum_{t < seg} c_t T_t with
+        // c_t = D_{t+1} ... D_{seg-1} (the unrolled E_{t+1} = D_t E_t + T_t); the terms
+        // are independent, so their loads are issued two segments at a time.  The
+        // totals launch starts every segment from zero instead.
+        if (!sg.totals) {
+            float c[2];
+            float cn = 1.0f;  // c_t for the highest t not yet added
+            for (int t = seg - 1; t >= 0; t -= 2) {
+                c[0] = cn;
+                cn *= sg.dec[bh * sg.total + t];
+                c[1] = t >= 1 ? cn : 0.0f;
+                if (t >= 1) cn *= sg.dec[bh * sg.total + t - 1];
+                const float* tb0 = seg_total(t);
+                const float* tb1 = seg_total(t >= 1 ? t - 1 : t);
+#pragma unroll
+                for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                        for (int ii = 0; ii < 4; ++ii) {
+                            const int o = tile_off(rt, ct, ii);
+                            acc[rt][ct][ii] += c[0] * tb0[o] + c[1] * tb1[o];
+                        }
+            }
+        }
+        float D0, D1 = 1.0f, D2 = 1.0f;
         {
             const Gate gt = gates(R0);
             stage_k(R0, 0);
@@ -623,28 +523,28 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
             D0 = gt.D;
         }
         __syncthreads();
-        for (int n = 0; n < s.n_chunks; n += 2) {
-            consume(n, D0, R1, R0, D1);       // stages chunk n+1 (R1), loads n+2 into R0
-            if (n + 1 < s.n_chunks) consume(n + 1, D1, R0, R1, D0);  // stages n+2 (R0), loads n+3 into R1
+        for (int n = nbeg; n < nend; n += 3) {
+            consume(n, D0, R1, R0, D1);  // stages chunk n+1 (R1), loads n+3 into R0
+            if (n + 1 < nend) consume(n + 1, D1, R2, R1, D2);  // stages n+2 (R2), loads n+4 into R1
+            if (n + 2 < nend) consume(n + 2, D2, R0, R2, D0);  // stages n+3 (R0), loads n+5 into R2
         }
-        // final states, fp32: tile value (R, c) is H[R][c] or G[c][R]
-        float* fin = part ? a.final_G : a.final_H;
-        if (fin) {
+        // fp32 output: the segment total and its decay, or, after the last segment, the
+        // final states
+        float* dst = nullptr;
+        if (sg.totals) {
+            dst = seg_total(seg);
+            if (part == 0 && tid == 0) sg.dec[bh * sg.total + seg] = dprod;
+        } else if (seg == sg.total - 1) {
+            float* fin = part ? a.final_G : a.final_H;
+            if (fin) dst = fin + bh * int64_t(NC) * DK;
+        }
+        if (dst) {
 #pragma unroll
-            for (int rt = 0; rt < 2; ++rt) {
-                const int R = 32 * sblk + 16 * rt + 4 * g;
+            for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-                for (int ct = 0; ct < NCT; ++ct) {
-                    const int c = 16 * (ct0 + ct) + ln;
+                for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-                    for (int ii = 0; ii < 4; ++ii) {
-                        if (part)
-                            fin[(bh * DV + c) * int64_t(DK) + R + ii] = acc[rt][ct][ii];
-                        else
-                            fin[(bh * DK + R + ii) * int64_t(DK) + c] = acc[rt][ct][ii];
-                    }
-                }
-            }
+                    for (int ii = 0; ii < 4; ++ii) dst[tile_off(rt, ct, ii)] = acc[rt][ct][ii];
         }
     };
     if (part == 0)
@@ -653,17 +553,66 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
         run(std::integral_constant<int, DV>{});
 }
 
+// Segments of the wide scan for bh sequences of n_chunks chunks: doubled while the
+// (sequence, part, segment) workgroups still fit the compute units once (the kernel's
+// LDS allows one workgroup per unit) and each segment keeps at least kMinSegChunks
+// chunks, so the extra totals launch stays small next to the walk it shortens.
+constexpr int kComputeUnits = 256;
+constexpr int kMinSegChunks = 8;
+int wide_segments(int64_t bh, int n_chunks)
+{
+    int S = 1;
+    while (2 * bh * (2 * S) <= kComputeUnits && n_chunks / (2 * S) >= kMinSegChunks) S *= 2;
+    return S;
+}
+
+template <int DK, int DV, bool STORE, bool SPLIT>
+void launch_wide_kernel(const StateArgs& a, const SegPlan& sg, int64_t bh, hipStream_t stream)
+{
+    const unsigned blocks = unsigned(bh * 2 * sg.count);
+    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, STORE, SPLIT>), dim3(blocks), dim3(kWideThreads), 0, stream, a, sg);
+}
+
 template <int DK, int DV>
 hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
 {
-    const unsigned blocks = unsigned(a.s.batch * a.s.heads * 2);
+    const int64_t bh = a.s.batch * a.s.heads;
+    const int nc = a.s.n_chunks;
     const bool fin = a.final_H != nullptr || a.final_G != nullptr;
+    int S = wide_segments(bh, nc);
+    int len = (nc + S - 1) / S;
+    S = (nc + len - 1) / len;
+    const int64_t tot_elems = bh * (S - 1) * int64_t(DK) * (DK + DV);
+    const size_t need = size_t(tot_elems + bh * S) * sizeof(float);
+    if (S > 1 && (a.seg_ws == nullptr || a.seg_bytes < need)) {
+        S = 1;
+        len = nc;
+    }
+    SegPlan sg{len, S, 0, S, false, a.seg_ws, S > 1 ? a.seg_ws + tot_elems : nullptr};
+    if (S > 1) {
+        // segment totals T_0 .. T_{S-2} (the last one is never needed); fp32-accurate
+        // (split products) when fp32 final states come out
+        SegPlan p1 = sg;
+        p1.count = S - 1;
+        p1.totals = true;
+        if (fin)
+            launch_wide_kernel<DK, DV, false, true>(a, p1, bh, stream);
+        else
+            launch_wide_kernel<DK, DV, false, false>(a, p1, bh, stream);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (!a.store_chunks) {
+        // final states only: the last segment's walk alone produces them
+        sg.first = S - 1;
+        sg.count = 1;
+    }
     if (a.store_chunks && a.frag && !fin)
-        hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, true, false>), dim3(blocks), dim3(kWideThreads), 0, stream, a);
+        launch_wide_kernel<DK, DV, true, false>(a, sg, bh, stream);
     else if (a.store_chunks && a.frag)
-        hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, true, true>), dim3(blocks), dim3(kWideThreads), 0, stream, a);
+        launch_wide_kernel<DK, DV, true, true>(a, sg, bh, stream);
     else
-        hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, false, true>), dim3(blocks), dim3(kWideThreads), 0, stream, a);
+        launch_wide_kernel<DK, DV, false, true>(a, sg, bh, stream);
     return hipGetLastError();
 }
 

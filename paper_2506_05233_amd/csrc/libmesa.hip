@@ -157,6 +157,13 @@ int launch_states(const FwdCall& c, bool store_chunks, hipStream_t s)
     mesa::StateArgs sa{shape_of(c), c.k, c.v, c.gamma, c.beta,
                        store_chunks ? ws_H(c) : nullptr, store_chunks ? ws_G(c) : nullptr,
                        c.final_H, c.final_G, store_chunks, frag};
+    // The bf16 chunk states fill half of the workspace (and a states-only call none
+    // of it): the other half is scratch for the segmented scan of few sequences.
+    if (c.workspace && (frag || !store_chunks)) {
+        const size_t full = mesa_forward_workspace_bytes(c.batch, c.heads, c.seq_len, c.d_k, c.d_v, c.chunk);
+        sa.seg_ws = reinterpret_cast<float*>(static_cast<char*>(const_cast<void*>(c.workspace)) + full / 2);
+        sa.seg_bytes = full - full / 2;
+    }
     return mesa::launch_chunk_state(sa, s) == hipSuccess ? MESA_OK : MESA_ERR_HIP;
 }
 
@@ -209,9 +216,10 @@ int mesa_forward_ex(const void* q, const void* k, const void* v, const float* ga
 {
     const bool states_only = out == nullptr;
     if (states_only && (qstar_out || !final_H || !final_G)) return MESA_ERR_NULL;
+    // a states-only call uses the workspace (as scratch) only when one is given
     FwdCall c{q, k, v, gamma, beta, lambda, batch, heads, seq_len, d_k, d_v, dtype, n_cg, chunk,
               precision, out, qstar_out, final_H, final_G, workspace, workspace_bytes,
-              !states_only, !states_only};
+              !states_only, !states_only || workspace != nullptr};
     int st = validate_forward(c);
     if (st != MESA_OK || batch == 0 || heads == 0) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);

@@ -37,6 +37,10 @@ struct StateArgs {
     float* final_G;
     bool store_chunks;
     bool frag;
+    // Scratch for the segmented scan (may be null: then one segment): fp32
+    // segment totals and decays, seg_bytes bytes.  Used by the bf16 scan only.
+    float* seg_ws = nullptr;
+    size_t seg_bytes = 0;
 };
 bool chunk_state_frag_supported(const ForwardShape& s);
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream);

@@ -254,9 +254,11 @@ class ForwardPlan:
         return self.solve()
 
 
-def prefill_states(k, v, gamma, beta, chunk=64):
+def prefill_states(k, v, gamma, beta, chunk=64, workspace=None):
     """States after the last token only (mesa_forward_ex with out = NULL):
-    returns (H [B,H,d_k,d_k], G [B,H,d_v,d_k]) fp32, the input of decode_step."""
+    returns (H [B,H,d_k,d_k], G [B,H,d_v,d_k]) fp32, the input of decode_step.
+    workspace: optional device tensor of at least mesa_forward_workspace_bytes,
+    scratch that lets the scan of few long sequences run in segments."""
     torch = _torch()
     lib = load()
     B, H, T, dk = k.shape
@@ -269,9 +271,13 @@ def prefill_states(k, v, gamma, beta, chunk=64):
     code = _dtype_code(k)
     fH = torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev)
     fG = torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        _check(workspace, "workspace", tuple(workspace.shape), device=dev)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
     st = lib.mesa_forward_ex(None, _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), None, B, H, T, dk, dv,
                              code, 0, int(chunk), MESA_PREC_AUTO, None, None, _ptr(fH), _ptr(fG),
-                             None, 0, _stream(dev))
+                             ws_ptr, ws_bytes, _stream(dev))
     if st != MESA_OK:
         raise MesaError(st, "mesa_forward_ex(states only)")
     return fH, fG

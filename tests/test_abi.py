@@ -104,6 +104,8 @@ def _fwd(lib, **kw):
     (dict(qstar=P["out"]), L.MESA_ERR_ARG),            # two outputs overlap
     (dict(out=None, fH=P["fh"], fG=None), L.MESA_ERR_NULL),    # states only needs both states
     (dict(out=None, fH=P["fh"], fG=P["fg"], qstar=P["qs"]), L.MESA_ERR_NULL),
+    (dict(out=None, fH=P["fh"], fG=P["fg"], ws_bytes=100), L.MESA_ERR_WORKSPACE),  # states only, scratch too small
+    (dict(out=None, fH=P["ws"] + 256, fG=P["fg"]), L.MESA_ERR_ARG),  # states only, scratch overlaps final_H
 ])
 def test_forward_rejects_bad_arguments(lib, kw, status):
     assert _fwd(lib, **kw) == status

@@ -206,6 +206,66 @@ def test_prefill_states_match_oracle():
     assert rel_l2(G.cpu().numpy(), ref["G"]) <= 1e-5
 
 
+@pytest.mark.parametrize("dk,dv", [(128, 128), (64, 128)])
+def test_segmented_state_scan_matches_oracle(dk, dv):
+    """Two sequences of 36 chunks (the last ragged): the bf16 scan runs in 4 segments
+    of 9 chunks, totals first, then every segment from the state entering it.  Zero
+    gates sit inside a segment and on the first token of one (a memory reset the
+    entering state must honour).  Every output, the final states (fp32) and the
+    states-only call with scratch against the oracle; the states-only call without
+    scratch walks unsegmented and must agree with it to fp32 rounding."""
+    T = 35 * 64 + 17
+    x = W.forward_inputs(1, 2, T, dk, dv, "bf16", 4.0, seed=61 + dk)
+    x["gamma"][0, 0, 9 * 64 + 100] = 0.0
+    x["gamma"][0, 1, 18 * 64] = 0.0
+    got = _gpu_forward(x, "bf16", 15, 64, precision=L.MESA_PREC_BF16, want_states=True)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 15, want_states=True)
+    e_out = rel_l2(got["out"], ref["out"])
+    e_h, e_g = rel_l2(got["H"], ref["H"]), rel_l2(got["G"], ref["G"])
+    _say("segmented scan d_k=%d d_v=%d: out %.3e  H %.3e  G %.3e" % (dk, dv, e_out, e_h, e_g))
+    assert e_out <= TOL_BF16 and e_h <= 1e-5 and e_g <= 1e-5
+    d = to_device(x, "bf16")
+    ws = torch.empty(L.forward_workspace_bytes(1, 2, T, dk, dv, 64), dtype=torch.uint8, device="cuda")
+    Hs, Gs = L.prefill_states(d["k"], d["v"], d["gamma"], d["beta"], workspace=ws)
+    H1, G1 = L.prefill_states(d["k"], d["v"], d["gamma"], d["beta"])
+    torch.cuda.synchronize()
+    assert rel_l2(Hs.cpu().numpy(), ref["H"]) <= 1e-5 and rel_l2(Gs.cpu().numpy(), ref["G"]) <= 1e-5
+    assert rel_l2(Hs.cpu().numpy(), H1.cpu().numpy()) <= 1e-6
+    assert rel_l2(Gs.cpu().numpy(), G1.cpu().numpy()) <= 1e-6
+
+
+def test_segmented_state_scan_long_memory():
+    """Gates within 1e-3 of one (a few exactly one): the decay across a 9-chunk segment
+    stays above 0.5, so every earlier segment's total reaches the final states with a
+    weight the fp32 check sees -- a wrong combination coefficient or a dropped segment
+    fails here.  The workspace starts filled with ones, so a read of scratch that the
+    scan has not written yet shows too.  The final states of the segmented scan
+    (forward and states-only with scratch) against the oracle, and against the
+    unsegmented states-only walk; the output against the oracle at the bf16 tolerance."""
+    T = 35 * 64 + 17
+    x = W.forward_inputs(1, 2, T, 128, 128, "bf16", 4.0, seed=67)
+    rng = np.random.default_rng(6701)
+    x["gamma"][...] = rng.uniform(0.999, 1.0, size=x["gamma"].shape).astype(np.float32)
+    x["gamma"][0, 0, ::97] = 1.0
+    need = L.forward_workspace_bytes(1, 2, T, 128, 128, 64)
+    got = _gpu_forward(x, "bf16", 15, 64, precision=L.MESA_PREC_BF16, want_states=True,
+                       workspace=torch.ones(need // 4, dtype=torch.float32, device="cuda"))
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 15, want_states=True)
+    e_out = rel_l2(got["out"], ref["out"])
+    e_h, e_g = rel_l2(got["H"], ref["H"]), rel_l2(got["G"], ref["G"])
+    _say("segmented scan, gates near one: out %.3e  H %.3e  G %.3e" % (e_out, e_h, e_g))
+    assert e_h <= 1e-5 and e_g <= 1e-5
+    assert e_out <= TOL_BF16
+    d = to_device(x, "bf16")
+    ws = torch.ones(need // 4, dtype=torch.float32, device="cuda")
+    Hs, Gs = L.prefill_states(d["k"], d["v"], d["gamma"], d["beta"], workspace=ws)
+    H1, G1 = L.prefill_states(d["k"], d["v"], d["gamma"], d["beta"])
+    torch.cuda.synchronize()
+    assert rel_l2(Hs.cpu().numpy(), ref["H"]) <= 1e-5 and rel_l2(Gs.cpu().numpy(), ref["G"]) <= 1e-5
+    assert rel_l2(Hs.cpu().numpy(), H1.cpu().numpy()) <= 1e-6
+    assert rel_l2(Gs.cpu().numpy(), G1.cpu().numpy()) <= 1e-6
+
+
 def test_forward_is_bitwise_deterministic():
     x = W.forward_inputs(2, 4, 512, 128, 128, "bf16", 4.0, seed=9)
     a = _gpu_forward(x, "bf16", 15, 64)
