@@ -65,6 +65,9 @@ def _load():
             lib.oracle_decode_step.argtypes = [P, P, P, P, P, P, P, P, i64, i64, i64, i64, ci, ci,
                                                ci, dbl, P, P, I32, ci]
             lib.oracle_decode_step.restype = ci
+            lib.oracle_backward.argtypes = [P, P, P, P, P, P, P, i64, i64, i64, i64, i64, ci, ci,
+                                            ci, P, P, P, P, P, P, P, P, ci]
+            lib.oracle_backward.restype = ci
             lib.oracle_cg.argtypes = [P, P, i64, ci, ci, dbl, P, P]
             lib.oracle_cg.restype = ci
             lib.oracle_cholesky_solve.argtypes = [P, P, i64, P, P]
@@ -171,6 +174,42 @@ def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, solver="cg", 
     if want_qstar:
         return out, H, G, qstar
     return out, H, G
+
+
+def backward(q, k, v, gamma, beta, lam, dout, n_cg, solver="cg", init="jacobi", want_solves=False,
+             threads=None):
+    """Gradients of the Mesa layer (App. D backward pass) given dout = dL/do [B,H,T,dv].
+
+    q*_t and e*_t = (H_t + Lambda)^{-1} G_t^T e_t come from the same solver
+    ("cg": Alg. 1 with n_cg loop iterations, tolerance zero; "cholesky": exact).
+    Returns a dict with "dq", "dk" [B,H,T,dk], "dv" [B,H,T,dv], "dgamma",
+    "dbeta" [B,H,T], "dlam" [H,dk] (summed over batch and time) and, with
+    want_solves, "qstar" and "estar" [B,H,T,dk].
+    """
+    lib = _load()
+    q, k, v, gamma, beta, lam, dout = map(_f64, (q, k, v, gamma, beta, lam, dout))
+    B, Hh, T, dk = q.shape
+    dv = v.shape[-1]
+    assert k.shape == (B, Hh, T, dk) and v.shape == (B, Hh, T, dv) and dout.shape == (B, Hh, T, dv)
+    assert gamma.shape == (B, Hh, T) and beta.shape == (B, Hh, T) and lam.shape == (Hh, dk)
+    res = {"dq": np.zeros((B, Hh, T, dk)), "dk": np.zeros((B, Hh, T, dk)), "dv": np.zeros((B, Hh, T, dv)),
+           "dgamma": np.zeros((B, Hh, T)), "dbeta": np.zeros((B, Hh, T))}
+    dlam_part = np.zeros((B, Hh, dk))
+    qstar = np.zeros((B, Hh, T, dk)) if want_solves else None
+    estar = np.zeros((B, Hh, T, dk)) if want_solves else None
+    s = {"cg": SOLVE_CG, "cholesky": SOLVE_CHOLESKY}[solver]
+    i = {"jacobi": INIT_JACOBI, "query": INIT_QUERY}[init]
+    rc = lib.oracle_backward(_ptr(q), _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam), _ptr(dout),
+                             B, Hh, T, dk, dv, int(n_cg), s, i, _ptr(res["dq"]), _ptr(res["dk"]),
+                             _ptr(res["dv"]), _ptr(res["dgamma"]), _ptr(res["dbeta"]), _ptr(dlam_part),
+                             _ptr(qstar), _ptr(estar), int(threads or default_threads()))
+    if rc != 0:
+        raise FloatingPointError("oracle: a system H_t + Lambda was not positive definite")
+    res["dlam"] = dlam_part.sum(axis=0)
+    if want_solves:
+        res["qstar"] = qstar
+        res["estar"] = estar
+    return res
 
 
 def cg_solve(A, b, n_cg, init="jacobi", eps=0.0, return_steps=False):

@@ -31,6 +31,22 @@
  *   - beta enters once: H += beta k k^T, G += beta v k^T;
  *   - decode updates the state with the new token first, then solves.
  *
+ * Backward pass (App. D, "Mesa layer backward pass"), given e_t = dL/do_t:
+ *     u_t  = G_t^T e_t,  e*_t = (H_t + Lambda)^{-1} u_t  (same solver as q*_t)
+ *     dL/dq_t = e*_t,   dL/dLambda_a = -sum_t q*_{t,a} e*_{t,a}
+ *   and, with the adjoints of the states accumulated backwards in time,
+ *     DG_s = sum_{t>=s} zeta_{t,s} e_t q*_t^T  = e_s q*_s^T + gamma_{s+1} DG_{s+1}
+ *     DH_s = -sum_{t>=s} zeta_{t,s} e*_t q*_t^T = -e*_s q*_s^T + gamma_{s+1} DH_{s+1},
+ *     dL/dv_s     = beta_s DG_s k_s
+ *     dL/dk_s     = beta_s (DG_s^T v_s + (DH_s + DH_s^T) k_s)
+ *     dL/dbeta_s  = v_s^T DG_s k_s + k_s^T DH_s k_s
+ *     dL/dgamma_s = <DG_s, G_{s-1}> + <DH_s, H_{s-1}>   (Frobenius products).
+ *   This is the gradient of the layer with q*_t taken as the exact solution
+ *   (the paper's implicit differentiation; CG approximates both solves).  The
+ *   paper writes its sums without the input gate and with e*_t in the value term
+ *   of dL/dk_s; differentiating e_t^T G_t q*_t with respect to k_s gives
+ *   beta_s zeta_{t,s} q*_t (e_t^T v_s), the reading taken here.
+ *
  * All arrays are dense, row-major, fp64, host memory, owned by the caller.
  */
 #include <math.h>
@@ -282,4 +298,187 @@ int oracle_decode_step(double* state_H, double* state_G, const double* q, const 
     proto.qstar = qstar; proto.state_H = state_H; proto.state_G = state_G;
     proto.eps = eps; proto.steps = steps;
     return run_jobs(&proto, decode_worker, n_threads);
+}
+
+/* ------------------------------------------------------------------ backward */
+
+typedef struct {
+    const double *q, *k, *v, *gamma, *beta, *lambda, *dout;
+    int64_t B, Hh, T, dk, dv;
+    int n_cg, solver, init;
+    double *dq, *dk_out, *dv_out, *dgamma, *dbeta, *dlam_part; /* dlam_part [B*Hh, dk] */
+    double *qstar, *estar;                                      /* may be NULL */
+    int n_threads, tid;
+    int status;
+} oracle_bwd_job;
+
+enum { BWD_BLOCK = 64 };  /* tokens between state checkpoints */
+
+/* A x = b with the job's solver; x and work as for mesa_token. */
+static int bwd_solve(const oracle_bwd_job* j, const double* A, const double* b, double* x, double* sw)
+{
+    if (j->solver == ORACLE_SOLVE_CHOLESKY) return oracle_cholesky_solve(A, b, j->dk, x, sw);
+    oracle_cg(A, b, j->dk, j->n_cg, j->init, 0.0, x, sw);
+    return 0;
+}
+
+static void state_step(double* H, double* G, const double* k, const double* v, double gamma, double beta,
+                       int64_t dk, int64_t dv)
+{
+    for (int64_t a = 0; a < dk; ++a)
+        for (int64_t b = 0; b < dk; ++b) H[a * dk + b] = gamma * H[a * dk + b] + beta * k[a] * k[b];
+    for (int64_t a = 0; a < dv; ++a)
+        for (int64_t b = 0; b < dk; ++b) G[a * dk + b] = gamma * G[a * dk + b] + beta * v[a] * k[b];
+}
+
+static void* backward_worker(void* arg)
+{
+    oracle_bwd_job* j = (oracle_bwd_job*)arg;
+    const int64_t dk = j->dk, dv = j->dv, T = j->T;
+    const int64_t nH = dk * dk, nG = dv * dk, nblk = (T + BWD_BLOCK - 1) / BWD_BLOCK;
+    double* H = (double*)malloc((size_t)nH * sizeof(double));
+    double* G = (double*)malloc((size_t)nG * sizeof(double));
+    double* A = (double*)malloc((size_t)nH * sizeof(double));
+    double* sw = (double*)malloc((size_t)(nH + 3 * dk) * sizeof(double));
+    double* u = (double*)malloc((size_t)dk * sizeof(double));
+    double* xs = (double*)malloc((size_t)(T > 0 ? T : 1) * dk * sizeof(double));  /* q*_t */
+    double* es = (double*)malloc((size_t)(T > 0 ? T : 1) * dk * sizeof(double));  /* e*_t */
+    double* ckH = (double*)malloc((size_t)(nblk > 0 ? nblk : 1) * nH * sizeof(double));
+    double* ckG = (double*)malloc((size_t)(nblk > 0 ? nblk : 1) * nG * sizeof(double));
+    double* bH = (double*)malloc((size_t)(BWD_BLOCK + 1) * nH * sizeof(double));
+    double* bG = (double*)malloc((size_t)(BWD_BLOCK + 1) * nG * sizeof(double));
+    double* DH = (double*)malloc((size_t)nH * sizeof(double));
+    double* DG = (double*)malloc((size_t)nG * sizeof(double));
+    j->status = 0;
+    for (int64_t bh = j->tid; bh < j->B * j->Hh; bh += j->n_threads) {
+        const int64_t h = bh % j->Hh;
+        const double* lam = j->lambda + h * dk;
+        double* dlam = j->dlam_part + bh * dk;
+        memset(dlam, 0, (size_t)dk * sizeof(double));
+        /* forward in time: states, q*_t, u_t = G_t^T e_t, e*_t; checkpoints of the
+         * state entering every block */
+        memset(H, 0, (size_t)nH * sizeof(double));
+        memset(G, 0, (size_t)nG * sizeof(double));
+        for (int64_t t = 0; t < T; ++t) {
+            const int64_t tok = bh * T + t;
+            if (t % BWD_BLOCK == 0) {
+                memcpy(ckH + (t / BWD_BLOCK) * nH, H, (size_t)nH * sizeof(double));
+                memcpy(ckG + (t / BWD_BLOCK) * nG, G, (size_t)nG * sizeof(double));
+            }
+            state_step(H, G, j->k + tok * dk, j->v + tok * dv, j->gamma[tok], j->beta[tok], dk, dv);
+            for (int64_t a = 0; a < dk; ++a)
+                for (int64_t b = 0; b < dk; ++b) A[a * dk + b] = H[a * dk + b] + (a == b ? lam[a] : 0.0);
+            if (bwd_solve(j, A, j->q + tok * dk, xs + t * dk, sw) != 0) j->status = -1;
+            const double* e = j->dout + tok * dv;
+            for (int64_t b = 0; b < dk; ++b) {
+                double acc = 0.0;
+                for (int64_t a = 0; a < dv; ++a) acc += G[a * dk + b] * e[a];
+                u[b] = acc;
+            }
+            if (bwd_solve(j, A, u, es + t * dk, sw) != 0) j->status = -1;
+            for (int64_t a = 0; a < dk; ++a) {
+                j->dq[tok * dk + a] = es[t * dk + a];
+                dlam[a] -= xs[t * dk + a] * es[t * dk + a];
+            }
+            if (j->qstar) memcpy(j->qstar + tok * dk, xs + t * dk, (size_t)dk * sizeof(double));
+            if (j->estar) memcpy(j->estar + tok * dk, es + t * dk, (size_t)dk * sizeof(double));
+        }
+        /* backward in time, block by block: recompute the block's states from its
+         * checkpoint (bH[i] = state after token c0 + i - 1), then walk s downwards */
+        memset(DH, 0, (size_t)nH * sizeof(double));
+        memset(DG, 0, (size_t)nG * sizeof(double));
+        double gamma_next = 0.0;  /* gamma_{s+1}; no token after the last */
+        for (int64_t blk = nblk - 1; blk >= 0; --blk) {
+            const int64_t c0 = blk * BWD_BLOCK;
+            const int64_t c1 = c0 + BWD_BLOCK < T ? c0 + BWD_BLOCK : T;
+            memcpy(bH, ckH + blk * nH, (size_t)nH * sizeof(double));
+            memcpy(bG, ckG + blk * nG, (size_t)nG * sizeof(double));
+            for (int64_t t = c0; t < c1; ++t) {
+                const int64_t tok = bh * T + t, i = t - c0;
+                memcpy(bH + (i + 1) * nH, bH + i * nH, (size_t)nH * sizeof(double));
+                memcpy(bG + (i + 1) * nG, bG + i * nG, (size_t)nG * sizeof(double));
+                state_step(bH + (i + 1) * nH, bG + (i + 1) * nG, j->k + tok * dk, j->v + tok * dv,
+                           j->gamma[tok], j->beta[tok], dk, dv);
+            }
+            for (int64_t s = c1 - 1; s >= c0; --s) {
+                const int64_t tok = bh * T + s, i = s - c0;
+                const double* ks = j->k + tok * dk;
+                const double* vs = j->v + tok * dv;
+                const double* e = j->dout + tok * dv;
+                const double* xq = xs + s * dk;
+                const double* xe = es + s * dk;
+                for (int64_t a = 0; a < dv; ++a)
+                    for (int64_t b = 0; b < dk; ++b) DG[a * dk + b] = gamma_next * DG[a * dk + b] + e[a] * xq[b];
+                for (int64_t a = 0; a < dk; ++a)
+                    for (int64_t b = 0; b < dk; ++b) DH[a * dk + b] = gamma_next * DH[a * dk + b] - xe[a] * xq[b];
+                const double beta = j->beta[tok];
+                double db = 0.0, dg = 0.0;
+                for (int64_t a = 0; a < dv; ++a) {
+                    double s1 = 0.0;
+                    for (int64_t b = 0; b < dk; ++b) s1 += DG[a * dk + b] * ks[b];
+                    j->dv_out[tok * dv + a] = beta * s1;
+                    db += vs[a] * s1;
+                }
+                for (int64_t b = 0; b < dk; ++b) {
+                    double s1 = 0.0;
+                    for (int64_t a = 0; a < dv; ++a) s1 += DG[a * dk + b] * vs[a];
+                    for (int64_t a = 0; a < dk; ++a) s1 += (DH[b * dk + a] + DH[a * dk + b]) * ks[a];
+                    j->dk_out[tok * dk + b] = beta * s1;
+                }
+                for (int64_t a = 0; a < dk; ++a) {
+                    double s1 = 0.0;
+                    for (int64_t b = 0; b < dk; ++b) s1 += DH[a * dk + b] * ks[b];
+                    db += ks[a] * s1;
+                }
+                const double* Hp = bH + i * nH;  /* H_{s-1} */
+                const double* Gp = bG + i * nG;  /* G_{s-1} */
+                for (int64_t x = 0; x < nG; ++x) dg += DG[x] * Gp[x];
+                for (int64_t x = 0; x < nH; ++x) dg += DH[x] * Hp[x];
+                j->dbeta[tok] = db;
+                j->dgamma[tok] = dg;
+                gamma_next = j->gamma[tok];
+            }
+        }
+    }
+    free(H); free(G); free(A); free(sw); free(u); free(xs); free(es);
+    free(ckH); free(ckG); free(bH); free(bG); free(DH); free(DG);
+    return NULL;
+}
+
+/* Gradients of L with dL/do_t = dout_t [B,Hh,T,dv].  Inputs as oracle_forward;
+ * outputs dq, dk [B,Hh,T,dk], dv [B,Hh,T,dv], dgamma, dbeta [B,Hh,T],
+ * dlam_part [B*Hh, dk] (per-sequence sums; the caller sums over the batch);
+ * qstar, estar [B,Hh,T,dk] may be NULL.  Returns 0, or -1 if a Cholesky solve
+ * met a non-positive pivot. */
+int oracle_backward(const double* q, const double* k, const double* v, const double* gamma,
+                    const double* beta, const double* lambda, const double* dout, int64_t B,
+                    int64_t Hh, int64_t T, int64_t dk, int64_t dv, int n_cg, int solver, int init,
+                    double* dq, double* dk_out, double* dv_out, double* dgamma, double* dbeta,
+                    double* dlam_part, double* qstar, double* estar, int n_threads)
+{
+    const int64_t units = B * Hh;
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > units) n_threads = (int)(units > 0 ? units : 1);
+    oracle_bwd_job* jobs = (oracle_bwd_job*)malloc((size_t)n_threads * sizeof(oracle_bwd_job));
+    pthread_t* th = (pthread_t*)malloc((size_t)n_threads * sizeof(pthread_t));
+    for (int i = 0; i < n_threads; ++i) {
+        oracle_bwd_job* j = &jobs[i];
+        memset(j, 0, sizeof(*j));
+        j->q = q; j->k = k; j->v = v; j->gamma = gamma; j->beta = beta; j->lambda = lambda;
+        j->dout = dout; j->B = B; j->Hh = Hh; j->T = T; j->dk = dk; j->dv = dv;
+        j->n_cg = n_cg; j->solver = solver; j->init = init;
+        j->dq = dq; j->dk_out = dk_out; j->dv_out = dv_out; j->dgamma = dgamma; j->dbeta = dbeta;
+        j->dlam_part = dlam_part; j->qstar = qstar; j->estar = estar;
+        j->n_threads = n_threads; j->tid = i;
+    }
+    for (int i = 1; i < n_threads; ++i) pthread_create(&th[i], NULL, backward_worker, &jobs[i]);
+    backward_worker(&jobs[0]);
+    int status = jobs[0].status;
+    for (int i = 1; i < n_threads; ++i) {
+        pthread_join(th[i], NULL);
+        if (jobs[i].status != 0) status = jobs[i].status;
+    }
+    free(jobs);
+    free(th);
+    return status;
 }
