@@ -207,6 +207,41 @@ const char* mesa_status_string(int status);
 /* Library ABI version (major * 100 + minor). */
 int mesa_version(void);
 
+/* Bytes of device workspace mesa_backward needs (fp32: the chunk states and
+ * their adjoints at 64-token chunks, the right-hand sides G_t^T e_t, partial
+ * dLambda sums).  Returns 0 for unsupported or empty sizes. */
+size_t mesa_backward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
+                                     int64_t d_v);
+
+/* Backward pass of the layer (App. D, "Mesa layer backward pass"): gradients of a
+ * loss L given dout = dL/do_t, with q*_t taken as the solution of its system (the
+ * paper's implicit differentiation):
+ *     e*_t = (H_t + Lambda)^{-1} G_t^T e_t             (n_cg CG iterations, Alg. 1)
+ *     dq_t = e*_t,   dlambda_a = -sum_{b,t} q*_{t,a} e*_{t,a}
+ *     with DG_s = sum_{t>=s} zeta_{t,s} e_t q*_t^T, DH_s = -sum_{t>=s} zeta_{t,s} e*_t q*_t^T:
+ *     dv_s = beta_s DG_s k_s,   dk_s = beta_s (DG_s^T v_s + (DH_s + DH_s^T) k_s),
+ *     dbeta_s = v_s^T DG_s k_s + k_s^T DH_s k_s,
+ *     dgamma_s = <DG_s, G_{s-1}> + <DH_s, H_{s-1}>.
+ * (The paper writes these without the input gate and with e*_t in the value term
+ * of dk_s; differentiating e_t^T G_t q*_t gives q*_t e_t^T v_s, used here.)
+ *   k, v, gamma, beta, lambda, sizes, dtype: as for mesa_forward
+ *   n_cg    CG iterations of the solve for e*_t (0 <= n_cg <= MESA_MAX_NCG)
+ *   qstar   [batch, heads, seq_len, d_k] fp32: q*_t of the forward (qstar_out of
+ *           mesa_forward_ex)
+ *   dout    [batch, heads, seq_len, d_v] fp32: e_t
+ *   dq, dk  [batch, heads, seq_len, d_k] fp32      dv [batch, heads, seq_len, d_v] fp32
+ *   dgamma, dbeta [batch, heads, seq_len] fp32     dlambda [heads, d_k] fp32
+ *   workspace / workspace_bytes: at least mesa_backward_workspace_bytes(...),
+ *           16-byte aligned, as are qstar and dout
+ * All arithmetic is fp32 (chunk states, adjoints and the CG solve).  Outputs
+ * must overlap neither an input nor each other (MESA_ERR_ARG).  seq_len 0 writes
+ * dlambda = 0 only.  Six kernel launches on `stream`. */
+int mesa_backward(const void* k, const void* v, const float* gamma, const float* beta,
+                  const float* lambda, int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
+                  int64_t d_v, int dtype, int n_cg, const float* qstar, const float* dout, float* dq,
+                  float* dk, float* dv, float* dgamma, float* dbeta, float* dlambda,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

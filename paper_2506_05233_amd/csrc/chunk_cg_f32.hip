@@ -66,7 +66,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
         const int i = e / DK, c = e % DK;
         const bool ok = i < valid;
         sKV[i * kLdW + c] = ok ? to_f32(kp[(tok0 + i) * DK + c]) : 0.0f;
-        sP[c * LDP + i] = ok ? to_f32(qp[(tok0 + i) * DK + c]) : 0.0f;
+        sP[c * LDP + i] = ok ? (a.rhs ? a.rhs[(tok0 + i) * DK + c] : to_f32(qp[(tok0 + i) * DK + c])) : 0.0f;
     }
     const float* Hc = static_cast<const float*>(a.Hs) + (bh * s.n_chunks + n) * int64_t(DK) * DK;
     for (int e = tid; e < DK * DK; e += kThreads) sH[(e / DK) * LDH + e % DK] = Hc[e];
@@ -205,6 +205,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
         sP[rr * LDP + j] = x[m];
         if (a.qstar && j < valid) a.qstar[(tok0 + j) * DK + rr] = x[m];
     }
+    if (!a.out) return;  // solve only (uniform across the workgroup)
     __syncthreads();
     masked_kx();
     __syncthreads();

@@ -331,3 +331,99 @@ int mesa_forward_tol(const void* q, const void* k, const void* v, const float* g
 }
 
 }  // extern "C"
+
+namespace {
+
+constexpr int kBwdChunk = 64;  // the backward's own chunking (independent of the forward's)
+
+// Backward workspace, fp32: forward chunk states H_c, G_c; the adjoints S^H, A^G
+// arriving at every chunk's end; the right-hand sides u; per-chunk dLambda sums.
+struct BwdLayout {
+    int64_t nc, hs, gs, sh, ag, u, dl, total;  // offsets and total, in floats
+};
+BwdLayout bwd_layout(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v)
+{
+    BwdLayout L;
+    const int64_t bh = batch * heads;
+    L.nc = n_chunks_of(seq_len, kBwdChunk);
+    L.hs = 0;
+    L.gs = L.hs + bh * L.nc * d_k * d_k;
+    L.sh = L.gs + bh * L.nc * d_v * d_k;
+    L.ag = L.sh + bh * L.nc * d_k * d_k;
+    L.u = L.ag + bh * L.nc * d_v * d_k;
+    L.dl = L.u + bh * seq_len * d_k;
+    L.total = L.dl + bh * L.nc * d_k;
+    return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t mesa_backward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v)
+{
+    if (batch <= 0 || heads <= 0 || seq_len <= 0) return 0;
+    if (!dim_ok(d_k) || !dim_ok(d_v)) return 0;
+    return size_t(bwd_layout(batch, heads, seq_len, d_k, d_v).total) * sizeof(float);
+}
+
+int mesa_backward(const void* k, const void* v, const float* gamma, const float* beta, const float* lambda,
+                  int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg,
+                  const float* qstar, const float* dout, float* dq, float* dk, float* dv, float* dgamma,
+                  float* dbeta, float* dlambda, void* workspace, size_t workspace_bytes, void* stream)
+{
+    int st = check_sizes(batch, heads, seq_len, d_k, d_v, dtype, n_cg);
+    if (st != MESA_OK) return st;
+    if (batch == 0 || heads == 0) return MESA_OK;
+    if (!lambda || !dlambda) return MESA_ERR_NULL;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t bh = batch * heads, tokens = bh * seq_len;
+    if (seq_len > 0) {
+        if (!k || !v || !gamma || !beta || !qstar || !dout || !dq || !dk || !dv || !dgamma || !dbeta)
+            return MESA_ERR_NULL;
+        if (n_chunks_of(seq_len, kBwdChunk) * bh > (int64_t(1) << 31) / 16) return MESA_ERR_SHAPE;
+        const size_t need = mesa_backward_workspace_bytes(batch, heads, seq_len, d_k, d_v);
+        if (!workspace) return MESA_ERR_NULL;
+        if (workspace_bytes < need) return MESA_ERR_WORKSPACE;
+        for (const void* ptr : {static_cast<const void*>(qstar), static_cast<const void*>(dout), static_cast<const void*>(workspace)})
+            if (uintptr_t(ptr) % 16 != 0) return MESA_ERR_ARG;
+        const int64_t in_sz = dtype == MESA_DTYPE_BF16 ? 2 : 4;
+        const Range ins[] = {range_of(k, tokens * d_k * in_sz), range_of(v, tokens * d_v * in_sz),
+                             range_of(gamma, tokens * 4), range_of(beta, tokens * 4),
+                             range_of(lambda, heads * d_k * 4), range_of(qstar, tokens * d_k * 4),
+                             range_of(dout, tokens * d_v * 4), range_of(workspace, int64_t(need))};
+        const Range outs[] = {range_of(dq, tokens * d_k * 4), range_of(dk, tokens * d_k * 4),
+                              range_of(dv, tokens * d_v * 4), range_of(dgamma, tokens * 4),
+                              range_of(dbeta, tokens * 4), range_of(dlambda, heads * d_k * 4)};
+        for (const Range& o : outs)
+            for (const Range& i : ins)
+                if (overlaps(o, i)) return MESA_ERR_ARG;
+        for (int x = 0; x < 6; ++x)
+            for (int y = x + 1; y < 6; ++y)
+                if (overlaps(outs[x], outs[y])) return MESA_ERR_ARG;
+    } else if (overlaps(range_of(dlambda, heads * d_k * 4), range_of(lambda, heads * d_k * 4))) {
+        return MESA_ERR_ARG;
+    }
+    if (seq_len == 0)  // no tokens: dLambda is an empty sum
+        return mesa::launch_fill_zero(dlambda, heads * d_k, s) == hipSuccess ? MESA_OK : MESA_ERR_HIP;
+
+    const BwdLayout L = bwd_layout(batch, heads, seq_len, d_k, d_v);
+    float* ws = static_cast<float*>(workspace);
+    const mesa::ForwardShape shape{batch, heads, seq_len, int(d_k), int(d_v), kBwdChunk, int(L.nc),
+                                   dtype == MESA_DTYPE_BF16};
+    // forward chunk states (fp32, plain layout)
+    mesa::StateArgs sa{shape, k, v, gamma, beta, ws + L.hs, ws + L.gs, nullptr, nullptr, true, false};
+    if (mesa::launch_chunk_state(sa, s) != hipSuccess) return MESA_ERR_HIP;
+    mesa::BwdArgs ba{shape, k, v, gamma, beta, qstar, dout, dq, ws + L.hs, ws + L.gs, ws + L.sh, ws + L.ag,
+                     ws + L.u, dk, dv, dgamma, dbeta, ws + L.dl, dlambda};
+    // u_t = G_t^T e_t, then e*_t = (H_t + Lambda)^{-1} u_t into dq
+    if (mesa::launch_backward_stage(ba, 0, s) != hipSuccess) return MESA_ERR_HIP;
+    mesa::CgArgs ca{shape, nullptr, k, v, gamma, beta, lambda, ws + L.hs, ws + L.gs, n_cg, nullptr, dq, 0.0f,
+                    nullptr, ws + L.u};
+    if (mesa::launch_chunk_cg_f32(ca, s) != hipSuccess) return MESA_ERR_HIP;
+    for (int stage = 1; stage <= 3; ++stage)
+        if (mesa::launch_backward_stage(ba, stage, s) != hipSuccess) return MESA_ERR_HIP;
+    return MESA_OK;
+}
+
+}  // extern "C"

@@ -64,8 +64,38 @@ struct CgArgs {
     float* qstar;    // may be null
     float eps2;      // Alg. 1 relative tolerance, squared: stop once |r|^2 <= eps2 |r_0|^2
     int32_t* steps;  // may be null: [B, H, T] iterations each token used
+    // fp32 right-hand sides [B, H, T, d_k] solved for instead of q (fp32 path only),
+    // may be null; with out null the read-out is skipped and only qstar is written
+    const float* rhs = nullptr;
 };
 hipError_t launch_chunk_cg_f32(const CgArgs& a, hipStream_t stream);
+
+// Backward pass (fp32, chunk 64), in stages on one stream: 0 the right-hand sides
+// u_t = G_t^T e_t, 1 the reverse adjoint scan, 2 the per-chunk gradients, 3 the
+// Lambda reduction (the chunk-state scan and the solve for e* run between, through
+// launch_chunk_state and launch_chunk_cg_f32).
+struct BwdArgs {
+    ForwardShape s;        // chunk 64
+    const void* k;
+    const void* v;
+    const float* gamma;
+    const float* beta;
+    const float* qstar;    // [B, H, T, d_k]
+    const float* dout;     // [B, H, T, d_v]: e_t
+    const float* estar;    // [B, H, T, d_k]: e*_t
+    const float* Hs;       // forward chunk states, plain fp32 [B*H, n_chunks, d_k, d_k]
+    const float* Gs;       // [B*H, n_chunks, d_v, d_k]
+    float* SH;             // symmetric H adjoint arriving at each chunk's end [B*H, n_chunks, d_k, d_k]
+    float* AG;             // G adjoint [B*H, n_chunks, d_v, d_k]
+    float* u;              // [B, H, T, d_k]
+    float* dk;
+    float* dv;
+    float* dgamma;
+    float* dbeta;
+    float* dlam_part;      // [B*H, n_chunks, d_k]
+    float* dlam;           // [H, d_k]
+};
+hipError_t launch_backward_stage(const BwdArgs& a, int stage, hipStream_t stream);
 hipError_t launch_chunk_cg_bf16(const CgArgs& a, hipStream_t stream);
 bool chunk_cg_bf16_supported(const ForwardShape& s);
 

@@ -29,7 +29,8 @@ MESA_MAX_NCG = 1024
 
 EXPORTED = ("mesa_forward", "mesa_forward_ex", "mesa_forward_states", "mesa_forward_solve",
             "mesa_forward_tol", "mesa_forward_workspace_bytes", "mesa_decode_step",
-            "mesa_decode_step_tol", "mesa_status_string", "mesa_version")
+            "mesa_decode_step_tol", "mesa_backward", "mesa_backward_workspace_bytes",
+            "mesa_status_string", "mesa_version")
 
 _lib = None
 
@@ -70,6 +71,11 @@ def load():
     lib.mesa_decode_step_tol.argtypes = [fp, fp, vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, ci, ci, cf,
                                          fp, vp, vp]
     lib.mesa_decode_step_tol.restype = ci
+    lib.mesa_backward_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
+    lib.mesa_backward_workspace_bytes.restype = sz
+    lib.mesa_backward.argtypes = [vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, fp, fp,
+                                  fp, fp, fp, fp, fp, fp, vp, sz, vp]
+    lib.mesa_backward.restype = ci
     lib.mesa_status_string.argtypes = [ci]
     lib.mesa_status_string.restype = ctypes.c_char_p
     lib.mesa_version.argtypes = []
@@ -252,6 +258,45 @@ class ForwardPlan:
     def __call__(self):
         self.states()
         return self.solve()
+
+
+def backward_workspace_bytes(batch, heads, seq_len, d_k, d_v) -> int:
+    return load().mesa_backward_workspace_bytes(batch, heads, seq_len, d_k, d_v)
+
+
+def backward(k, v, gamma, beta, lam, qstar, dout, n_cg, workspace=None):
+    """Gradients of the layer given dout = dL/do [B,H,T,d_v] fp32 and the forward's
+    q* [B,H,T,d_k] fp32 (mesa_backward).  k, v [B,H,T,d] fp32 or bf16; gamma, beta
+    [B,H,T]; lam [H,d_k].  Returns a dict of fp32 tensors: "dq", "dk" [B,H,T,d_k],
+    "dv" [B,H,T,d_v], "dgamma", "dbeta" [B,H,T], "dlam" [H,d_k].
+    Runs on torch's current stream of k's device."""
+    torch = _torch()
+    lib = load()
+    B, H, T, dk = k.shape
+    dv = v.shape[-1]
+    dev = k.device
+    _check(k, "k", (B, H, T, dk), device=dev)
+    _check(v, "v", (B, H, T, dv), k.dtype, dev)
+    _check(gamma, "gamma", (B, H, T), torch.float32, dev)
+    _check(beta, "beta", (B, H, T), torch.float32, dev)
+    _check(lam, "lam", (H, dk), torch.float32, dev)
+    _check(qstar, "qstar", (B, H, T, dk), torch.float32, dev)
+    _check(dout, "dout", (B, H, T, dv), torch.float32, dev)
+    need = lib.mesa_backward_workspace_bytes(B, H, T, dk, dv)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    res = {"dq": torch.empty((B, H, T, dk), **f32), "dk": torch.empty((B, H, T, dk), **f32),
+           "dv": torch.empty((B, H, T, dv), **f32), "dgamma": torch.empty((B, H, T), **f32),
+           "dbeta": torch.empty((B, H, T), **f32), "dlam": torch.empty((H, dk), **f32)}
+    st = lib.mesa_backward(_ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam), B, H, T, dk, dv,
+                           _dtype_code(k), int(n_cg), _ptr(qstar), _ptr(dout), _ptr(res["dq"]),
+                           _ptr(res["dk"]), _ptr(res["dv"]), _ptr(res["dgamma"]), _ptr(res["dbeta"]),
+                           _ptr(res["dlam"]), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                           _stream(dev))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_backward")
+    return res
 
 
 def prefill_states(k, v, gamma, beta, chunk=64, workspace=None):

@@ -67,7 +67,7 @@ def test_workspace_bytes(lib):
 
 # fake, non-overlapping device addresses
 P = {n: 0x10000000 * (i + 1) for i, n in enumerate(
-    ["q", "k", "v", "g", "b", "lam", "out", "qs", "fh", "fg", "ws", "H", "G", "st"])}
+    ["q", "k", "v", "g", "b", "lam", "out", "qs", "fh", "fg", "ws", "H", "G", "st", "dl"])}
 
 
 def _fwd(lib, **kw):
@@ -212,3 +212,41 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         L.load()
+
+
+def _bwd(lib, **kw):
+    a = dict(k=P["k"], v=P["v"], gamma=P["g"], beta=P["b"], lam=P["lam"], B=2, H=3, T=128, dk=64, dv=64,
+             dtype=0, n_cg=10, qs=P["qs"], dout=P["out"], dq=P["fh"], dk_=P["fg"], dv_=P["H"], dg=P["G"],
+             db=P["st"], dl=P["dl"], ws=P["ws"], ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.mesa_backward(a["k"], a["v"], a["gamma"], a["beta"], a["lam"], a["B"], a["H"], a["T"], a["dk"],
+                             a["dv"], a["dtype"], a["n_cg"], a["qs"], a["dout"], a["dq"], a["dk_"], a["dv_"],
+                             a["dg"], a["db"], a["dl"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(qs=None), L.MESA_ERR_NULL),
+    (dict(dout=None), L.MESA_ERR_NULL),
+    (dict(dl=None), L.MESA_ERR_NULL),
+    (dict(ws=None), L.MESA_ERR_NULL),
+    (dict(dk=96), L.MESA_ERR_UNSUPPORTED),
+    (dict(n_cg=-1), L.MESA_ERR_ARG),
+    (dict(T=-1), L.MESA_ERR_SHAPE),
+    (dict(ws_bytes=64), L.MESA_ERR_WORKSPACE),
+    (dict(qs=P["qs"] + 4), L.MESA_ERR_ARG),          # q* not 16-byte aligned
+    (dict(dq=P["k"] + 64), L.MESA_ERR_ARG),          # dq overlaps k
+    (dict(db=P["fh"] + 8), L.MESA_ERR_ARG),          # two gradients overlap
+    (dict(dl=P["ws"] + 4096), L.MESA_ERR_ARG),       # dlambda inside the workspace
+])
+def test_backward_rejects_bad_arguments(lib, kw, status):
+    assert _bwd(lib, **kw) == status
+
+
+def test_backward_workspace_size(lib):
+    # fp32: H_c, G_c, S^H, A^G per 64-token chunk, u per token, dLambda parts per chunk
+    B, H, T, dk, dv = 2, 3, 130, 64, 128
+    nc = 3
+    want = 4 * (2 * B * H * nc * dk * (dk + dv) + B * H * T * dk + B * H * nc * dk)
+    assert lib.mesa_backward_workspace_bytes(B, H, T, dk, dv) == want
+    assert lib.mesa_backward_workspace_bytes(B, H, 0, dk, dv) == 0
+    assert _bwd(lib, B=0) == L.MESA_OK

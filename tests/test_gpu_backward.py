@@ -1,0 +1,101 @@
+"""GPU parity of the backward pass (mesa_backward) against the fp64 oracle.
+
+q*_t comes from the GPU forward on the fp32 path (mesa_forward_ex, qstar_out);
+the oracle's backward recomputes q*_t and e*_t with the same-step CG (Alg. 1,
+tolerance zero), so every gradient is compared element by element at the fp32
+tolerance.  Inputs given to the GPU in bf16 widen exactly for the oracle.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from mesa_testutil import TOL_F32, rel_l2, to_device
+from paper_2506_05233_amd import libmesa as L
+from paper_2506_05233_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+GRADS = ("dq", "dk", "dv", "dgamma", "dbeta", "dlam")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    L.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _dout(x, seed):
+    B, H, T, _ = x["v"].shape
+    return np.random.default_rng(seed).normal(size=(B, H, T, x["v"].shape[-1])).astype(np.float32)
+
+
+def _gpu_backward(x, dtype, n_cg, dout):
+    d = to_device(x, dtype)
+    fwd = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], n_cg, 64,
+                    precision=L.MESA_PREC_F32, want_qstar=True)
+    g = L.backward(d["k"], d["v"], d["gamma"], d["beta"], d["lam"], fwd["qstar"],
+                   torch.from_numpy(dout).cuda(), n_cg)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in g.items()}
+
+
+def _check(x, dtype, n_cg, dout, label, tol=TOL_F32):
+    got = _gpu_backward(x, dtype, n_cg, dout)
+    ref = oracle.backward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], dout, n_cg)
+    errs = {k: rel_l2(got[k], ref[k]) for k in GRADS}
+    _say("%s: %s" % (label, "  ".join("%s %.2e" % (k, e) for k, e in errs.items())))
+    for k in GRADS:
+        assert np.isfinite(got[k]).all(), k
+        assert errs[k] <= tol, (k, errs[k])
+    return got, ref
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 64), (64, 128), (128, 64), (128, 128)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_backward_matches_oracle(dk, dv, dtype):
+    """Three chunks and a ragged tail, every gradient against the oracle."""
+    x = W.forward_inputs(1, 2, 3 * 64 + 17, dk, dv, dtype, 3.0, seed=dk + dv)
+    _check(x, dtype, 10, _dout(x, 1), "backward %s d_k=%d d_v=%d" % (dtype, dk, dv))
+
+
+def test_backward_batch_sums_dlambda_and_edge_cases():
+    """Three sequences (dLambda sums over the batch), zero forget gates at a chunk
+    start, inside and at a chunk end, ignored tokens (beta = 0), a zero query."""
+    x = W.forward_inputs(3, 2, 150, 64, 64, "f32", 3.0, seed=23)
+    x["gamma"][0, 1, 40] = 0.0
+    x["gamma"][1, 0, 64] = 0.0
+    x["gamma"][2, 1, 63] = 0.0
+    x["beta"][1, 1, 5:9] = 0.0
+    x["q"][0, 0, 10] = 0.0
+    _check(x, "f32", 12, _dout(x, 2), "backward edge cases")
+
+
+@pytest.mark.parametrize("T", [1, 2, 63, 64, 65])
+def test_backward_short_sequences(T):
+    x = W.forward_inputs(1, 1, T, 64, 64, "f32", 3.0, seed=T)
+    _check(x, "f32", 6, _dout(x, T), "backward T=%d" % T)
+
+
+def test_backward_zero_dout_gives_zero_gradients():
+    x = W.forward_inputs(1, 2, 100, 64, 64, "f32", 3.0, seed=3)
+    got = _gpu_backward(x, "f32", 8, np.zeros((1, 2, 100, 64), np.float32))
+    for k in GRADS:
+        assert np.all(got[k] == 0.0), k
+
+
+def test_backward_empty_sequence_zero_dlambda():
+    d = to_device(W.forward_inputs(2, 3, 0, 64, 64, "f32", 3.0, 0), "f32")
+    qs = torch.empty((2, 3, 0, 64), dtype=torch.float32, device="cuda")
+    g = L.backward(d["k"], d["v"], d["gamma"], d["beta"], d["lam"], qs,
+                   torch.empty((2, 3, 0, 64), dtype=torch.float32, device="cuda"), 5)
+    torch.cuda.synchronize()
+    assert g["dlam"].shape == (3, 64) and float(g["dlam"].abs().max()) == 0.0
