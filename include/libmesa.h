@@ -209,7 +209,8 @@ int mesa_version(void);
 
 /* Bytes of device workspace mesa_backward needs (fp32: the chunk states and
  * their adjoints at 64-token chunks, the right-hand sides G_t^T e_t, partial
- * dLambda sums).  Returns 0 for unsupported or empty sizes. */
+ * dLambda sums; bf16 copies of the states and right-hand sides for the
+ * matrix-core solve).  Returns 0 for unsupported or empty sizes. */
 size_t mesa_backward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
                                      int64_t d_v);
 
@@ -226,6 +227,10 @@ size_t mesa_backward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_l
  * of dk_s; differentiating e_t^T G_t q*_t gives q*_t e_t^T v_s, used here.)
  *   k, v, gamma, beta, lambda, sizes, dtype: as for mesa_forward
  *   n_cg    CG iterations of the solve for e*_t (0 <= n_cg <= MESA_MAX_NCG)
+ *   precision  the solve for e*_t: MESA_PREC_F32 (fp32 products), MESA_PREC_BF16
+ *           (matrix cores, as the forward's bf16 path: bf16 inputs and chunk
+ *           states, the right-hand side G_t^T e_t rounded to bf16; bf16 dtype,
+ *           MESA_ERR_UNSUPPORTED otherwise), MESA_PREC_AUTO (BF16 for bf16 inputs)
  *   qstar   [batch, heads, seq_len, d_k] fp32: q*_t of the forward (qstar_out of
  *           mesa_forward_ex)
  *   dout    [batch, heads, seq_len, d_v] fp32: e_t
@@ -233,14 +238,15 @@ size_t mesa_backward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_l
  *   dgamma, dbeta [batch, heads, seq_len] fp32     dlambda [heads, d_k] fp32
  *   workspace / workspace_bytes: at least mesa_backward_workspace_bytes(...),
  *           16-byte aligned, as are qstar and dout
- * All arithmetic is fp32 (chunk states, adjoints and the CG solve).  Outputs
- * must overlap neither an input nor each other (MESA_ERR_ARG).  seq_len 0 writes
- * dlambda = 0 only.  Six kernel launches on `stream`. */
+ * Chunk states, adjoints and every gradient sum are fp32; the solve follows
+ * `precision`.  Outputs must overlap neither an input nor each other
+ * (MESA_ERR_ARG).  seq_len 0 writes dlambda = 0 only.  Six kernel launches on
+ * `stream` (seven on the bf16 route). */
 int mesa_backward(const void* k, const void* v, const float* gamma, const float* beta,
                   const float* lambda, int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
-                  int64_t d_v, int dtype, int n_cg, const float* qstar, const float* dout, float* dq,
-                  float* dk, float* dv, float* dgamma, float* dbeta, float* dlambda,
-                  void* workspace, size_t workspace_bytes, void* stream);
+                  int64_t d_v, int dtype, int n_cg, int precision, const float* qstar,
+                  const float* dout, float* dq, float* dk, float* dv, float* dgamma, float* dbeta,
+                  float* dlambda, void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

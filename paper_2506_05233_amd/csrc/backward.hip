@@ -26,6 +26,7 @@
 // reverse adjoint scan, the per-chunk gradients, and the Lambda reduction.
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
+#include "mesa_mfma.hpp"
 
 namespace mesa {
 namespace {
@@ -129,7 +130,11 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
 #pragma unroll
     for (int m = 0; m < NS; ++m) {
         const int t = tg * NS + m;
-        if (t < valid) a.u[(tok0 + t) * DK + b] = acc[m];
+        if (t >= valid) continue;
+        if (a.u16)
+            a.u16[(tok0 + t) * DK + b] = uint16_t(pack_bf16x2(acc[m], 0.0f) & 0xffffu);  // round to nearest even
+        else
+            a.u[(tok0 + t) * DK + b] = acc[m];
     }
 }
 

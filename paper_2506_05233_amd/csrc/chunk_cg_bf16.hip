@@ -138,7 +138,7 @@ struct CgSmem {
                   "LDS use exceeds 160 KiB");
 };
 
-template <int DK, int DV>
+template <int DK, int DV, bool READOUT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void chunk_cg_bf16_kernel(CgArgs a, int total)
 {
@@ -547,7 +547,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         if (more) __syncthreads();
         // G_c is needed only by the read-out: its loads run under the CG loop (no LDS
         // access of this chunk's build or Jacobi start is ordered behind them)
-        {
+        if constexpr (READOUT) {
             const uint16_t* Gf = static_cast<const uint16_t*>(a.Gs) + int64_t(cc) * DV * DK;
 #pragma unroll
             for (int u = 0; u < NGF; ++u) {
@@ -622,47 +622,49 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
             for (int mt = 0; mt < MT; ++mt)
                 *reinterpret_cast<f32x4*>(a.qstar + (tok0 + j) * DK + 16 * mt + 4 * g) = x[mt];
         }
-        const float zeta = sZ0[j];
-        f32x4 zo[4];  // beta_i Z[i][j] over the four token tiles (0 past the causal ones)
+        if constexpr (READOUT) {
+            const float zeta = sZ0[j];
+            f32x4 zo[4];  // beta_i Z[i][j] over the four token tiles (0 past the causal ones)
 #pragma unroll
-        for (int it = 0; it < 4; ++it) zo[it] = decay_weights4(sLg, sBeta, lgj, zlj, 16 * it + 4 * g, j);
-        bf16x8 xb[KS], xz[KS];
+            for (int it = 0; it < 4; ++it) zo[it] = decay_weights4(sLg, sBeta, lgj, zlj, 16 * it + 4 * g, j);
+            bf16x8 xb[KS], xz[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            xb[ks] = pack8(x[2 * ks], x[2 * ks + 1]);
-            xz[ks] = pack8(zeta * x[2 * ks], zeta * x[2 * ks + 1]);
-        }
-        // every wave runs all four token tiles (zo is zero past the causal ones)
-        f32x4 sacc[4];
+            for (int ks = 0; ks < KS; ++ks) {
+                xb[ks] = pack8(x[2 * ks], x[2 * ks + 1]);
+                xz[ks] = pack8(zeta * x[2 * ks], zeta * x[2 * ks + 1]);
+            }
+            // every wave runs all four token tiles (zo is zero past the causal ones)
+            f32x4 sacc[4];
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-            sacc[it] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int it = 0; it < 4; ++it) {
+                sacc[it] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                sacc[it] = mfma16(lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g), xb[ks], sacc[it]);
-        }
-        f32x4 o[MTV];
+                for (int ks = 0; ks < KS; ++ks)
+                    sacc[it] = mfma16(lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g), xb[ks], sacc[it]);
+            }
+            f32x4 o[MTV];
 #pragma unroll
-        for (int mt = 0; mt < MTV; ++mt) {
-            o[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int mt = 0; mt < MTV; ++mt) {
+                o[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                o[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sGf + ((mt * KS + ks) * kWave + lane) * 8)),
-                               xz[ks], o[mt]);
-        }
+                for (int ks = 0; ks < KS; ++ks)
+                    o[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sGf + ((mt * KS + ks) * kWave + lane) * 8)),
+                                   xz[ks], o[mt]);
+            }
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            const bf16x8 sb = pack8(sacc[2 * u] * zo[2 * u], sacc[2 * u + 1] * zo[2 * u + 1]);
+            for (int u = 0; u < 2; ++u) {
+                const bf16x8 sb = pack8(sacc[2 * u] * zo[2 * u], sacc[2 * u + 1] * zo[2 * u + 1]);
 #pragma unroll
-            for (int mt = 0; mt < MTV; ++mt)
-                o[mt] = mfma16(lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, o[mt]);
-        }
+                for (int mt = 0; mt < MTV; ++mt)
+                    o[mt] = mfma16(lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, o[mt]);
+            }
 
-        if (j < valid) {
+            if (j < valid) {
 #pragma unroll
-            for (int mt = 0; mt < MTV; ++mt)
-                *reinterpret_cast<f32x4*>(a.out + (tok0 + j) * DV + 16 * mt + 4 * g) = o[mt];
-        }
+                for (int mt = 0; mt < MTV; ++mt)
+                    *reinterpret_cast<f32x4*>(a.out + (tok0 + j) * DV + 16 * mt + 4 * g) = o[mt];
+            }
+        }  // READOUT
 
         if (!more) break;
         cc = cn;
@@ -693,7 +695,11 @@ hipError_t launch_shape(const CgArgs& a, hipStream_t stream)
     if (total > INT32_MAX) return hipErrorInvalidValue;
     const int64_t cus = device_cus();
     const unsigned blocks = unsigned(total < cus ? total : cus);
-    hipLaunchKernelGGL((chunk_cg_bf16_kernel<DK, DV>), dim3(blocks), dim3(kThreads), 0, stream, a, int(total));
+    // without an output the read-out (and the loads of G_c and v it needs) is skipped
+    if (a.out)
+        hipLaunchKernelGGL((chunk_cg_bf16_kernel<DK, DV, true>), dim3(blocks), dim3(kThreads), 0, stream, a, int(total));
+    else
+        hipLaunchKernelGGL((chunk_cg_bf16_kernel<DK, DV, false>), dim3(blocks), dim3(kThreads), 0, stream, a, int(total));
     return hipGetLastError();
 }
 

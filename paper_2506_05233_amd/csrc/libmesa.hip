@@ -336,23 +336,30 @@ namespace {
 
 constexpr int kBwdChunk = 64;  // the backward's own chunking (independent of the forward's)
 
-// Backward workspace, fp32: forward chunk states H_c, G_c; the adjoints S^H, A^G
-// arriving at every chunk's end; the right-hand sides u; per-chunk dLambda sums.
+// Backward workspace: fp32 forward chunk states H_c, G_c; the fp32 adjoints S^H,
+// A^G arriving at every chunk's end; the fp32 right-hand sides u; per-chunk dLambda
+// sums; then, for the matrix-core solve, the bf16 chunk states (fragment layout) and
+// u rounded to bf16.
 struct BwdLayout {
-    int64_t nc, hs, gs, sh, ag, u, dl, total;  // offsets and total, in floats
+    int64_t nc, hs, gs, sh, ag, u, dl, fh, fg, u16, total;  // byte offsets and total
 };
 BwdLayout bwd_layout(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v)
 {
     BwdLayout L;
     const int64_t bh = batch * heads;
     L.nc = n_chunks_of(seq_len, kBwdChunk);
+    const int64_t nH = bh * L.nc * d_k * d_k, nG = bh * L.nc * d_v * d_k;
     L.hs = 0;
-    L.gs = L.hs + bh * L.nc * d_k * d_k;
-    L.sh = L.gs + bh * L.nc * d_v * d_k;
-    L.ag = L.sh + bh * L.nc * d_k * d_k;
-    L.u = L.ag + bh * L.nc * d_v * d_k;
-    L.dl = L.u + bh * seq_len * d_k;
-    L.total = L.dl + bh * L.nc * d_k;
+    L.gs = L.hs + 4 * nH;
+    L.sh = L.gs + 4 * nG;
+    L.ag = L.sh + 4 * nH;
+    L.u = L.ag + 4 * nG;
+    L.dl = L.u + 4 * bh * seq_len * d_k;
+    L.fh = L.dl + 4 * bh * L.nc * d_k;
+    L.fg = L.fh + 2 * nH;
+    L.u16 = L.fg + 2 * nG;
+    L.total = L.u16 + 2 * bh * seq_len * d_k;
+    L.total = (L.total + 15) / 16 * 16;
     return L;
 }
 
@@ -364,16 +371,23 @@ size_t mesa_backward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_l
 {
     if (batch <= 0 || heads <= 0 || seq_len <= 0) return 0;
     if (!dim_ok(d_k) || !dim_ok(d_v)) return 0;
-    return size_t(bwd_layout(batch, heads, seq_len, d_k, d_v).total) * sizeof(float);
+    return size_t(bwd_layout(batch, heads, seq_len, d_k, d_v).total);
 }
 
 int mesa_backward(const void* k, const void* v, const float* gamma, const float* beta, const float* lambda,
                   int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg,
-                  const float* qstar, const float* dout, float* dq, float* dk, float* dv, float* dgamma,
-                  float* dbeta, float* dlambda, void* workspace, size_t workspace_bytes, void* stream)
+                  int precision, const float* qstar, const float* dout, float* dq, float* dk, float* dv,
+                  float* dgamma, float* dbeta, float* dlambda, void* workspace, size_t workspace_bytes,
+                  void* stream)
 {
     int st = check_sizes(batch, heads, seq_len, d_k, d_v, dtype, n_cg);
     if (st != MESA_OK) return st;
+    if (precision != MESA_PREC_AUTO && precision != MESA_PREC_F32 && precision != MESA_PREC_BF16)
+        return MESA_ERR_UNSUPPORTED;
+    const mesa::ForwardShape probe{batch, heads, seq_len, int(d_k), int(d_v), kBwdChunk, 0, dtype == MESA_DTYPE_BF16};
+    const bool cg_bf16 = mesa::chunk_cg_bf16_supported(probe);
+    if (precision == MESA_PREC_BF16 && !cg_bf16) return MESA_ERR_UNSUPPORTED;
+    const bool use_bf16 = precision == MESA_PREC_BF16 || (precision == MESA_PREC_AUTO && cg_bf16);
     if (batch == 0 || heads == 0) return MESA_OK;
     if (!lambda || !dlambda) return MESA_ERR_NULL;
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -408,19 +422,34 @@ int mesa_backward(const void* k, const void* v, const float* gamma, const float*
         return mesa::launch_fill_zero(dlambda, heads * d_k, s) == hipSuccess ? MESA_OK : MESA_ERR_HIP;
 
     const BwdLayout L = bwd_layout(batch, heads, seq_len, d_k, d_v);
-    float* ws = static_cast<float*>(workspace);
+    char* base = static_cast<char*>(workspace);
+    auto f32_at = [&](int64_t off) { return reinterpret_cast<float*>(base + off); };
+    auto u16_at = [&](int64_t off) { return reinterpret_cast<uint16_t*>(base + off); };
     const mesa::ForwardShape shape{batch, heads, seq_len, int(d_k), int(d_v), kBwdChunk, int(L.nc),
                                    dtype == MESA_DTYPE_BF16};
-    // forward chunk states (fp32, plain layout)
-    mesa::StateArgs sa{shape, k, v, gamma, beta, ws + L.hs, ws + L.gs, nullptr, nullptr, true, false};
+    // forward chunk states (fp32, plain layout), and for the matrix-core solve the bf16
+    // fragment states as the forward's solve reads them
+    mesa::StateArgs sa{shape, k, v, gamma, beta, f32_at(L.hs), f32_at(L.gs), nullptr, nullptr, true, false};
     if (mesa::launch_chunk_state(sa, s) != hipSuccess) return MESA_ERR_HIP;
-    mesa::BwdArgs ba{shape, k, v, gamma, beta, qstar, dout, dq, ws + L.hs, ws + L.gs, ws + L.sh, ws + L.ag,
-                     ws + L.u, dk, dv, dgamma, dbeta, ws + L.dl, dlambda};
-    // u_t = G_t^T e_t, then e*_t = (H_t + Lambda)^{-1} u_t into dq
+    if (use_bf16) {
+        mesa::StateArgs fa{shape, k, v, gamma, beta, u16_at(L.fh), u16_at(L.fg), nullptr, nullptr, true, true};
+        if (mesa::launch_chunk_state(fa, s) != hipSuccess) return MESA_ERR_HIP;
+    }
+    mesa::BwdArgs ba{shape, k, v, gamma, beta, qstar, dout, dq, f32_at(L.hs), f32_at(L.gs), f32_at(L.sh),
+                     f32_at(L.ag), f32_at(L.u), use_bf16 ? u16_at(L.u16) : nullptr, dk, dv, dgamma, dbeta,
+                     f32_at(L.dl), dlambda};
+    // u_t = G_t^T e_t, then e*_t = (H_t + Lambda)^{-1} u_t into dq: on the matrix cores
+    // (bf16 operands, u rounded to bf16, no read-out) or with fp32 products
     if (mesa::launch_backward_stage(ba, 0, s) != hipSuccess) return MESA_ERR_HIP;
-    mesa::CgArgs ca{shape, nullptr, k, v, gamma, beta, lambda, ws + L.hs, ws + L.gs, n_cg, nullptr, dq, 0.0f,
-                    nullptr, ws + L.u};
-    if (mesa::launch_chunk_cg_f32(ca, s) != hipSuccess) return MESA_ERR_HIP;
+    if (use_bf16) {
+        mesa::CgArgs ca{shape, u16_at(L.u16), k, v, gamma, beta, lambda, u16_at(L.fh), u16_at(L.fg), n_cg,
+                        nullptr, dq, 0.0f, nullptr};
+        if (mesa::launch_chunk_cg_bf16(ca, s) != hipSuccess) return MESA_ERR_HIP;
+    } else {
+        mesa::CgArgs ca{shape, nullptr, k, v, gamma, beta, lambda, f32_at(L.hs), f32_at(L.gs), n_cg, nullptr, dq,
+                        0.0f, nullptr, f32_at(L.u)};
+        if (mesa::launch_chunk_cg_f32(ca, s) != hipSuccess) return MESA_ERR_HIP;
+    }
     for (int stage = 1; stage <= 3; ++stage)
         if (mesa::launch_backward_stage(ba, stage, s) != hipSuccess) return MESA_ERR_HIP;
     return MESA_OK;

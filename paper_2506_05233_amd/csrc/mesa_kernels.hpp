@@ -88,6 +88,7 @@ struct BwdArgs {
     float* SH;             // symmetric H adjoint arriving at each chunk's end [B*H, n_chunks, d_k, d_k]
     float* AG;             // G adjoint [B*H, n_chunks, d_v, d_k]
     float* u;              // [B, H, T, d_k]
+    uint16_t* u16;         // if non-null, u is written here instead, rounded to bf16
     float* dk;
     float* dv;
     float* dgamma;

@@ -73,7 +73,7 @@ def load():
     lib.mesa_decode_step_tol.restype = ci
     lib.mesa_backward_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
     lib.mesa_backward_workspace_bytes.restype = sz
-    lib.mesa_backward.argtypes = [vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, fp, fp,
+    lib.mesa_backward.argtypes = [vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, fp, fp,
                                   fp, fp, fp, fp, fp, fp, vp, sz, vp]
     lib.mesa_backward.restype = ci
     lib.mesa_status_string.argtypes = [ci]
@@ -264,11 +264,13 @@ def backward_workspace_bytes(batch, heads, seq_len, d_k, d_v) -> int:
     return load().mesa_backward_workspace_bytes(batch, heads, seq_len, d_k, d_v)
 
 
-def backward(k, v, gamma, beta, lam, qstar, dout, n_cg, workspace=None):
+def backward(k, v, gamma, beta, lam, qstar, dout, n_cg, precision=MESA_PREC_AUTO, workspace=None):
     """Gradients of the layer given dout = dL/do [B,H,T,d_v] fp32 and the forward's
     q* [B,H,T,d_k] fp32 (mesa_backward).  k, v [B,H,T,d] fp32 or bf16; gamma, beta
-    [B,H,T]; lam [H,d_k].  Returns a dict of fp32 tensors: "dq", "dk" [B,H,T,d_k],
-    "dv" [B,H,T,d_v], "dgamma", "dbeta" [B,H,T], "dlam" [H,d_k].
+    [B,H,T]; lam [H,d_k].  precision selects the solve for e* (MESA_PREC_F32, or
+    MESA_PREC_BF16 on the matrix cores; AUTO: BF16 for bf16 inputs).  Returns a dict
+    of fp32 tensors: "dq", "dk" [B,H,T,d_k], "dv" [B,H,T,d_v], "dgamma", "dbeta"
+    [B,H,T], "dlam" [H,d_k].
     Runs on torch's current stream of k's device."""
     torch = _torch()
     lib = load()
@@ -290,7 +292,7 @@ def backward(k, v, gamma, beta, lam, qstar, dout, n_cg, workspace=None):
            "dv": torch.empty((B, H, T, dv), **f32), "dgamma": torch.empty((B, H, T), **f32),
            "dbeta": torch.empty((B, H, T), **f32), "dlam": torch.empty((H, dk), **f32)}
     st = lib.mesa_backward(_ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam), B, H, T, dk, dv,
-                           _dtype_code(k), int(n_cg), _ptr(qstar), _ptr(dout), _ptr(res["dq"]),
+                           _dtype_code(k), int(n_cg), int(precision), _ptr(qstar), _ptr(dout), _ptr(res["dq"]),
                            _ptr(res["dk"]), _ptr(res["dv"]), _ptr(res["dgamma"]), _ptr(res["dbeta"]),
                            _ptr(res["dlam"]), _ptr(workspace), workspace.numel() * workspace.element_size(),
                            _stream(dev))

@@ -216,11 +216,11 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
 
 def _bwd(lib, **kw):
     a = dict(k=P["k"], v=P["v"], gamma=P["g"], beta=P["b"], lam=P["lam"], B=2, H=3, T=128, dk=64, dv=64,
-             dtype=0, n_cg=10, qs=P["qs"], dout=P["out"], dq=P["fh"], dk_=P["fg"], dv_=P["H"], dg=P["G"],
+             dtype=0, n_cg=10, prec=0, qs=P["qs"], dout=P["out"], dq=P["fh"], dk_=P["fg"], dv_=P["H"], dg=P["G"],
              db=P["st"], dl=P["dl"], ws=P["ws"], ws_bytes=1 << 40)
     a.update(kw)
     return lib.mesa_backward(a["k"], a["v"], a["gamma"], a["beta"], a["lam"], a["B"], a["H"], a["T"], a["dk"],
-                             a["dv"], a["dtype"], a["n_cg"], a["qs"], a["dout"], a["dq"], a["dk_"], a["dv_"],
+                             a["dv"], a["dtype"], a["n_cg"], a["prec"], a["qs"], a["dout"], a["dq"], a["dk_"], a["dv_"],
                              a["dg"], a["db"], a["dl"], a["ws"], a["ws_bytes"], None)
 
 
@@ -231,6 +231,8 @@ def _bwd(lib, **kw):
     (dict(ws=None), L.MESA_ERR_NULL),
     (dict(dk=96), L.MESA_ERR_UNSUPPORTED),
     (dict(n_cg=-1), L.MESA_ERR_ARG),
+    (dict(prec=5), L.MESA_ERR_UNSUPPORTED),
+    (dict(prec=L.MESA_PREC_BF16), L.MESA_ERR_UNSUPPORTED),  # fp32 inputs have no matrix-core solve
     (dict(T=-1), L.MESA_ERR_SHAPE),
     (dict(ws_bytes=64), L.MESA_ERR_WORKSPACE),
     (dict(qs=P["qs"] + 4), L.MESA_ERR_ARG),          # q* not 16-byte aligned
@@ -243,10 +245,12 @@ def test_backward_rejects_bad_arguments(lib, kw, status):
 
 
 def test_backward_workspace_size(lib):
-    # fp32: H_c, G_c, S^H, A^G per 64-token chunk, u per token, dLambda parts per chunk
+    # fp32: H_c, G_c, S^H, A^G per 64-token chunk, u per token, dLambda parts per chunk;
+    # bf16: H_c, G_c fragments per chunk, u per token
     B, H, T, dk, dv = 2, 3, 130, 64, 128
     nc = 3
     want = 4 * (2 * B * H * nc * dk * (dk + dv) + B * H * T * dk + B * H * nc * dk)
+    want += 2 * (B * H * nc * dk * (dk + dv) + B * H * T * dk)
     assert lib.mesa_backward_workspace_bytes(B, H, T, dk, dv) == want
     assert lib.mesa_backward_workspace_bytes(B, H, 0, dk, dv) == 0
     assert _bwd(lib, B=0) == L.MESA_OK

@@ -2,14 +2,16 @@
 
 q*_t comes from the GPU forward on the fp32 path (mesa_forward_ex, qstar_out);
 the oracle's backward recomputes q*_t and e*_t with the same-step CG (Alg. 1,
-tolerance zero), so every gradient is compared element by element at the fp32
-tolerance.  Inputs given to the GPU in bf16 widen exactly for the oracle.
+tolerance zero), so every gradient is compared element by element: at the fp32
+tolerance when the solve for e*_t uses fp32 products, at the bf16 tolerance on
+the matrix-core route (bf16 chunk states and right-hand sides, as the forward's
+bf16 path).  Inputs given to the GPU in bf16 widen exactly for the oracle.
 """
 import numpy as np
 import pytest
 
 import oracle
-from mesa_testutil import TOL_F32, rel_l2, to_device
+from mesa_testutil import TOL_BF16, TOL_F32, rel_l2, to_device
 from paper_2506_05233_amd import libmesa as L
 from paper_2506_05233_amd import workloads as W
 
@@ -38,18 +40,18 @@ def _dout(x, seed):
     return np.random.default_rng(seed).normal(size=(B, H, T, x["v"].shape[-1])).astype(np.float32)
 
 
-def _gpu_backward(x, dtype, n_cg, dout):
+def _gpu_backward(x, dtype, n_cg, dout, precision=L.MESA_PREC_F32):
     d = to_device(x, dtype)
     fwd = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], n_cg, 64,
                     precision=L.MESA_PREC_F32, want_qstar=True)
     g = L.backward(d["k"], d["v"], d["gamma"], d["beta"], d["lam"], fwd["qstar"],
-                   torch.from_numpy(dout).cuda(), n_cg)
+                   torch.from_numpy(dout).cuda(), n_cg, precision=precision)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in g.items()}
 
 
-def _check(x, dtype, n_cg, dout, label, tol=TOL_F32):
-    got = _gpu_backward(x, dtype, n_cg, dout)
+def _check(x, dtype, n_cg, dout, label, tol=TOL_F32, precision=L.MESA_PREC_F32):
+    got = _gpu_backward(x, dtype, n_cg, dout, precision)
     ref = oracle.backward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], dout, n_cg)
     errs = {k: rel_l2(got[k], ref[k]) for k in GRADS}
     _say("%s: %s" % (label, "  ".join("%s %.2e" % (k, e) for k, e in errs.items())))
@@ -62,9 +64,20 @@ def _check(x, dtype, n_cg, dout, label, tol=TOL_F32):
 @pytest.mark.parametrize("dk,dv", [(64, 64), (64, 128), (128, 64), (128, 128)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_backward_matches_oracle(dk, dv, dtype):
-    """Three chunks and a ragged tail, every gradient against the oracle."""
+    """Three chunks and a ragged tail, every gradient against the oracle (fp32 solve)."""
     x = W.forward_inputs(1, 2, 3 * 64 + 17, dk, dv, dtype, 3.0, seed=dk + dv)
     _check(x, dtype, 10, _dout(x, 1), "backward %s d_k=%d d_v=%d" % (dtype, dk, dv))
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 64), (64, 128), (128, 64), (128, 128)])
+def test_backward_matrix_core_solve_matches_oracle(dk, dv):
+    """bf16 inputs, the solve for e* on the matrix cores (the default for bf16):
+    every gradient within the bf16 tolerance, on two sequences with ragged tails and
+    a zero gate."""
+    x = W.forward_inputs(2, 2, 4 * 64 + 29, dk, dv, "bf16", 4.0, seed=3 * dk + dv)
+    x["gamma"][1, 0, 100] = 0.0
+    _check(x, "bf16", 15, _dout(x, 4), "backward matrix-core solve d_k=%d d_v=%d" % (dk, dv),
+           tol=TOL_BF16, precision=L.MESA_PREC_AUTO)
 
 
 def test_backward_batch_sums_dlambda_and_edge_cases():
