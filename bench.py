@@ -13,7 +13,8 @@ time give the roofline entry.  Decode (256 sequences x 16 heads, d=128,
 Two extra entries run the same forward and decode with Alg. 1's relative
 stopping test (eps = 1e-4, at most 30 iterations, the paper's dynamic
 test-time compute setting) and report tokens/s and the mean iterations used;
-they are context, not the metric.
+they are context, not the metric.  A third times the backward pass
+(mesa_backward, App. D) of the same workload given dL/do and the forward's q*.
 
 The CPU baseline is the fp64 oracle (the sequential recurrence with fixed-step
 CG) on a bounded sample of the same workload, run on the host's cores.
@@ -155,6 +156,41 @@ def run_forward_dynamic(args, torch, L, fw):
             "ms_per_call": ms, "mean_cg_steps": float(steps.float().mean())}
 
 
+def run_backward(args, torch, L, fw):
+    """mesa_backward on the forward workload: gradients of q, k, v, gamma, beta and
+    Lambda given a seeded dL/do and the q* of the forward (computed before timing)."""
+    w, d = fw["w"], fw["d"]
+    res = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], w.n_cg, w.chunk,
+                    precision=args.precision, want_qstar=True)
+    qstar = res["qstar"]
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    dout = torch.randn(d["v"].shape, dtype=torch.float32, device="cuda", generator=gen)
+    ws = torch.empty(L.backward_workspace_bytes(w.batch, w.heads, w.seq_len, w.d_k, w.d_v),
+                     dtype=torch.uint8, device="cuda")
+    def call():
+        return L.backward(d["k"], d["v"], d["gamma"], d["beta"], d["lam"], qstar, dout, w.n_cg,
+                          precision=args.precision, workspace=ws)
+    for _ in range(2):
+        g = call()
+    torch.cuda.synchronize()
+    if not all(bool(torch.isfinite(t).all()) for t in g.values()):
+        raise RuntimeError("non-finite gradient")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del ws
+    return {"tokens_per_s": w.batch * w.seq_len / (ms / 1e3), "ms_per_call": ms, "n_cg": w.n_cg,
+            "solve": "matrix cores (bf16 operands)" if args.precision != L.MESA_PREC_F32 else "fp32",
+            "launches": "fp32 and bf16 chunk states, rhs G^T e, CG solve for e*, reverse adjoint scan, "
+                        "per-chunk gradients, Lambda sum"}
+
+
 def run_decode(args, torch, L, W):
     w = W.DECODE_BF16
     dev = torch.device("cuda:0")
@@ -269,6 +305,7 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=1024)
     ap.add_argument("--cpu-sequences", type=int, default=128)
     ap.add_argument("--skip-decode", action="store_true")
+    ap.add_argument("--skip-backward", action="store_true")
     ap.add_argument("--eps", type=float, default=1e-4,
                     help="relative CG tolerance of the extra dynamic-stopping runs (0: skip them)")
     ap.add_argument("--dyn-max-cg", type=int, default=30, help="iteration limit of those runs")
@@ -301,6 +338,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     dyn = run_forward_dynamic(args, torch, L, fw) if args.eps > 0 else None
+    bwd = None if args.skip_backward else run_backward(args, torch, L, fw)
     dec = None if args.skip_decode else run_decode(args, torch, L, W)
     cpu = None if args.skip_cpu else cpu_baseline(args, fw["x"], w)
 
@@ -340,6 +378,7 @@ def main():
         "state_kernel_hbm": {"GBps": fw["state_bytes"] / (fw["state_ms"] / 1e3) / 1e9,
                              "frac": fw["state_bytes"] / (fw["state_ms"] / 1e3) / 1e9 / PEAKS["hbm_gbps"]},
         "forward_dynamic_stopping": dyn,
+        "backward": bwd,
         "decode": dec,
         "cpu_baseline": cpu,
     }
