@@ -237,7 +237,7 @@ size_t mesa_backward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_l
  *   dq, dk  [batch, heads, seq_len, d_k] fp32      dv [batch, heads, seq_len, d_v] fp32
  *   dgamma, dbeta [batch, heads, seq_len] fp32     dlambda [heads, d_k] fp32
  *   workspace / workspace_bytes: at least mesa_backward_workspace_bytes(...),
- *           16-byte aligned, as are qstar and dout
+ *           16-byte aligned, as are k, v, qstar, dout and dq
  * Chunk states, adjoints and every gradient sum are fp32; the solve follows
  * `precision`.  Outputs must overlap neither an input nor each other
  * (MESA_ERR_ARG).  seq_len 0 writes dlambda = 0 only.  Six kernel launches on

@@ -23,7 +23,12 @@
 //
 // Launches (one stream): the forward chunk-state scan (fp32 states), the right-hand
 // sides u_t = G_t^T e_t, the chunked CG solve of (H_t + Lambda) e*_t = u_t, the
-// reverse adjoint scan, the per-chunk gradients, and the Lambda reduction.
+// reverse adjoint scan, the per-chunk gradients, and the Lambda reduction.  Every
+// product over tokens or features is a dense contraction of fp32 operands and runs
+// on the matrix cores in fp32 (v_mfma_f32_16x16x4f32: exact fp32 products, fp32
+// accumulation), 16 x 16 output tiles per wave.
+#include <type_traits>
+
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
 #include "mesa_mfma.hpp"
@@ -31,53 +36,144 @@
 namespace mesa {
 namespace {
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int kThreads = 256;
 constexpr int kC = 64;       // tokens per chunk of the backward
-constexpr int kLdT = 132;    // row stride of [token][feature] tiles (16-byte rows)
-constexpr int kLdC = 68;     // row stride of [token][token] matrices (16-byte rows)
+constexpr int kLdT = 130;    // row stride of [token][feature] tiles
+constexpr int kLdC = 66;     // row stride of [token][token] matrices
 
-constexpr int kLdO = 129;    // odd row stride: tiles read one row per lane
-
-template <typename T>
-__device__ __forceinline__ void load_tile(float* dst, const T* src, int64_t tok0, int valid, int d, int ld = kLdT)
+// One 16 x 16 output tile += A (16 x K) B (K x 16) on the matrix cores, fp32:
+// A(m, k) = A[m * AM + k * AK], B(k, n) = B[k * BK + n * BN].  With
+// v_mfma_f32_16x16x4f32 lane l supplies A(l % 16, k0 + l / 16) and B(k0 + l / 16, l % 16);
+// element i of the result holds row 4 (l / 16) + i, column l % 16.
+template <int K, int AM, int AK, int BK, int BN>
+__device__ __forceinline__ f32x4 mma16(const float* A, const float* B, f32x4 acc)
 {
-    for (int e = threadIdx.x; e < kC * d; e += kThreads) {
-        const int i = e / d, f = e % d;
-        dst[i * ld + f] = i < valid ? to_f32(src[(tok0 + i) * d + f]) : 0.0f;
+    const int lane = threadIdx.x % kWave, r = lane % 16, sl = lane / 16;
+    const float* a = A + r * AM + sl * AK;
+    const float* b = B + sl * BK + r * BN;
+    // all operand loads first (one round trip for the whole contraction), then the products
+    float av[K / 4], bv[K / 4];
+#pragma unroll
+    for (int i = 0; i < K / 4; ++i) {
+        av[i] = a[4 * i * AK];
+        bv[i] = b[4 * i * BK];
+    }
+#pragma unroll
+    for (int i = 0; i < K / 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[i], acc, 0, 0, 0);
+    return acc;
+}
+
+// The same product split in two: the B operand values of one tile (a global matrix,
+// loaded one tile ahead so its latency overlaps the previous tile's products), then
+// the products with A read from LDS.
+template <int K, int BK, int BN>
+__device__ __forceinline__ void load_b(const float* B, float (&bv)[K / 4])
+{
+    const int lane = threadIdx.x % kWave, r = lane % 16, sl = lane / 16;
+    const float* b = B + sl * BK + r * BN;
+#pragma unroll
+    for (int i = 0; i < K / 4; ++i) bv[i] = b[4 * i * BK];
+}
+template <int K, int AM, int AK>
+__device__ __forceinline__ f32x4 mma16_b(const float* A, const float (&bv)[K / 4], f32x4 acc)
+{
+    const int lane = threadIdx.x % kWave, r = lane % 16, sl = lane / 16;
+    const float* a = A + r * AM + sl * AK;
+    float av[K / 4];
+#pragma unroll
+    for (int i = 0; i < K / 4; ++i) av[i] = a[4 * i * AK];
+#pragma unroll
+    for (int i = 0; i < K / 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[i], acc, 0, 0, 0);
+    return acc;
+}
+
+// Products of the rows 16w.. of an LDS token tile with NT consecutive 16-column tiles
+// of a global matrix (B(k, n) = M[k * BK + (16 t + n) * BN] for tile t), the matrix
+// operands double-buffered; epi(t, result) consumes each tile.
+template <int K, int NT, int AM, int BK, int BN, typename Epi>
+__device__ __forceinline__ void rows_times_matrix(const float* A, const float* M, Epi&& epi)
+{
+    float b0[K / 4], b1[K / 4];
+    load_b<K, BK, BN>(M, b0);
+#pragma unroll
+    for (int t = 0; t < NT; t += 2) {
+        if (t + 1 < NT) load_b<K, BK, BN>(M + (16 * (t + 1)) * BN, b1);
+        epi(t, mma16_b<K, AM, 1>(A, b0, f32x4{0.0f, 0.0f, 0.0f, 0.0f}));
+        if (t + 2 < NT) load_b<K, BK, BN>(M + (16 * (t + 2)) * BN, b0);
+        if (t + 1 < NT) epi(t + 1, mma16_b<K, AM, 1>(A, b1, f32x4{0.0f, 0.0f, 0.0f, 0.0f}));
     }
 }
 
-// Per-token sums over the D features of a token group (thread layout: feature
-// tid % D, token group tid / D, tokens tg * NS + m): wave sums, then the waves of a
-// group through LDS.  out[t] receives the sum for token t.
-template <int D>
-__device__ __forceinline__ void token_sums(const float (&part)[kC / (kThreads / D)], float* out, float (*sPart)[kC])
+constexpr f32x4 kZero4 = {0.0f, 0.0f, 0.0f, 0.0f};
+
+// Sum over the 16 lanes of a lane row (the columns of a result tile); every lane of
+// the row receives it.
+__device__ __forceinline__ float row16_sum(float x)
 {
-    constexpr int NTG = kThreads / D, NS = kC / NTG, WPG = D / kWave;
-    const int tid = threadIdx.x, tg = tid / D, w = tid / kWave, lane = tid % kWave;
+    x += dpp_f32<kDppQuadSwap1>(x, x);
+    x += dpp_f32<kDppQuadSwap2>(x, x);
+    x += dpp_f32<kDppRowRor4>(x, x);
+    x += dpp_f32<kDppRowRor8>(x, x);
+    return x;
+}
+
+// [token][feature] tile of a chunk (rows past `valid` zero) into LDS rows of `ld` floats:
+// 16-byte global loads (4 fp32 or 8 bf16), every load of the thread issued before the
+// first store.  Rows past the end re-read the last valid token and are zeroed.
+template <int D, int LD = kLdT>
+__device__ __forceinline__ void load_tile(float* dst, const float* src, int64_t tok0, int valid)
+{
+    constexpr int V = kC * D / 4 / kThreads;  // float4 per thread
+    float4 x[V];
 #pragma unroll
-    for (int m = 0; m < NS; ++m) {
-        const float v = wave_sum(part[m]);
-        if (lane == 0) sPart[w][tg * NS + m] = v;
+    for (int m = 0; m < V; ++m) {
+        const int e = threadIdx.x + kThreads * m, i = e / (D / 4), f = 4 * (e % (D / 4));
+        x[m] = *reinterpret_cast<const float4*>(src + (tok0 + min(i, valid - 1)) * D + f);
     }
-    __syncthreads();
-    if (tid < kC) {
-        const int g = tid / NS;
-        float acc = 0.0f;
 #pragma unroll
-        for (int u = 0; u < WPG; ++u) acc += sPart[g * WPG + u][tid];
-        out[tid] = acc;
+    for (int m = 0; m < V; ++m) {
+        const int e = threadIdx.x + kThreads * m, i = e / (D / 4), f = 4 * (e % (D / 4));
+        const bool ok = i < valid;
+        float* o = dst + i * LD + f;
+        o[0] = ok ? x[m].x : 0.0f;
+        o[1] = ok ? x[m].y : 0.0f;
+        o[2] = ok ? x[m].z : 0.0f;
+        o[3] = ok ? x[m].w : 0.0f;
     }
-    __syncthreads();
+}
+template <int D, int LD = kLdT>
+__device__ __forceinline__ void load_tile(float* dst, const bf16_t* src, int64_t tok0, int valid)
+{
+    constexpr int V = kC * D / 8 / kThreads;  // 8-element loads per thread
+    uint4 x[V];
+#pragma unroll
+    for (int m = 0; m < V; ++m) {
+        const int e = threadIdx.x + kThreads * m, i = e / (D / 8), f = 8 * (e % (D / 8));
+        x[m] = *reinterpret_cast<const uint4*>(src + (tok0 + min(i, valid - 1)) * D + f);
+    }
+#pragma unroll
+    for (int m = 0; m < V; ++m) {
+        const int e = threadIdx.x + kThreads * m, i = e / (D / 8), f = 8 * (e % (D / 8));
+        const bool ok = i < valid;
+        const uint32_t w4[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
+        float* o = dst + i * LD + f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            o[2 * q] = ok ? __uint_as_float(w4[q] << 16) : 0.0f;
+            o[2 * q + 1] = ok ? __uint_as_float(w4[q] & 0xffff0000u) : 0.0f;
+        }
+    }
 }
 
 // ---------------------------------------------------------------- u = G^T e
 // u_t = zeta_{t,c-1} G_c^T e_t + sum_{i<=t} zeta_{t,i} beta_i (v_i . e_t) k_i for
 // the tokens of one chunk (the GLA form of App. D with the roles of k and v swapped).
+// Wave w owns tokens 16w .. 16w+15.
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
 {
-    constexpr int NTG = kThreads / DK, NS = kC / NTG;  // token groups; tokens per thread
     const ForwardShape s = a.s;
     const int nc = s.n_chunks;
     const int n = blockIdx.x % nc;
@@ -86,140 +182,148 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     const int valid = int(min<int64_t>(kC, s.seq_len - t0));
     const int64_t tok0 = bh * s.seq_len + t0;
     const int tid = threadIdx.x;
+    const int w = tid / kWave, lane = tid % kWave, g = lane / 16, ln = lane % 16;
 
-    __shared__ float sE[kC * kLdO];   // e_t [t][a]
-    __shared__ float sX[kC * kLdO];   // v_i, then k_i
+    __shared__ float sE[kC * kLdT];   // e_t [t][a]
+    __shared__ float sX[kC * kLdT];   // v_i, then k_i
     __shared__ float sS[kC * kLdC];   // beta_i zeta_{t,i} (v_i . e_t) as [t][i]
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
 
-    load_tile(sE, a.dout, tok0, valid, DV, kLdO);
-    load_tile(sX, static_cast<const Tin*>(a.v), tok0, valid, DV, kLdO);
+    load_tile<DV>(sX, static_cast<const Tin*>(a.v), tok0, valid);
+    load_tile<DV>(sE, a.dout, tok0, valid);
     if (tid < kWave) chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
     __syncthreads();
-    for (int e = tid; e < kC * kC; e += kThreads) {
-        const int t = e / kC, i = e % kC;
-        float acc = 0.0f;
-        if (i <= t && i < valid) {
-            for (int c = 0; c < DV; ++c) acc += sX[i * kLdO + c] * sE[t * kLdO + c];
-            acc *= a.beta[tok0 + i] * decay_between(sLg, sZl, i, t);
+    // S rows 16w.. (tokens t), columns i: (e_t . v_i) weighted
+#pragma unroll
+    for (int it = 0; it < kC / 16; ++it) {
+        const f32x4 ev = mma16<DV, kLdT, 1, 1, kLdT>(sE + 16 * w * kLdT, sX + 16 * it * kLdT, kZero4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int t = 16 * w + 4 * g + r, i = 16 * it + ln;
+            sS[t * kLdC + i] = (i <= t && i < valid) ? a.beta[tok0 + i] * decay_between(sLg, sZl, i, t) * ev[r] : 0.0f;
         }
-        sS[t * kLdC + i] = acc;
     }
     __syncthreads();
-    load_tile(sX, static_cast<const Tin*>(a.k), tok0, valid, DK, kLdO);
+    load_tile<DK>(sX, static_cast<const Tin*>(a.k), tok0, valid);
     __syncthreads();
-
-    const int b = tid % DK, tg = tid / DK;  // this thread's feature and token group
-    float acc[NS];
-#pragma unroll
-    for (int m = 0; m < NS; ++m) acc[m] = 0.0f;
     const float* Gc = a.Gs + (bh * nc + n) * int64_t(DV) * DK;
-    for (int c = 0; c < DV; ++c) {
-        const float g = Gc[c * DK + b];  // G_c[c][b]: one row of G_c per step, coalesced
+    float zs[4];
 #pragma unroll
-        for (int m = 0; m < NS; ++m) acc[m] += g * sE[(tg * NS + m) * kLdO + c];
-    }
+    for (int r = 0; r < 4; ++r) zs[r] = decay_from_start(sLg, sZl, 16 * w + 4 * g + r);
+    // (E G_c)[t][b] = sum_a e_t[a] G_c[a][b];  (S K)[t][b] = sum_i S[t][i] k_i[b]
+    rows_times_matrix<DV, DK / 16, kLdT, DK, 1>(sE + 16 * w * kLdT, Gc, [&](int bt, const f32x4& eg) {
+        const f32x4 sk = mma16<kC, kLdC, 1, kLdT, 1>(sS + 16 * w * kLdC, sX + 16 * bt, kZero4);
 #pragma unroll
-    for (int m = 0; m < NS; ++m) acc[m] *= decay_from_start(sLg, sZl, tg * NS + m);
-    for (int i = 0; i < kC; ++i) {
-        const float ki = sX[i * kLdO + b];
-#pragma unroll
-        for (int m = 0; m < NS; ++m) acc[m] += sS[(tg * NS + m) * kLdC + i] * ki;
-    }
-#pragma unroll
-    for (int m = 0; m < NS; ++m) {
-        const int t = tg * NS + m;
-        if (t >= valid) continue;
-        if (a.u16)
-            a.u16[(tok0 + t) * DK + b] = uint16_t(pack_bf16x2(acc[m], 0.0f) & 0xffffu);  // round to nearest even
-        else
-            a.u[(tok0 + t) * DK + b] = acc[m];
-    }
+        for (int r = 0; r < 4; ++r) {
+            const int t = 16 * w + 4 * g + r, b = 16 * bt + ln;
+            if (t >= valid) continue;
+            const float u = zs[r] * eg[r] + sk[r];
+            if (a.u16)
+                a.u16[(tok0 + t) * DK + b] = uint16_t(pack_bf16x2(u, 0.0f) & 0xffffu);  // round to nearest even
+            else
+                a.u[(tok0 + t) * DK + b] = u;
+        }
+    });
 }
 
 // ---------------------------------------------------------------- adjoint scan
-// One workgroup owns 16 rows of S^H (d_k x d_k) or of A^G (d_v x d_k) of one
-// sequence and walks the chunks from last to first; the tile stays in registers.
-constexpr int kTileRows = 16;
-constexpr int kPerThread = kTileRows * 128 / kThreads;  // 8
+// One workgroup owns 64 rows of S^H (d_k x d_k) or of A^G (d_v x d_k) of one
+// sequence and walks the chunks from last to first; wave w keeps rows 16w .. +15 of
+// the slice as d_k / 16 result tiles in registers and adds each chunk's rank-64
+// update on the matrix cores.  The gate weight zeta_{j,c-1} is folded into the row
+// operands as they are staged.
+constexpr int kAdjRows = 64;
+constexpr int kLdX = 144;   // row stride of the [token][column] operands (16 banks apart)
+constexpr int kLdR = 80;    // row stride of the [token][row] operands
 
 template <int DK, int DV>
 __global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a)
 {
-    constexpr int NTH = DK / kTileRows;          // row tiles of S^H
-    constexpr int NTILE = NTH + DV / kTileRows;  // then row tiles of A^G
-    constexpr int NEL = kTileRows * DK;
+    constexpr int NCT = DK / 16;                  // column tiles
+    constexpr int NTH = DK / kAdjRows;            // row slices of S^H
+    constexpr int NTILE = NTH + DV / kAdjRows;    // then row slices of A^G
     const ForwardShape s = a.s;
     const int nc = s.n_chunks;
     const int blk = xcd_major_block(blockIdx.x, gridDim.x);
     const int tile = blk % NTILE;
     const int64_t bh = blk / NTILE;
     const bool isG = tile >= NTH;
-    const int r0 = (isG ? tile - NTH : tile) * kTileRows;
+    const int r0 = (isG ? tile - NTH : tile) * kAdjRows;
     const int nrow = isG ? DV : DK;
     const int tid = threadIdx.x;
+    const int w = tid / kWave, lane = tid % kWave, g = lane / 16, ln = lane % 16;
 
-    __shared__ float sX[kC][DK + 1];             // q*_j, all columns
-    __shared__ float sY[kC][DK + 1];             // -e*_j, all columns (S^H only)
-    __shared__ float sYr[kC][kTileRows + 1];     // rows r0.. of e_j (A^G) or -e*_j (S^H)
-    __shared__ float sXr[kC][kTileRows + 1];     // rows r0.. of q*_j (S^H only)
-    __shared__ float sW[kC];                     // zeta_{j, c-1}: decay from the chunk's entry to j
+    __shared__ float sX[kC * kLdX];   // q*_j [j][c]
+    __shared__ float sY[kC * kLdX];   // e*_j [j][c] (S^H only)
+    __shared__ float sYr[kC * kLdR];  // zeta_{j,c-1} e_j (A^G) or -zeta e*_j (S^H), rows r0.. [j][r]
+    __shared__ float sXr[kC * kLdR];  // -zeta_{j,c-1} q*_j, rows r0.. [j][r] (S^H only)
+    __shared__ float sW[kC];
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
 
-    float st[kPerThread];
+    f32x4 st[NCT];
 #pragma unroll
-    for (int m = 0; m < kPerThread; ++m) st[m] = 0.0f;
+    for (int ct = 0; ct < NCT; ++ct) st[ct] = kZero4;
     float* out = isG ? a.AG : a.SH;
     for (int n = nc - 1; n >= 0; --n) {
         const int64_t t0 = int64_t(n) * kC;
         const int valid = int(min<int64_t>(kC, s.seq_len - t0));
         const int64_t tok0 = bh * s.seq_len + t0;
-        float* dst = out + ((bh * nc + n) * nrow + r0) * int64_t(DK);
+        float* dst = out + ((bh * nc + n) * nrow + r0 + 16 * w) * int64_t(DK);
 #pragma unroll
-        for (int m = 0; m < kPerThread; ++m) {
-            const int e = tid + kThreads * m;
-            if (e < NEL) dst[e] = st[m];
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dst[(4 * g + r) * DK + 16 * ct + ln] = st[ct][r];
+        // row slices: 64 tokens x 64 rows, four 16-byte loads per thread and array
+        constexpr int VR = kC * kAdjRows / 4 / kThreads;
+        float4 yr[VR], xr[VR];
+        const float* ysrc = isG ? a.dout : a.estar;
+        const int yd = isG ? DV : DK;
+#pragma unroll
+        for (int m = 0; m < VR; ++m) {
+            const int e = tid + kThreads * m, j = e / (kAdjRows / 4), r = 4 * (e % (kAdjRows / 4));
+            const int64_t row = tok0 + min(j, valid - 1);
+            yr[m] = *reinterpret_cast<const float4*>(ysrc + row * yd + r0 + r);
+            if (!isG) xr[m] = *reinterpret_cast<const float4*>(a.qstar + row * DK + r0 + r);
         }
-        for (int e = tid; e < kC * DK; e += kThreads) {
-            const int j = e / DK, c = e % DK;
-            const bool ok = j < valid;
-            sX[j][c] = ok ? a.qstar[(tok0 + j) * DK + c] : 0.0f;
-            if (!isG) sY[j][c] = ok ? -a.estar[(tok0 + j) * DK + c] : 0.0f;
+        load_tile<DK, kLdX>(sX, a.qstar, tok0, valid);
+        if (!isG) load_tile<DK, kLdX>(sY, a.estar, tok0, valid);
+        if (tid < kWave) {
+            chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
+            sW[tid] = tid < valid ? decay_from_start(sLg, sZl, tid) : 0.0f;  // own lane's values
         }
-        for (int e = tid; e < kC * kTileRows; e += kThreads) {
-            const int j = e / kTileRows, r = e % kTileRows;
-            const bool ok = j < valid;
-            sYr[j][r] = ok ? (isG ? a.dout[(tok0 + j) * DV + r0 + r] : -a.estar[(tok0 + j) * DK + r0 + r]) : 0.0f;
-            if (!isG) sXr[j][r] = ok ? a.qstar[(tok0 + j) * DK + r0 + r] : 0.0f;
-        }
-        if (tid < kWave) chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
         __syncthreads();
-        if (tid < kC) sW[tid] = tid < valid ? decay_from_start(sLg, sZl, tid) : 0.0f;
+#pragma unroll
+        for (int m = 0; m < VR; ++m) {
+            const int e = tid + kThreads * m, j = e / (kAdjRows / 4), r = 4 * (e % (kAdjRows / 4));
+            const float wy = isG ? sW[j] : -sW[j];  // zero past the valid tokens
+            float* oy = sYr + j * kLdR + r;
+            oy[0] = wy * yr[m].x; oy[1] = wy * yr[m].y; oy[2] = wy * yr[m].z; oy[3] = wy * yr[m].w;
+            if (!isG) {
+                const float wx = -sW[j];
+                float* ox = sXr + j * kLdR + r;
+                ox[0] = wx * xr[m].x; ox[1] = wx * xr[m].y; ox[2] = wx * xr[m].z; ox[3] = wx * xr[m].w;
+            }
+        }
         __syncthreads();
         const float D = decay_from_start(sLg, sZl, kC - 1);
 #pragma unroll
-        for (int m = 0; m < kPerThread; ++m) {
-            const int e = tid + kThreads * m;
-            if (e < NEL) {
-                const int row = e / DK, col = e % DK;
-                float acc = 0.0f;
-                if (isG) {
-                    for (int j = 0; j < kC; ++j) acc += sW[j] * sYr[j][row] * sX[j][col];
-                } else {
-                    for (int j = 0; j < kC; ++j) acc += sW[j] * (sYr[j][row] * sX[j][col] + sXr[j][row] * sY[j][col]);
-                }
-                st[m] = D * st[m] + acc;
-            }
+        for (int ct = 0; ct < NCT; ++ct) {
+            f32x4 acc = st[ct] * D;
+            // X[r][c] += sum_j Yr[j][r] X[j][c]  (A(m, k) = sYr[k][m], B(k, n) = sX[k][n])
+            acc = mma16<kC, 1, kLdR, kLdX, 1>(sYr + 16 * w, sX + 16 * ct, acc);
+            if (!isG) acc = mma16<kC, 1, kLdR, kLdX, 1>(sXr + 16 * w, sY + 16 * ct, acc);
+            st[ct] = acc;
         }
         __syncthreads();
     }
 }
 
 // ---------------------------------------------------------------- per-chunk gradients
-// Thread layout for per-feature outputs over D features: feature f = tid % D, token
-// group tg = tid / D (uniform in a wave), tokens tg * (C / NTG) + m.
+// One workgroup per chunk; in the token-by-feature phases wave w owns tokens
+// 16w .. 16w+15 (the rows of its result tiles), so every per-token sum over features
+// is a sum over the 16 lanes of a lane row.
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
 {
@@ -231,6 +335,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     const int valid = int(min<int64_t>(kC, s.seq_len - t0));
     const int64_t tok0 = bh * s.seq_len + t0;
     const int tid = threadIdx.x;
+    const int w = tid / kWave, lane = tid % kWave, g = lane / 16, ln = lane % 16;
     const Tin* kp = static_cast<const Tin*>(a.k);
     const Tin* vp = static_cast<const Tin*>(a.v);
     const int64_t mat = bh * nc + n;
@@ -239,17 +344,17 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     const float* Gc = a.Gs + mat * int64_t(DV) * DK;
     const float* Hc = a.Hs + mat * int64_t(DK) * DK;
 
-    __shared__ __attribute__((aligned(16))) float sT0[kC * kLdT];
-    __shared__ __attribute__((aligned(16))) float sT1[kC * kLdT];
-    __shared__ __attribute__((aligned(16))) float sM0[kC * kLdC];  // KQ, then M1 = Z ⊙ KQ, then W
-    __shared__ __attribute__((aligned(16))) float sM1[kC * kLdC];  // VE, then VE - KE, then M2 = Z ⊙ (VE - KE)
-    __shared__ __attribute__((aligned(16))) float sM2[kC * kLdC];  // KE, then Qm = beta_p (VE - KE) KQ
-    __shared__ __attribute__((aligned(16))) float sZ[kC * kLdC];   // Z[s][t] = zeta_{t,s} (s <= t)
+    __shared__ float sT0[kC * kLdT];
+    __shared__ float sT1[kC * kLdT];
+    __shared__ float sM0[kC * kLdC];  // KQ, then M1 = Z ⊙ KQ, then W
+    __shared__ float sM1[kC * kLdC];  // VE, then VE - KE, then M2 = Z ⊙ (VE - KE)
+    __shared__ float sM2[kC * kLdC];  // KE, then Qm = beta_p (VE - KE) KQ
+    __shared__ float sZ[kC * kLdC];   // Z[s][t] = zeta_{t,s} (s <= t)
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
     __shared__ float sBeta[kC], sZe[kC], sPhi[kC];
-    __shared__ float sTok[5][kC];   // per-token: dbeta (intra), v^T A^G k, k^T A^H k, g, h
-    __shared__ float sPart[kThreads / kWave][kC];
+    __shared__ float sTok[5][kC];     // per token: dbeta (intra), v^T A^G k, k^T A^H k, g, h
+    __shared__ float sPart[kThreads / kWave];
     __shared__ float sF;
 
     // ---- gates: Z, zeta_{E,s}, phi_s = zeta_{s-1,c-1}
@@ -265,44 +370,29 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         sPhi[tid] = tid == 0 ? 1.0f : decay_from_start(sLg, sZl, tid - 1);
     }
 
-    // ---- grams of the chunk's tokens, 4x4 register blocks: entry (p, t) with
-    // p = pb + 16 i, t = tb + 16 j
-    const int pb = tid / 16, tb = tid % 16;
-    auto gram = [&](float* dst, int d) {
-        float g[4][4];
+    // ---- gram matrices [p][t] of the chunk's tokens; wave w forms rows 16w..
+    auto gram = [&](float* dst, auto d_tag) {
+        constexpr int D = decltype(d_tag)::value;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int tt = 0; tt < kC / 16; ++tt) {
+            const f32x4 gm = mma16<D, kLdT, 1, 1, kLdT>(sT0 + 16 * w * kLdT, sT1 + 16 * tt * kLdT, kZero4);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) g[i][j] = 0.0f;
-        for (int f = 0; f < d; ++f) {
-            float x[4], y[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) x[i] = sT0[(pb + 16 * i) * kLdT + f];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) y[j] = sT1[(tb + 16 * j) * kLdT + f];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) g[i][j] += x[i] * y[j];
+            for (int r = 0; r < 4; ++r) dst[(16 * w + 4 * g + r) * kLdC + 16 * tt + ln] = gm[r];
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) dst[(pb + 16 * i) * kLdC + tb + 16 * j] = g[i][j];
     };
-    load_tile(sT0, kp, tok0, valid, DK);
-    load_tile(sT1, a.qstar, tok0, valid, DK);
+    load_tile<DK>(sT0, kp, tok0, valid);
+    load_tile<DK>(sT1, a.qstar, tok0, valid);
     __syncthreads();
-    gram(sM0, DK);  // KQ[p][t] = k_p . q*_t
+    gram(sM0, std::integral_constant<int, DK>{});  // KQ[p][t] = k_p . q*_t
     __syncthreads();
-    load_tile(sT1, a.estar, tok0, valid, DK);
+    load_tile<DK>(sT1, a.estar, tok0, valid);
     __syncthreads();
-    gram(sM2, DK);  // KE[p][t] = k_p . e*_t
+    gram(sM2, std::integral_constant<int, DK>{});  // KE[p][t] = k_p . e*_t
     __syncthreads();
-    load_tile(sT0, vp, tok0, valid, DV);
-    load_tile(sT1, a.dout, tok0, valid, DV);
+    load_tile<DV>(sT0, vp, tok0, valid);
+    load_tile<DV>(sT1, a.dout, tok0, valid);
     __syncthreads();
-    gram(sM1, DV);  // VE[p][t] = v_p . e_t
+    gram(sM1, std::integral_constant<int, DV>{});  // VE[p][t] = v_p . e_t
     __syncthreads();
 
     // ---- C x C combinations: DVK = VE - KE; Qm = beta_p DVK KQ; the intra part of
@@ -325,166 +415,128 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         sM0[o] *= sZ[o];
         sM1[o] *= sZ[o];
     }
+    // this wave's tokens
+    int srow[4];
+    float beta_r[4], ze_r[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        srow[r] = 16 * w + 4 * g + r;
+        beta_r[r] = sBeta[srow[r]];
+        ze_r[r] = sZe[srow[r]];
+    }
+
+    // ---- dv_s = beta_s (sum_t M1[s][t] e_t + zeta_E[s] A^G k_s)   (sT1 holds e_t)
     __syncthreads();
+    load_tile<DK>(sT0, kp, tok0, valid);
+    __syncthreads();
+    // (K A^G^T)[s][a] = sum_b k_s[b] A^G[a][b]
+    rows_times_matrix<DK, DV / 16, kLdT, 1, DK>(sT0 + 16 * w * kLdT, AG, [&](int at, const f32x4& ex) {
+        const f32x4 in = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * w * kLdC, sT1 + 16 * at, kZero4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            if (srow[r] < valid) a.dv[(tok0 + srow[r]) * DV + 16 * at + ln] = beta_r[r] * (in[r] + ze_r[r] * ex[r]);
+    });
 
-    // ---- dv (features a over DV): beta_s (sum_t M1[s][t] e_t[a] + zeta_E[s] (A^G k_s)[a])
+    // ---- dk_s = beta_s (sum_t M2[s][t] q*_t - sum_t M1[s][t] e*_t + zeta_E[s] ((A^G)^T v_s + S^H k_s)),
+    //      with v^T A^G k and k^T A^H k = (1/2) k^T S^H k per token
     {
-        constexpr int NTG = kThreads / DV, NS = kC / NTG;
-        const int f = tid % DV, tg = tid / DV;
-        float acc[NS], inter[NS];
-        // sT1 still holds e_t; sT0 gets k_s
+        f32x4 in[DK / 16];
         __syncthreads();
-        load_tile(sT0, kp, tok0, valid, DK);
+        load_tile<DK>(sT0, a.qstar, tok0, valid);
+        load_tile<DK>(sT1, a.estar, tok0, valid);
         __syncthreads();
 #pragma unroll
-        for (int m = 0; m < NS; ++m) acc[m] = inter[m] = 0.0f;
-        for (int t = 0; t < kC; ++t) {
-            const float et = sT1[t * kLdT + f];
-#pragma unroll
-            for (int m = 0; m < NS; ++m) acc[m] += sM0[(tg * NS + m) * kLdC + t] * et;
+        for (int bt = 0; bt < DK / 16; ++bt) {
+            const f32x4 pq = mma16<kC, kLdC, 1, kLdT, 1>(sM1 + 16 * w * kLdC, sT0 + 16 * bt, kZero4);
+            const f32x4 pe = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * w * kLdC, sT1 + 16 * bt, kZero4);
+            in[bt] = pq - pe;
         }
-        const float* row = AG + int64_t(f) * DK;  // A^G[f][.]
-        for (int c = 0; c < DK; c += 4) {
-            const float4 g4 = *reinterpret_cast<const float4*>(row + c);
+        __syncthreads();
+        load_tile<DK>(sT0, kp, tok0, valid);
+        load_tile<DV>(sT1, vp, tok0, valid);
+        __syncthreads();
+        float pa[4] = {0.0f, 0.0f, 0.0f, 0.0f}, pk[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        // ((A^G)^T v_s)[b] first (kept in `in` scaled and added), then (S^H k_s)[b]
+        rows_times_matrix<DV, DK / 16, kLdT, DK, 1>(sT1 + 16 * w * kLdT, AG, [&](int bt, const f32x4& ag) {
 #pragma unroll
-            for (int m = 0; m < NS; ++m) {
-                const float4 k4 = *reinterpret_cast<const float4*>(sT0 + (tg * NS + m) * kLdT + c);
-                inter[m] += g4.x * k4.x + g4.y * k4.y + g4.z * k4.z + g4.w * k4.w;
+            for (int r = 0; r < 4; ++r) {
+                const float kb = sT0[srow[r] * kLdT + 16 * bt + ln];
+                in[bt][r] += ze_r[r] * ag[r];
+                pa[r] += kb * ag[r];
             }
-        }
+        });
+        rows_times_matrix<DK, DK / 16, kLdT, DK, 1>(sT0 + 16 * w * kLdT, SH, [&](int bt, const f32x4& sh) {
 #pragma unroll
-        for (int m = 0; m < NS; ++m) {
-            const int t = tg * NS + m;
-            const float dgk = acc[m] + sZe[t] * inter[m];  // (DG_s k_s)[f]
-            if (t < valid) a.dv[(tok0 + t) * DV + f] = sBeta[t] * dgk;
+            for (int r = 0; r < 4; ++r) {
+                const int b = 16 * bt + ln;
+                const float kb = sT0[srow[r] * kLdT + b];
+                if (srow[r] < valid) a.dk[(tok0 + srow[r]) * DK + b] = beta_r[r] * (in[bt][r] + ze_r[r] * sh[r]);
+                pk[r] += 0.5f * kb * sh[r];
+            }
+        });
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float sa = row16_sum(pa[r]), sk = row16_sum(pk[r]);
+            if (ln == 0) {
+                sTok[1][srow[r]] = sa;
+                sTok[2][srow[r]] = sk;
+            }
         }
     }
 
-    // ---- dk (features b over DK): beta_s (sum_t M2[s][t] q*_t[b] - sum_t M1[s][t] e*_t[b]
-    //      + zeta_E[s] ((A^G)^T v_s + S^H k_s)[b]);  also aG_s = v_s^T A^G k_s and
-    //      kAHk_s = k_s^T A^H k_s = (1/2) k_s^T S^H k_s
+    // ---- g_t = e_t^T G_c q*_t, h_t = e*_t^T H_c q*_t, F = <A^G, G_c> + (1/2) <S^H, H_c>,
+    //      and dLambda of the chunk
     {
-        constexpr int NTG = kThreads / DK, NS = kC / NTG;
-        const int f = tid % DK, tg = tid / DK;
-        float acc[NS], ag[NS], sh[NS];
         __syncthreads();
-        load_tile(sT0, a.qstar, tok0, valid, DK);
-        load_tile(sT1, a.estar, tok0, valid, DK);
+        load_tile<DK>(sT0, a.qstar, tok0, valid);
+        load_tile<DV>(sT1, a.dout, tok0, valid);
         __syncthreads();
+        float pg[4] = {0.0f, 0.0f, 0.0f, 0.0f}, ph[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        rows_times_matrix<DV, DK / 16, kLdT, DK, 1>(sT1 + 16 * w * kLdT, Gc, [&](int bt, const f32x4& eg) {
 #pragma unroll
-        for (int m = 0; m < NS; ++m) acc[m] = ag[m] = sh[m] = 0.0f;
-        for (int t = 0; t < kC; ++t) {
-            const float qt = sT0[t * kLdT + f], et = sT1[t * kLdT + f];
+            for (int r = 0; r < 4; ++r) pg[r] += eg[r] * sT0[srow[r] * kLdT + 16 * bt + ln];
+        });
+        __syncthreads();
+        load_tile<DK>(sT1, a.estar, tok0, valid);
+        __syncthreads();
+        rows_times_matrix<DK, DK / 16, kLdT, DK, 1>(sT1 + 16 * w * kLdT, Hc, [&](int bt, const f32x4& eh) {
 #pragma unroll
-            for (int m = 0; m < NS; ++m) {
-                const int o = (tg * NS + m) * kLdC + t;
-                acc[m] += sM1[o] * qt - sM0[o] * et;
+            for (int r = 0; r < 4; ++r) ph[r] += eh[r] * sT0[srow[r] * kLdT + 16 * bt + ln];
+        });
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float sg = row16_sum(pg[r]), sh = row16_sum(ph[r]);
+            if (ln == 0) {
+                sTok[3][srow[r]] = sg;
+                sTok[4][srow[r]] = sh;
             }
         }
-        __syncthreads();
-        load_tile(sT0, kp, tok0, valid, DK);
-        load_tile(sT1, vp, tok0, valid, DV);
-        __syncthreads();
-        for (int c = 0; c < DV; ++c) {
-            const float g = AG[c * DK + f];  // A^G[c][f], coalesced over f
-#pragma unroll
-            for (int m = 0; m < NS; ++m) ag[m] += g * sT1[(tg * NS + m) * kLdT + c];
-        }
-        for (int c = 0; c < DK; ++c) {
-            const float h = SH[c * DK + f];  // S^H[c][f] = S^H[f][c]
-#pragma unroll
-            for (int m = 0; m < NS; ++m) sh[m] += h * sT0[(tg * NS + m) * kLdT + c];
-        }
-        float pa[NS], pk[NS];
-#pragma unroll
-        for (int m = 0; m < NS; ++m) {
-            const int t = tg * NS + m;
-            const float kf = sT0[t * kLdT + f];
-            if (t < valid) a.dk[(tok0 + t) * DK + f] = sBeta[t] * (acc[m] + sZe[t] * (ag[m] + sh[m]));
-            pa[m] = kf * ag[m];          // k_s[f] ((A^G)^T v_s)[f]  -> v_s^T A^G k_s
-            pk[m] = 0.5f * kf * sh[m];   // (1/2) k_s[f] (S^H k_s)[f] -> k_s^T A^H k_s
-        }
-        token_sums<DK>(pa, sTok[1], sPart);
-        token_sums<DK>(pk, sTok[2], sPart);
-    }
-
-    // ---- g_t = e_t^T G_c q*_t and h_t = e*_t^T H_c q*_t (features b over DK), and
-    //      F = <A^G, G_c> + (1/2) <S^H, H_c>
-    {
-        constexpr int NTG = kThreads / DK, NS = kC / NTG;
-        const int f = tid % DK, tg = tid / DK;
-        float w[NS];
-        __syncthreads();
-        load_tile(sT0, a.qstar, tok0, valid, DK);
-        load_tile(sT1, a.dout, tok0, valid, DV);
-        __syncthreads();
-#pragma unroll
-        for (int m = 0; m < NS; ++m) w[m] = 0.0f;
-        for (int c = 0; c < DV; ++c) {
-            const float g = Gc[c * DK + f];
-#pragma unroll
-            for (int m = 0; m < NS; ++m) w[m] += g * sT1[(tg * NS + m) * kLdT + c];
-        }
-        float pg[NS];
-#pragma unroll
-        for (int m = 0; m < NS; ++m) pg[m] = w[m] * sT0[(tg * NS + m) * kLdT + f];
-        token_sums<DK>(pg, sTok[3], sPart);
-        load_tile(sT1, a.estar, tok0, valid, DK);
-        __syncthreads();
-#pragma unroll
-        for (int m = 0; m < NS; ++m) w[m] = 0.0f;
-        for (int c = 0; c < DK; ++c) {
-            const float h = Hc[c * DK + f];
-#pragma unroll
-            for (int m = 0; m < NS; ++m) w[m] += h * sT1[(tg * NS + m) * kLdT + c];
-        }
-#pragma unroll
-        for (int m = 0; m < NS; ++m) pg[m] = w[m] * sT0[(tg * NS + m) * kLdT + f];
-        token_sums<DK>(pg, sTok[4], sPart);
-        // F: every thread a strided slice of the two Frobenius products
         float fr = 0.0f;
         for (int e = tid; e < DV * DK; e += kThreads) fr += AG[e] * Gc[e];
         for (int e = tid; e < DK * DK; e += kThreads) fr += 0.5f * SH[e] * Hc[e];
         fr = wave_sum(fr);
-        if (tid % kWave == 0) sPart[tid / kWave][0] = fr;
-        __syncthreads();
-        if (tid == 0) {
-            float t = 0.0f;
-            for (int u = 0; u < kThreads / kWave; ++u) t += sPart[u][0];
-            sF = t;
-        }
-        // dLambda of this chunk: -sum_t q*_t[b] e*_t[b]
+        if (lane == 0) sPart[w] = fr;
         if (tid < DK) {
             float acc = 0.0f;
             for (int t = 0; t < kC; ++t) acc += sT0[t * kLdT + tid] * sT1[t * kLdT + tid];
             a.dlam_part[mat * DK + tid] = -acc;
         }
         __syncthreads();
+        if (tid == 0) {
+            float t = 0.0f;
+            for (int u = 0; u < kThreads / kWave; ++u) t += sPart[u];
+            sF = t;
+        }
     }
 
-    // ---- W[p][s] = sum_{t>=s} zeta_{t,s} Qm[p][t] (4x4 blocks, into sM0)
+    // ---- W[p][s] = sum_{t>=s} zeta_{t,s} Qm[p][t]: rows 16w.. of Qm Z^T, into sM0
     {
-        float g[4][4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int st = 0; st < kC / 16; ++st) {
+            const f32x4 wq = mma16<kC, kLdC, 1, 1, kLdC>(sM2 + 16 * w * kLdC, sZ + 16 * st * kLdC, kZero4);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) g[i][j] = 0.0f;
-        for (int t = 0; t < kC; ++t) {
-            float x[4], y[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) x[i] = sM2[(pb + 16 * i) * kLdC + t];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) y[j] = sZ[(tb + 16 * j) * kLdC + t];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) g[i][j] += x[i] * y[j];
+            for (int r = 0; r < 4; ++r) sM0[srow[r] * kLdC + 16 * st + ln] = wq[r];
         }
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) sM0[(pb + 16 * i) * kLdC + tb + 16 * j] = g[i][j];
         __syncthreads();
     }
 
@@ -536,7 +588,7 @@ hipError_t launch_bwd_dims(const BwdArgs& a, hipStream_t stream, int stage)
             hipLaunchKernelGGL((bwd_rhs_kernel<Tin, DK, DV>), dim3(chunks), dim3(kThreads), 0, stream, a);
             break;
         case 1:
-            hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV>), dim3(unsigned(bh * (DK + DV) / kTileRows)), dim3(kThreads), 0,
+            hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV>), dim3(unsigned(bh * (DK + DV) / kAdjRows)), dim3(kThreads), 0,
                                stream, a);
             break;
         case 2:

@@ -399,7 +399,8 @@ int mesa_backward(const void* k, const void* v, const float* gamma, const float*
         const size_t need = mesa_backward_workspace_bytes(batch, heads, seq_len, d_k, d_v);
         if (!workspace) return MESA_ERR_NULL;
         if (workspace_bytes < need) return MESA_ERR_WORKSPACE;
-        for (const void* ptr : {static_cast<const void*>(qstar), static_cast<const void*>(dout), static_cast<const void*>(workspace)})
+        for (const void* ptr : {k, v, static_cast<const void*>(qstar), static_cast<const void*>(dout),
+                                static_cast<const void*>(dq), static_cast<const void*>(workspace)})
             if (uintptr_t(ptr) % 16 != 0) return MESA_ERR_ARG;
         const int64_t in_sz = dtype == MESA_DTYPE_BF16 ? 2 : 4;
         const Range ins[] = {range_of(k, tokens * d_k * in_sz), range_of(v, tokens * d_v * in_sz),

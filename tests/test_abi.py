@@ -236,6 +236,8 @@ def _bwd(lib, **kw):
     (dict(T=-1), L.MESA_ERR_SHAPE),
     (dict(ws_bytes=64), L.MESA_ERR_WORKSPACE),
     (dict(qs=P["qs"] + 4), L.MESA_ERR_ARG),          # q* not 16-byte aligned
+    (dict(k=P["k"] + 2), L.MESA_ERR_ARG),            # k not 16-byte aligned
+    (dict(dq=P["fh"] + 8), L.MESA_ERR_ARG),          # dq not 16-byte aligned
     (dict(dq=P["k"] + 64), L.MESA_ERR_ARG),          # dq overlaps k
     (dict(db=P["fh"] + 8), L.MESA_ERR_ARG),          # two gradients overlap
     (dict(dl=P["ws"] + 4096), L.MESA_ERR_ARG),       # dlambda inside the workspace
