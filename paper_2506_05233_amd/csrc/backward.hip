@@ -355,6 +355,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     __shared__ float sBeta[kC], sZe[kC], sPhi[kC];
     __shared__ float sTok[5][kC];     // per token: dbeta (intra), v^T A^G k, k^T A^H k, g, h
     __shared__ float sPart[kThreads / kWave];
+    __shared__ float sRed[kThreads / kWave][kC];  // per-wave partial sums per token
     __shared__ float sF;
 
     // ---- gates: Z, zeta_{E,s}, phi_s = zeta_{s-1,c-1}
@@ -415,105 +416,154 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         sM0[o] *= sZ[o];
         sM1[o] *= sZ[o];
     }
-    // this wave's tokens
-    int srow[4];
-    float beta_r[4], ze_r[4];
+    // In the token-by-feature phases below wave w owns the 16-column tiles
+    // w * TPW .. of the feature dimension for all 64 tokens (4 token tiles), so it
+    // loads each d x d matrix's column tiles once; per-token sums over features are
+    // 16-lane row sums, then sums over the waves through sRed.
+    auto tok = [&](int st, int r) { return 16 * st + 4 * g + r; };
+    // sum the partials p[st][r] (token tok(st, r)) over lanes and waves into out[token]
+    auto reduce_tokens = [&](const float (&p)[4][4], float* out) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        srow[r] = 16 * w + 4 * g + r;
-        beta_r[r] = sBeta[srow[r]];
-        ze_r[r] = sZe[srow[r]];
-    }
+        for (int st = 0; st < 4; ++st)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float v = row16_sum(p[st][r]);
+                if (ln == 0) sRed[w][tok(st, r)] = v;
+            }
+        __syncthreads();
+        if (tid < kC) out[tid] = (sRed[0][tid] + sRed[1][tid]) + (sRed[2][tid] + sRed[3][tid]);
+        __syncthreads();
+    };
 
     // ---- dv_s = beta_s (sum_t M1[s][t] e_t + zeta_E[s] A^G k_s)   (sT1 holds e_t)
-    __syncthreads();
-    load_tile<DK>(sT0, kp, tok0, valid);
-    __syncthreads();
-    // (K A^G^T)[s][a] = sum_b k_s[b] A^G[a][b]
-    rows_times_matrix<DK, DV / 16, kLdT, 1, DK>(sT0 + 16 * w * kLdT, AG, [&](int at, const f32x4& ex) {
-        const f32x4 in = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * w * kLdC, sT1 + 16 * at, kZero4);
+    {
+        constexpr int TPW = DV / 16 / 4;
+        __syncthreads();
+        load_tile<DK>(sT0, kp, tok0, valid);
+        __syncthreads();
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-            if (srow[r] < valid) a.dv[(tok0 + srow[r]) * DV + 16 * at + ln] = beta_r[r] * (in[r] + ze_r[r] * ex[r]);
-    });
+        for (int j = 0; j < TPW; ++j) {
+            const int at = w * TPW + j;
+            float bv[DK / 4];
+            load_b<DK, 1, DK>(AG + 16 * at * DK, bv);  // B(k, n) = A^G[16 at + n][k]
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const f32x4 in = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * at, kZero4);
+                const f32x4 ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv, kZero4);  // (K A^G^T)[s][a]
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = tok(st, r);
+                    if (t < valid) a.dv[(tok0 + t) * DV + 16 * at + ln] = sBeta[t] * (in[r] + sZe[t] * ex[r]);
+                }
+            }
+        }
+    }
 
     // ---- dk_s = beta_s (sum_t M2[s][t] q*_t - sum_t M1[s][t] e*_t + zeta_E[s] ((A^G)^T v_s + S^H k_s)),
     //      with v^T A^G k and k^T A^H k = (1/2) k^T S^H k per token
     {
-        f32x4 in[DK / 16];
+        constexpr int TPW = DK / 16 / 4;
+        f32x4 in[TPW][4];
         __syncthreads();
         load_tile<DK>(sT0, a.qstar, tok0, valid);
         load_tile<DK>(sT1, a.estar, tok0, valid);
         __syncthreads();
 #pragma unroll
-        for (int bt = 0; bt < DK / 16; ++bt) {
-            const f32x4 pq = mma16<kC, kLdC, 1, kLdT, 1>(sM1 + 16 * w * kLdC, sT0 + 16 * bt, kZero4);
-            const f32x4 pe = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * w * kLdC, sT1 + 16 * bt, kZero4);
-            in[bt] = pq - pe;
-        }
+        for (int j = 0; j < TPW; ++j)
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const int bt = w * TPW + j;
+                const f32x4 pq = mma16<kC, kLdC, 1, kLdT, 1>(sM1 + 16 * st * kLdC, sT0 + 16 * bt, kZero4);
+                const f32x4 pe = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * bt, kZero4);
+                in[j][st] = pq - pe;
+            }
         __syncthreads();
         load_tile<DK>(sT0, kp, tok0, valid);
         load_tile<DV>(sT1, vp, tok0, valid);
         __syncthreads();
-        float pa[4] = {0.0f, 0.0f, 0.0f, 0.0f}, pk[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        // ((A^G)^T v_s)[b] first (kept in `in` scaled and added), then (S^H k_s)[b]
-        rows_times_matrix<DV, DK / 16, kLdT, DK, 1>(sT1 + 16 * w * kLdT, AG, [&](int bt, const f32x4& ag) {
+        float pa[4][4] = {}, pk[4][4] = {};
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float kb = sT0[srow[r] * kLdT + 16 * bt + ln];
-                in[bt][r] += ze_r[r] * ag[r];
-                pa[r] += kb * ag[r];
-            }
-        });
-        rows_times_matrix<DK, DK / 16, kLdT, DK, 1>(sT0 + 16 * w * kLdT, SH, [&](int bt, const f32x4& sh) {
+        for (int j = 0; j < TPW; ++j) {
+            const int bt = w * TPW + j;
+            float bag[DV / 4], bsh[DK / 4];
+            load_b<DV, DK, 1>(AG + 16 * bt, bag);  // B(k, n) = A^G[k][16 bt + n]
+            load_b<DK, DK, 1>(SH + 16 * bt, bsh);  // B(k, n) = S^H[k][16 bt + n]
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int b = 16 * bt + ln;
-                const float kb = sT0[srow[r] * kLdT + b];
-                if (srow[r] < valid) a.dk[(tok0 + srow[r]) * DK + b] = beta_r[r] * (in[bt][r] + ze_r[r] * sh[r]);
-                pk[r] += 0.5f * kb * sh[r];
-            }
-        });
+            for (int st = 0; st < 4; ++st) {
+                const f32x4 ag = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bag, kZero4);
+                const f32x4 sh = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bsh, kZero4);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float sa = row16_sum(pa[r]), sk = row16_sum(pk[r]);
-            if (ln == 0) {
-                sTok[1][srow[r]] = sa;
-                sTok[2][srow[r]] = sk;
+                for (int r = 0; r < 4; ++r) {
+                    const int t = tok(st, r), b = 16 * bt + ln;
+                    const float kb = sT0[t * kLdT + b];
+                    if (t < valid) a.dk[(tok0 + t) * DK + b] = sBeta[t] * (in[j][st][r] + sZe[t] * (ag[r] + sh[r]));
+                    pa[st][r] += kb * ag[r];
+                    pk[st][r] += 0.5f * kb * sh[r];
+                }
             }
         }
+        reduce_tokens(pa, sTok[1]);
+        reduce_tokens(pk, sTok[2]);
     }
 
     // ---- g_t = e_t^T G_c q*_t, h_t = e*_t^T H_c q*_t, F = <A^G, G_c> + (1/2) <S^H, H_c>,
     //      and dLambda of the chunk
     {
+        constexpr int TPW = DK / 16 / 4;
         __syncthreads();
         load_tile<DK>(sT0, a.qstar, tok0, valid);
         load_tile<DV>(sT1, a.dout, tok0, valid);
         __syncthreads();
-        float pg[4] = {0.0f, 0.0f, 0.0f, 0.0f}, ph[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        rows_times_matrix<DV, DK / 16, kLdT, DK, 1>(sT1 + 16 * w * kLdT, Gc, [&](int bt, const f32x4& eg) {
+        float pg[4][4] = {}, ph[4][4] = {};
 #pragma unroll
-            for (int r = 0; r < 4; ++r) pg[r] += eg[r] * sT0[srow[r] * kLdT + 16 * bt + ln];
-        });
-        __syncthreads();
-        load_tile<DK>(sT1, a.estar, tok0, valid);
-        __syncthreads();
-        rows_times_matrix<DK, DK / 16, kLdT, DK, 1>(sT1 + 16 * w * kLdT, Hc, [&](int bt, const f32x4& eh) {
+        for (int j = 0; j < TPW; ++j) {
+            const int bt = w * TPW + j;
+            float bg[DV / 4];
+            load_b<DV, DK, 1>(Gc + 16 * bt, bg);  // B(k, n) = G_c[k][16 bt + n]
 #pragma unroll
-            for (int r = 0; r < 4; ++r) ph[r] += eh[r] * sT0[srow[r] * kLdT + 16 * bt + ln];
-        });
+            for (int st = 0; st < 4; ++st) {
+                const f32x4 eg = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bg, kZero4);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float sg = row16_sum(pg[r]), sh = row16_sum(ph[r]);
-            if (ln == 0) {
-                sTok[3][srow[r]] = sg;
-                sTok[4][srow[r]] = sh;
+                for (int r = 0; r < 4; ++r) pg[st][r] += eg[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
             }
         }
+        reduce_tokens(pg, sTok[3]);
+        load_tile<DK>(sT1, a.estar, tok0, valid);
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+            const int bt = w * TPW + j;
+            float bh_[DK / 4];
+            load_b<DK, DK, 1>(Hc + 16 * bt, bh_);  // B(k, n) = H_c[k][16 bt + n]
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const f32x4 eh = mma16_b<DK, kLdT, 1>(sT1 + 16 * st * kLdT, bh_, kZero4);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) ph[st][r] += eh[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
+            }
+        }
+        reduce_tokens(ph, sTok[4]);
+        // F: every thread a strided slice of the two Frobenius products, 16-byte loads,
+        // all issued before the products
         float fr = 0.0f;
-        for (int e = tid; e < DV * DK; e += kThreads) fr += AG[e] * Gc[e];
-        for (int e = tid; e < DK * DK; e += kThreads) fr += 0.5f * SH[e] * Hc[e];
+        {
+            constexpr int NG = DV * DK / 4 / kThreads, NH = DK * DK / 4 / kThreads;
+            float4 x[NG], y[NG], u[NH], v[NH];
+#pragma unroll
+            for (int m = 0; m < NG; ++m) {
+                x[m] = *reinterpret_cast<const float4*>(AG + 4 * (tid + kThreads * m));
+                y[m] = *reinterpret_cast<const float4*>(Gc + 4 * (tid + kThreads * m));
+            }
+#pragma unroll
+            for (int m = 0; m < NH; ++m) {
+                u[m] = *reinterpret_cast<const float4*>(SH + 4 * (tid + kThreads * m));
+                v[m] = *reinterpret_cast<const float4*>(Hc + 4 * (tid + kThreads * m));
+            }
+#pragma unroll
+            for (int m = 0; m < NG; ++m) fr += x[m].x * y[m].x + x[m].y * y[m].y + x[m].z * y[m].z + x[m].w * y[m].w;
+#pragma unroll
+            for (int m = 0; m < NH; ++m) fr += 0.5f * (u[m].x * v[m].x + u[m].y * v[m].y + u[m].z * v[m].z + u[m].w * v[m].w);
+        }
         fr = wave_sum(fr);
         if (lane == 0) sPart[w] = fr;
         if (tid < DK) {
@@ -535,7 +585,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         for (int st = 0; st < kC / 16; ++st) {
             const f32x4 wq = mma16<kC, kLdC, 1, 1, kLdC>(sM2 + 16 * w * kLdC, sZ + 16 * st * kLdC, kZero4);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sM0[srow[r] * kLdC + 16 * st + ln] = wq[r];
+            for (int r = 0; r < 4; ++r) sM0[tok(w, r) * kLdC + 16 * st + ln] = wq[r];
         }
         __syncthreads();
     }
