@@ -112,3 +112,40 @@ def test_backward_empty_sequence_zero_dlambda():
                    torch.empty((2, 3, 0, 64), dtype=torch.float32, device="cuda"), 5)
     torch.cuda.synchronize()
     assert g["dlam"].shape == (3, 64) and float(g["dlam"].abs().max()) == 0.0
+
+
+def test_backward_full_size_sampled():
+    """The 1B-shaped workload (B8 H16 T2048 d128, bf16) in the launch configuration
+    the benchmark times (forward on the bf16 path for q*, backward with the
+    matrix-core solve), checked on sampled sequences: all eight batches of head 7
+    (so that head's dLambda, a sum over the batch, is complete) plus (0, 0) and
+    (7, 15); the oracle recomputes q* and e* in fp64 for those sequences."""
+    import concurrent.futures as cf
+    w = W.LAYER_1B_BF16
+    x = W.workload_inputs(w)
+    dout = np.random.default_rng(11).normal(size=x["v"].shape).astype(np.float32)
+    d = to_device(x, "bf16")
+    fwd = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], w.n_cg, w.chunk, want_qstar=True)
+    g = L.backward(d["k"], d["v"], d["gamma"], d["beta"], d["lam"], fwd["qstar"], torch.from_numpy(dout).cuda(), w.n_cg)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in g.items()}
+    for k in GRADS:
+        assert np.isfinite(got[k]).all(), k
+    pairs = [(b, 7) for b in range(w.batch)] + [(0, 0), (7, 15)]
+
+    def one(bh):
+        b, h = bh
+        sl = {n: x[n][b:b + 1, h:h + 1] for n in ("q", "k", "v", "gamma", "beta")}
+        return oracle.backward(sl["q"], sl["k"], sl["v"], sl["gamma"], sl["beta"], x["lam"][h:h + 1],
+                               dout[b:b + 1, h:h + 1], w.n_cg, threads=1)
+    with cf.ThreadPoolExecutor(max_workers=min(16, len(pairs))) as ex:
+        refs = list(ex.map(one, pairs))
+    errs = {}
+    for k in ("dq", "dk", "dv", "dgamma", "dbeta"):
+        gg = np.stack([got[k][b, h] for b, h in pairs])
+        rr = np.stack([r[k][0, 0] for r in refs])
+        errs[k] = rel_l2(gg, rr)
+    errs["dlam"] = rel_l2(got["dlam"][7], sum(r["dlam"][0] for r in refs[:w.batch]))
+    _say("full-size backward, sampled: %s" % "  ".join("%s %.2e" % kv for kv in errs.items()))
+    for k, e in errs.items():
+        assert e <= TOL_BF16, (k, e)
