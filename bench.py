@@ -240,6 +240,25 @@ def run_decode(args, torch, L, W):
     if not bool(torch.isfinite(out).all()):
         raise RuntimeError("non-finite decode output")
     bytes_per_step = N * H * (2 * d * d * 4 * 2 + 3 * d * 2 + d * 4)
+    # the same steps on the packed symmetric state (cyclic diagonals of H)
+    sHP = L.pack_state(sH)
+    sG2 = sG.clone()
+    for i in range(min(3, S)):
+        L.decode_step(sHP.clone(), sG2.clone(), q[i], k[i], v[i], gam[i], bet[i], lam, w.n_cg, out=out, packed=True)
+    torch.cuda.synchronize()
+    log("decode: timing %d steps on the packed state" % S)
+    e0.record()
+    for i in range(S):
+        L.decode_step(sHP, sG2, q[i], k[i], v[i], gam[i], bet[i], lam, w.n_cg, out=out, packed=True)
+    e1.record()
+    torch.cuda.synchronize()
+    msp = e0.elapsed_time(e1)
+    bytes_packed = N * H * (2 * (d // 2 + 1) * d * 4 + 2 * d * d * 4 + 3 * d * 2 + d * 4)
+    packed = {"tokens_per_s": N * S / (msp / 1e3), "ms_per_step": msp / S,
+              "hbm_GBps": bytes_packed * S / (msp / 1e3) / 1e9,
+              "hbm_frac": bytes_packed * S / (msp / 1e3) / 1e9 / PEAKS["hbm_gbps"],
+              "state": "H as its d/2+1 cyclic diagonals (mesa_decode_step_packed)"}
+    del sHP, sG2
     dyn = None
     if args.eps > 0:  # dynamic stopping on the continuing states
         S2 = min(S, 64)
@@ -262,6 +281,7 @@ def run_decode(args, torch, L, W):
         "ms_per_step": ms / S,
         "hbm_GBps": bytes_per_step * S / (ms / 1e3) / 1e9,
         "hbm_frac": bytes_per_step * S / (ms / 1e3) / 1e9 / PEAKS["hbm_gbps"],
+        "packed_state": packed,
         "dynamic_stopping": dyn,
     }
 

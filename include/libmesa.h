@@ -201,6 +201,33 @@ int mesa_decode_step_tol(float* state_H, float* state_G, const void* q, const vo
                          int64_t heads, int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps,
                          float* out, int32_t* steps_out, void* stream);
 
+/* Packed symmetric decode state.  H is symmetric, so it is kept as its cyclic
+ * diagonals: state_HP [batch, heads, d_k/2 + 1, d_k] fp32 with
+ *     HP[k][i] = H[i][(i + k) mod d_k],   k = 0 .. d_k/2,
+ * which stores every entry of H once (on the last diagonal, k = d_k/2, the
+ * copy at i < d_k/2 is the one read and written; the others are ignored), so
+ * a decode step moves about half the bytes of H (a quarter of all state bytes
+ * at d_k = d_v).
+ *
+ * mesa_decode_step_packed: mesa_decode_step_tol on a packed H (same arguments,
+ *   state_HP in place of state_H; eps = 0 for fixed steps).  The result equals
+ *   the full-layout step up to rounding (the two halves of a full H are updated
+ *   by different threads, in a different operation order). */
+int mesa_decode_step_packed(float* state_HP, float* state_G, const void* q, const void* k,
+                            const void* v, const float* gamma, const float* beta,
+                            const float* lambda, int64_t batch, int64_t heads, int64_t d_k,
+                            int64_t d_v, int dtype, int max_cg, float eps, float* out,
+                            int32_t* steps_out, void* stream);
+
+/* mesa_pack_state: state_H [batch, heads, d_k, d_k] (e.g. final_H of the
+ *   prefill, mesa_forward_ex) -> state_HP; takes H[i][(i + k) mod d_k], i.e.
+ *   assumes H symmetric.  mesa_unpack_state: state_HP -> the full symmetric
+ *   state_H.  The arrays must not overlap (MESA_ERR_ARG).  One kernel launch. */
+int mesa_pack_state(const float* state_H, float* state_HP, int64_t batch, int64_t heads,
+                    int64_t d_k, void* stream);
+int mesa_unpack_state(const float* state_HP, float* state_H, int64_t batch, int64_t heads,
+                      int64_t d_k, void* stream);
+
 /* Static text for a status code (never NULL). */
 const char* mesa_status_string(int status);
 

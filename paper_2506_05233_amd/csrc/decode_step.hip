@@ -29,8 +29,9 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // Word 3 of a raw buffer resource on gfx9 (32-bit data format, no swizzle).
 constexpr int kBufferRsrcWord3 = 0x00020000;
+constexpr int kXB = 8;  // diagonals per LDS exchange of the packed layout
 
-template <typename Tin, int DK, int DV>
+template <typename Tin, int DK, int DV, bool PACKED>
 __global__ __launch_bounds__(DK) __attribute__((amdgpu_waves_per_eu(3)))
 void decode_step_kernel(DecodeArgs a)
 {
@@ -40,11 +41,14 @@ void decode_step_kernel(DecodeArgs a)
     const int tid = threadIdx.x;    // this thread's row of H and element of the CG vectors
     const int lane = tid % kWave, wv = tid / kWave;
 
-    __shared__ __attribute__((aligned(16))) float sk[DK];
-    __shared__ __attribute__((aligned(16))) float sp[DK];
+    // k and p are kept twice over (entries i and i + d_k) in the packed layout, so the
+    // rotated reads of its diagonals are a base register plus immediate offsets
+    __shared__ __attribute__((aligned(16))) float sk[PACKED ? 2 * DK : DK];
+    __shared__ __attribute__((aligned(16))) float sp[PACKED ? 2 * DK : DK];
     __shared__ float sred[2][NW];
     __shared__ __attribute__((aligned(16))) float sv[DV];
     __shared__ float so[NW][DV];
+    __shared__ float sx[PACKED ? kXB : 1][2 * DK];  // packed layout: diagonal exchange
 
     const Tin* qp = static_cast<const Tin*>(a.q) + pair * DK;
     const Tin* kp = static_cast<const Tin*>(a.k) + pair * DK;
@@ -52,27 +56,70 @@ void decode_step_kernel(DecodeArgs a)
     const float gam = a.gamma[pair], bet = a.beta[pair];
     const float kR = to_f32(kp[tid]), qR = to_f32(qp[tid]), lR = a.lambda[int64_t(h) * DK + tid];
     sk[tid] = kR;
+    if constexpr (PACKED) sk[tid + DK] = kR;
     for (int e = tid; e < DV; e += DK) sv[e] = to_f32(vp[e]);
 
-    // ---- 1. state update of H, row tid held as hc[c] = H[c][tid].  The pair's H is
-    // addressed through a buffer resource: the column offset c d_k is a scalar, so the
-    // 2 d_k accesses need no per-access address registers (the buffer builtins move raw
-    // 32-bit words, hence the bit casts).
-    float* Hp = a.H + pair * DK * DK;
-    const __amdgpu_buffer_rsrc_t hr = __builtin_amdgcn_make_buffer_rsrc(Hp, 0, DK * DK * 4, kBufferRsrcWord3);
-    float hc[DK];
+    // ---- 1. state update of H.  The pair's H is addressed through a buffer resource:
+    // the row offsets are scalars, so the accesses need no per-access address registers
+    // (the buffer builtins move raw 32-bit words, hence the bit casts).
+    // Full layout: thread R holds hc[c] = H[c][R] (row R, read as column R).
+    // Packed layout (HP[k][i] = H[i][(i + k) mod d_k]): thread R holds ho[k] = H[R][R + k]
+    // = HP[k][R] for k = 0 .. d_k/2 (its own entries, which it updates and writes back)
+    // and hx[k] = H[R][R - k] = HP[k][R - k] for k = 1 .. d_k/2 - 1 (owned by thread
+    // R - k; thread R applies the same update, with the owner's operation order, to its
+    // copy).  On the last diagonal the copy at i < d_k/2 is the stored one.
+    constexpr int NH = PACKED ? DK / 2 + 1 : DK;   // rows of the stored state
+    float* Hp = a.H + pair * NH * DK;
+    const __amdgpu_buffer_rsrc_t hr = __builtin_amdgcn_make_buffer_rsrc(Hp, 0, NH * DK * 4, kBufferRsrcWord3);
+    float hc[PACKED ? 1 : DK];
+    float ho[PACKED ? DK / 2 + 1 : 1], hx[PACKED ? DK / 2 : 1];
+    float hdiag;
+    if constexpr (!PACKED) {
 #pragma unroll
-    for (int c = 0; c < DK; ++c) hc[c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(hr, tid * 4, c * DK * 4, 0));
-    const float hdiag = gam * __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(hr, tid * (DK + 1) * 4, 0, 0)) + bet * kR * kR + lR;
-    __syncthreads();
+        for (int c = 0; c < DK; ++c) hc[c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(hr, tid * 4, c * DK * 4, 0));
+        hdiag = gam * __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(hr, tid * (DK + 1) * 4, 0, 0)) + bet * kR * kR + lR;
+        __syncthreads();
 #pragma unroll
-    for (int c4 = 0; c4 < DK; c4 += 4) {
-        const f32x4 kc = *reinterpret_cast<const f32x4*>(sk + c4);
+        for (int c4 = 0; c4 < DK; c4 += 4) {
+            const f32x4 kc = *reinterpret_cast<const f32x4*>(sk + c4);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            hc[c4 + e] = gam * hc[c4 + e] + bet * kR * kc[e];
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(hc[c4 + e]), hr, tid * 4, (c4 + e) * DK * 4, 0);
+            for (int e = 0; e < 4; ++e) {
+                hc[c4 + e] = gam * hc[c4 + e] + bet * kR * kc[e];
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(hc[c4 + e]), hr, tid * 4, (c4 + e) * DK * 4, 0);
+            }
         }
+    } else {
+        constexpr int HALF = DK / 2;
+        const int rl = tid % HALF;  // the owner of this thread's last-diagonal entry
+#pragma unroll
+        for (int k = 0; k < HALF; ++k) ho[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(hr, tid * 4, k * DK * 4, 0));
+        ho[HALF] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(hr, rl * 4, HALF * DK * 4, 0));
+        __syncthreads();
+        const float bkR = bet * kR;
+#pragma unroll
+        for (int k = 0; k < HALF; ++k) {
+            ho[k] = gam * ho[k] + bkR * sk[tid + k];
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ho[k]), hr, tid * 4, k * DK * 4, 0);
+        }
+        ho[HALF] = gam * ho[HALF] + (bet * sk[rl]) * sk[rl + HALF];
+        if (tid < HALF) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ho[HALF]), hr, tid * 4, HALF * DK * 4, 0);
+        // H[R][R - k] is thread (R - k)'s updated entry of diagonal k: exchanged through
+        // LDS, kXB diagonals at a time
+#pragma unroll
+        for (int k0 = 1; k0 < HALF; k0 += kXB) {
+#pragma unroll
+            for (int j = 0; j < kXB; ++j)
+                if (k0 + j < HALF) {
+                    sx[j][tid] = ho[k0 + j];
+                    sx[j][tid + DK] = ho[k0 + j];
+                }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kXB; ++j)
+                if (k0 + j < HALF) hx[k0 + j] = sx[j][tid + DK - k0 - j];
+            __syncthreads();
+        }
+        hdiag = ho[0] + lR;
     }
 
     // ---- 2. CG on (H + Lambda) x = q
@@ -80,13 +127,24 @@ void decode_step_kernel(DecodeArgs a)
     // passed at least one barrier of a dot product since)
     auto gemv = [&](float pin) -> float {
         sp[tid] = pin;
+        if constexpr (PACKED) sp[tid + DK] = pin;
         __syncthreads();
         f32x4 acc = {lR * pin, 0.0f, 0.0f, 0.0f};
+        if constexpr (!PACKED) {
 #pragma unroll
-        for (int c4 = 0; c4 < DK; c4 += 4) {
-            const f32x4 pc = *reinterpret_cast<const f32x4*>(sp + c4);
+            for (int c4 = 0; c4 < DK; c4 += 4) {
+                const f32x4 pc = *reinterpret_cast<const f32x4*>(sp + c4);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) acc[e] += hc[c4 + e] * pc[e];
+                for (int e = 0; e < 4; ++e) acc[e] += hc[c4 + e] * pc[e];
+            }
+        } else {
+            // H[R][R + k] p_{R+k} for k = 0 .. d_k/2 and H[R][R - k] p_{R-k} for k = 1 .. d_k/2 - 1
+            // (rotated LDS reads: consecutive lanes, consecutive words)
+            const float* pr = sp + tid;
+#pragma unroll
+            for (int k = 0; k <= DK / 2; ++k) acc[k & 3] += ho[k] * pr[k];
+#pragma unroll
+            for (int k = 1; k < DK / 2; ++k) acc[(k + 2) & 3] += hx[k] * pr[DK - k];
         }
         return (acc[0] + acc[1]) + (acc[2] + acc[3]);
     };
@@ -187,21 +245,53 @@ void decode_step_kernel(DecodeArgs a)
     }
 }
 
-template <typename Tin, int DK>
+template <typename Tin, int DK, bool PACKED>
 hipError_t launch_dk(const DecodeArgs& a, hipStream_t stream)
 {
     const unsigned blocks = unsigned(a.batch * a.heads);
     if (a.d_v == 64)
-        hipLaunchKernelGGL((decode_step_kernel<Tin, DK, 64>), dim3(blocks), dim3(DK), 0, stream, a);
+        hipLaunchKernelGGL((decode_step_kernel<Tin, DK, 64, PACKED>), dim3(blocks), dim3(DK), 0, stream, a);
     else
-        hipLaunchKernelGGL((decode_step_kernel<Tin, DK, 128>), dim3(blocks), dim3(DK), 0, stream, a);
+        hipLaunchKernelGGL((decode_step_kernel<Tin, DK, 128, PACKED>), dim3(blocks), dim3(DK), 0, stream, a);
     return hipGetLastError();
+}
+
+// full <-> packed symmetric state (one thread per stored element; the packed
+// element HP[k][i] is H[i][(i + k) mod d_k], so unpacking writes it to (i, i + k)
+// and (i + k, i))
+__global__ __launch_bounds__(256) void pack_state_kernel(const float* H, float* HP, int64_t pairs, int dk)
+{
+    const int64_t per = int64_t(dk / 2 + 1) * dk;
+    const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (idx >= pairs * per) return;
+    const int64_t pr = idx / per;
+    const int e = int(idx % per), k = e / dk, i = e % dk;
+    HP[idx] = H[pr * dk * dk + int64_t(i) * dk + ((i + k) & (dk - 1))];
+}
+
+__global__ __launch_bounds__(256) void unpack_state_kernel(const float* HP, float* H, int64_t pairs, int dk)
+{
+    const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (idx >= pairs * dk * dk) return;
+    const int64_t pr = idx / (int64_t(dk) * dk);
+    const int e = int(idx % (int64_t(dk) * dk)), i = e / dk, j = e % dk;
+    // H[i][j] is stored as HP[k][i] with k = (j - i) mod d_k when k <= d_k/2, else as
+    // HP[(i - j) mod d_k][j]; on the last diagonal the copy at the smaller index of
+    // {i, j} mod d_k/2 is the stored one
+    int k = (j - i) & (dk - 1), at = i;
+    if (k > dk / 2) {
+        k = (i - j) & (dk - 1);
+        at = j;
+    }
+    if (k == dk / 2) at = i % (dk / 2);
+    H[idx] = HP[pr * (dk / 2 + 1) * dk + int64_t(k) * dk + at];
 }
 
 template <typename Tin>
 hipError_t launch_tin(const DecodeArgs& a, hipStream_t stream)
 {
-    return a.d_k == 64 ? launch_dk<Tin, 64>(a, stream) : launch_dk<Tin, 128>(a, stream);
+    if (a.packed) return a.d_k == 64 ? launch_dk<Tin, 64, true>(a, stream) : launch_dk<Tin, 128, true>(a, stream);
+    return a.d_k == 64 ? launch_dk<Tin, 64, false>(a, stream) : launch_dk<Tin, 128, false>(a, stream);
 }
 
 }  // namespace
@@ -209,6 +299,22 @@ hipError_t launch_tin(const DecodeArgs& a, hipStream_t stream)
 hipError_t launch_decode_step(const DecodeArgs& a, hipStream_t stream)
 {
     return a.bf16 ? launch_tin<bf16_t>(a, stream) : launch_tin<float>(a, stream);
+}
+
+hipError_t launch_pack_state(const float* H, float* HP, int64_t pairs, int d_k, hipStream_t stream)
+{
+    const int64_t n = pairs * (d_k / 2 + 1) * d_k;
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(pack_state_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, stream, H, HP, pairs, d_k);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack_state(const float* HP, float* H, int64_t pairs, int d_k, hipStream_t stream)
+{
+    const int64_t n = pairs * int64_t(d_k) * d_k;
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(unpack_state_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, stream, HP, H, pairs, d_k);
+    return hipGetLastError();
 }
 
 }  // namespace mesa

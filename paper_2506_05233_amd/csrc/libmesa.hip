@@ -274,10 +274,14 @@ int mesa_decode_step(float* state_H, float* state_G, const void* q, const void* 
                                 dtype, n_cg, 0.0f, out, nullptr, stream);
 }
 
-int mesa_decode_step_tol(float* state_H, float* state_G, const void* q, const void* k, const void* v,
-                         const float* gamma, const float* beta, const float* lambda, int64_t batch,
-                         int64_t heads, int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps,
-                         float* out, int32_t* steps_out, void* stream)
+}  // extern "C"
+
+namespace {
+
+int decode_step(float* state_H, float* state_G, const void* q, const void* k, const void* v,
+                const float* gamma, const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps, float* out, int32_t* steps_out,
+                bool packed, void* stream)
 {
     int st = check_sizes(batch, heads, 1, d_k, d_v, dtype, max_cg);
     if (st != MESA_OK) return st;
@@ -293,7 +297,8 @@ int mesa_decode_step_tol(float* state_H, float* state_G, const void* q, const vo
         const Range ins[] = {range_of(q, pairs * d_k * in_sz), range_of(k, pairs * d_k * in_sz),
                              range_of(v, pairs * d_v * in_sz), range_of(gamma, pairs * 4),
                              range_of(beta, pairs * 4), range_of(lambda, heads * d_k * 4)};
-        const Range outs[] = {range_of(state_H, pairs * d_k * d_k * 4),
+        const int64_t h_rows = packed ? d_k / 2 + 1 : d_k;
+        const Range outs[] = {range_of(state_H, pairs * h_rows * d_k * 4),
                               range_of(state_G, pairs * d_v * d_k * 4), range_of(out, pairs * d_v * 4),
                               range_of(steps_out, steps_out ? pairs * 4 : 0)};
         for (const Range& o : outs) {
@@ -307,9 +312,59 @@ int mesa_decode_step_tol(float* state_H, float* state_G, const void* q, const vo
                     return MESA_ERR_ARG;
     }
     mesa::DecodeArgs da{batch, heads, int(d_k), int(d_v), dtype == MESA_DTYPE_BF16, state_H, state_G,
-                        q, k, v, gamma, beta, lambda, max_cg, out, eps * eps, steps_out};
+                        q, k, v, gamma, beta, lambda, max_cg, out, eps * eps, steps_out, packed};
     return mesa::launch_decode_step(da, static_cast<hipStream_t>(stream)) == hipSuccess ? MESA_OK
                                                                                        : MESA_ERR_HIP;
+}
+
+// pack (to_packed) or unpack the symmetric decode state H of batch x heads pairs
+int convert_state(const float* src, float* dst, int64_t batch, int64_t heads, int64_t d_k, bool to_packed,
+                  void* stream)
+{
+    if (batch < 0 || heads < 0 || d_k < 0) return MESA_ERR_SHAPE;
+    if (!dim_ok(d_k)) return MESA_ERR_UNSUPPORTED;
+    if (batch > 0 && heads > (int64_t(1) << 30) / batch) return MESA_ERR_SHAPE;
+    const int64_t pairs = batch * heads;
+    if (pairs == 0) return MESA_OK;
+    if (!src || !dst) return MESA_ERR_NULL;
+    const int64_t full = pairs * d_k * d_k * 4, pk = pairs * (d_k / 2 + 1) * d_k * 4;
+    if (overlaps(range_of(src, to_packed ? full : pk), range_of(dst, to_packed ? pk : full))) return MESA_ERR_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const hipError_t e = to_packed ? mesa::launch_pack_state(src, dst, pairs, int(d_k), s)
+                                   : mesa::launch_unpack_state(src, dst, pairs, int(d_k), s);
+    return e == hipSuccess ? MESA_OK : MESA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mesa_decode_step_tol(float* state_H, float* state_G, const void* q, const void* k, const void* v,
+                         const float* gamma, const float* beta, const float* lambda, int64_t batch,
+                         int64_t heads, int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps,
+                         float* out, int32_t* steps_out, void* stream)
+{
+    return decode_step(state_H, state_G, q, k, v, gamma, beta, lambda, batch, heads, d_k, d_v, dtype, max_cg, eps,
+                       out, steps_out, false, stream);
+}
+
+int mesa_decode_step_packed(float* state_HP, float* state_G, const void* q, const void* k, const void* v,
+                            const float* gamma, const float* beta, const float* lambda, int64_t batch,
+                            int64_t heads, int64_t d_k, int64_t d_v, int dtype, int max_cg, float eps,
+                            float* out, int32_t* steps_out, void* stream)
+{
+    return decode_step(state_HP, state_G, q, k, v, gamma, beta, lambda, batch, heads, d_k, d_v, dtype, max_cg, eps,
+                       out, steps_out, true, stream);
+}
+
+int mesa_pack_state(const float* state_H, float* state_HP, int64_t batch, int64_t heads, int64_t d_k, void* stream)
+{
+    return convert_state(state_H, state_HP, batch, heads, d_k, true, stream);
+}
+
+int mesa_unpack_state(const float* state_HP, float* state_H, int64_t batch, int64_t heads, int64_t d_k, void* stream)
+{
+    return convert_state(state_HP, state_H, batch, heads, d_k, false, stream);
 }
 
 int mesa_forward_tol(const void* q, const void* k, const void* v, const float* gamma,

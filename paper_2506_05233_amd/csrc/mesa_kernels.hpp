@@ -117,7 +117,15 @@ struct DecodeArgs {
     float* out;
     float eps2;      // Alg. 1 relative tolerance, squared (0: fixed steps)
     int32_t* steps;  // may be null: [batch, heads] iterations each pair used
+    bool packed = false;  // H in the packed symmetric layout (see launch_pack_state)
 };
 hipError_t launch_decode_step(const DecodeArgs& a, hipStream_t stream);
+
+// Packed symmetric decode state: HP [pairs, d_k/2 + 1, d_k] with
+// HP[k][i] = H[i][(i + k) mod d_k] (row k = the k-th cyclic diagonal).  Every
+// unordered pair {i, j} is stored once, except on the last diagonal (k = d_k/2),
+// where the copy at i < d_k/2 is the one read and written.
+hipError_t launch_pack_state(const float* H, float* HP, int64_t pairs, int d_k, hipStream_t stream);
+hipError_t launch_unpack_state(const float* HP, float* H, int64_t pairs, int d_k, hipStream_t stream);
 
 }  // namespace mesa

@@ -29,7 +29,8 @@ MESA_MAX_NCG = 1024
 
 EXPORTED = ("mesa_forward", "mesa_forward_ex", "mesa_forward_states", "mesa_forward_solve",
             "mesa_forward_tol", "mesa_forward_workspace_bytes", "mesa_decode_step",
-            "mesa_decode_step_tol", "mesa_backward", "mesa_backward_workspace_bytes",
+            "mesa_decode_step_tol", "mesa_decode_step_packed", "mesa_pack_state", "mesa_unpack_state",
+            "mesa_backward", "mesa_backward_workspace_bytes",
             "mesa_status_string", "mesa_version")
 
 _lib = None
@@ -71,6 +72,13 @@ def load():
     lib.mesa_decode_step_tol.argtypes = [fp, fp, vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, ci, ci, cf,
                                          fp, vp, vp]
     lib.mesa_decode_step_tol.restype = ci
+    lib.mesa_decode_step_packed.argtypes = [fp, fp, vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, ci, ci, cf,
+                                            fp, vp, vp]
+    lib.mesa_decode_step_packed.restype = ci
+    lib.mesa_pack_state.argtypes = [fp, fp, i64, i64, i64, vp]
+    lib.mesa_pack_state.restype = ci
+    lib.mesa_unpack_state.argtypes = [fp, fp, i64, i64, i64, vp]
+    lib.mesa_unpack_state.restype = ci
     lib.mesa_backward_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
     lib.mesa_backward_workspace_bytes.restype = sz
     lib.mesa_backward.argtypes = [vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, fp, fp,
@@ -330,17 +338,46 @@ def prefill_states(k, v, gamma, beta, chunk=64, workspace=None):
     return fH, fG
 
 
-def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, out=None, eps=None, steps_out=None):
-    """One recurrent step, in place on state_H [N,H,d_k,d_k] and state_G [N,H,d_v,d_k].
+def pack_state(state_H):
+    """Full symmetric decode state H [N,H,d_k,d_k] -> packed cyclic diagonals
+    [N,H,d_k/2+1,d_k] (mesa_pack_state)."""
+    torch = _torch()
+    lib = load()
+    N, H, dk, _ = state_H.shape
+    _check(state_H, "state_H", (N, H, dk, dk), torch.float32, state_H.device)
+    hp = torch.empty((N, H, dk // 2 + 1, dk), dtype=torch.float32, device=state_H.device)
+    st = lib.mesa_pack_state(_ptr(state_H), _ptr(hp), N, H, dk, _stream(state_H.device))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_pack_state")
+    return hp
+
+
+def unpack_state(state_HP):
+    """Packed [N,H,d_k/2+1,d_k] -> full symmetric H [N,H,d_k,d_k] (mesa_unpack_state)."""
+    torch = _torch()
+    lib = load()
+    N, H, _, dk = state_HP.shape
+    _check(state_HP, "state_HP", (N, H, dk // 2 + 1, dk), torch.float32, state_HP.device)
+    h = torch.empty((N, H, dk, dk), dtype=torch.float32, device=state_HP.device)
+    st = lib.mesa_unpack_state(_ptr(state_HP), _ptr(h), N, H, dk, _stream(state_HP.device))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_unpack_state")
+    return h
+
+
+def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, out=None, eps=None, steps_out=None,
+                packed=False):
+    """One recurrent step, in place on state_H [N,H,d_k,d_k] (or, with packed, the
+    cyclic-diagonal form [N,H,d_k/2+1,d_k] of pack_state) and state_G [N,H,d_v,d_k].
     q, k [N,H,d_k], v [N,H,d_v] fp32 or bf16; gamma, beta [N,H]; lam [H,d_k].
     eps / steps_out (int32 [N,H]): CG relative tolerance and iteration counts, through
-    mesa_decode_step_tol.  Returns out [N,H,d_v] fp32."""
+    mesa_decode_step_tol (or mesa_decode_step_packed).  Returns out [N,H,d_v] fp32."""
     torch = _torch()
     lib = load()
     N, H, dk = q.shape
     dv = v.shape[-1]
     dev = q.device
-    _check(state_H, "state_H", (N, H, dk, dk), torch.float32, dev)
+    _check(state_H, "state_H", (N, H, dk // 2 + 1 if packed else dk, dk), torch.float32, dev)
     _check(state_G, "state_G", (N, H, dv, dk), torch.float32, dev)
     _check(q, "q", (N, H, dk), device=dev)
     _check(k, "k", (N, H, dk), q.dtype, dev)
@@ -351,6 +388,16 @@ def decode_step(state_H, state_G, q, k, v, gamma, beta, lam, n_cg, out=None, eps
     if out is None:
         out = torch.empty((N, H, dv), dtype=torch.float32, device=dev)
     _check(out, "out", (N, H, dv), torch.float32, dev)
+    if packed:
+        if steps_out is not None:
+            _check(steps_out, "steps_out", (N, H), torch.int32, dev)
+        st = lib.mesa_decode_step_packed(_ptr(state_H), _ptr(state_G), _ptr(q), _ptr(k), _ptr(v),
+                                         _ptr(gamma), _ptr(beta), _ptr(lam), N, H, dk, dv, _dtype_code(q),
+                                         int(n_cg), float(eps or 0.0), _ptr(out), _ptr(steps_out),
+                                         _stream(dev))
+        if st != MESA_OK:
+            raise MesaError(st, "mesa_decode_step_packed")
+        return out
     if eps is not None or steps_out is not None:
         if steps_out is not None:
             _check(steps_out, "steps_out", (N, H), torch.int32, dev)

@@ -256,3 +256,16 @@ def test_backward_workspace_size(lib):
     assert lib.mesa_backward_workspace_bytes(B, H, T, dk, dv) == want
     assert lib.mesa_backward_workspace_bytes(B, H, 0, dk, dv) == 0
     assert _bwd(lib, B=0) == L.MESA_OK
+
+
+def test_packed_state_entry_points_reject_bad_arguments(lib):
+    assert lib.mesa_pack_state(None, P["H"], 2, 2, 128, None) == L.MESA_ERR_NULL
+    assert lib.mesa_pack_state(P["H"], P["H"] + 64, 2, 2, 128, None) == L.MESA_ERR_ARG   # overlap
+    assert lib.mesa_unpack_state(P["H"], P["G"], 2, 2, 96, None) == L.MESA_ERR_UNSUPPORTED
+    assert lib.mesa_unpack_state(P["H"], P["G"], -1, 2, 64, None) == L.MESA_ERR_SHAPE
+    assert lib.mesa_pack_state(P["H"], P["G"], 0, 2, 64, None) == L.MESA_OK
+    args = [P["H"], P["G"], P["q"], P["k"], P["v"], P["g"], P["b"], P["lam"], 4, 2, 128, 128, 1, 15]
+    assert lib.mesa_decode_step_packed(*args[:8], 4, 2, 128, 128, 1, 15, -1.0, P["out"], None, None) == L.MESA_ERR_ARG
+    assert lib.mesa_decode_step_packed(None, *args[1:], 0.0, P["out"], None, None) == L.MESA_ERR_NULL
+    # the packed H of 8 pairs spans 8 * 65 * 128 floats: an output inside that extent overlaps
+    assert lib.mesa_decode_step_packed(*args, 0.0, P["H"] + 8 * 65 * 128 * 4 - 4, None, None) == L.MESA_ERR_ARG

@@ -456,3 +456,89 @@ def test_decode_tolerance_matches_oracle():
         same = got == rst
         assert rel_l2(out.cpu().numpy()[same], ro[same]) <= TOL_F32
         assert rel_l2(dH.cpu().numpy(), rH) <= 1e-6 and rel_l2(dG.cpu().numpy(), rG) <= 1e-6
+
+
+# ------------------------------------------------------ packed symmetric decode state
+def _np_pack(H):
+    """Cyclic diagonals of symmetric H [..., d, d]: HP[..., k, i] = H[..., i, (i + k) mod d]."""
+    d = H.shape[-1]
+    i = np.arange(d)
+    return np.stack([H[..., i, (i + k) % d] for k in range(d // 2 + 1)], axis=-2)
+
+
+@pytest.mark.parametrize("dk", [64, 128])
+def test_pack_unpack_state_roundtrip(dk):
+    rng = np.random.default_rng(dk)
+    A = rng.standard_normal((3, 2, dk, dk)).astype(np.float32)
+    H = (A + np.swapaxes(A, -1, -2)).astype(np.float32)   # exactly symmetric
+    hp = L.pack_state(torch.from_numpy(H).cuda())
+    back = L.unpack_state(hp)
+    torch.cuda.synchronize()
+    assert np.array_equal(hp.cpu().numpy(), _np_pack(H))
+    assert np.array_equal(back.cpu().numpy(), H)
+
+
+@pytest.mark.parametrize("dk,dv,dtype", [(128, 128, "bf16"), (64, 128, "f32"), (128, 64, "f32")])
+def test_packed_decode_matches_full_layout_and_oracle(dk, dv, dtype):
+    """Twelve steps on the packed state and on the full state from the same prefilled
+    (symmetric) states: outputs agree to fp32 rounding, the unpacked state matches the
+    full one, and both match the oracle's decode."""
+    rng = np.random.default_rng(dk + dv)
+    N, Hh = 5, 2
+    H0, G0 = oracle.unrolled_states(rng.standard_normal((N, Hh, 200, dk)) / np.sqrt(dk),
+                                    rng.standard_normal((N, Hh, 200, dv)),
+                                    np.full((N, Hh, 200), 0.98), np.full((N, Hh, 200), 0.5))
+    H0 = H0.astype(np.float32)
+    H0 = np.triu(H0) + np.swapaxes(np.triu(H0, 1), -1, -2)   # exactly symmetric fp32
+    G0 = G0.astype(np.float32)
+    lam = W.forward_inputs(1, Hh, 1, dk, dv, "f32", 3.0, seed=1)["lam"]
+    dlam = torch.from_numpy(lam).cuda()
+    fH, fG = torch.from_numpy(H0).cuda(), torch.from_numpy(G0).cuda()
+    pG = torch.from_numpy(G0).cuda()
+    pH = L.pack_state(fH.clone())
+    rH, rG = H0.astype(np.float64), G0.astype(np.float64)
+    worst_fp, worst_or = 0.0, 0.0
+    for step in range(12):
+        x = W.forward_inputs(N, Hh, 1, dk, dv, dtype, 3.0, seed=100 + step)
+        d = to_device({k: v[:, :, 0] for k, v in x.items() if k != "lam"}, dtype)
+        of = L.decode_step(fH, fG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], dlam, 15)
+        op = L.decode_step(pH, pG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], dlam, 15, packed=True)
+        torch.cuda.synchronize()
+        ro, rH, rG = oracle.decode_step(rH, rG, x["q"][:, :, 0], x["k"][:, :, 0], x["v"][:, :, 0],
+                                        x["gamma"][:, :, 0], x["beta"][:, :, 0], lam, 15)
+        worst_fp = max(worst_fp, rel_l2(op.cpu().numpy(), of.cpu().numpy()))
+        worst_or = max(worst_or, rel_l2(op.cpu().numpy(), ro))
+    _say("packed decode d_k=%d d_v=%d %s: vs full layout %.2e, vs oracle %.2e" % (dk, dv, dtype, worst_fp, worst_or))
+    assert worst_fp <= 1e-5
+    assert worst_or <= (TOL_BF16 if dtype == "bf16" else TOL_F32)
+    full_from_packed = L.unpack_state(pH).cpu().numpy()
+    assert rel_l2(full_from_packed, fH.cpu().numpy()) <= 1e-6
+    assert rel_l2(full_from_packed, rH) <= 1e-6 and rel_l2(pG.cpu().numpy(), rG) <= 1e-6
+    # the stored diagonals stay exactly those of a symmetric matrix
+    assert np.array_equal(L.pack_state(torch.from_numpy(full_from_packed).cuda()).cpu().numpy()[:, :, :dk // 2],
+                          pH.cpu().numpy()[:, :, :dk // 2])
+
+
+def test_packed_decode_tolerance_counts():
+    x = W.forward_inputs(3, 2, 1, 128, 128, "f32", 3.0, seed=65)
+    rng = np.random.default_rng(65)
+    H0, G0 = oracle.unrolled_states(rng.standard_normal((3, 2, 300, 128)) / 11,
+                                    rng.standard_normal((3, 2, 300, 128)),
+                                    np.full((3, 2, 300), 0.99), np.full((3, 2, 300), 0.5))
+    H0 = H0.astype(np.float32)
+    H0 = np.triu(H0) + np.swapaxes(np.triu(H0, 1), -1, -2)
+    G0 = G0.astype(np.float32)
+    d = to_device({k: v[:, :, 0] for k, v in x.items() if k != "lam"}, "f32")
+    lam = torch.from_numpy(x["lam"]).cuda()
+    pH = L.pack_state(torch.from_numpy(H0).cuda())
+    pG = torch.from_numpy(G0).cuda()
+    st = torch.zeros((3, 2), dtype=torch.int32, device="cuda")
+    out = L.decode_step(pH, pG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], lam, 40, eps=1e-4,
+                        steps_out=st, packed=True)
+    rst = np.zeros((3, 2), dtype=np.int32)
+    ro, _, _ = oracle.decode_step(H0, G0, x["q"][:, :, 0], x["k"][:, :, 0], x["v"][:, :, 0], x["gamma"][:, :, 0],
+                                  x["beta"][:, :, 0], x["lam"], 40, eps=1e-4, steps_out=rst)
+    got = st.cpu().numpy()
+    assert np.abs(got - rst).max() <= 1
+    same = got == rst
+    assert rel_l2(out.cpu().numpy()[same], ro[same]) <= TOL_F32
