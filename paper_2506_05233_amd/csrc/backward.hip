@@ -611,21 +611,29 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
 }
 
 // ---------------------------------------------------------------- dLambda
-// dLambda[h][b] = sum over the batch and the chunks of the per-chunk partial sums.
+// dLambda[h][b] = sum over the batch and the chunks of the per-chunk partial sums:
+// one workgroup per head; thread (b, slot) sums every kThreads / d_k-th (batch, chunk)
+// entry, then the slots are summed in a fixed order.
 __global__ __launch_bounds__(kThreads) void bwd_dlam_kernel(BwdArgs a)
 {
     const ForwardShape s = a.s;
-    const int dk = s.d_k;
-    const int64_t idx = int64_t(blockIdx.x) * kThreads + threadIdx.x;
-    if (idx >= s.heads * dk) return;
-    const int64_t h = idx / dk;
-    const int b = int(idx % dk);
+    const int dk = s.d_k, slots = kThreads / dk;
+    const int64_t h = blockIdx.x;
+    const int b = threadIdx.x % dk, slot = threadIdx.x / dk;
+    const int64_t per = s.batch * s.n_chunks;  // partial sums of this head
+    __shared__ float sAcc[kThreads];
     float acc = 0.0f;
-    for (int64_t bb = 0; bb < s.batch; ++bb) {
-        const int64_t bh = bb * s.heads + h;
-        for (int n = 0; n < s.n_chunks; ++n) acc += a.dlam_part[(bh * s.n_chunks + n) * dk + b];
+    for (int64_t e = slot; e < per; e += slots) {
+        const int64_t bb = e / s.n_chunks, n = e % s.n_chunks;
+        acc += a.dlam_part[((bb * s.heads + h) * s.n_chunks + n) * dk + b];
     }
-    a.dlam[idx] = acc;
+    sAcc[threadIdx.x] = acc;
+    __syncthreads();
+    if (slot == 0) {
+        float t = 0.0f;
+        for (int u = 0; u < slots; ++u) t += sAcc[u * dk + b];
+        a.dlam[h * dk + b] = t;
+    }
 }
 
 template <typename Tin, int DK, int DV>
@@ -644,10 +652,8 @@ hipError_t launch_bwd_dims(const BwdArgs& a, hipStream_t stream, int stage)
         case 2:
             hipLaunchKernelGGL((bwd_grad_kernel<Tin, DK, DV>), dim3(chunks), dim3(kThreads), 0, stream, a);
             break;
-        default: {
-            const int64_t n = a.s.heads * DK;
-            hipLaunchKernelGGL(bwd_dlam_kernel, dim3(unsigned((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, stream, a);
-        }
+        default:
+            hipLaunchKernelGGL(bwd_dlam_kernel, dim3(unsigned(a.s.heads)), dim3(kThreads), 0, stream, a);
     }
     return hipGetLastError();
 }

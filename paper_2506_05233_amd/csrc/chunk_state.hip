@@ -294,7 +294,7 @@ struct SegPlan {
     float* dec;   // [B*H, total]: D_s
 };
 
-template <int DK, int DV, bool STORE, bool SPLIT>
+template <int DK, int DV, bool STORE, bool SPLIT, bool PLAIN = false>
 __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArgs a, SegPlan sg)
 {
     constexpr int C = 64;
@@ -417,6 +417,13 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
         constexpr bool frag_out = STORE;
         uint16_t* frag_base = static_cast<uint16_t*>(part ? a.Gs : a.Hs);
         constexpr int kStateElems = NC * DK;  // bf16 per chunk state of this part
+        float* plain_base = part ? a.Gs32 : a.Hs32;  // fp32 plain chunk states (PLAIN)
+        // element offset of this thread's tile value (rt, ct, ii) -- row R, column c of the
+        // part -- in a [R][c] (H) or [c][R] (G) fp32 state
+        auto tile_off = [&](int rt, int ct, int ii) -> int {
+            const int R = 32 * sblk + 16 * rt + 4 * g + ii, c = 16 * (ct0 + ct) + ln;
+            return part ? c * DK + R : R * DK + c;
+        };
 
         // chunk n: its state is stored, then acc = D acc + K^T (w ⊙ Y) from buffer n % 2;
         // chunk n + 1 is staged (from Rn1) into the other buffer and chunk n + 3 loaded
@@ -430,6 +437,15 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                                                 pack_bf16x2(acc[1][ct][0], acc[1][ct][1]), pack_bf16x2(acc[1][ct][2], acc[1][ct][3]));
                     *reinterpret_cast<uint4*>(base + (((ct0 + ct) * NS + sblk) * kWave + lane) * 8) = pk;
                 }
+            }
+            if constexpr (PLAIN) {
+                float* dst = plain_base + (bh * s.n_chunks + n) * int64_t(kStateElems);
+#pragma unroll
+                for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                        for (int ii = 0; ii < 4; ++ii) dst[tile_off(rt, ct, ii)] = acc[rt][ct][ii];
             }
             const int b = (n - nbeg) % 2;
             dprod *= D;
@@ -476,12 +492,6 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
             __syncthreads();
         };
 
-        // element offset of this thread's tile value (rt, ct, ii) -- row R, column c of the
-        // part -- in a [R][c] (H) or [c][R] (G) fp32 state
-        auto tile_off = [&](int rt, int ct, int ii) -> int {
-            const int R = 32 * sblk + 16 * rt + 4 * g + ii, c = 16 * (ct0 + ct) + ln;
-            return part ? c * DK + R : R * DK + c;
-        };
         constexpr int64_t kSegElems = int64_t(DK) * (DK + DV);  // one segment total, H then G
         auto seg_total = [&](int t) -> float* { return sg.tot + (bh * (sg.total - 1) + t) * kSegElems + (part ? DK * DK : 0); };
         // inputs of the first three chunks (the walk keeps three chunks in flight)
@@ -566,11 +576,11 @@ int wide_segments(int64_t bh, int n_chunks)
     return S;
 }
 
-template <int DK, int DV, bool STORE, bool SPLIT>
+template <int DK, int DV, bool STORE, bool SPLIT, bool PLAIN = false>
 void launch_wide_kernel(const StateArgs& a, const SegPlan& sg, int64_t bh, hipStream_t stream)
 {
     const unsigned blocks = unsigned(bh * 2 * sg.count);
-    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, STORE, SPLIT>), dim3(blocks), dim3(kWideThreads), 0, stream, a, sg);
+    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, STORE, SPLIT, PLAIN>), dim3(blocks), dim3(kWideThreads), 0, stream, a, sg);
 }
 
 template <int DK, int DV>
@@ -595,7 +605,7 @@ hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
         SegPlan p1 = sg;
         p1.count = S - 1;
         p1.totals = true;
-        if (fin)
+        if (fin || a.Hs32)
             launch_wide_kernel<DK, DV, false, true>(a, p1, bh, stream);
         else
             launch_wide_kernel<DK, DV, false, false>(a, p1, bh, stream);
@@ -607,7 +617,9 @@ hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
         sg.first = S - 1;
         sg.count = 1;
     }
-    if (a.store_chunks && a.frag && !fin)
+    if (a.store_chunks && a.frag && a.Hs32)  // fragments and fp32 plain states, fp32-accurate
+        launch_wide_kernel<DK, DV, true, true, true>(a, sg, bh, stream);
+    else if (a.store_chunks && a.frag && !fin)
         launch_wide_kernel<DK, DV, true, false>(a, sg, bh, stream);
     else if (a.store_chunks && a.frag)
         launch_wide_kernel<DK, DV, true, true>(a, sg, bh, stream);

@@ -485,11 +485,18 @@ int mesa_backward(const void* k, const void* v, const float* gamma, const float*
                                    dtype == MESA_DTYPE_BF16};
     // forward chunk states (fp32, plain layout), and for the matrix-core solve the bf16
     // fragment states as the forward's solve reads them
-    mesa::StateArgs sa{shape, k, v, gamma, beta, f32_at(L.hs), f32_at(L.gs), nullptr, nullptr, true, false};
-    if (mesa::launch_chunk_state(sa, s) != hipSuccess) return MESA_ERR_HIP;
     if (use_bf16) {
+        // one pass: bf16 fragments for the solve and fp32 plain states for the gradients;
+        // the adjoint region, written only later, is the scratch of a segmented walk
         mesa::StateArgs fa{shape, k, v, gamma, beta, u16_at(L.fh), u16_at(L.fg), nullptr, nullptr, true, true};
+        fa.Hs32 = f32_at(L.hs);
+        fa.Gs32 = f32_at(L.gs);
+        fa.seg_ws = f32_at(L.sh);
+        fa.seg_bytes = size_t(L.u - L.sh);
         if (mesa::launch_chunk_state(fa, s) != hipSuccess) return MESA_ERR_HIP;
+    } else {
+        mesa::StateArgs sa{shape, k, v, gamma, beta, f32_at(L.hs), f32_at(L.gs), nullptr, nullptr, true, false};
+        if (mesa::launch_chunk_state(sa, s) != hipSuccess) return MESA_ERR_HIP;
     }
     mesa::BwdArgs ba{shape, k, v, gamma, beta, qstar, dout, dq, f32_at(L.hs), f32_at(L.gs), f32_at(L.sh),
                      f32_at(L.ag), f32_at(L.u), use_bf16 ? u16_at(L.u16) : nullptr, dk, dv, dgamma, dbeta,

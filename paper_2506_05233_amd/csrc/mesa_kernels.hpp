@@ -41,6 +41,10 @@ struct StateArgs {
     // segment totals and decays, seg_bytes bytes.  Used by the bf16 scan only.
     float* seg_ws = nullptr;
     size_t seg_bytes = 0;
+    // With frag: also the same chunk states as plain fp32 (layout of frag == false), from
+    // the same fp32-accurate pass (may be null).
+    float* Hs32 = nullptr;
+    float* Gs32 = nullptr;
 };
 bool chunk_state_frag_supported(const ForwardShape& s);
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream);
