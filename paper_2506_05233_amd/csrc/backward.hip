@@ -233,12 +233,25 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
 // the slice as d_k / 16 result tiles in registers and adds each chunk's rank-64
 // update on the matrix cores.  The gate weight zeta_{j,c-1} is folded into the row
 // operands as they are staged.
+// Few long sequences walk in segments, in time reverse of the forward scan's: a first
+// launch computes each later segment's contribution from a zero state, T_s, and its decay
+// D_s; the second starts segment s from E_s = sum_{t>s} (D_{s+1} ... D_{t-1}) T_t.
 constexpr int kAdjRows = 64;
 constexpr int kLdX = 144;   // row stride of the [token][column] operands (16 banks apart)
 constexpr int kLdR = 80;    // row stride of the [token][row] operands
 
+struct AdjSeg {
+    int len;      // chunks per segment (the last may be shorter)
+    int total;    // segments of a sequence
+    int first;    // first segment this launch walks
+    int count;    // segments this launch walks
+    bool totals;  // write T_s and D_s instead of the per-chunk adjoints
+    float* tot;   // [B*H, total, d_k (d_k + d_v)]: T_s of S^H then of A^G (chunk layout)
+    float* dec;   // [B*H, total]: D_s
+};
+
 template <int DK, int DV>
-__global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a)
+__global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a, AdjSeg sg)
 {
     constexpr int NCT = DK / 16;                  // column tiles
     constexpr int NTH = DK / kAdjRows;            // row slices of S^H
@@ -247,12 +260,18 @@ __global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a)
     const int nc = s.n_chunks;
     const int blk = xcd_major_block(blockIdx.x, gridDim.x);
     const int tile = blk % NTILE;
-    const int64_t bh = blk / NTILE;
+    const int seg = sg.first + (blk / NTILE) % sg.count;
+    const int64_t bh = blk / NTILE / sg.count;
+    const int nbeg = seg * sg.len, nend = min(nbeg + sg.len, nc);  // this segment's chunks
     const bool isG = tile >= NTH;
     const int r0 = (isG ? tile - NTH : tile) * kAdjRows;
     const int nrow = isG ? DV : DK;
     const int tid = threadIdx.x;
     const int w = tid / kWave, lane = tid % kWave, g = lane / 16, ln = lane % 16;
+    constexpr int64_t kSegElems = int64_t(DK) * (DK + DV);
+    // this thread's elements of segment t's total: rows r0 + 16w + 4g + r, columns 16 ct + ln
+    auto seg_tile = [&](int t) { return sg.tot + (bh * sg.total + t) * kSegElems + (isG ? DK * DK : 0) +
+                                        int64_t(r0 + 16 * w + 4 * g) * DK + ln; };
 
     __shared__ float sX[kC * kLdX];   // q*_j [j][c]
     __shared__ float sY[kC * kLdX];   // e*_j [j][c] (S^H only)
@@ -265,16 +284,31 @@ __global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a)
     f32x4 st[NCT];
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct) st[ct] = kZero4;
+    if (!sg.totals) {
+        // the adjoint arriving from the later segments
+        float c = 1.0f;
+        for (int t = seg + 1; t < sg.total; ++t) {
+            const float* tb = seg_tile(t);
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) st[ct][r] += c * tb[r * DK + 16 * ct];
+            c *= sg.dec[bh * sg.total + t];
+        }
+    }
+    float dprod = 1.0f;
     float* out = isG ? a.AG : a.SH;
-    for (int n = nc - 1; n >= 0; --n) {
+    for (int n = nend - 1; n >= nbeg; --n) {
         const int64_t t0 = int64_t(n) * kC;
         const int valid = int(min<int64_t>(kC, s.seq_len - t0));
         const int64_t tok0 = bh * s.seq_len + t0;
-        float* dst = out + ((bh * nc + n) * nrow + r0 + 16 * w) * int64_t(DK);
+        if (!sg.totals) {
+            float* dst = out + ((bh * nc + n) * nrow + r0 + 16 * w) * int64_t(DK);
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct)
+            for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dst[(4 * g + r) * DK + 16 * ct + ln] = st[ct][r];
+                for (int r = 0; r < 4; ++r) dst[(4 * g + r) * DK + 16 * ct + ln] = st[ct][r];
+        }
         // row slices: 64 tokens x 64 rows, four 16-byte loads per thread and array
         constexpr int VR = kC * kAdjRows / 4 / kThreads;
         float4 yr[VR], xr[VR];
@@ -308,6 +342,7 @@ __global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a)
         }
         __syncthreads();
         const float D = decay_from_start(sLg, sZl, kC - 1);
+        dprod *= D;
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
             f32x4 acc = st[ct] * D;
@@ -318,12 +353,19 @@ __global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a)
         }
         __syncthreads();
     }
+    if (sg.totals) {
+        float* tb = seg_tile(seg);
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) tb[r * DK + 16 * ct] = st[ct][r];
+        if (tile == 0 && tid == 0) sg.dec[bh * sg.total + seg] = dprod;
+    }
 }
 
 // ---------------------------------------------------------------- per-chunk gradients
-// One workgroup per chunk; in the token-by-feature phases wave w owns tokens
-// 16w .. 16w+15 (the rows of its result tiles), so every per-token sum over features
-// is a sum over the 16 lanes of a lane row.
+// One workgroup per chunk.  The gram and C x C phases give wave w the tokens 16w ..
+// 16w+15; the token-by-feature phases give it a quarter of the feature column tiles.
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
 {
@@ -645,10 +687,31 @@ hipError_t launch_bwd_dims(const BwdArgs& a, hipStream_t stream, int stage)
         case 0:
             hipLaunchKernelGGL((bwd_rhs_kernel<Tin, DK, DV>), dim3(chunks), dim3(kThreads), 0, stream, a);
             break;
-        case 1:
-            hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV>), dim3(unsigned(bh * (DK + DV) / kAdjRows)), dim3(kThreads), 0,
-                               stream, a);
+        case 1: {
+            // segments while the (sequence, slice, segment) workgroups fit the compute units
+            // once (one per unit) and each keeps at least 8 chunks; the totals go to the
+            // fp32 right-hand-side region, free once the solve has read it
+            constexpr int NTILE = (DK + DV) / kAdjRows;
+            const int nc = a.s.n_chunks;
+            int S = 1;
+            while (bh * NTILE * (2 * S) <= 256 && nc / (2 * S) >= 8) S *= 2;
+            const int len = (nc + S - 1) / S;
+            S = (nc + len - 1) / len;
+            AdjSeg sg{len, S, 0, S, false, a.u, a.u + bh * S * int64_t(DK) * (DK + DV)};
+            if (S > 1) {
+                AdjSeg p1 = sg;
+                p1.first = 1;
+                p1.count = S - 1;
+                p1.totals = true;
+                hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV>), dim3(unsigned(bh * NTILE * p1.count)), dim3(kThreads), 0,
+                                   stream, a, p1);
+                const hipError_t e = hipGetLastError();
+                if (e != hipSuccess) return e;
+            }
+            hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV>), dim3(unsigned(bh * NTILE * sg.count)), dim3(kThreads), 0,
+                               stream, a, sg);
             break;
+        }
         case 2:
             hipLaunchKernelGGL((bwd_grad_kernel<Tin, DK, DV>), dim3(chunks), dim3(kThreads), 0, stream, a);
             break;

@@ -149,3 +149,30 @@ def test_backward_full_size_sampled():
     _say("full-size backward, sampled: %s" % "  ".join("%s %.2e" % kv for kv in errs.items()))
     for k, e in errs.items():
         assert e <= TOL_BF16, (k, e)
+
+
+@pytest.mark.parametrize("precision,tol", [(L.MESA_PREC_F32, TOL_F32), (L.MESA_PREC_BF16, TOL_BF16)],
+                         ids=["f32_solve", "bf16_solve"])
+def test_backward_segmented_walks_long_memory(precision, tol):
+    """Two sequences of 36 chunks: the reverse adjoint scan (and, on the bf16 route, the
+    state scan) run in 4 segments of 9 chunks.  Gates within 1e-3 of one keep every
+    later segment's total relevant to the earlier ones; the workspace starts filled
+    with ones, so scratch read before it is written would show.  Every gradient
+    against the oracle."""
+    T = 35 * 64 + 17
+    x = W.forward_inputs(1, 2, T, 128, 128, "bf16", 4.0, seed=71)
+    rng = np.random.default_rng(7101)
+    x["gamma"][...] = rng.uniform(0.999, 1.0, size=x["gamma"].shape).astype(np.float32)
+    dout = _dout(x, 9)
+    d = to_device(x, "bf16")
+    fwd = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], 15, 64,
+                    precision=L.MESA_PREC_F32, want_qstar=True)
+    ws = torch.ones(L.backward_workspace_bytes(1, 2, T, 128, 128) // 4, dtype=torch.float32, device="cuda")
+    g = L.backward(d["k"], d["v"], d["gamma"], d["beta"], d["lam"], fwd["qstar"], torch.from_numpy(dout).cuda(), 15,
+                   precision=precision, workspace=ws)
+    torch.cuda.synchronize()
+    ref = oracle.backward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], dout, 15)
+    errs = {k: rel_l2(g[k].cpu().numpy(), ref[k]) for k in GRADS}
+    _say("segmented backward: %s" % "  ".join("%s %.2e" % kv for kv in errs.items()))
+    for k, e in errs.items():
+        assert e <= tol, (k, e)
