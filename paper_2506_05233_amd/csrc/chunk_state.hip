@@ -252,6 +252,149 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
     }
 }
 
+// fp32 variant (fp32 k and v, chunk 64): the same update, M <- D M + X^T (w ⊙ K),
+// on the matrix cores in fp32 (v_mfma_f32_16x16x4f32: exact fp32 products and
+// fp32 sums, as the scalar kernel).  Each wave owns one 16x16 tile of the stacked
+// state [H; G] -- a workgroup's four waves the four 16-column tiles of 64 columns
+// of the same 16 rows -- and runs on its own: it scans the chunk's gates itself
+// and passes its operands through a private LDS slice, so no barrier couples the
+// waves.  A chunk is 16 dependent products (~512 cycles), shorter than a memory
+// round trip, so a chunk's inputs are loaded kF32Depth chunks ahead; they travel
+// as 16-byte row pieces (token-major), are scaled by w_i once, and each product
+// reads k-slot g = tokens 4j + g of the staged slices.
+constexpr int kF32Depth = 4;
+
+template <int DK, bool STORE>
+__global__ __launch_bounds__(kThreads) void chunk_state_f32_kernel(StateArgs a)
+{
+    constexpr int C = 64;
+    constexpr int kGroups = DK / 64;  // 64-column groups per row tile
+    const ForwardShape s = a.s;
+    const int dv = s.d_v;
+    const int nrt = (DK + dv) / 16;
+    const int blk = xcd_major_block(blockIdx.x, gridDim.x);
+    const int grp = blk % kGroups;
+    const int rt = (blk / kGroups) % nrt;
+    const int64_t bh = blk / (kGroups * nrt);
+    const bool isG = rt * 16 >= DK;
+    const int xr0 = isG ? rt * 16 - DK : rt * 16;  // first row of the tile within H or G
+    const int nX = isG ? dv : DK;                  // rows of that state = width of its source
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int lane = tid % kWave;
+    const int g = lane / 16, m = lane % 16;
+    const int c0 = grp * 64 + 16 * wave;
+    // staging: lane holds columns q4 .. q4 + 3 of in-chunk tokens tq + 16 r, r < 4
+    const int q4 = 4 * (lane % 4), tq = lane / 4;
+    const float* xp = static_cast<const float*>(isG ? a.v : a.k) + xr0 + q4;
+    const float* yp = static_cast<const float*>(a.k) + c0 + q4;
+
+    __shared__ __attribute__((aligned(16))) float sX[kThreads / kWave][C * 16];  // [token][row]
+    __shared__ __attribute__((aligned(16))) float sY[kThreads / kWave][C * 16];  // [token][column], times w
+    float* const wx = sX[wave];
+    float* const wy = sY[wave];
+
+    struct Regs {
+        f32x4 x[4], y[4];
+        float gam, bet;
+        int valid;
+    };
+    // chunk n of a sequence with n_chunks >= 1.  Tokens past the end re-read the
+    // chunk's last token (in bounds, branch-free); the step gives them beta = 0 and
+    // gamma = 1, so they add exact zeros.  Nothing here waits for the loads.
+    auto load = [&](int n, Regs& R) {
+        const int64_t t0 = int64_t(n) * C;
+        const int valid = int(min<int64_t>(C, s.seq_len - t0));
+        const int64_t tok0 = bh * s.seq_len + t0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t tok = tok0 + min(tq + 16 * r, valid - 1);
+            R.x[r] = *reinterpret_cast<const f32x4*>(xp + tok * nX);
+            R.y[r] = *reinterpret_cast<const f32x4*>(yp + tok * DK);
+        }
+        R.gam = a.gamma[tok0 + min(lane, valid - 1)];
+        R.bet = a.beta[tok0 + min(lane, valid - 1)];
+        R.valid = valid;
+    };
+
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    const int64_t tile_off = (xr0 + 4 * g) * int64_t(DK) + c0 + m;  // element (4g, m) of the tile
+    float* chunk_dst = STORE ? static_cast<float*>(isG ? a.Gs : a.Hs) + bh * s.n_chunks * nX * int64_t(DK) + tile_off
+                                      : nullptr;
+    auto step = [&](int n, const Regs& R) {
+        // gate scan (lane i = in-chunk token i; absent tokens have gamma 1, beta 0)
+        const bool in = lane < R.valid;
+        const float gam = in ? R.gam : 1.0f;
+        const float lg = wave_scan_add(gam > 0.0f ? logf(gam) : 0.0f);
+        const int zl = wave_scan_max(gam > 0.0f ? -1 : lane);
+        const float lgE = lane_value(lg, C - 1);
+        const int zlE = lane_value(zl, C - 1);
+        const float wl = in ? R.bet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
+        const float D = zlE >= 0 ? 0.0f : expf(lgE);
+
+        if (STORE) {
+            float* dst = chunk_dst + int64_t(n) * nX * DK;
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) dst[ii * DK] = acc[ii];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float w = __shfl(wl, tq + 16 * r);
+            *reinterpret_cast<f32x4*>(wx + (tq + 16 * r) * 16 + q4) = R.x[r];
+            *reinterpret_cast<f32x4*>(wy + (tq + 16 * r) * 16 + q4) = w * R.y[r];
+        }
+        // the wave's own LDS traffic completes in order: its reads below see these writes
+        __builtin_amdgcn_wave_barrier();
+        acc *= D;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int e = (4 * j + g) * 16 + m;
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wx[e], wy[e], acc, 0, 0, 0);
+        }
+        __builtin_amdgcn_wave_barrier();
+    };
+
+    // A ring of kF32Depth (= 4) chunks in flight, in named registers.  Every pass of
+    // the main loop issues the same loads (past the end: the last chunk again, in
+    // bounds and unused), so the count of loads in flight is the same at every
+    // point of every pass and each wait covers exactly the chunk it needs.
+    static_assert(kF32Depth == 4, "the ring below holds four chunks");
+    Regs R0, R1, R2, R3;
+    const int nc = s.n_chunks;
+    if (nc > 0) {
+        load(0, R0);
+        load(min(1, nc - 1), R1);
+        load(min(2, nc - 1), R2);
+        load(min(3, nc - 1), R3);
+    }
+    // The scheduling barriers keep each chunk's work in its slot: hoisted to the top
+    // of the pass, the later chunks' gate scans would wait for their loads there.
+    int n0 = 0;
+    for (; n0 + kF32Depth <= nc; n0 += kF32Depth) {
+        step(n0, R0);
+        load(min(n0 + 4, nc - 1), R0);
+        __builtin_amdgcn_sched_barrier(0);
+        step(n0 + 1, R1);
+        load(min(n0 + 5, nc - 1), R1);
+        __builtin_amdgcn_sched_barrier(0);
+        step(n0 + 2, R2);
+        load(min(n0 + 6, nc - 1), R2);
+        __builtin_amdgcn_sched_barrier(0);
+        step(n0 + 3, R3);
+        load(min(n0 + 7, nc - 1), R3);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (n0 < nc) step(n0, R0);
+    if (n0 + 1 < nc) step(n0 + 1, R1);
+    if (n0 + 2 < nc) step(n0 + 2, R2);
+    float* fin = isG ? a.final_G : a.final_H;
+    if (fin) {
+        float* dst = fin + bh * nX * int64_t(DK) + tile_off;
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) dst[ii * DK] = acc[ii];
+    }
+}
+
 // Wide variant (bf16 k and v, chunk 64, d_k and d_v in {64, 128}), used for the
 // bf16 fragment chunk states and for the states-only call.  One workgroup owns a
 // whole part of the state of one (batch, head) sequence -- part 0 is H (d_k x d_k),
@@ -657,6 +800,13 @@ hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream)
     if (chunk_state_frag_supported(a.s) && (a.frag || !a.store_chunks)) {
         if (a.s.d_k == 64) return a.s.d_v == 64 ? launch_wide<64, 64>(a, stream) : launch_wide<64, 128>(a, stream);
         return a.s.d_v == 64 ? launch_wide<128, 64>(a, stream) : launch_wide<128, 128>(a, stream);
+    }
+    if (!a.s.bf16 && a.s.chunk == 64) {
+        const unsigned blocks = unsigned(bh * ((a.s.d_k + a.s.d_v) / 16) * (a.s.d_k / 64));
+        auto kern = a.s.d_k == 64 ? (a.store_chunks ? chunk_state_f32_kernel<64, true> : chunk_state_f32_kernel<64, false>)
+                                  : (a.store_chunks ? chunk_state_f32_kernel<128, true> : chunk_state_f32_kernel<128, false>);
+        hipLaunchKernelGGL(kern, dim3(blocks), dim3(kThreads), 0, stream, a);
+        return hipGetLastError();
     }
     if (a.s.bf16 && a.s.chunk == 64) {
         const unsigned blocks = unsigned(bh * ((a.s.d_k + a.s.d_v) / 64) * (a.s.d_k / 32));

@@ -206,6 +206,28 @@ def test_prefill_states_match_oracle():
     assert rel_l2(G.cpu().numpy(), ref["G"]) <= 1e-5
 
 
+@pytest.mark.parametrize("dk,dv", [(64, 64), (128, 64), (64, 128), (128, 128)])
+def test_f32_state_scan_ring_tails(dk, dv):
+    """fp32 scan (chunk 64): sequences of 1, 3, 4, 5 and 9 chunks, most with a ragged
+    last chunk, cover the scan's four-chunk load ring in full passes and with every
+    tail length; a zero gate on a chunk's first token and one inside a chunk reset
+    memory exactly.  The states-only call's final states and the forward's output
+    (which reads every chunk state) and final states against the oracle."""
+    for T in (37, 3 * 64, 4 * 64, 4 * 64 + 1, 8 * 64 + 50):
+        x = W.forward_inputs(2, 2, T, dk, dv, "f32", 3.0, seed=T + dk + dv)
+        x["gamma"][0, 1, T // 2] = 0.0
+        if T > 128:
+            x["gamma"][1, 0, 128] = 0.0
+        d = to_device(x, "f32")
+        H, G = L.prefill_states(d["k"], d["v"], d["gamma"], d["beta"])
+        got = _gpu_forward(x, "f32", 6, 64, precision=L.MESA_PREC_F32, want_states=True)
+        ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 6, want_states=True)
+        e = [rel_l2(H.cpu().numpy(), ref["H"]), rel_l2(G.cpu().numpy(), ref["G"]),
+             rel_l2(got["H"], ref["H"]), rel_l2(got["G"], ref["G"]), rel_l2(got["out"], ref["out"])]
+        _say("f32 scan d_k=%d d_v=%d T=%d: H %.2e G %.2e (forward H %.2e G %.2e out %.2e)" % (dk, dv, T, *e))
+        assert max(e[:4]) <= 2e-6 and e[4] <= TOL_F32, T
+
+
 @pytest.mark.parametrize("dk,dv", [(128, 128), (64, 128)])
 def test_segmented_state_scan_matches_oracle(dk, dv):
     """Two sequences of 36 chunks (the last ragged): the bf16 scan runs in 4 segments
