@@ -455,18 +455,26 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         }
         const f32x4 zero4 = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
         int qsh = 0;  // log2 of the power-of-two scale of q_j (below)
+        // CG vectors; the search direction alternates between p and pa (below)
+        f32x4 x[MT], r[MT], p[MT], pa[MT], w[MT];
 
         // W = A_j vec for this wave's 16 columns (A_j = H_t + Lambda of token j), from the
         // bf16 operand vb of vec: W = zs_j (B'_w vec) + K_w^T S' + Lambda vec, the column
         // scale applied to the state products' accumulators.  The state products run
         // feature-step-major, so the first ones need only vb[0].
-        auto matvec = [&](const bf16x8 (&vb)[KS], f32x4 (&w)[MT]) {
+        // Inside the CG loop the previous iteration's x update (x += alpha p, deferred: it is
+        // off the loop's dependency chain) runs between the state products, two tiles of x
+        // per feature step, where the matrix cores leave the vector unit idle.
+        auto matvec_x = [&](const bf16x8 (&vb)[KS], f32x4 (&w)[MT], const f32x4 (&pd)[MT], float ad) {
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) w[mt] = zero4;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
+            for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) w[mt] = mfma16(hf[mt][ks], vb[ks], w[mt]);
+#pragma unroll
+                for (int mt = ks * MT / KS; mt < (ks + 1) * MT / KS; ++mt) x[mt] += ad * pd[mt];
+            }
             f32x4 sacc = zero4;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) sacc = mfma16(kf2[ks], vb[ks], sacc);
@@ -488,7 +496,6 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         // into [1/4, 2): CG iterates are homogeneous in q and a power-of-two scale is exact, so
         // this changes no rounding, and it keeps the CG scalars in the range where the
         // hardware reciprocal is exact to an ulp.
-        f32x4 x[MT], r[MT], p[MT], w[MT];
         {
             const bf16x8 zwb = pack8(zw, zero4);
             f32x4 qf[MT];
@@ -526,7 +533,9 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
             bf16x8 xb[KS];
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) xb[ks] = pack8(x[2 * ks], x[2 * ks + 1]);
-            matvec(xb, w);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) pa[mt] = zero4;
+            matvec_x(xb, w, pa, 0.0f);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) r[mt] = qf[mt] - w[mt];
         }
@@ -564,43 +573,72 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         // or falls below the smallest normal number (relative to |q|^2, which the scaling
         // above keeps in [1/4, 2)); it stops without an update when p^T A p is not a
         // positive normal number (alpha would need the reciprocal of a subnormal).
-        for (int it = 0; it < a.n_cg; ++it) {
-            if (!__any(active)) break;
+        // Iteration k reads the direction from pc and writes the next one into pn, the
+        // buffer holding the previous direction: its deferred x update has run by then
+        // (inside the matrix-vector product).  Two iterations per pass swap the roles,
+        // so no vector is copied.
+        float alpha_d = 0.0f;  // the pending x update: x += alpha_d * (previous direction)
+        auto cg_step = [&](f32x4 (&pc)[MT], f32x4 (&pn)[MT]) {
             if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
             {
                 bf16x8 pb[KS];
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) pb[ks] = pack8(p[2 * ks], p[2 * ks + 1]);
-                matvec(pb, w);
+                for (int ks = 0; ks < KS; ++ks) pb[ks] = pack8(pc[2 * ks], pc[2 * ks + 1]);
+                matvec_x(pb, w, pn, alpha_d);
             }
             // column dot products in four independent partial sums (one per element of a
             // tile), so consecutive fused multiply-adds do not wait on each other
             f32x4 acc = zero4;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) acc += p[mt] * w[mt];
+            for (int mt = 0; mt < MT; ++mt) acc += pc[mt] * w[mt];
             const float pw = col_sum((acc[0] + acc[1]) + (acc[2] + acc[3]));
             const bool act1 = active && pw >= kMinNormal;
             steps += act1 ? 1 : 0;
-            if (act1) {
-                const float alpha = delta * __builtin_amdgcn_rcpf(pw);
+            // Branch-free: a stopped column takes alpha = 0 and beta = 0.  Its r and x stay
+            // as they are, and its direction becomes r (finite), which only ever meets
+            // alpha = 0 again: a column never restarts.
+            const float alpha = act1 ? delta * __builtin_amdgcn_rcpf(pw) : 0.0f;
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    r[mt] -= alpha * w[mt];
-                    x[mt] += alpha * p[mt];
-                }
-            }
+            for (int mt = 0; mt < MT; ++mt) r[mt] -= alpha * w[mt];
+            alpha_d = alpha;
             acc = zero4;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) acc += r[mt] * r[mt];
             const float dn = col_sum((acc[0] + acc[1]) + (acc[2] + acc[3]));
             const bool act2 = act1 && dn >= kMinNormal && dn > thr;
-            if (act2) {
-                const float bcg = dn * __builtin_amdgcn_rcpf(delta);
+            const float bcg = act2 ? dn * __builtin_amdgcn_rcpf(delta) : 0.0f;
+            // pn = r + bcg pc into pn's own registers: one three-address fma per element (the
+            // compiler's two-address form would first copy r, which stays live)
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) p[mt] = r[mt] + bcg * p[mt];
-            }
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) asm("v_fma_f32 %0, %1, %2, %3" : "=v"(pn[mt][e]) : "v"(bcg), "v"(pc[mt][e]), "v"(r[mt][e]));
             delta = act2 ? dn : delta;
             active = act2;
+        };
+        // Pairs of iterations (an odd count ends with one more); the wave leaves as soon
+        // as every column has stopped.
+        int it = 0;
+        bool last_pa = false;  // the last iteration run read its direction from pa
+        for (; it + 2 <= a.n_cg; it += 2) {
+            if (!__any(active)) break;
+            cg_step(p, pa);
+            last_pa = false;
+            if (!__any(active)) break;
+            cg_step(pa, p);
+            last_pa = true;
+        }
+        if (it + 2 > a.n_cg && it < a.n_cg && __any(active)) {
+            cg_step(p, pa);
+            last_pa = false;
+        }
+        // the last iteration's x update
+        if (last_pa) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) x[mt] += alpha_d * pa[mt];
+        } else {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) x[mt] += alpha_d * p[mt];
         }
         {
             const float us = __builtin_ldexpf(1.0f, qsh);  // undoes the power-of-two scale of q
