@@ -167,6 +167,66 @@ __device__ __forceinline__ void load_tile(float* dst, const bf16_t* src, int64_t
     }
 }
 
+// The same tile in two steps, so its global loads can be in flight while the previous
+// phase computes: fetch issues the 16-byte loads into registers, put (after the LDS
+// tile is free) zeroes rows past `valid` and stores it.
+template <int D, typename T>
+struct Tile;
+template <int D>
+struct Tile<D, float> {
+    static constexpr int V = kC * D / 4 / kThreads;
+    float4 x[V];
+    __device__ __forceinline__ void fetch(const float* src, int64_t tok0, int valid)
+    {
+#pragma unroll
+        for (int m = 0; m < V; ++m) {
+            const int e = threadIdx.x + kThreads * m, i = e / (D / 4), f = 4 * (e % (D / 4));
+            x[m] = *reinterpret_cast<const float4*>(src + (tok0 + min(i, valid - 1)) * D + f);
+        }
+    }
+    __device__ __forceinline__ void put(float* dst, int valid) const
+    {
+#pragma unroll
+        for (int m = 0; m < V; ++m) {
+            const int e = threadIdx.x + kThreads * m, i = e / (D / 4), f = 4 * (e % (D / 4));
+            const bool ok = i < valid;
+            float* o = dst + i * kLdT + f;
+            o[0] = ok ? x[m].x : 0.0f;
+            o[1] = ok ? x[m].y : 0.0f;
+            o[2] = ok ? x[m].z : 0.0f;
+            o[3] = ok ? x[m].w : 0.0f;
+        }
+    }
+};
+template <int D>
+struct Tile<D, bf16_t> {
+    static constexpr int V = kC * D / 8 / kThreads;
+    uint4 x[V];
+    __device__ __forceinline__ void fetch(const bf16_t* src, int64_t tok0, int valid)
+    {
+#pragma unroll
+        for (int m = 0; m < V; ++m) {
+            const int e = threadIdx.x + kThreads * m, i = e / (D / 8), f = 8 * (e % (D / 8));
+            x[m] = *reinterpret_cast<const uint4*>(src + (tok0 + min(i, valid - 1)) * D + f);
+        }
+    }
+    __device__ __forceinline__ void put(float* dst, int valid) const
+    {
+#pragma unroll
+        for (int m = 0; m < V; ++m) {
+            const int e = threadIdx.x + kThreads * m, i = e / (D / 8), f = 8 * (e % (D / 8));
+            const bool ok = i < valid;
+            const uint32_t w4[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
+            float* o = dst + i * kLdT + f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                o[2 * q] = ok ? __uint_as_float(w4[q] << 16) : 0.0f;
+                o[2 * q + 1] = ok ? __uint_as_float(w4[q] & 0xffff0000u) : 0.0f;
+            }
+        }
+    }
+};
+
 // ---------------------------------------------------------------- u = G^T e
 // u_t = zeta_{t,c-1} G_c^T e_t + sum_{i<=t} zeta_{t,i} beta_i (v_i . e_t) k_i for
 // the tokens of one chunk (the GLA form of App. D with the roles of k and v swapped).
@@ -400,6 +460,15 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     __shared__ float sRed[kThreads / kWave][kC];  // per-wave partial sums per token
     __shared__ float sF;
 
+    // Token tiles in registers: each phase's tiles are fetched while the phase before it
+    // computes, then put into sT0 / sT1 once those are free.
+    Tile<DK, Tin> tk;
+    Tile<DV, Tin> tv;
+    Tile<DK, float> tq, te;
+    Tile<DV, float> td;
+    tk.fetch(kp, tok0, valid);
+    tq.fetch(a.qstar, tok0, valid);
+
     // ---- gates: Z, zeta_{E,s}, phi_s = zeta_{s-1,c-1}
     if (tid < kWave) chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
     __syncthreads();
@@ -423,40 +492,37 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
             for (int r = 0; r < 4; ++r) dst[(16 * w + 4 * g + r) * kLdC + 16 * tt + ln] = gm[r];
         }
     };
-    load_tile<DK>(sT0, kp, tok0, valid);
-    load_tile<DK>(sT1, a.qstar, tok0, valid);
+    tk.put(sT0, valid);
+    tq.put(sT1, valid);
+    te.fetch(a.estar, tok0, valid);
     __syncthreads();
     gram(sM0, std::integral_constant<int, DK>{});  // KQ[p][t] = k_p . q*_t
     __syncthreads();
-    load_tile<DK>(sT1, a.estar, tok0, valid);
+    te.put(sT1, valid);
+    tv.fetch(vp, tok0, valid);
+    td.fetch(a.dout, tok0, valid);
     __syncthreads();
     gram(sM2, std::integral_constant<int, DK>{});  // KE[p][t] = k_p . e*_t
     __syncthreads();
-    load_tile<DV>(sT0, vp, tok0, valid);
-    load_tile<DV>(sT1, a.dout, tok0, valid);
+    tv.put(sT0, valid);
+    td.put(sT1, valid);
+    tk.fetch(kp, tok0, valid);
     __syncthreads();
     gram(sM1, std::integral_constant<int, DV>{});  // VE[p][t] = v_p . e_t
     __syncthreads();
 
-    // ---- C x C combinations: DVK = VE - KE; Qm = beta_p DVK KQ; the intra part of
-    // dbeta_s = sum_t Z[s][t] KQ[s][t] DVK[s][t]; then M1 = Z ⊙ KQ, M2 = Z ⊙ DVK
-    for (int e = tid; e < kC * kC; e += kThreads) {
-        const int p = e / kC, t = e % kC, o = p * kLdC + t;
+    // ---- C x C combinations, one row p per wave pass (lane = t): DVK = VE - KE;
+    // Qm = beta_p DVK KQ; the intra part of dbeta_p = sum_t Z[p][t] KQ[p][t] DVK[p][t]
+    // (a wave sum); M1 = Z ⊙ KQ, M2 = Z ⊙ DVK
+    for (int p = w; p < kC; p += kThreads / kWave) {
+        const int o = p * kLdC + lane;
+        const float kq = sM0[o], z = sZ[o];
         const float dvk = sM1[o] - sM2[o];
-        sM1[o] = dvk;
-        sM2[o] = sBeta[p] * dvk * sM0[o];
-    }
-    __syncthreads();
-    if (tid < kC) {
-        float acc = 0.0f;
-        for (int t = 0; t < kC; ++t) acc += sZ[tid * kLdC + t] * sM0[tid * kLdC + t] * sM1[tid * kLdC + t];
-        sTok[0][tid] = acc;
-    }
-    __syncthreads();
-    for (int e = tid; e < kC * kC; e += kThreads) {
-        const int p = e / kC, t = e % kC, o = p * kLdC + t;
-        sM0[o] *= sZ[o];
-        sM1[o] *= sZ[o];
+        sM2[o] = sBeta[p] * dvk * kq;
+        sM0[o] = z * kq;
+        sM1[o] = z * dvk;
+        const float db = wave_sum(z * kq * dvk);
+        if (lane == 0) sTok[0][p] = db;
     }
     // In the token-by-feature phases below wave w owns the 16-column tiles
     // w * TPW .. of the feature dimension for all 64 tokens (4 token tiles), so it
@@ -480,18 +546,23 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     // ---- dv_s = beta_s (sum_t M1[s][t] e_t + zeta_E[s] A^G k_s)   (sT1 holds e_t)
     {
         constexpr int TPW = DV / 16 / 4;
+        // the d x d operands of each column tile are loaded one tile ahead (the first
+        // before the phase's barriers)
+        float bv[2][DK / 4];
+        load_b<DK, 1, DK>(AG + 16 * (w * TPW) * DK, bv[0]);  // B(k, n) = A^G[16 at + n][k]
         __syncthreads();
-        load_tile<DK>(sT0, kp, tok0, valid);
+        tk.put(sT0, valid);
+        tq.fetch(a.qstar, tok0, valid);
+        te.fetch(a.estar, tok0, valid);
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
             const int at = w * TPW + j;
-            float bv[DK / 4];
-            load_b<DK, 1, DK>(AG + 16 * at * DK, bv);  // B(k, n) = A^G[16 at + n][k]
+            if (j + 1 < TPW) load_b<DK, 1, DK>(AG + 16 * (at + 1) * DK, bv[(j + 1) % 2]);
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
                 const f32x4 in = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * at, kZero4);
-                const f32x4 ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv, kZero4);  // (K A^G^T)[s][a]
+                const f32x4 ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv[j % 2], kZero4);  // (K A^G^T)[s][a]
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int t = tok(st, r);
@@ -506,9 +577,14 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     {
         constexpr int TPW = DK / 16 / 4;
         f32x4 in[TPW][4];
+        float bag[2][DV / 4], bsh[2][DK / 4];  // the inter part's operands, one tile ahead
+        load_b<DV, DK, 1>(AG + 16 * (w * TPW), bag[0]);  // B(k, n) = A^G[k][16 bt + n]
+        load_b<DK, DK, 1>(SH + 16 * (w * TPW), bsh[0]);  // B(k, n) = S^H[k][16 bt + n]
         __syncthreads();
-        load_tile<DK>(sT0, a.qstar, tok0, valid);
-        load_tile<DK>(sT1, a.estar, tok0, valid);
+        tq.put(sT0, valid);
+        te.put(sT1, valid);
+        tk.fetch(kp, tok0, valid);
+        tv.fetch(vp, tok0, valid);
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < TPW; ++j)
@@ -520,20 +596,23 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
                 in[j][st] = pq - pe;
             }
         __syncthreads();
-        load_tile<DK>(sT0, kp, tok0, valid);
-        load_tile<DV>(sT1, vp, tok0, valid);
+        tk.put(sT0, valid);
+        tv.put(sT1, valid);
+        tq.fetch(a.qstar, tok0, valid);
+        td.fetch(a.dout, tok0, valid);
         __syncthreads();
         float pa[4][4] = {}, pk[4][4] = {};
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
             const int bt = w * TPW + j;
-            float bag[DV / 4], bsh[DK / 4];
-            load_b<DV, DK, 1>(AG + 16 * bt, bag);  // B(k, n) = A^G[k][16 bt + n]
-            load_b<DK, DK, 1>(SH + 16 * bt, bsh);  // B(k, n) = S^H[k][16 bt + n]
+            if (j + 1 < TPW) {
+                load_b<DV, DK, 1>(AG + 16 * (bt + 1), bag[(j + 1) % 2]);
+                load_b<DK, DK, 1>(SH + 16 * (bt + 1), bsh[(j + 1) % 2]);
+            }
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
-                const f32x4 ag = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bag, kZero4);
-                const f32x4 sh = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bsh, kZero4);
+                const f32x4 ag = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bag[j % 2], kZero4);
+                const f32x4 sh = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bsh[j % 2], kZero4);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int t = tok(st, r), b = 16 * bt + ln;
@@ -552,34 +631,39 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     //      and dLambda of the chunk
     {
         constexpr int TPW = DK / 16 / 4;
+        // G_c's and then H_c's column tiles, each loaded one tile ahead
+        float bg[2][DV / 4], bh_[2][DK / 4];
+        load_b<DV, DK, 1>(Gc + 16 * (w * TPW), bg[0]);  // B(k, n) = G_c[k][16 bt + n]
         __syncthreads();
-        load_tile<DK>(sT0, a.qstar, tok0, valid);
-        load_tile<DV>(sT1, a.dout, tok0, valid);
+        tq.put(sT0, valid);
+        td.put(sT1, valid);
+        te.fetch(a.estar, tok0, valid);
         __syncthreads();
         float pg[4][4] = {}, ph[4][4] = {};
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
             const int bt = w * TPW + j;
-            float bg[DV / 4];
-            load_b<DV, DK, 1>(Gc + 16 * bt, bg);  // B(k, n) = G_c[k][16 bt + n]
+            if (j + 1 < TPW)
+                load_b<DV, DK, 1>(Gc + 16 * (bt + 1), bg[(j + 1) % 2]);
+            else
+                load_b<DK, DK, 1>(Hc + 16 * (w * TPW), bh_[0]);  // B(k, n) = H_c[k][16 bt + n]
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
-                const f32x4 eg = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bg, kZero4);
+                const f32x4 eg = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bg[j % 2], kZero4);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) pg[st][r] += eg[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
             }
         }
         reduce_tokens(pg, sTok[3]);
-        load_tile<DK>(sT1, a.estar, tok0, valid);
+        te.put(sT1, valid);
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
             const int bt = w * TPW + j;
-            float bh_[DK / 4];
-            load_b<DK, DK, 1>(Hc + 16 * bt, bh_);  // B(k, n) = H_c[k][16 bt + n]
+            if (j + 1 < TPW) load_b<DK, DK, 1>(Hc + 16 * (bt + 1), bh_[(j + 1) % 2]);
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
-                const f32x4 eh = mma16_b<DK, kLdT, 1>(sT1 + 16 * st * kLdT, bh_, kZero4);
+                const f32x4 eh = mma16_b<DK, kLdT, 1>(sT1 + 16 * st * kLdT, bh_[j % 2], kZero4);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) ph[st][r] += eh[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
             }
@@ -608,12 +692,24 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         }
         fr = wave_sum(fr);
         if (lane == 0) sPart[w] = fr;
-        if (tid < DK) {
+        // dLambda of the chunk, -sum_t q*_t e*_t per feature: the tokens split into
+        // kThreads / DK slices, one per thread of a feature, partial sums through sRed
+        {
+            constexpr int NP = kThreads / DK;
+            const int f = tid % DK, sl = tid / DK;
             float acc = 0.0f;
-            for (int t = 0; t < kC; ++t) acc += sT0[t * kLdT + tid] * sT1[t * kLdT + tid];
-            a.dlam_part[mat * DK + tid] = -acc;
+#pragma unroll 8
+            for (int t = sl * (kC / NP); t < (sl + 1) * (kC / NP); ++t) acc += sT0[t * kLdT + f] * sT1[t * kLdT + f];
+            (&sRed[0][0])[tid] = acc;
         }
         __syncthreads();
+        if (tid < DK) {
+            constexpr int NP = kThreads / DK;
+            float acc = 0.0f;
+#pragma unroll
+            for (int sl = 0; sl < NP; ++sl) acc += (&sRed[0][0])[sl * DK + tid];
+            a.dlam_part[mat * DK + tid] = -acc;
+        }
         if (tid == 0) {
             float t = 0.0f;
             for (int u = 0; u < kThreads / kWave; ++u) t += sPart[u];
@@ -632,22 +728,30 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         __syncthreads();
     }
 
-    // ---- assemble dgamma_s and dbeta_s (one thread per token)
-    if (tid < kC) {
-        const int si = tid;
-        const float ze = sZe[si], phi = sPhi[si];
-        float t2 = 0.0f, t3 = 0.0f, t4 = 0.0f;
-        for (int t = si; t < kC; ++t) t2 += sZ[si * kLdC + t] * (sTok[3][t] - sTok[4][t]);
-        for (int p = 0; p < si; ++p) {
-            const float z = sZ[p * kLdC + si - 1];  // zeta_{s-1,p}
-            t3 += z * sBeta[p] * (sTok[1][p] + sTok[2][p]);
-            t4 += z * sM0[p * kLdC + si];
-        }
-        const float dg = ze * phi * sF + phi * t2 + ze * t3 + t4;
-        const float db = sTok[0][si] + ze * (sTok[1][si] + sTok[2][si]);
-        if (si < valid) {
-            a.dgamma[tok0 + si] = dg;
-            a.dbeta[tok0 + si] = db;
+    // ---- assemble dgamma_s and dbeta_s: wave w takes tokens s = 16w.., its lanes the
+    // summation index q of the three sums (wave sums), the masks coming from Z:
+    //   t2 = sum_{t >= s} zeta_{t,s} (g_t - h_t)                  (Z[s][q], 0 for q < s)
+    //   t3 = sum_{p < s} zeta_{s-1,p} beta_p (v^T A^G k + k^T A^H k)_p,
+    //   t4 = sum_{p < s} zeta_{s-1,p} W[p][s]                     (Z[q][s-1], 0 for q >= s)
+    {
+        const float gh = sTok[3][lane] - sTok[4][lane];
+        const float bk = sBeta[lane] * (sTok[1][lane] + sTok[2][lane]);
+#pragma unroll 4
+        for (int i = 0; i < 16; ++i) {
+            const int si = 16 * w + i;
+            const float v2 = sZ[si * kLdC + lane] * gh;
+            float v3 = 0.0f, v4 = 0.0f;
+            if (si > 0) {
+                const float z = sZ[lane * kLdC + si - 1];  // zeta_{s-1,q}
+                v3 = z * bk;
+                v4 = z * sM0[lane * kLdC + si];
+            }
+            const float t2 = wave_sum(v2), t3 = wave_sum(v3), t4 = wave_sum(v4);
+            if (lane == 0 && si < valid) {
+                const float ze = sZe[si], phi = sPhi[si];
+                a.dgamma[tok0 + si] = ze * phi * sF + phi * t2 + ze * t3 + t4;
+                a.dbeta[tok0 + si] = sTok[0][si] + ze * (sTok[1][si] + sTok[2][si]);
+            }
         }
     }
 }
