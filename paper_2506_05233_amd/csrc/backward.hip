@@ -230,7 +230,13 @@ struct Tile<D, bf16_t> {
 // ---------------------------------------------------------------- u = G^T e
 // u_t = zeta_{t,c-1} G_c^T e_t + sum_{i<=t} zeta_{t,i} beta_i (v_i . e_t) k_i for
 // the tokens of one chunk (the GLA form of App. D with the roles of k and v swapped).
-// Wave w owns tokens 16w .. 16w+15.
+// Wave w owns tokens t = 16w .. 16w+15, as the columns of transposed products:
+// S^T = V E^T (rows i, the gate weights applied in place) stays in the result
+// registers and is the B operand of K^T S^T (in the product for element r of row
+// tile it, k-slot g stands for token i = 16 it + 4 g + r, exactly the element lane
+// (g, n) holds), and u^T = zeta ⊙ (G_c^T E^T) + K^T S^T comes out as [feature][token]
+// tiles, four consecutive features of one token per lane.  No C x C matrix goes
+// through LDS, so two workgroups share a compute unit.
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
 {
@@ -243,48 +249,74 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     const int64_t tok0 = bh * s.seq_len + t0;
     const int tid = threadIdx.x;
     const int w = tid / kWave, lane = tid % kWave, g = lane / 16, ln = lane % 16;
+    const int t = 16 * w + ln;  // this lane's token (column of the transposed products)
 
     __shared__ float sE[kC * kLdT];   // e_t [t][a]
     __shared__ float sX[kC * kLdT];   // v_i, then k_i
-    __shared__ float sS[kC * kLdC];   // beta_i zeta_{t,i} (v_i . e_t) as [t][i]
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
 
     load_tile<DV>(sX, static_cast<const Tin*>(a.v), tok0, valid);
     load_tile<DV>(sE, a.dout, tok0, valid);
     if (tid < kWave) chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
+    Tile<DK, Tin> tk;  // the keys, in flight during the value products
+    tk.fetch(static_cast<const Tin*>(a.k), tok0, valid);
     __syncthreads();
-    // S rows 16w.. (tokens t), columns i: (e_t . v_i) weighted
+    // S^T[i][t] = beta_i zeta_{t,i} (v_i . e_t) for i <= t (0 otherwise and past the end)
+    f32x4 sT[kC / 16];
 #pragma unroll
     for (int it = 0; it < kC / 16; ++it) {
-        const f32x4 ev = mma16<DV, kLdT, 1, 1, kLdT>(sE + 16 * w * kLdT, sX + 16 * it * kLdT, kZero4);
+        const f32x4 ve = mma16<DV, kLdT, 1, 1, kLdT>(sX + 16 * it * kLdT, sE + 16 * w * kLdT, kZero4);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int t = 16 * w + 4 * g + r, i = 16 * it + ln;
-            sS[t * kLdC + i] = (i <= t && i < valid) ? a.beta[tok0 + i] * decay_between(sLg, sZl, i, t) * ev[r] : 0.0f;
+            const int i = 16 * it + 4 * g + r;
+            sT[it][r] = (i <= t && i < valid) ? a.beta[tok0 + i] * decay_between(sLg, sZl, i, t) * ve[r] : 0.0f;
         }
     }
+    // E^T as the B operand of every G_c^T E^T tile: B(k = a, n = t) = e_t[a]
+    float eb[DV / 4];
+#pragma unroll
+    for (int i = 0; i < DV / 4; ++i) eb[i] = sE[t * kLdT + 4 * i + g];
     __syncthreads();
-    load_tile<DK>(sX, static_cast<const Tin*>(a.k), tok0, valid);
+    tk.put(sX, valid);
     __syncthreads();
+    const float zs = decay_from_start(sLg, sZl, t);
+    // A operand of G_c^T E^T for feature tile bt: A(m = b, k = a) = G_c[a][16 bt + m], one
+    // tile ahead
     const float* Gc = a.Gs + (bh * nc + n) * int64_t(DV) * DK;
-    float zs[4];
+    auto load_ga = [&](int bt, float (&ga)[DV / 4]) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) zs[r] = decay_from_start(sLg, sZl, 16 * w + 4 * g + r);
-    // (E G_c)[t][b] = sum_a e_t[a] G_c[a][b];  (S K)[t][b] = sum_i S[t][i] k_i[b]
-    rows_times_matrix<DV, DK / 16, kLdT, DK, 1>(sE + 16 * w * kLdT, Gc, [&](int bt, const f32x4& eg) {
-        const f32x4 sk = mma16<kC, kLdC, 1, kLdT, 1>(sS + 16 * w * kLdC, sX + 16 * bt, kZero4);
+        for (int i = 0; i < DV / 4; ++i) ga[i] = Gc[(4 * i + g) * DK + 16 * bt + ln];
+    };
+    float ga[2][DV / 4];
+    load_ga(0, ga[0]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int t = 16 * w + 4 * g + r, b = 16 * bt + ln;
-            if (t >= valid) continue;
-            const float u = zs[r] * eg[r] + sk[r];
+    for (int bt = 0; bt < DK / 16; ++bt) {
+        if (bt + 1 < DK / 16) load_ga(bt + 1, ga[(bt + 1) % 2]);
+        f32x4 eg = kZero4;
+#pragma unroll
+        for (int i = 0; i < DV / 4; ++i) eg = __builtin_amdgcn_mfma_f32_16x16x4f32(ga[bt % 2][i], eb[i], eg, 0, 0, 0);
+        // K^T S^T: A(m = b, k = i) = k_i[16 bt + m] with i = 16 it + 4 g + r
+        float ka[kC / 4];
+#pragma unroll
+        for (int it = 0; it < kC / 16; ++it)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) ka[4 * it + r] = sX[(16 * it + 4 * g + r) * kLdT + 16 * bt + ln];
+        f32x4 sk = kZero4;
+#pragma unroll
+        for (int it = 0; it < kC / 16; ++it)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sk = __builtin_amdgcn_mfma_f32_16x16x4f32(ka[4 * it + r], sT[it][r], sk, 0, 0, 0);
+        // lane (g, n): u_t[16 bt + 4g + r], r = 0..3
+        if (t < valid) {
+            const f32x4 u = zs * eg + sk;
+            const int64_t o = (tok0 + t) * DK + 16 * bt + 4 * g;
             if (a.u16)
-                a.u16[(tok0 + t) * DK + b] = uint16_t(pack_bf16x2(u, 0.0f) & 0xffffu);  // round to nearest even
+                *reinterpret_cast<uint2*>(a.u16 + o) = make_uint2(pack_bf16x2(u[0], u[1]), pack_bf16x2(u[2], u[3]));  // nearest even
             else
-                a.u[(tok0 + t) * DK + b] = u;
+                *reinterpret_cast<float4*>(a.u + o) = make_float4(u[0], u[1], u[2], u[3]);
         }
-    });
+    }
 }
 
 // ---------------------------------------------------------------- adjoint scan
@@ -311,7 +343,7 @@ struct AdjSeg {
 };
 
 template <int DK, int DV>
-__global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a, AdjSeg sg)
+__global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, AdjSeg sg)
 {
     constexpr int NCT = DK / 16;                  // column tiles
     constexpr int NTH = DK / kAdjRows;            // row slices of S^H
@@ -333,10 +365,11 @@ __global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a, AdjSeg
     auto seg_tile = [&](int t) { return sg.tot + (bh * sg.total + t) * kSegElems + (isG ? DK * DK : 0) +
                                         int64_t(r0 + 16 * w + 4 * g) * DK + ln; };
 
-    __shared__ float sX[kC * kLdX];   // q*_j [j][c]
-    __shared__ float sY[kC * kLdX];   // e*_j [j][c] (S^H only)
-    __shared__ float sYr[kC * kLdR];  // zeta_{j,c-1} e_j (A^G) or -zeta e*_j (S^H), rows r0.. [j][r]
-    __shared__ float sXr[kC * kLdR];  // -zeta_{j,c-1} q*_j, rows r0.. [j][r] (S^H only)
+    // One pass per rank-64 product: the token tile goes to sX, the weighted row slice to
+    // sYr.  A^G has one pass per chunk (q*, zeta e), S^H two (q*, -zeta e*) and (e*, -zeta q*).
+    // The inputs of the next pass are fetched into registers while this one multiplies.
+    __shared__ float sX[kC * kLdX];   // token tile [j][c]
+    __shared__ float sYr[kC * kLdR];  // weighted row slice [j][r] (rows r0..)
     __shared__ float sW[kC];
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
@@ -356,8 +389,63 @@ __global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a, AdjSeg
             c *= sg.dec[bh * sg.total + t];
         }
     }
+    constexpr int VT = kC * DK / 4 / kThreads;        // tile: 16-byte pieces per thread
+    constexpr int VR = kC * kAdjRows / 4 / kThreads;  // row slice: 16-byte pieces per thread
+    struct PassRegs {
+        float4 t[VT], r[VR];
+    };
+    // pass p of chunk n: tokens past the end re-read the last valid one (zeroed in put)
+    auto fetch = [&](int n, int p, PassRegs& R) {
+        const int64_t t0 = int64_t(n) * kC;
+        const int valid = int(min<int64_t>(kC, s.seq_len - t0));
+        const int64_t tok0 = bh * s.seq_len + t0;
+        const float* ts = (isG || p == 0) ? a.qstar : a.estar;
+        const float* rs = isG ? a.dout : (p == 0 ? a.estar : a.qstar);
+        const int rd = isG ? DV : DK;
+#pragma unroll
+        for (int m = 0; m < VT; ++m) {
+            const int e = tid + kThreads * m, j = e / (DK / 4), f = 4 * (e % (DK / 4));
+            R.t[m] = *reinterpret_cast<const float4*>(ts + (tok0 + min(j, valid - 1)) * DK + f);
+        }
+#pragma unroll
+        for (int m = 0; m < VR; ++m) {
+            const int e = tid + kThreads * m, j = e / (kAdjRows / 4), r = 4 * (e % (kAdjRows / 4));
+            R.r[m] = *reinterpret_cast<const float4*>(rs + (tok0 + min(j, valid - 1)) * rd + r0 + r);
+        }
+    };
+    // tile rows past `valid` zeroed; row slice weighted by zeta_{j,c-1} (zero past the end),
+    // negated for S^H
+    auto put = [&](const PassRegs& R, int valid) {
+#pragma unroll
+        for (int m = 0; m < VT; ++m) {
+            const int e = tid + kThreads * m, j = e / (DK / 4), f = 4 * (e % (DK / 4));
+            const bool ok = j < valid;
+            float* o = sX + j * kLdX + f;
+            o[0] = ok ? R.t[m].x : 0.0f;
+            o[1] = ok ? R.t[m].y : 0.0f;
+            o[2] = ok ? R.t[m].z : 0.0f;
+            o[3] = ok ? R.t[m].w : 0.0f;
+        }
+#pragma unroll
+        for (int m = 0; m < VR; ++m) {
+            const int e = tid + kThreads * m, j = e / (kAdjRows / 4), r = 4 * (e % (kAdjRows / 4));
+            const float wy = isG ? sW[j] : -sW[j];
+            float* o = sYr + j * kLdR + r;
+            o[0] = wy * R.r[m].x;
+            o[1] = wy * R.r[m].y;
+            o[2] = wy * R.r[m].z;
+            o[3] = wy * R.r[m].w;
+        }
+    };
+    // X[r][c] += sum_j Yr[j][r] T[j][c]  (A(m, k) = sYr[k][m], B(k, n) = sX[k][n])
+    auto multiply = [&](f32x4 (&acc)[NCT]) {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) acc[ct] = mma16<kC, 1, kLdR, kLdX, 1>(sYr + 16 * w, sX + 16 * ct, acc[ct]);
+    };
     float dprod = 1.0f;
     float* out = isG ? a.AG : a.SH;
+    PassRegs P0, P1;
+    if (nend > nbeg) fetch(nend - 1, 0, P0);
     for (int n = nend - 1; n >= nbeg; --n) {
         const int64_t t0 = int64_t(n) * kC;
         const int valid = int(min<int64_t>(kC, s.seq_len - t0));
@@ -369,49 +457,35 @@ __global__ __launch_bounds__(kThreads) void bwd_adjoint_kernel(BwdArgs a, AdjSeg
 #pragma unroll
                 for (int r = 0; r < 4; ++r) dst[(4 * g + r) * DK + 16 * ct + ln] = st[ct][r];
         }
-        // row slices: 64 tokens x 64 rows, four 16-byte loads per thread and array
-        constexpr int VR = kC * kAdjRows / 4 / kThreads;
-        float4 yr[VR], xr[VR];
-        const float* ysrc = isG ? a.dout : a.estar;
-        const int yd = isG ? DV : DK;
-#pragma unroll
-        for (int m = 0; m < VR; ++m) {
-            const int e = tid + kThreads * m, j = e / (kAdjRows / 4), r = 4 * (e % (kAdjRows / 4));
-            const int64_t row = tok0 + min(j, valid - 1);
-            yr[m] = *reinterpret_cast<const float4*>(ysrc + row * yd + r0 + r);
-            if (!isG) xr[m] = *reinterpret_cast<const float4*>(a.qstar + row * DK + r0 + r);
-        }
-        load_tile<DK, kLdX>(sX, a.qstar, tok0, valid);
-        if (!isG) load_tile<DK, kLdX>(sY, a.estar, tok0, valid);
         if (tid < kWave) {
             chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
             sW[tid] = tid < valid ? decay_from_start(sLg, sZl, tid) : 0.0f;  // own lane's values
         }
-        __syncthreads();
-#pragma unroll
-        for (int m = 0; m < VR; ++m) {
-            const int e = tid + kThreads * m, j = e / (kAdjRows / 4), r = 4 * (e % (kAdjRows / 4));
-            const float wy = isG ? sW[j] : -sW[j];  // zero past the valid tokens
-            float* oy = sYr + j * kLdR + r;
-            oy[0] = wy * yr[m].x; oy[1] = wy * yr[m].y; oy[2] = wy * yr[m].z; oy[3] = wy * yr[m].w;
-            if (!isG) {
-                const float wx = -sW[j];
-                float* ox = sXr + j * kLdR + r;
-                ox[0] = wx * xr[m].x; ox[1] = wx * xr[m].y; ox[2] = wx * xr[m].z; ox[3] = wx * xr[m].w;
-            }
-        }
+        __syncthreads();  // the gates are published; the previous pass is done with sX, sYr
+        put(P0, valid);
+        if (!isG)
+            fetch(n, 1, P1);
+        else if (n > nbeg)
+            fetch(n - 1, 0, P1);
         __syncthreads();
         const float D = decay_from_start(sLg, sZl, kC - 1);
         dprod *= D;
+        f32x4 acc[NCT];
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) {
-            f32x4 acc = st[ct] * D;
-            // X[r][c] += sum_j Yr[j][r] X[j][c]  (A(m, k) = sYr[k][m], B(k, n) = sX[k][n])
-            acc = mma16<kC, 1, kLdR, kLdX, 1>(sYr + 16 * w, sX + 16 * ct, acc);
-            if (!isG) acc = mma16<kC, 1, kLdR, kLdX, 1>(sXr + 16 * w, sY + 16 * ct, acc);
-            st[ct] = acc;
+        for (int ct = 0; ct < NCT; ++ct) acc[ct] = st[ct] * D;
+        multiply(acc);
+        if (!isG) {
+            __syncthreads();
+            put(P1, valid);
+            if (n > nbeg) fetch(n - 1, 0, P0);
+            __syncthreads();
+            multiply(acc);
+        } else {
+            P0 = P1;
         }
-        __syncthreads();
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) st[ct] = acc[ct];
+        __syncthreads();  // every wave is done with this chunk's gates before they are rewritten
     }
     if (sg.totals) {
         float* tb = seg_tile(seg);

@@ -111,7 +111,9 @@ def test_bf16_path_edge_cases():
     x["gamma"][1, 1, 63] = 0.0
     x["q"][0, 0, 10] = 0.0
     x["beta"][1, 0, 5:9] = 0.0
-    for n_cg in (0, 1, 15):
+    # 0 (Jacobi start only), 1 and 3 (the CG loop's odd tail), 2 and 15 (whole pairs of
+    # iterations, then a tail)
+    for n_cg in (0, 1, 2, 3, 15):
         got = _gpu_forward(x, "bf16", n_cg, 64, precision=L.MESA_PREC_BF16)
         ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], n_cg)["out"]
         e = rel_l2(got, ref)
