@@ -833,7 +833,8 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
 // ---------------------------------------------------------------- dLambda
 // dLambda[h][b] = sum over the batch and the chunks of the per-chunk partial sums:
 // one workgroup per head; thread (b, slot) sums every kThreads / d_k-th (batch, chunk)
-// entry, then the slots are summed in a fixed order.
+// entry, eight loads in flight at a time into eight partial sums, then the partial
+// sums and the slots are combined in a fixed order.
 __global__ __launch_bounds__(kThreads) void bwd_dlam_kernel(BwdArgs a)
 {
     const ForwardShape s = a.s;
@@ -842,11 +843,21 @@ __global__ __launch_bounds__(kThreads) void bwd_dlam_kernel(BwdArgs a)
     const int b = threadIdx.x % dk, slot = threadIdx.x / dk;
     const int64_t per = s.batch * s.n_chunks;  // partial sums of this head
     __shared__ float sAcc[kThreads];
-    float acc = 0.0f;
-    for (int64_t e = slot; e < per; e += slots) {
+    auto part = [&](int64_t e) {
         const int64_t bb = e / s.n_chunks, n = e % s.n_chunks;
-        acc += a.dlam_part[((bb * s.heads + h) * s.n_chunks + n) * dk + b];
+        return a.dlam_part[((bb * s.heads + h) * s.n_chunks + n) * dk + b];
+    };
+    float acc8[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    int64_t e = slot;
+    for (; e + 7 * slots < per; e += 8 * slots) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = part(e + u * slots);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc8[u] += v[u];
     }
+    for (; e < per; e += slots) acc8[0] += part(e);
+    const float acc = ((acc8[0] + acc8[1]) + (acc8[2] + acc8[3])) + ((acc8[4] + acc8[5]) + (acc8[6] + acc8[7]));
     sAcc[threadIdx.x] = acc;
     __syncthreads();
     if (slot == 0) {
