@@ -170,17 +170,17 @@ __device__ __forceinline__ void load_tile(float* dst, const bf16_t* src, int64_t
 // The same tile in two steps, so its global loads can be in flight while the previous
 // phase computes: fetch issues the 16-byte loads into registers, put (after the LDS
 // tile is free) zeroes rows past `valid` and stores it.
-template <int D, typename T>
+template <int D, typename T, int NT = kThreads>
 struct Tile;
-template <int D>
-struct Tile<D, float> {
-    static constexpr int V = kC * D / 4 / kThreads;
+template <int D, int NT>
+struct Tile<D, float, NT> {
+    static constexpr int V = kC * D / 4 / NT;
     float4 x[V];
     __device__ __forceinline__ void fetch(const float* src, int64_t tok0, int valid)
     {
 #pragma unroll
         for (int m = 0; m < V; ++m) {
-            const int e = threadIdx.x + kThreads * m, i = e / (D / 4), f = 4 * (e % (D / 4));
+            const int e = threadIdx.x + NT * m, i = e / (D / 4), f = 4 * (e % (D / 4));
             x[m] = *reinterpret_cast<const float4*>(src + (tok0 + min(i, valid - 1)) * D + f);
         }
     }
@@ -188,7 +188,7 @@ struct Tile<D, float> {
     {
 #pragma unroll
         for (int m = 0; m < V; ++m) {
-            const int e = threadIdx.x + kThreads * m, i = e / (D / 4), f = 4 * (e % (D / 4));
+            const int e = threadIdx.x + NT * m, i = e / (D / 4), f = 4 * (e % (D / 4));
             const bool ok = i < valid;
             float* o = dst + i * kLdT + f;
             o[0] = ok ? x[m].x : 0.0f;
@@ -198,15 +198,15 @@ struct Tile<D, float> {
         }
     }
 };
-template <int D>
-struct Tile<D, bf16_t> {
-    static constexpr int V = kC * D / 8 / kThreads;
+template <int D, int NT>
+struct Tile<D, bf16_t, NT> {
+    static constexpr int V = kC * D / 8 / NT;
     uint4 x[V];
     __device__ __forceinline__ void fetch(const bf16_t* src, int64_t tok0, int valid)
     {
 #pragma unroll
         for (int m = 0; m < V; ++m) {
-            const int e = threadIdx.x + kThreads * m, i = e / (D / 8), f = 8 * (e % (D / 8));
+            const int e = threadIdx.x + NT * m, i = e / (D / 8), f = 8 * (e % (D / 8));
             x[m] = *reinterpret_cast<const uint4*>(src + (tok0 + min(i, valid - 1)) * D + f);
         }
     }
@@ -214,7 +214,7 @@ struct Tile<D, bf16_t> {
     {
 #pragma unroll
         for (int m = 0; m < V; ++m) {
-            const int e = threadIdx.x + kThreads * m, i = e / (D / 8), f = 8 * (e % (D / 8));
+            const int e = threadIdx.x + NT * m, i = e / (D / 8), f = 8 * (e % (D / 8));
             const bool ok = i < valid;
             const uint32_t w4[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
             float* o = dst + i * kLdT + f;
@@ -498,10 +498,28 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, Adj
 }
 
 // ---------------------------------------------------------------- per-chunk gradients
-// One workgroup per chunk.  The gram and C x C phases give wave w the tokens 16w ..
-// 16w+15; the token-by-feature phases give it a quarter of the feature column tiles.
+// One workgroup of eight waves per chunk, two per SIMD, so one wave's LDS and memory
+// waits overlap the other's products.  The C x C phases split the 4 x 4 result tiles
+// over the waves (row tile w % 4, two column tiles); the token-by-feature phases give
+// each wave one 16-column feature tile and the token tiles GradSplit assigns.
+constexpr int kGradThreads = 512;
+constexpr int kGW = kGradThreads / kWave;  // waves per workgroup
+
+// Token-by-feature tiles of wave w for a feature dimension D: column tile col(w), token
+// tiles st0(w) .. st0(w) + NST - 1.
+template <int D>
+struct GradSplit {
+    static constexpr int NCOL = D / 16;          // feature column tiles
+    static constexpr int WPC = kGW / NCOL;       // waves per column tile
+    static constexpr int NST = (kC / 16) / WPC;  // token tiles per wave
+    static_assert(WPC * NCOL == kGW && NST * WPC == kC / 16, "eight waves over the feature tiles");
+    __device__ static int col(int w) { return w / WPC; }
+    __device__ static int st0(int w) { return (w % WPC) * NST; }
+    __device__ static bool own(int w, int st) { return st >= st0(w) && st < st0(w) + NST; }
+};
+
 template <typename Tin, int DK, int DV>
-__global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
+__global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
 {
     const ForwardShape s = a.s;
     const int nc = s.n_chunks;
@@ -523,30 +541,30 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     __shared__ float sT0[kC * kLdT];
     __shared__ float sT1[kC * kLdT];
     __shared__ float sM0[kC * kLdC];  // KQ, then M1 = Z ⊙ KQ, then W
-    __shared__ float sM1[kC * kLdC];  // VE, then VE - KE, then M2 = Z ⊙ (VE - KE)
+    __shared__ float sM1[kC * kLdC];  // VE, then M2 = Z ⊙ (VE - KE)
     __shared__ float sM2[kC * kLdC];  // KE, then Qm = beta_p (VE - KE) KQ
     __shared__ float sZ[kC * kLdC];   // Z[s][t] = zeta_{t,s} (s <= t)
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
     __shared__ float sBeta[kC], sZe[kC], sPhi[kC];
     __shared__ float sTok[5][kC];     // per token: dbeta (intra), v^T A^G k, k^T A^H k, g, h
-    __shared__ float sPart[kThreads / kWave];
-    __shared__ float sRed[kThreads / kWave][kC];  // per-wave partial sums per token
+    __shared__ float sPart[kGW];
+    __shared__ float sRed[kGW][kC];   // per-wave partial sums per token
     __shared__ float sF;
 
     // Token tiles in registers: each phase's tiles are fetched while the phase before it
     // computes, then put into sT0 / sT1 once those are free.
-    Tile<DK, Tin> tk;
-    Tile<DV, Tin> tv;
-    Tile<DK, float> tq, te;
-    Tile<DV, float> td;
+    Tile<DK, Tin, kGradThreads> tk;
+    Tile<DV, Tin, kGradThreads> tv;
+    Tile<DK, float, kGradThreads> tq, te;
+    Tile<DV, float, kGradThreads> td;
     tk.fetch(kp, tok0, valid);
     tq.fetch(a.qstar, tok0, valid);
 
     // ---- gates: Z, zeta_{E,s}, phi_s = zeta_{s-1,c-1}
     if (tid < kWave) chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
     __syncthreads();
-    for (int e = tid; e < kC * kC; e += kThreads) {
+    for (int e = tid; e < kC * kC; e += kGradThreads) {
         const int i = e / kC, j = e % kC;
         sZ[i * kLdC + j] = decay_between(sLg, sZl, i, j);
     }
@@ -556,14 +574,17 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         sPhi[tid] = tid == 0 ? 1.0f : decay_from_start(sLg, sZl, tid - 1);
     }
 
-    // ---- gram matrices [p][t] of the chunk's tokens; wave w forms rows 16w..
+    // ---- gram matrices [p][t] of the chunk's tokens: wave w forms row tile w % 4,
+    // column tiles 2 (w / 4) and 2 (w / 4) + 1
     auto gram = [&](float* dst, auto d_tag) {
         constexpr int D = decltype(d_tag)::value;
+        const int rt = w % 4;
 #pragma unroll
-        for (int tt = 0; tt < kC / 16; ++tt) {
-            const f32x4 gm = mma16<D, kLdT, 1, 1, kLdT>(sT0 + 16 * w * kLdT, sT1 + 16 * tt * kLdT, kZero4);
+        for (int h = 0; h < 2; ++h) {
+            const int tt = 2 * (w / 4) + h;
+            const f32x4 gm = mma16<D, kLdT, 1, 1, kLdT>(sT0 + 16 * rt * kLdT, sT1 + 16 * tt * kLdT, kZero4);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dst[(16 * w + 4 * g + r) * kLdC + 16 * tt + ln] = gm[r];
+            for (int r = 0; r < 4; ++r) dst[(16 * rt + 4 * g + r) * kLdC + 16 * tt + ln] = gm[r];
         }
     };
     tk.put(sT0, valid);
@@ -588,7 +609,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     // ---- C x C combinations, one row p per wave pass (lane = t): DVK = VE - KE;
     // Qm = beta_p DVK KQ; the intra part of dbeta_p = sum_t Z[p][t] KQ[p][t] DVK[p][t]
     // (a wave sum); M1 = Z ⊙ KQ, M2 = Z ⊙ DVK
-    for (int p = w; p < kC; p += kThreads / kWave) {
+    for (int p = w; p < kC; p += kGW) {
         const int o = p * kLdC + lane;
         const float kq = sM0[o], z = sZ[o];
         const float dvk = sM1[o] - sM2[o];
@@ -598,12 +619,9 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         const float db = wave_sum(z * kq * dvk);
         if (lane == 0) sTok[0][p] = db;
     }
-    // In the token-by-feature phases below wave w owns the 16-column tiles
-    // w * TPW .. of the feature dimension for all 64 tokens (4 token tiles), so it
-    // loads each d x d matrix's column tiles once; per-token sums over features are
-    // 16-lane row sums, then sums over the waves through sRed.
     auto tok = [&](int st, int r) { return 16 * st + 4 * g + r; };
-    // sum the partials p[st][r] (token tok(st, r)) over lanes and waves into out[token]
+    // sum the partials p[st][r] (token tok(st, r); zero on the token tiles the wave does not
+    // own) over lanes and waves into out[token], in a fixed order
     auto reduce_tokens = [&](const float (&p)[4][4], float* out) {
 #pragma unroll
         for (int st = 0; st < 4; ++st)
@@ -613,35 +631,35 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
                 if (ln == 0) sRed[w][tok(st, r)] = v;
             }
         __syncthreads();
-        if (tid < kC) out[tid] = (sRed[0][tid] + sRed[1][tid]) + (sRed[2][tid] + sRed[3][tid]);
+        if (tid < kC) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int u = 0; u < kGW; ++u) acc += sRed[u][tid];
+            out[tid] = acc;
+        }
         __syncthreads();
     };
 
     // ---- dv_s = beta_s (sum_t M1[s][t] e_t + zeta_E[s] A^G k_s)   (sT1 holds e_t)
     {
-        constexpr int TPW = DV / 16 / 4;
-        // the d x d operands of each column tile are loaded one tile ahead (the first
-        // before the phase's barriers)
-        float bv[2][DK / 4];
-        load_b<DK, 1, DK>(AG + 16 * (w * TPW) * DK, bv[0]);  // B(k, n) = A^G[16 at + n][k]
+        using S = GradSplit<DV>;
+        const int at = S::col(w);
+        float bv[DK / 4];
+        load_b<DK, 1, DK>(AG + 16 * at * DK, bv);  // B(k, n) = A^G[16 at + n][k], before the barriers
         __syncthreads();
         tk.put(sT0, valid);
         tq.fetch(a.qstar, tok0, valid);
         te.fetch(a.estar, tok0, valid);
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) {
-            const int at = w * TPW + j;
-            if (j + 1 < TPW) load_b<DK, 1, DK>(AG + 16 * (at + 1) * DK, bv[(j + 1) % 2]);
+        for (int st = 0; st < 4; ++st) {
+            if (!S::own(w, st)) continue;
+            const f32x4 in = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * at, kZero4);
+            const f32x4 ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv, kZero4);  // (K A^G^T)[s][a]
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                const f32x4 in = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * at, kZero4);
-                const f32x4 ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv[j % 2], kZero4);  // (K A^G^T)[s][a]
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = tok(st, r);
-                    if (t < valid) a.dv[(tok0 + t) * DV + 16 * at + ln] = sBeta[t] * (in[r] + sZe[t] * ex[r]);
-                }
+            for (int r = 0; r < 4; ++r) {
+                const int t = tok(st, r);
+                if (t < valid) a.dv[(tok0 + t) * DV + 16 * at + ln] = sBeta[t] * (in[r] + sZe[t] * ex[r]);
             }
         }
     }
@@ -649,11 +667,12 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     // ---- dk_s = beta_s (sum_t M2[s][t] q*_t - sum_t M1[s][t] e*_t + zeta_E[s] ((A^G)^T v_s + S^H k_s)),
     //      with v^T A^G k and k^T A^H k = (1/2) k^T S^H k per token
     {
-        constexpr int TPW = DK / 16 / 4;
-        f32x4 in[TPW][4];
-        float bag[2][DV / 4], bsh[2][DK / 4];  // the inter part's operands, one tile ahead
-        load_b<DV, DK, 1>(AG + 16 * (w * TPW), bag[0]);  // B(k, n) = A^G[k][16 bt + n]
-        load_b<DK, DK, 1>(SH + 16 * (w * TPW), bsh[0]);  // B(k, n) = S^H[k][16 bt + n]
+        using S = GradSplit<DK>;
+        const int bt = S::col(w);
+        f32x4 in[4];
+        float bag[DV / 4], bsh[DK / 4];  // the inter part's operands, in flight during the intra part
+        load_b<DV, DK, 1>(AG + 16 * bt, bag);  // B(k, n) = A^G[k][16 bt + n]
+        load_b<DK, DK, 1>(SH + 16 * bt, bsh);  // B(k, n) = S^H[k][16 bt + n]
         __syncthreads();
         tq.put(sT0, valid);
         te.put(sT1, valid);
@@ -661,14 +680,12 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         tv.fetch(vp, tok0, valid);
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < TPW; ++j)
-#pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                const int bt = w * TPW + j;
-                const f32x4 pq = mma16<kC, kLdC, 1, kLdT, 1>(sM1 + 16 * st * kLdC, sT0 + 16 * bt, kZero4);
-                const f32x4 pe = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * bt, kZero4);
-                in[j][st] = pq - pe;
-            }
+        for (int st = 0; st < 4; ++st) {
+            if (!S::own(w, st)) continue;
+            const f32x4 pq = mma16<kC, kLdC, 1, kLdT, 1>(sM1 + 16 * st * kLdC, sT0 + 16 * bt, kZero4);
+            const f32x4 pe = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * bt, kZero4);
+            in[st] = pq - pe;
+        }
         __syncthreads();
         tk.put(sT0, valid);
         tv.put(sT1, valid);
@@ -677,24 +694,17 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         __syncthreads();
         float pa[4][4] = {}, pk[4][4] = {};
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) {
-            const int bt = w * TPW + j;
-            if (j + 1 < TPW) {
-                load_b<DV, DK, 1>(AG + 16 * (bt + 1), bag[(j + 1) % 2]);
-                load_b<DK, DK, 1>(SH + 16 * (bt + 1), bsh[(j + 1) % 2]);
-            }
+        for (int st = 0; st < 4; ++st) {
+            if (!S::own(w, st)) continue;
+            const f32x4 ag = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bag, kZero4);
+            const f32x4 sh = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bsh, kZero4);
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                const f32x4 ag = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bag[j % 2], kZero4);
-                const f32x4 sh = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bsh[j % 2], kZero4);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = tok(st, r), b = 16 * bt + ln;
-                    const float kb = sT0[t * kLdT + b];
-                    if (t < valid) a.dk[(tok0 + t) * DK + b] = sBeta[t] * (in[j][st][r] + sZe[t] * (ag[r] + sh[r]));
-                    pa[st][r] += kb * ag[r];
-                    pk[st][r] += 0.5f * kb * sh[r];
-                }
+            for (int r = 0; r < 4; ++r) {
+                const int t = tok(st, r), b = 16 * bt + ln;
+                const float kb = sT0[t * kLdT + b];
+                if (t < valid) a.dk[(tok0 + t) * DK + b] = sBeta[t] * (in[st][r] + sZe[t] * (ag[r] + sh[r]));
+                pa[st][r] += kb * ag[r];
+                pk[st][r] += 0.5f * kb * sh[r];
             }
         }
         reduce_tokens(pa, sTok[1]);
@@ -704,60 +714,50 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
     // ---- g_t = e_t^T G_c q*_t, h_t = e*_t^T H_c q*_t, F = <A^G, G_c> + (1/2) <S^H, H_c>,
     //      and dLambda of the chunk
     {
-        constexpr int TPW = DK / 16 / 4;
-        // G_c's and then H_c's column tiles, each loaded one tile ahead
-        float bg[2][DV / 4], bh_[2][DK / 4];
-        load_b<DV, DK, 1>(Gc + 16 * (w * TPW), bg[0]);  // B(k, n) = G_c[k][16 bt + n]
+        using S = GradSplit<DK>;
+        const int bt = S::col(w);
+        float bg[DV / 4], bh_[DK / 4];
+        load_b<DV, DK, 1>(Gc + 16 * bt, bg);  // B(k, n) = G_c[k][16 bt + n], before the barriers
         __syncthreads();
         tq.put(sT0, valid);
         td.put(sT1, valid);
         te.fetch(a.estar, tok0, valid);
         __syncthreads();
+        load_b<DK, DK, 1>(Hc + 16 * bt, bh_);  // B(k, n) = H_c[k][16 bt + n], in flight during g
         float pg[4][4] = {}, ph[4][4] = {};
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) {
-            const int bt = w * TPW + j;
-            if (j + 1 < TPW)
-                load_b<DV, DK, 1>(Gc + 16 * (bt + 1), bg[(j + 1) % 2]);
-            else
-                load_b<DK, DK, 1>(Hc + 16 * (w * TPW), bh_[0]);  // B(k, n) = H_c[k][16 bt + n]
+        for (int st = 0; st < 4; ++st) {
+            if (!S::own(w, st)) continue;
+            const f32x4 eg = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bg, kZero4);
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                const f32x4 eg = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bg[j % 2], kZero4);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) pg[st][r] += eg[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
-            }
+            for (int r = 0; r < 4; ++r) pg[st][r] += eg[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
         }
         reduce_tokens(pg, sTok[3]);
         te.put(sT1, valid);
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) {
-            const int bt = w * TPW + j;
-            if (j + 1 < TPW) load_b<DK, DK, 1>(Hc + 16 * (bt + 1), bh_[(j + 1) % 2]);
+        for (int st = 0; st < 4; ++st) {
+            if (!S::own(w, st)) continue;
+            const f32x4 eh = mma16_b<DK, kLdT, 1>(sT1 + 16 * st * kLdT, bh_, kZero4);
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                const f32x4 eh = mma16_b<DK, kLdT, 1>(sT1 + 16 * st * kLdT, bh_[j % 2], kZero4);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) ph[st][r] += eh[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
-            }
+            for (int r = 0; r < 4; ++r) ph[st][r] += eh[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
         }
         reduce_tokens(ph, sTok[4]);
         // F: every thread a strided slice of the two Frobenius products, 16-byte loads,
         // all issued before the products
         float fr = 0.0f;
         {
-            constexpr int NG = DV * DK / 4 / kThreads, NH = DK * DK / 4 / kThreads;
+            constexpr int NG = DV * DK / 4 / kGradThreads, NH = DK * DK / 4 / kGradThreads;
             float4 x[NG], y[NG], u[NH], v[NH];
 #pragma unroll
             for (int m = 0; m < NG; ++m) {
-                x[m] = *reinterpret_cast<const float4*>(AG + 4 * (tid + kThreads * m));
-                y[m] = *reinterpret_cast<const float4*>(Gc + 4 * (tid + kThreads * m));
+                x[m] = *reinterpret_cast<const float4*>(AG + 4 * (tid + kGradThreads * m));
+                y[m] = *reinterpret_cast<const float4*>(Gc + 4 * (tid + kGradThreads * m));
             }
 #pragma unroll
             for (int m = 0; m < NH; ++m) {
-                u[m] = *reinterpret_cast<const float4*>(SH + 4 * (tid + kThreads * m));
-                v[m] = *reinterpret_cast<const float4*>(Hc + 4 * (tid + kThreads * m));
+                u[m] = *reinterpret_cast<const float4*>(SH + 4 * (tid + kGradThreads * m));
+                v[m] = *reinterpret_cast<const float4*>(Hc + 4 * (tid + kGradThreads * m));
             }
 #pragma unroll
             for (int m = 0; m < NG; ++m) fr += x[m].x * y[m].x + x[m].y * y[m].y + x[m].z * y[m].z + x[m].w * y[m].w;
@@ -767,9 +767,9 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         fr = wave_sum(fr);
         if (lane == 0) sPart[w] = fr;
         // dLambda of the chunk, -sum_t q*_t e*_t per feature: the tokens split into
-        // kThreads / DK slices, one per thread of a feature, partial sums through sRed
+        // kGradThreads / DK slices, one per thread of a feature, partial sums through sRed
         {
-            constexpr int NP = kThreads / DK;
+            constexpr int NP = kGradThreads / DK;
             const int f = tid % DK, sl = tid / DK;
             float acc = 0.0f;
 #pragma unroll 8
@@ -778,7 +778,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         }
         __syncthreads();
         if (tid < DK) {
-            constexpr int NP = kThreads / DK;
+            constexpr int NP = kGradThreads / DK;
             float acc = 0.0f;
 #pragma unroll
             for (int sl = 0; sl < NP; ++sl) acc += (&sRed[0][0])[sl * DK + tid];
@@ -786,24 +786,27 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         }
         if (tid == 0) {
             float t = 0.0f;
-            for (int u = 0; u < kThreads / kWave; ++u) t += sPart[u];
+            for (int u = 0; u < kGW; ++u) t += sPart[u];
             sF = t;
         }
     }
 
-    // ---- W[p][s] = sum_{t>=s} zeta_{t,s} Qm[p][t]: rows 16w.. of Qm Z^T, into sM0
+    // ---- W[p][s] = sum_{t>=s} zeta_{t,s} Qm[p][t] (Qm Z^T), into sM0: wave w row tile
+    // w % 4, column tiles 2 (w / 4) ..
     {
+        const int rt = w % 4;
 #pragma unroll
-        for (int st = 0; st < kC / 16; ++st) {
-            const f32x4 wq = mma16<kC, kLdC, 1, 1, kLdC>(sM2 + 16 * w * kLdC, sZ + 16 * st * kLdC, kZero4);
+        for (int h = 0; h < 2; ++h) {
+            const int st = 2 * (w / 4) + h;
+            const f32x4 wq = mma16<kC, kLdC, 1, 1, kLdC>(sM2 + 16 * rt * kLdC, sZ + 16 * st * kLdC, kZero4);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sM0[tok(w, r) * kLdC + 16 * st + ln] = wq[r];
+            for (int r = 0; r < 4; ++r) sM0[(16 * rt + 4 * g + r) * kLdC + 16 * st + ln] = wq[r];
         }
         __syncthreads();
     }
 
-    // ---- assemble dgamma_s and dbeta_s: wave w takes tokens s = 16w.., its lanes the
-    // summation index q of the three sums (wave sums), the masks coming from Z:
+    // ---- assemble dgamma_s and dbeta_s: wave w takes tokens s = (kC / kGW) w.., its lanes
+    // the summation index q of the three sums (wave sums), the masks coming from Z:
     //   t2 = sum_{t >= s} zeta_{t,s} (g_t - h_t)                  (Z[s][q], 0 for q < s)
     //   t3 = sum_{p < s} zeta_{s-1,p} beta_p (v^T A^G k + k^T A^H k)_p,
     //   t4 = sum_{p < s} zeta_{s-1,p} W[p][s]                     (Z[q][s-1], 0 for q >= s)
@@ -811,8 +814,8 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(BwdArgs a)
         const float gh = sTok[3][lane] - sTok[4][lane];
         const float bk = sBeta[lane] * (sTok[1][lane] + sTok[2][lane]);
 #pragma unroll 4
-        for (int i = 0; i < 16; ++i) {
-            const int si = 16 * w + i;
+        for (int i = 0; i < kC / kGW; ++i) {
+            const int si = (kC / kGW) * w + i;
             const float v2 = sZ[si * kLdC + lane] * gh;
             float v3 = 0.0f, v4 = 0.0f;
             if (si > 0) {
@@ -902,7 +905,7 @@ hipError_t launch_bwd_dims(const BwdArgs& a, hipStream_t stream, int stage)
             break;
         }
         case 2:
-            hipLaunchKernelGGL((bwd_grad_kernel<Tin, DK, DV>), dim3(chunks), dim3(kThreads), 0, stream, a);
+            hipLaunchKernelGGL((bwd_grad_kernel<Tin, DK, DV>), dim3(chunks), dim3(kGradThreads), 0, stream, a);
             break;
         default:
             hipLaunchKernelGGL(bwd_dlam_kernel, dim3(unsigned(a.s.heads)), dim3(kThreads), 0, stream, a);
