@@ -27,7 +27,12 @@
  *     relative test |r_{k+1}| <= eps |r_0| (squared: delta_new <= eps^2 delta_0;
  *     with eps = 0 that is a residual of exactly zero); it also stops, keeping
  *     x, when the squared residual is zero before a step or when p^T A p <= 0
- *     (guards for q = 0 and breakdown);
+ *     (guards for q = 0 and breakdown).  "Zero" is read in floating point: in
+ *     exact arithmetic CG reaches a zero residual within n steps, but the
+ *     recursively updated residual of a floating-point run keeps shrinking past
+ *     the attainable accuracy and finally underflows, where alpha = delta / p^T A p
+ *     loses all precision.  So a squared residual at or below 2^-200 |b|^2 counts
+ *     as zero (x then changes by less than 2^-100 relative per step);
  *   - beta enters once: H += beta k k^T, G += beta v k^T;
  *   - decode updates the state with the new token first, then solves.
  *
@@ -73,18 +78,20 @@ int oracle_cg(const double* A, const double* b, int64_t n, int n_cg, int init, d
     double* w = work + 2 * n;
     for (int64_t i = 0; i < n; ++i)
         x[i] = (init == ORACLE_INIT_QUERY) ? b[i] : b[i] / A[i * n + i];
-    double delta = 0.0;
+    double delta = 0.0, bb = 0.0;
     for (int64_t i = 0; i < n; ++i) {
         double ax = 0.0;
         for (int64_t j = 0; j < n; ++j) ax += A[i * n + j] * x[j];
         r[i] = b[i] - ax;
         p[i] = r[i];
         delta += r[i] * r[i];
+        bb += b[i] * b[i];
     }
     const double delta0 = delta;  /* |r_0|^2, the reference of the relative test */
+    const double zero = ldexp(bb, -200);  /* squared residuals at or below this are zero */
     int it = 0;
     for (; it < n_cg; ++it) {
-        if (delta == 0.0) break;
+        if (!(delta > zero)) break;
         double pw = 0.0;
         for (int64_t i = 0; i < n; ++i) {
             double s = 0.0;
@@ -100,7 +107,7 @@ int oracle_cg(const double* A, const double* b, int64_t n, int n_cg, int init, d
             r[i] -= alpha * w[i];
             delta_new += r[i] * r[i];
         }
-        if (delta_new <= eps * eps * delta0) { ++it; break; }
+        if (delta_new <= eps * eps * delta0 || delta_new <= zero) { ++it; break; }
         double beta_cg = delta_new / delta;
         for (int64_t i = 0; i < n; ++i) p[i] = r[i] + beta_cg * p[i];
         delta = delta_new;

@@ -90,6 +90,18 @@ def test_cg_with_dk_steps_matches_cholesky():
     assert _rel(cg["out"], ex["out"]) < 1e-9
 
 
+def test_cg_far_past_convergence_stays_at_the_exact_solution():
+    """1024 loop iterations (the ABI's maximum) on d_k = 8: the updated residual reaches
+    the zero floor long before, and the iterate must stay at the Cholesky solution
+    (without the floor it drifts into subnormal p^T A p and blows up)."""
+    x = _inputs(dk=8, dv=6, T=40)
+    cg = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 1024, want_qstar=True)
+    ex = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 0, solver="cholesky",
+                        want_qstar=True)
+    assert _rel(cg["qstar"], ex["qstar"]) < 1e-9
+    assert _rel(cg["out"], ex["out"]) < 1e-9
+
+
 # ---------------------------------------------------- P2: ridge regression, dual
 def _dual_ridge(x, b, h):
     """o_t = V_t W (I + K_t^T Lambda^{-1} K_t W)^{-1} K_t^T Lambda^{-1} q_t with
