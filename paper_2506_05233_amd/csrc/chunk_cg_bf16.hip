@@ -88,9 +88,6 @@ __device__ __forceinline__ uint4 keep_if(bool c, const uint4& v)
 // their reciprocal (see the sub-chunk states below).
 constexpr float kMinDecay = 1e-20f;
 
-// Smallest normal fp32 number (2^-126): CG scalars below it stop a column (see the loop).
-constexpr float kMinNormal = 1.17549435e-38f;
-
 // 8 bf16 (bits in v) times u, rounded back to bf16.
 __device__ __forceinline__ uint4 scale_bf16x8(const uint4& v, float u)
 {

@@ -137,6 +137,17 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
         r[m] = sP[rr * LDP + j];
         w[m] = zeta_j * sH[rr * LDH + rr] + lam[rr];
     }
+    // the column solves for q 2^-qsh (|q 2^-qsh|^2 in [1/2, 2)); x is scaled back at the end
+    int qsh;
+    {
+        float part = 0.0f;
+#pragma unroll
+        for (int m = 0; m < NE; ++m) part += r[m] * r[m];
+        qsh = cg_scale_shift(colsum(part));
+        const float qs = __builtin_ldexpf(1.0f, -qsh);
+#pragma unroll
+        for (int m = 0; m < NE; ++m) r[m] *= qs;
+    }
 #pragma unroll 1
     for (int i = 0; i <= j; ++i) {
         const float wij = sBeta[i] * decay_between(sLg, sZl, i, j);
@@ -161,7 +172,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
     }
     float delta = colsum(part);
     const float thr = a.eps2 * delta;  // Alg. 1: the column stops once |r|^2 <= eps^2 |r_0|^2
-    bool active = delta > 0.0f;
+    bool active = delta >= kMinNormal;
     int steps = 0;  // iterations that updated x
     for (int it = 0; it < a.n_cg; ++it) {
         if (!__syncthreads_or(active)) break;
@@ -170,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
 #pragma unroll
         for (int m = 0; m < NE; ++m) part += p[m] * w[m];
         const float pw = colsum(part);
-        if (active && !(pw > 0.0f)) active = false;
+        if (active && !(pw >= kMinNormal)) active = false;
         if (active) {
             const float alpha = delta / pw;
 #pragma unroll
@@ -185,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
         for (int m = 0; m < NE; ++m) part += r[m] * r[m];
         const float dn = colsum(part);
         if (active) {
-            if (dn <= thr) {
+            if (dn <= thr || !(dn >= kMinNormal)) {
                 active = false;
             } else {
                 const float beta_cg = dn / delta;
@@ -194,6 +205,11 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_kernel(CgArgs a)
                 delta = dn;
             }
         }
+    }
+    {
+        const float us = __builtin_ldexpf(1.0f, qsh);
+#pragma unroll
+        for (int m = 0; m < NE; ++m) x[m] *= us;
     }
 
     if (a.steps && a0 == 0 && j < valid) a.steps[tok0 + j] = steps;
@@ -398,6 +414,13 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_mma_kernel(CgArgs a)
         return row_pair_sums((acc[0] + acc[1]) + (acc[2] + acc[3]));
     };
 
+    // the column solves for q 2^-qsh (|q 2^-qsh|^2 in [1/2, 2)); x is scaled back at the end
+    const int qsh = cg_scale_shift(colsum(qv, qv));
+    {
+        const float qs = __builtin_ldexpf(1.0f, -qsh);
+#pragma unroll
+        for (int t = 0; t < MT; ++t) qv[t] *= qs;
+    }
     // ---- Jacobi start: diag(H_t + Lambda) = zeta diag(H_c) + sum_i beta_i zeta_{j,i} k_i ⊙ k_i + lambda
     f32x4 x[MT], r[MT], p[MT], wv[MT];
 #pragma unroll
@@ -428,13 +451,13 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_mma_kernel(CgArgs a)
     }
     float delta = colsum(r, r);
     const float thr = a.eps2 * delta;  // Alg. 1: the column stops once |r|^2 <= eps^2 |r_0|^2
-    bool active = delta > 0.0f;
+    bool active = delta >= kMinNormal;
     int steps = 0;
     for (int it = 0; it < a.n_cg; ++it) {
         if (!__any(active)) break;
         matvec(p, wv);
         const float pw = colsum(p, wv);
-        if (active && !(pw > 0.0f)) active = false;
+        if (active && !(pw >= kMinNormal)) active = false;
         if (active) {
             const float alpha = delta / pw;
 #pragma unroll
@@ -446,7 +469,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_mma_kernel(CgArgs a)
         }
         const float dn = colsum(r, r);
         if (active) {
-            if (dn <= thr) {
+            if (dn <= thr || !(dn >= kMinNormal)) {
                 active = false;
             } else {
                 const float bcg = dn / delta;
@@ -455,6 +478,11 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_mma_kernel(CgArgs a)
                 delta = dn;
             }
         }
+    }
+    {
+        const float us = __builtin_ldexpf(1.0f, qsh);
+#pragma unroll
+        for (int t = 0; t < MT; ++t) x[t] *= us;
     }
     if (a.steps && g == 0 && j < valid) a.steps[tok0 + j] = steps;
     if (a.qstar && j < valid) {

@@ -163,27 +163,31 @@ void decode_step_kernel(DecodeArgs a)
         return t;
     };
 
-    float x = qR / hdiag;
-    float r = qR - gemv(x);
+    // solve for q 2^-qsh (|q 2^-qsh|^2 in [1/2, 2)); x is scaled back after the loop
+    const int qsh = cg_scale_shift(dot(qR, qR));
+    const float qRs = qR * __builtin_ldexpf(1.0f, -qsh);
+    float x = qRs / hdiag;
+    float r = qRs - gemv(x);
     float p = r;
     float delta = dot(r, r);
     const float thr = a.eps2 * delta;  // Alg. 1: stop once |r|^2 <= eps^2 |r_0|^2
     int steps = 0;                     // iterations that updated x
-    if (delta > 0.0f) {
+    if (delta >= kMinNormal) {
         for (int it = 0; it < a.n_cg; ++it) {
             const float w = gemv(p);
             const float pw = dot(p, w);
-            if (!(pw > 0.0f)) break;
+            if (!(pw >= kMinNormal)) break;
             const float alpha = delta / pw;
             x += alpha * p;
             r -= alpha * w;
             ++steps;
             const float dn = dot(r, r);
-            if (dn <= thr) break;
+            if (dn <= thr || !(dn >= kMinNormal)) break;
             p = r + (dn / delta) * p;
             delta = dn;
         }
     }
+    x *= __builtin_ldexpf(1.0f, qsh);
 
     if (a.steps && tid == 0) a.steps[pair] = steps;
 

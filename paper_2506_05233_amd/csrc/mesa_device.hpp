@@ -120,6 +120,16 @@ __device__ __forceinline__ float decay_from_start(const float* lg, const int* zl
     return zl[j] >= 0 ? 0.0f : expf(lg[j]);
 }
 
+// Smallest normal fp32 number (2^-126).  The CG loops stop a column once p^T A p or
+// |r|^2 falls below it (alpha would need the reciprocal of a subnormal, and the
+// recursively updated residual goes on shrinking long after the true one stops
+// improving); each column solves for q scaled by a power of two that brings |q|^2 into
+// [1/2, 2), so the threshold is relative to |q|^2 and no rounding changes.
+constexpr float kMinNormal = 1.17549435e-38f;
+
+// log2 of the power-of-two scale that brings |q|^2 = qq into [1/2, 2) (0 for qq = 0)
+__device__ __forceinline__ int cg_scale_shift(float qq) { return __builtin_amdgcn_frexp_expf(qq) >> 1; }
+
 // Workgroups are dealt to the 8 XCDs round-robin (block b runs on XCD b % 8),
 // and each XCD has its own L2.  This maps the hardware block index to a logical
 // one so that logically consecutive workgroups share an XCD: workgroups that

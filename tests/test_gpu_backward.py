@@ -80,6 +80,16 @@ def test_backward_matrix_core_solve_matches_oracle(dk, dv):
            tol=TOL_BF16, precision=L.MESA_PREC_AUTO)
 
 
+@pytest.mark.parametrize("precision,tol", [(L.MESA_PREC_F32, TOL_F32), (L.MESA_PREC_AUTO, TOL_BF16)],
+                         ids=["f32_solve", "matrix_core_solve"])
+def test_backward_max_ncg(precision, tol):
+    """The largest accepted iteration count (MESA_MAX_NCG) in the forward and in the
+    solve for e*, bf16 inputs, against the oracle."""
+    x = W.forward_inputs(1, 2, 70, 64, 64, "bf16", 4.0, seed=43)
+    _check(x, "bf16", L.MESA_MAX_NCG, _dout(x, 5), "backward n_cg=%d" % L.MESA_MAX_NCG, tol=tol,
+           precision=precision)
+
+
 def test_backward_batch_sums_dlambda_and_edge_cases():
     """Three sequences (dLambda sums over the batch), zero forget gates at a chunk
     start, inside and at a chunk end, ignored tokens (beta = 0), a zero query."""

@@ -383,6 +383,34 @@ def test_decode_f32_matches_oracle_tightly():
     assert rel_l2(dH.cpu().numpy(), rH) <= 1e-6 and rel_l2(dG.cpu().numpy(), rG) <= 1e-6
 
 
+def test_max_ncg_forward_and_decode():
+    """The largest accepted iteration count, MESA_MAX_NCG, on small inputs: the forward's
+    CG loop on both matrix-core paths (bf16 operands: 512 pairs of iterations; fp32) and
+    the decode step run every iteration (eps = 0, so fp32 columns keep iterating on a
+    residual at the rounding floor) and still agree with the oracle's fp64 CG."""
+    n = L.MESA_MAX_NCG
+    x = W.forward_inputs(1, 2, 70, 64, 64, "bf16", 4.0, seed=41)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], n)["out"]
+    e_b = rel_l2(_gpu_forward(x, "bf16", n, 64, precision=L.MESA_PREC_BF16), ref)
+    e_f = rel_l2(_gpu_forward(x, "bf16", n, 64, precision=L.MESA_PREC_F32), ref)
+    _say("n_cg = %d: bf16 operands %.3e, fp32 %.3e" % (n, e_b, e_f))
+    assert e_b <= TOL_BF16 and e_f <= TOL_F32
+    y = W.forward_inputs(2, 2, 1, 64, 64, "f32", 3.0, seed=42)
+    rng = np.random.default_rng(1)
+    H0, G0 = oracle.unrolled_states(rng.standard_normal((2, 2, 40, 64)) / 8,
+                                    rng.standard_normal((2, 2, 40, 64)),
+                                    np.full((2, 2, 40), 0.95), np.full((2, 2, 40), 0.5))
+    H0, G0 = H0.astype(np.float32), G0.astype(np.float32)
+    d = to_device({k: v[:, :, 0] for k, v in y.items() if k != "lam"}, "f32")
+    dH, dG = torch.from_numpy(H0).cuda(), torch.from_numpy(G0).cuda()
+    out = L.decode_step(dH, dG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], torch.from_numpy(y["lam"]).cuda(), n)
+    ro, _, _ = oracle.decode_step(H0, G0, y["q"][:, :, 0], y["k"][:, :, 0], y["v"][:, :, 0],
+                                  y["gamma"][:, :, 0], y["beta"][:, :, 0], y["lam"], n)
+    e_d = rel_l2(out.cpu().numpy(), ro)
+    _say("n_cg = %d: decode %.3e" % (n, e_d))
+    assert e_d <= TOL_F32
+
+
 def test_decode_steps_from_zero_equal_forward():
     x = W.forward_inputs(2, 2, 70, 128, 128, "bf16", 4.0, seed=12)
     fwd = _gpu_forward(x, "bf16", 10, 64, precision=L.MESA_PREC_F32)
