@@ -385,7 +385,8 @@ def test_decode_f32_matches_oracle_tightly():
 
 def test_max_ncg_forward_and_decode():
     """The largest accepted iteration count, MESA_MAX_NCG, on small inputs: the forward's
-    CG loop on both matrix-core paths (bf16 operands: 512 pairs of iterations; fp32) and
+    CG loop on both matrix-core paths (bf16 operands: 512 pairs of iterations; fp32), the
+    scalar fp32 kernel (chunk 32) and
     the decode step run every iteration (eps = 0, so fp32 columns keep iterating on a
     residual at the rounding floor) and still agree with the oracle's fp64 CG."""
     n = L.MESA_MAX_NCG
@@ -393,8 +394,9 @@ def test_max_ncg_forward_and_decode():
     ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], n)["out"]
     e_b = rel_l2(_gpu_forward(x, "bf16", n, 64, precision=L.MESA_PREC_BF16), ref)
     e_f = rel_l2(_gpu_forward(x, "bf16", n, 64, precision=L.MESA_PREC_F32), ref)
-    _say("n_cg = %d: bf16 operands %.3e, fp32 %.3e" % (n, e_b, e_f))
-    assert e_b <= TOL_BF16 and e_f <= TOL_F32
+    e_s = rel_l2(_gpu_forward(x, "bf16", n, 32, precision=L.MESA_PREC_F32), ref)  # scalar fp32 kernel
+    _say("n_cg = %d: bf16 operands %.3e, fp32 %.3e, fp32 chunk 32 %.3e" % (n, e_b, e_f, e_s))
+    assert e_b <= TOL_BF16 and e_f <= TOL_F32 and e_s <= TOL_F32
     y = W.forward_inputs(2, 2, 1, 64, 64, "f32", 3.0, seed=42)
     rng = np.random.default_rng(1)
     H0, G0 = oracle.unrolled_states(rng.standard_normal((2, 2, 40, 64)) / 8,
