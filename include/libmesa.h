@@ -15,9 +15,13 @@
  * first residual, then at most n_cg iterations (n_cg + 1 products).  An
  * iteration that updates x stops its column when the new residual meets Alg.
  * 1's relative test |r_k| <= eps |r_0|; the plain entry points use eps = 0,
- * the fixed-step solve, which stops early only at a residual of exactly zero
- * (on the matrix-core path: below the smallest normal fp32 number, relative to
- * |q_t|^2).  A column also stops, keeping its x, when p^T A p <= 0.
+ * the fixed-step solve, which stops early only at a zero residual.  "Zero" is
+ * read in floating point: each column solves for q_t scaled by a power of two
+ * that brings |q_t|^2 into [1/2, 2) (exact), and stops once its squared
+ * residual falls below the smallest normal fp32 number; past that point the
+ * updated residual carries no information and alpha would need the reciprocal
+ * of a subnormal.  A column also stops, keeping its x, when p^T A p is not a
+ * positive normal number (breakdown).
  *
  * The forward pass is evaluated chunkwise (Sec. 3, Eq. gla_matrix; App. D,
  * Eq. gla and Eq. q_star_parallel): states are materialised only at chunk
