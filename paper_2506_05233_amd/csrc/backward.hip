@@ -89,23 +89,6 @@ __device__ __forceinline__ f32x4 mma16_b(const float* A, const float (&bv)[K / 4
     return acc;
 }
 
-// Products of the rows 16w.. of an LDS token tile with NT consecutive 16-column tiles
-// of a global matrix (B(k, n) = M[k * BK + (16 t + n) * BN] for tile t), the matrix
-// operands double-buffered; epi(t, result) consumes each tile.
-template <int K, int NT, int AM, int BK, int BN, typename Epi>
-__device__ __forceinline__ void rows_times_matrix(const float* A, const float* M, Epi&& epi)
-{
-    float b0[K / 4], b1[K / 4];
-    load_b<K, BK, BN>(M, b0);
-#pragma unroll
-    for (int t = 0; t < NT; t += 2) {
-        if (t + 1 < NT) load_b<K, BK, BN>(M + (16 * (t + 1)) * BN, b1);
-        epi(t, mma16_b<K, AM, 1>(A, b0, f32x4{0.0f, 0.0f, 0.0f, 0.0f}));
-        if (t + 2 < NT) load_b<K, BK, BN>(M + (16 * (t + 2)) * BN, b0);
-        if (t + 1 < NT) epi(t + 1, mma16_b<K, AM, 1>(A, b1, f32x4{0.0f, 0.0f, 0.0f, 0.0f}));
-    }
-}
-
 constexpr f32x4 kZero4 = {0.0f, 0.0f, 0.0f, 0.0f};
 
 // Sum over the 16 lanes of a lane row (the columns of a result tile); every lane of
