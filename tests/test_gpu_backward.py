@@ -90,6 +90,18 @@ def test_backward_max_ncg(precision, tol):
            precision=precision)
 
 
+@pytest.mark.parametrize("precision", [L.MESA_PREC_F32, L.MESA_PREC_AUTO], ids=["f32_solve", "matrix_core_solve"])
+def test_backward_is_bitwise_deterministic(precision):
+    """No atomics and fixed summation orders: two calls give identical bits, also with
+    the segmented adjoint walk (one sequence of 40 chunks)."""
+    x = W.forward_inputs(1, 2, 40 * 64 - 5, 128, 128, "bf16", 4.0, seed=44)
+    dout = _dout(x, 6)
+    a = _gpu_backward(x, "bf16", 8, dout, precision)
+    b = _gpu_backward(x, "bf16", 8, dout, precision)
+    for k in GRADS:
+        assert np.array_equal(a[k], b[k]), k
+
+
 def test_backward_batch_sums_dlambda_and_edge_cases():
     """Three sequences (dLambda sums over the batch), zero forget gates at a chunk
     start, inside and at a chunk end, ignored tokens (beta = 0), a zero query."""
