@@ -396,12 +396,16 @@ __global__ __launch_bounds__(kThreads) void chunk_state_f32_kernel(StateArgs a)
 }
 
 // Wide variant (bf16 k and v, chunk 64, d_k and d_v in {64, 128}), used for the
-// bf16 fragment chunk states and for the states-only call.  One workgroup owns a
-// whole part of the state of one (batch, head) sequence -- part 0 is H (d_k x d_k),
-// part 1 is G^T (d_k x d_v), both as [key feature R][column c] -- in registers,
-// and walks its chunks in order:
+// bf16 fragment chunk states and for the states-only call.  Two workgroups share the
+// state of one (batch, head) sequence -- part 0 is H (d_k x d_k), part 1 is G^T
+// (d_k x d_v), both as [key feature R][column c] -- in registers, and walk its chunks
+// in order:
 //
 //   X_{next} = D X + K^T (w ⊙ Y),   Y = K (part 0) or V (part 1), w_i = beta_i zeta_{end,i}.
+//
+// With d_k = d_v and single products each workgroup owns half of the columns of both
+// parts, so both read the same bytes (k and half of v) and write the same share of the
+// states; otherwise one workgroup owns H and the other G^T.
 //
 // When fp32 states leave the kernel (the final states), w ⊙ Y is split into bf16
 // high and low parts (two products, ~16-bit weights, states fp32-accurate); when
@@ -446,8 +450,12 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
     constexpr int CS = kWideThreads / kWave / NS;  // column shares per row block
     constexpr int FPP = 8 * kWideThreads / 32;     // features staged per pass (8 per thread group)
     const ForwardShape s = a.s;
-    const int blk = xcd_major_block(blockIdx.x, gridDim.x);  // H and G^T of one segment share an L2
-    const int part = blk % 2;
+    const int blk = xcd_major_block(blockIdx.x, gridDim.x);  // the two halves of a segment share an L2
+    // d_k = d_v, bf16 states only: workgroup `half` owns H's columns and G^T's columns
+    // half * d/2 .. + d/2 - 1 (both halves then read k and half of v); otherwise half 0
+    // owns H and half 1 owns G^T.  (The split-product variants ran 22-28% slower balanced.)
+    constexpr bool BAL = DK == DV && !SPLIT;
+    const int half = blk % 2;
     const int seg = sg.first + (blk / 2) % sg.count;
     const int64_t bh = blk / 2 / sg.count;
     const int nbeg = seg * sg.len, nend = min(nbeg + sg.len, s.n_chunks);  // this segment's chunks
@@ -462,13 +470,20 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
     __shared__ __attribute__((aligned(16))) uint16_t sBl[2][(DK > DV ? DK : DV) * LDT];         // lo(w_i y_i[c])
 
     auto run = [&](auto nc_tag) {
-        constexpr int NC = decltype(nc_tag)::value;  // columns of this part
+        constexpr int NC = decltype(nc_tag)::value;  // columns of this workgroup
         constexpr int NCT = NC / 16 / CS;            // 16-column tiles of this wave
         constexpr int NKQ = (DK + FPP - 1) / FPP, NY = (NC + FPP - 1) / FPP;  // staging passes
         const int sblk = wave % NS, cs = wave / NS;
-        const int ct0 = cs * NCT;
+        // Staged y column c: balanced, k feature c if c lies in this half's own region
+        // (c / (NC/2) == half), else v feature half * NC/2 + c % (NC/2); otherwise k (half 0)
+        // or v (half 1) feature c.  The wave's local column tiles lct0 .. are H's or G^T's
+        // (`part`), its global column tiles ct0 .. of that part.
+        auto y_from_k = [&](int c) { return BAL ? c / (NC / 2) == half : half == 0; };
+        const int lct0 = cs * NCT;
+        const int part = BAL ? int(!y_from_k(16 * lct0)) : half;
+        const int ct0 = (BAL && part) ? half * (NC / 32) + lct0 % (NC / 32) : lct0;
         const uint16_t* kp = static_cast<const uint16_t*>(a.k);
-        const uint16_t* yp = static_cast<const uint16_t*>(part ? a.v : a.k);
+        const uint16_t* vp = static_cast<const uint16_t*>(a.v);
 
         struct Regs {
             uint4 k[NKQ][2];  // k of tokens 2p, 2p+1, features 64m + 8fg ..
@@ -492,13 +507,13 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                 R.k[m][0] = *reinterpret_cast<const uint4*>(kp + r0 * DK + f0);
                 R.k[m][1] = *reinterpret_cast<const uint4*>(kp + r1 * DK + f0);
             }
-            if (part) {
 #pragma unroll
-                for (int m = 0; m < NY; ++m) {
-                    const int f0 = (FPP * m + 8 * fg) % NC;
-                    R.y[m][0] = *reinterpret_cast<const uint4*>(yp + r0 * DV + f0);
-                    R.y[m][1] = *reinterpret_cast<const uint4*>(yp + r1 * DV + f0);
-                }
+            for (int m = 0; m < NY; ++m) {
+                const int f0 = (FPP * m + 8 * fg) % NC;
+                if (y_from_k(f0)) continue;  // wave-uniform: k is already in R.k
+                const int vf = BAL ? half * (NC / 2) + f0 % (NC / 2) : f0;
+                R.y[m][0] = *reinterpret_cast<const uint4*>(vp + r0 * DV + vf);
+                R.y[m][1] = *reinterpret_cast<const uint4*>(vp + r1 * DV + vf);
             }
         };
         // Staging of a chunk into buffer b, in three pieces that the chunk loop interleaves
@@ -533,8 +548,9 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
 #pragma unroll
             for (int m = 0; m < NY; ++m) {
                 if (FPP * m + 8 * fg >= NC) continue;
-                const uint4 ya = part ? R.y[m][0] : R.k[m][0];
-                const uint4 yb = part ? R.y[m][1] : R.k[m][1];
+                const bool fk = m < NKQ && y_from_k(FPP * m + 8 * fg);
+                const uint4 ya = fk ? R.k[m < NKQ ? m : 0][0] : R.y[m][0];
+                const uint4 yb = fk ? R.k[m < NKQ ? m : 0][1] : R.y[m][1];
                 const uint32_t a4[4] = {ya.x, ya.y, ya.z, ya.w};
                 const uint32_t b4[4] = {yb.x, yb.y, yb.z, yb.w};
                 uint32_t* hi32 = reinterpret_cast<uint32_t*>(sBh[b]);
@@ -606,7 +622,7 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                 for (int rt = 0; rt < 2; ++rt) af[u][rt] = lds_frag(sA[b] + (32 * sblk + 16 * rt + ln) * LDT + 32 * u + 4 * g);
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
-                    const int c = 16 * (ct0 + ct) + ln;
+                    const int c = 16 * (lct0 + ct) + ln;
                     bfh[u][ct] = lds_frag(sBh[b] + c * LDT + 32 * u + 4 * g);
                     if (SPLIT) bfl[u][ct] = lds_frag(sBl[b] + c * LDT + 32 * u + 4 * g);
                 }
@@ -686,7 +702,7 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
         float* dst = nullptr;
         if (sg.totals) {
             dst = seg_total(seg);
-            if (part == 0 && tid == 0) sg.dec[bh * sg.total + seg] = dprod;
+            if (half == 0 && tid == 0) sg.dec[bh * sg.total + seg] = dprod;
         } else if (seg == sg.total - 1) {
             float* fin = part ? a.final_G : a.final_H;
             if (fin) dst = fin + bh * int64_t(NC) * DK;
@@ -700,7 +716,7 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
                     for (int ii = 0; ii < 4; ++ii) dst[tile_off(rt, ct, ii)] = acc[rt][ct][ii];
         }
     };
-    if (part == 0)
+    if (BAL || half == 0)
         run(std::integral_constant<int, DK>{});
     else
         run(std::integral_constant<int, DV>{});
