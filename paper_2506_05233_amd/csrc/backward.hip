@@ -65,6 +65,28 @@ __device__ __forceinline__ f32x4 mma16(const float* A, const float* B, f32x4 acc
     return acc;
 }
 
+// mma16 over contraction indices k0 .. K - 1 only (k0 a multiple of 4): for products
+// with a causally masked matrix whose entries below k0 are zero.  The skipped steps are
+// resolved at compile time wherever k0 is a constant of an unrolled loop.
+template <int K, int AM, int AK, int BK, int BN>
+__device__ __forceinline__ f32x4 mma16_from(const float* A, const float* B, int k0, f32x4 acc)
+{
+    const int lane = threadIdx.x % kWave, r = lane % 16, sl = lane / 16;
+    const float* a = A + r * AM + sl * AK;
+    const float* b = B + sl * BK + r * BN;
+    float av[K / 4], bv[K / 4];
+#pragma unroll
+    for (int i = 0; i < K / 4; ++i) {
+        if (4 * i < k0) continue;
+        av[i] = a[4 * i * AK];
+        bv[i] = b[4 * i * BK];
+    }
+#pragma unroll
+    for (int i = 0; i < K / 4; ++i)
+        if (4 * i >= k0) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[i], acc, 0, 0, 0);
+    return acc;
+}
+
 // The same product split in two: the B operand values of one tile (a global matrix,
 // loaded one tile ahead so its latency overlaps the previous tile's products), then
 // the products with A read from LDS.
@@ -637,7 +659,8 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
             if (!S::own(w, st)) continue;
-            const f32x4 in = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * at, kZero4);
+            // M1[s][t] = 0 for t < s: the token sum of row tile st starts at 16 st
+            const f32x4 in = mma16_from<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * at, 16 * st, kZero4);
             const f32x4 ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv, kZero4);  // (K A^G^T)[s][a]
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -665,8 +688,8 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
             if (!S::own(w, st)) continue;
-            const f32x4 pq = mma16<kC, kLdC, 1, kLdT, 1>(sM1 + 16 * st * kLdC, sT0 + 16 * bt, kZero4);
-            const f32x4 pe = mma16<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * bt, kZero4);
+            const f32x4 pq = mma16_from<kC, kLdC, 1, kLdT, 1>(sM1 + 16 * st * kLdC, sT0 + 16 * bt, 16 * st, kZero4);
+            const f32x4 pe = mma16_from<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * bt, 16 * st, kZero4);
             in[st] = pq - pe;
         }
         __syncthreads();
@@ -775,13 +798,14 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     }
 
     // ---- W[p][s] = sum_{t>=s} zeta_{t,s} Qm[p][t] (Qm Z^T), into sM0: wave w row tile
-    // w % 4, column tiles 2 (w / 4) ..
+    // w % 4, column tiles w / 4 and 3 - w / 4 (the sum of column tile st starts at 16 st,
+    // so every wave runs 20 of the 32 steps)
     {
         const int rt = w % 4;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            const int st = 2 * (w / 4) + h;
-            const f32x4 wq = mma16<kC, kLdC, 1, 1, kLdC>(sM2 + 16 * rt * kLdC, sZ + 16 * st * kLdC, kZero4);
+            const int st = h ? 3 - w / 4 : w / 4;
+            const f32x4 wq = mma16_from<kC, kLdC, 1, 1, kLdC>(sM2 + 16 * rt * kLdC, sZ + 16 * st * kLdC, 16 * st, kZero4);
 #pragma unroll
             for (int r = 0; r < 4; ++r) sM0[(16 * rt + 4 * g + r) * kLdC + 16 * st + ln] = wq[r];
         }
