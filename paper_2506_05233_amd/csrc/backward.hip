@@ -253,7 +253,7 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     const int valid = int(min<int64_t>(kC, s.seq_len - t0));
     const int64_t tok0 = bh * s.seq_len + t0;
     const int tid = threadIdx.x;
-    const int w = tid / kWave, lane = tid % kWave, g = lane / 16, ln = lane % 16;
+    const int w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave, g = lane / 16, ln = lane % 16;
     const int t = 16 * w + ln;  // this lane's token (column of the transposed products)
 
     __shared__ float sE[kC * kLdT];   // e_t [t][a]
@@ -267,10 +267,15 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     Tile<DK, Tin> tk;  // the keys, in flight during the value products
     tk.fetch(static_cast<const Tin*>(a.k), tok0, valid);
     __syncthreads();
-    // S^T[i][t] = beta_i zeta_{t,i} (v_i . e_t) for i <= t (0 otherwise and past the end)
+    // S^T[i][t] = beta_i zeta_{t,i} (v_i . e_t) for i <= t (0 otherwise and past the end);
+    // row tiles it > w lie wholly above this wave's tokens and are zero
     f32x4 sT[kC / 16];
 #pragma unroll
     for (int it = 0; it < kC / 16; ++it) {
+        if (it > w) {
+            sT[it] = kZero4;
+            continue;
+        }
         const f32x4 ve = mma16<DV, kLdT, 1, 1, kLdT>(sX + 16 * it * kLdT, sE + 16 * w * kLdT, kZero4);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -301,17 +306,22 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
         f32x4 eg = kZero4;
 #pragma unroll
         for (int i = 0; i < DV / 4; ++i) eg = __builtin_amdgcn_mfma_f32_16x16x4f32(ga[bt % 2][i], eb[i], eg, 0, 0, 0);
-        // K^T S^T: A(m = b, k = i) = k_i[16 bt + m] with i = 16 it + 4 g + r
+        // K^T S^T: A(m = b, k = i) = k_i[16 bt + m] with i = 16 it + 4 g + r (the zero
+        // tiles it > w skipped)
         float ka[kC / 4];
 #pragma unroll
-        for (int it = 0; it < kC / 16; ++it)
+        for (int it = 0; it < kC / 16; ++it) {
+            if (it > w) continue;
 #pragma unroll
             for (int r = 0; r < 4; ++r) ka[4 * it + r] = sX[(16 * it + 4 * g + r) * kLdT + 16 * bt + ln];
+        }
         f32x4 sk = kZero4;
 #pragma unroll
-        for (int it = 0; it < kC / 16; ++it)
+        for (int it = 0; it < kC / 16; ++it) {
+            if (it > w) continue;
 #pragma unroll
             for (int r = 0; r < 4; ++r) sk = __builtin_amdgcn_mfma_f32_16x16x4f32(ka[4 * it + r], sT[it][r], sk, 0, 0, 0);
+        }
         // lane (g, n): u_t[16 bt + 4g + r], r = 0..3
         if (t < valid) {
             const f32x4 u = zs * eg + sk;
