@@ -258,6 +258,25 @@ def test_segmented_state_scan_matches_oracle(dk, dv):
     assert rel_l2(Gs.cpu().numpy(), G1.cpu().numpy()) <= 1e-6
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_segmented_forward_bf16_states_only_path(d):
+    """The forward without fp32 final states: the bf16 scan's segment totals and its
+    walk both run on the single-product kernels (each of a sequence's two workgroups
+    owning half the columns of H and of G^T).  Gates within 1e-3 of one keep every
+    earlier segment visible in the outputs, and a zero gate resets memory inside a
+    segment; every output against the oracle."""
+    T = 35 * 64 + 17
+    x = W.forward_inputs(1, 2, T, d, d, "bf16", 4.0, seed=71 + d)
+    rng = np.random.default_rng(7101 + d)
+    x["gamma"][...] = rng.uniform(0.999, 1.0, size=x["gamma"].shape).astype(np.float32)
+    x["gamma"][0, 1, 20 * 64 + 5] = 0.0
+    got = _gpu_forward(x, "bf16", 15, 64, precision=L.MESA_PREC_BF16)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 15)["out"]
+    e = rel_l2(got, ref)
+    _say("segmented forward d=%d, gates near one: out %.3e" % (d, e))
+    assert e <= TOL_BF16
+
+
 def test_segmented_state_scan_long_memory():
     """Gates within 1e-3 of one (a few exactly one): the decay across a 9-chunk segment
     stays above 0.5, so every earlier segment's total reaches the final states with a
