@@ -565,6 +565,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     __shared__ float sTok[5][kC];     // per token: dbeta (intra), v^T A^G k, k^T A^H k, g, h
     __shared__ float sPart[kGW];
     __shared__ float sRed[kGW][kC];   // per-wave partial sums per token
+    __shared__ float sRed2[kGW][kC];  // the same for a second quantity
     __shared__ float sF;
 
     // Token tiles in registers: each phase's tiles are fetched while the phase before it
@@ -635,22 +636,29 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         if (lane == 0) sTok[0][p] = db;
     }
     auto tok = [&](int st, int r) { return 16 * st + 4 * g + r; };
-    // sum the partials p[st][r] (token tok(st, r); zero on the token tiles the wave does not
-    // own) over lanes and waves into out[token], in a fixed order
-    auto reduce_tokens = [&](const float (&p)[4][4], float* out) {
+    // sum the partials p[st][r] and q[st][r] (token tok(st, r); zero on the token tiles the
+    // wave does not own) over lanes and waves into out[token] and out2[token], each in a
+    // fixed order (16-lane row sums, then waves 0 .. kGW - 1); wave 0 forms out, wave 1 out2
+    auto reduce_tokens2 = [&](const float (&p)[4][4], const float (&q)[4][4], float* out, float* out2) {
 #pragma unroll
         for (int st = 0; st < 4; ++st)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const float v = row16_sum(p[st][r]);
-                if (ln == 0) sRed[w][tok(st, r)] = v;
+                const float u = row16_sum(q[st][r]);
+                if (ln == 0) {
+                    sRed[w][tok(st, r)] = v;
+                    sRed2[w][tok(st, r)] = u;
+                }
             }
         __syncthreads();
-        if (tid < kC) {
+        if (tid < 2 * kC) {
+            const int tk_ = tid % kC;
+            float (*src)[kC] = tid < kC ? sRed : sRed2;
             float acc = 0.0f;
 #pragma unroll
-            for (int u = 0; u < kGW; ++u) acc += sRed[u][tid];
-            out[tid] = acc;
+            for (int u = 0; u < kGW; ++u) acc += src[u][tk_];
+            (tid < kC ? out : out2)[tk_] = acc;
         }
         __syncthreads();
     };
@@ -723,8 +731,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
                 pk[st][r] += 0.5f * kb * sh[r];
             }
         }
-        reduce_tokens(pa, sTok[1]);
-        reduce_tokens(pk, sTok[2]);
+        reduce_tokens2(pa, pk, sTok[1], sTok[2]);
     }
 
     // ---- g_t = e_t^T G_c q*_t, h_t = e*_t^T H_c q*_t, F = <A^G, G_c> + (1/2) <S^H, H_c>,
@@ -748,7 +755,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
 #pragma unroll
             for (int r = 0; r < 4; ++r) pg[st][r] += eg[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
         }
-        reduce_tokens(pg, sTok[3]);
+        __syncthreads();  // every wave is done with d in sT1 (g's token sums wait for h's)
         te.put(sT1, valid);
         __syncthreads();
 #pragma unroll
@@ -758,7 +765,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
 #pragma unroll
             for (int r = 0; r < 4; ++r) ph[st][r] += eh[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
         }
-        reduce_tokens(ph, sTok[4]);
+        reduce_tokens2(pg, ph, sTok[3], sTok[4]);
         // F: every thread a strided slice of the two Frobenius products, 16-byte loads,
         // all issued before the products
         float fr = 0.0f;
