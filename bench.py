@@ -286,11 +286,38 @@ def run_decode(args, torch, L, W):
     }
 
 
+def cpu_model():
+    """Model name of the host CPU from /proc/cpuinfo (None where unreadable)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_quota():
+    """CPUs this process may keep busy: the cgroup CPU quota (cgroup v2 cpu.max),
+    else the CPUs in its affinity mask."""
+    import oracle
+    usable = oracle.default_threads()
+    try:
+        with open("/sys/fs/cgroup/cpu.max") as f:
+            quota, period = f.read().split()[:2]
+        if quota != "max":
+            return max(1, min(usable, int(int(quota) // int(period))))
+    except (OSError, ValueError):
+        pass
+    return usable
+
+
 def cpu_baseline(args, x, w):
     import numpy as np
     import oracle
     n_seq = args.cpu_sequences
-    threads = min(n_seq, oracle.default_threads(), 16)
+    threads = min(n_seq, cpu_quota())
     pairs = [(i // w.heads % w.batch, i % w.heads) for i in range(n_seq)]
     sl = {n: np.stack([x[n][b, h] for b, h in pairs])[:, None] for n in ("q", "k", "v", "gamma", "beta")}
     # one head row of lambda per sequence: run the oracle once per distinct head set
@@ -309,6 +336,8 @@ def cpu_baseline(args, x, w):
     token_heads = n_seq * w.seq_len
     return {
         "value": token_heads / w.heads / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+        "host_cpus": os.cpu_count(), "host_cpus_in_affinity": oracle.default_threads(),
+        "host_cpus_quota": cpu_quota(), "cpu_model": cpu_model(),
         "sample": "%d of the %d (batch, head) sequences of %s (all of them when equal), %d tokens "
                   "each, fp64 sequential recurrence with %d-step CG, one sequence per thread; "
                   "tokens/s = token-heads/s / %d heads; %.1f s wall"

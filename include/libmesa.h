@@ -3,7 +3,7 @@
  * AMD Instinct MI355X (gfx950).
  *
  * For every (batch b, head h) the layer keeps two gated states, starting from
- * H_0 = G_0 = 0 (Sec. 3, "A new parallelizable Mesa layer"; App. D, Eq.
+ * H_0 = G_0 = 0 (Sec. 2, "A new parallelizable Mesa layer"; App. D, Eq.
  * app-mesa-dynamics; App. E for the input gate):
  *
  *     H_t = gamma_t H_{t-1} + beta_t k_t k_t^T        (d_k x d_k, symmetric)
@@ -23,7 +23,7 @@
  * of a subnormal.  A column also stops, keeping its x, when p^T A p is not a
  * positive normal number (breakdown).
  *
- * The forward pass is evaluated chunkwise (Sec. 3, Eq. gla_matrix; App. D,
+ * The forward pass is evaluated chunkwise (Sec. 2, Eq. gla_matrix; App. D,
  * Eq. gla and Eq. q_star_parallel): states are materialised only at chunk
  * boundaries, and every CG product (H_t + Lambda) p inside a chunk is an
  * inter-chunk state term plus a causally masked, gate-weighted K K^T term.
@@ -38,7 +38,11 @@
  *     gates, Lambda, states and outputs are fp32.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *     the call returns without synchronising.  Errors raised while kernels run
- *     surface at the caller's next synchronisation.
+ *     surface at the caller's next synchronisation.  When the environment
+ *     variable MESA_SYNC_AFTER_LAUNCH is set to anything other than "" or "0"
+ *     (read once, at the library's first call), every call that launched work
+ *     synchronises `stream` before it returns and reports a failed kernel as
+ *     MESA_ERR_HIP (a debugging aid; it serialises the caller with the GPU).
  *   - Argument checks run on the host before any launch; a failed check
  *     returns its status code and neither launches nor writes anything.
  *   - Value ranges are preconditions and are not checked (that would read
@@ -66,7 +70,7 @@ extern "C" {
  *   MESA_PREC_BF16 : matrix-core products with bf16 operands (the fp32 state and
  *                    the fp32 CG direction are rounded to bf16 as operands) and
  *                    fp32 accumulation; every CG vector, scalar and reduction
- *                    stays fp32 (App. H.5 keeps the solver in fp32; this mode
+ *                    stays fp32 (App. G.5 keeps the solver in fp32; this mode
  *                    trades operand precision for matrix-core throughput). */
 #define MESA_PREC_AUTO 0
 #define MESA_PREC_F32 1
@@ -163,7 +167,7 @@ int mesa_forward_solve(const void* q, const void* k, const void* v, const float*
                        int precision, float* out, float* qstar_out, const void* workspace,
                        size_t workspace_bytes, void* stream);
 
-/* One recurrent decode step for `batch` independent sequences (Sec. 3,
+/* One recurrent decode step for `batch` independent sequences (Sec. 2,
  * recurrent inference mode; App. C last paragraph: CG is applied to H_t + Lambda
  * directly).  For each (sequence, head), in place:
  *     H <- gamma H + beta k k^T;  G <- gamma G + beta v k^T;
@@ -181,7 +185,7 @@ int mesa_decode_step(float* state_H, float* state_G, const void* q, const void* 
                      int64_t heads, int64_t d_k, int64_t d_v, int dtype, int n_cg, float* out,
                      void* stream);
 
-/* Dynamic stopping (App. C, Alg. 1 with a tolerance; Sec. 4: the layer spends
+/* Dynamic stopping (App. C, Alg. 1 with a tolerance; Secs. 3 and 5: the layer spends
  * as many CG iterations on a token as its system needs).  Each token's solve
  * stops after the first iteration whose residual satisfies |r_k| <= eps |r_0|
  * (r_0 the residual of the Jacobi start), or after max_cg iterations.

@@ -6,7 +6,7 @@ CPU-baseline leg of ``bench.py`` may import this package.  The product path
 it shares no code with that path.
 
 The arithmetic lives in ``mesa_oracle.c`` (plain C, fp64, the sequential
-recurrence of Sec. 3 / App. D with Alg. 1 conjugate gradients or an exact
+recurrence of Sec. 2 / App. D with Alg. 1 conjugate gradients or an exact
 Cholesky solve).  This module compiles it with gcc on first use, wraps it with
 ctypes, and adds one more route to the states: the unrolled sums of App. D,
 H_t = sum_i zeta_{t,i} beta_i k_i k_i^T and G_t = sum_i zeta_{t,i} beta_i v_i k_i^T,

@@ -8,7 +8,7 @@
  *
  * What it computes (MesaNet, arXiv 2506.05233):
  *   For each (batch, head) independently, starting from H_0 = G_0 = 0:
- *     H_t = gamma_t H_{t-1} + beta_t k_t k_t^T          (Sec. 3, state recurrences;
+ *     H_t = gamma_t H_{t-1} + beta_t k_t k_t^T          (Sec. 2, state recurrences;
  *     G_t = gamma_t G_{t-1} + beta_t v_t k_t^T           App. E, gated form)
  *     q*_t = (H_t + Lambda)^{-1} q_t                     (Eq. mesa-layer-final)
  *     o_t  = G_t q*_t                                    (App. D, Eq. app-mesa-dynamics)
@@ -67,7 +67,7 @@ enum { ORACLE_INIT_JACOBI = 0, ORACLE_INIT_QUERY = 1 };
  * relative tolerance eps >= 0 (eps = 0: the fixed-step solve).
  * init = ORACLE_INIT_JACOBI: x0 = b / diag(A)  (the paper's choice);
  * init = ORACLE_INIT_QUERY : x0 = b            (the "zero CG steps gives GLA"
- *                                               remark of Sec. 4; tests only).
+ *                                               remark of Sec. 3; tests only).
  * work must hold 3n doubles.  Returns the number of loop iterations that
  * updated x. */
 int oracle_cg(const double* A, const double* b, int64_t n, int n_cg, int init, double eps,

@@ -1,6 +1,7 @@
 """Build libmesa (hipcc, gfx950) in-tree: paper_2506_05233_amd/_lib/libmesa.so."""
 from __future__ import annotations
 
+import concurrent.futures
 import glob
 import os
 import subprocess
@@ -19,7 +20,6 @@ HIPCC_FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-Wall",
     "-Wno-unused-function",
     # keep the compiler from forming packed fp32 instructions
@@ -37,15 +37,31 @@ def sources():
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every HIP source into libmesa.so (always recompiles)."""
+    """Compile every HIP source into libmesa.so (always recompiles): one object per
+    source, compiled side by side, then one shared-library link."""
     os.makedirs(LIB_DIR, exist_ok=True)
+    obj_dir = os.path.join(LIB_DIR, "obj")
+    os.makedirs(obj_dir, exist_ok=True)
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB_PATH + ".tmp%d" % os.getpid()
-    cmd = [hipcc] + HIPCC_FLAGS + ["-o", tmp] + sources()
+    tag = "%d" % os.getpid()
+    jobs = []
+    for src in sources():
+        obj = os.path.join(obj_dir, os.path.basename(src)[:-4] + "." + tag + ".o")
+        jobs.append((src, obj, [hipcc] + HIPCC_FLAGS + ["-c", "-o", obj, src]))
+    workers = max(1, min(len(jobs), int(os.environ.get("MAX_JOBS", "0")) or os.cpu_count() or 1, 16))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+        for src, obj, cmd in jobs:
+            if verbose:
+                print(" ".join(cmd), flush=True)
+        list(ex.map(lambda j: subprocess.run(j[2], check=True), jobs))
+    tmp = LIB_PATH + ".tmp" + tag
+    link = [hipcc, "--offload-arch=" + OFFLOAD_ARCH, "-shared", "-fPIC", "-o", tmp] + [j[1] for j in jobs]
     if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+        print(" ".join(link), flush=True)
+    subprocess.run(link, check=True)
     os.replace(tmp, LIB_PATH)
+    for _, obj, _ in jobs:
+        os.remove(obj)
     return LIB_PATH
 
 

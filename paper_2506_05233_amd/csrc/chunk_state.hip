@@ -4,7 +4,7 @@
 //   H_{c+C} = zeta_{c+C,c} H_c + sum_{i in chunk} zeta_{c+C,i} beta_i k_i k_i^T
 //   G_{c+C} = zeta_{c+C,c} G_c + sum_{i in chunk} zeta_{c+C,i} beta_i v_i k_i^T
 //
-// (the gated recurrences of Sec. 3 summed over one chunk, unrolled as in App. D).
+// (the gated recurrences of Sec. 2 summed over one chunk, unrolled as in App. D).
 // One workgroup owns a 16-row tile of H or of G for one (batch, head) and
 // walks the chunks in order, so every state element is written exactly once per
 // chunk with coalesced stores.  The tile stays in registers between chunks.

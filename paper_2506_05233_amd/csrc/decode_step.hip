@@ -1,4 +1,4 @@
-// Recurrent decode step of the Mesa layer (Sec. 3, recurrent inference mode;
+// Recurrent decode step of the Mesa layer (Sec. 2, recurrent inference mode;
 // App. C, last paragraph: at inference CG runs on H_t + Lambda directly).
 //
 // One workgroup of d_k threads (d_k / 64 waves) per (sequence, head); the step

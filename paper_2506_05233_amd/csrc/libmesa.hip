@@ -4,6 +4,7 @@
 
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "mesa_kernels.hpp"
@@ -23,6 +24,26 @@ struct Range {
 };
 Range range_of(const void* p, int64_t bytes) { return {uintptr_t(p), uintptr_t(p) + uintptr_t(bytes)}; }
 bool overlaps(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+// MESA_SYNC_AFTER_LAUNCH (read once, at the first call): when set to anything but
+// "" or "0", every entry point synchronises its stream after its launches and turns
+// an execution error into MESA_ERR_HIP.
+bool sync_after_launch()
+{
+    static const bool on = [] {
+        const char* e = getenv("MESA_SYNC_AFTER_LAUNCH");
+        return e != nullptr && e[0] != '\0' && strcmp(e, "0") != 0;
+    }();
+    return on;
+}
+
+// The status an entry point returns once its launches are enqueued on `stream`.
+int finish(int status, void* stream)
+{
+    if (status != MESA_OK || !sync_after_launch()) return status;
+    if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return MESA_ERR_HIP;
+    return hipGetLastError() == hipSuccess ? MESA_OK : MESA_ERR_HIP;
+}
 
 int check_sizes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v,
                 int dtype, int n_cg)
@@ -224,8 +245,8 @@ int mesa_forward_ex(const void* q, const void* k, const void* v, const float* ga
     if (st != MESA_OK || batch == 0 || heads == 0) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     st = launch_states(c, !states_only, s);
-    if (st != MESA_OK || states_only) return st;
-    return launch_solve(c, s);
+    if (st == MESA_OK && !states_only) st = launch_solve(c, s);
+    return finish(st, stream);
 }
 
 int mesa_forward(const void* q, const void* k, const void* v, const float* gamma,
@@ -249,7 +270,7 @@ int mesa_forward_states(const void* k, const void* v, const float* gamma, const 
               true};
     int st = validate_forward(c);
     if (st != MESA_OK || batch == 0 || heads == 0) return st;
-    return launch_states(c, true, static_cast<hipStream_t>(stream));
+    return finish(launch_states(c, true, static_cast<hipStream_t>(stream)), stream);
 }
 
 int mesa_forward_solve(const void* q, const void* k, const void* v, const float* gamma,
@@ -262,7 +283,7 @@ int mesa_forward_solve(const void* q, const void* k, const void* v, const float*
               precision, out, qstar_out, nullptr, nullptr, workspace, workspace_bytes, true, true};
     int st = validate_forward(c);
     if (st != MESA_OK || batch == 0 || heads == 0) return st;
-    return launch_solve(c, static_cast<hipStream_t>(stream));
+    return finish(launch_solve(c, static_cast<hipStream_t>(stream)), stream);
 }
 
 int mesa_decode_step(float* state_H, float* state_G, const void* q, const void* k, const void* v,
@@ -313,8 +334,9 @@ int decode_step(float* state_H, float* state_G, const void* q, const void* k, co
     }
     mesa::DecodeArgs da{batch, heads, int(d_k), int(d_v), dtype == MESA_DTYPE_BF16, state_H, state_G,
                         q, k, v, gamma, beta, lambda, max_cg, out, eps * eps, steps_out, packed};
-    return mesa::launch_decode_step(da, static_cast<hipStream_t>(stream)) == hipSuccess ? MESA_OK
-                                                                                       : MESA_ERR_HIP;
+    return finish(mesa::launch_decode_step(da, static_cast<hipStream_t>(stream)) == hipSuccess ? MESA_OK
+                                                                                              : MESA_ERR_HIP,
+                  stream);
 }
 
 // pack (to_packed) or unpack the symmetric decode state H of batch x heads pairs
@@ -332,7 +354,7 @@ int convert_state(const float* src, float* dst, int64_t batch, int64_t heads, in
     hipStream_t s = static_cast<hipStream_t>(stream);
     const hipError_t e = to_packed ? mesa::launch_pack_state(src, dst, pairs, int(d_k), s)
                                    : mesa::launch_unpack_state(src, dst, pairs, int(d_k), s);
-    return e == hipSuccess ? MESA_OK : MESA_ERR_HIP;
+    return finish(e == hipSuccess ? MESA_OK : MESA_ERR_HIP, stream);
 }
 
 }  // namespace
@@ -381,8 +403,8 @@ int mesa_forward_tol(const void* q, const void* k, const void* v, const float* g
     if (st != MESA_OK || batch == 0 || heads == 0) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     st = launch_states(c, true, s);
-    if (st != MESA_OK) return st;
-    return launch_solve(c, s);
+    if (st == MESA_OK) st = launch_solve(c, s);
+    return finish(st, stream);
 }
 
 }  // extern "C"
@@ -429,12 +451,17 @@ size_t mesa_backward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_l
     return size_t(bwd_layout(batch, heads, seq_len, d_k, d_v).total);
 }
 
-int mesa_backward(const void* k, const void* v, const float* gamma, const float* beta, const float* lambda,
-                  int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg,
-                  int precision, const float* qstar, const float* dout, float* dq, float* dk, float* dv,
-                  float* dgamma, float* dbeta, float* dlambda, void* workspace, size_t workspace_bytes,
-                  void* stream)
+}  // extern "C"
+
+namespace {
+
+int backward_launch(const void* k, const void* v, const float* gamma, const float* beta, const float* lambda,
+                    int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg,
+                    int precision, const float* qstar, const float* dout, float* dq, float* dk, float* dv,
+                    float* dgamma, float* dbeta, float* dlambda, void* workspace, size_t workspace_bytes,
+                    void* stream, bool& launched)
 {
+    launched = false;
     int st = check_sizes(batch, heads, seq_len, d_k, d_v, dtype, n_cg);
     if (st != MESA_OK) return st;
     if (precision != MESA_PREC_AUTO && precision != MESA_PREC_F32 && precision != MESA_PREC_BF16)
@@ -474,6 +501,7 @@ int mesa_backward(const void* k, const void* v, const float* gamma, const float*
     } else if (overlaps(range_of(dlambda, heads * d_k * 4), range_of(lambda, heads * d_k * 4))) {
         return MESA_ERR_ARG;
     }
+    launched = true;
     if (seq_len == 0)  // no tokens: dLambda is an empty sum
         return mesa::launch_fill_zero(dlambda, heads * d_k, s) == hipSuccess ? MESA_OK : MESA_ERR_HIP;
 
@@ -516,6 +544,23 @@ int mesa_backward(const void* k, const void* v, const float* gamma, const float*
     for (int stage = 1; stage <= 3; ++stage)
         if (mesa::launch_backward_stage(ba, stage, s) != hipSuccess) return MESA_ERR_HIP;
     return MESA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mesa_backward(const void* k, const void* v, const float* gamma, const float* beta, const float* lambda,
+                  int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg,
+                  int precision, const float* qstar, const float* dout, float* dq, float* dk, float* dv,
+                  float* dgamma, float* dbeta, float* dlambda, void* workspace, size_t workspace_bytes,
+                  void* stream)
+{
+    bool launched = false;
+    const int st = backward_launch(k, v, gamma, beta, lambda, batch, heads, seq_len, d_k, d_v, dtype, n_cg,
+                                   precision, qstar, dout, dq, dk, dv, dgamma, dbeta, dlambda, workspace,
+                                   workspace_bytes, stream, launched);
+    return launched ? finish(st, stream) : st;
 }
 
 }  // extern "C"

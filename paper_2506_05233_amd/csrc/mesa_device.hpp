@@ -87,7 +87,7 @@ __device__ __forceinline__ int wave_scan_max(int x)
 __device__ __forceinline__ float lane_value(float x, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l)); }
 __device__ __forceinline__ int lane_value(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
 
-// Gate log-cumsums of one chunk (Sec. 3: zeta_{t,s} = prod_{s<i<=t} gamma_i).
+// Gate log-cumsums of one chunk (Sec. 2: zeta_{t,s} = prod_{s<i<=t} gamma_i).
 // Called by the 64 lanes of ONE wave, for C <= 64 tokens starting at `gamma`
 // (tokens at or beyond `valid` count as gamma = 1, i.e. absent).  For in-chunk
 // token j it stores

@@ -5,9 +5,9 @@ layer's arithmetic, so both the HIP path and the fp64 oracle can consume its
 output without sharing any of the method.  Distributions follow the layer's
 front end (App. E): queries and keys are L2-normalised, forget and input gates
 are sigmoids of Gaussian logits, and the regulariser Lambda is a positive
-diagonal with the 0.25 lower bound of App. H.5 (here U[0.25, 1] per head and
-dimension).  Key size 128 matches the 1B model (App. H), train length 2048 and
-10-30 CG steps match Sec. 4-5.  No dataset is used.
+diagonal with the 0.25 lower bound of App. G.5 (here U[0.25, 1] per head and
+dimension).  Key size 128 matches the 1B model (App. G.4), train length 2048 and
+10-30 CG steps match Secs. 3-5 and App. G.7.  No dataset is used.
 
 Draw order per workload: q, k, v, gamma logits, beta logits, lambda.  Values
 are produced in fp64, rounded to fp32, and, for bf16 workloads, q/k/v are then
@@ -153,7 +153,7 @@ def repeated_key_inputs(batch, heads, seq_len, d_k, d_v, pool=1, dtype="bf16", g
                         seed=7):
     """Ill-conditioned stress input: keys drawn from a pool of `pool` unit
     vectors per head, gates near one.  Repeated tokens with gamma close to one
-    are the case App. H.5 singles out as hard for the solver."""
+    are the case App. G.5 singles out as hard for the solver."""
     rng = np.random.default_rng(seed)
     q = _unit_rows(rng, (batch, heads, seq_len, d_k))
     pool_keys = _unit_rows(rng, (batch, heads, pool, d_k))

@@ -156,15 +156,16 @@ def test_bf16_path_query_scale_is_exact():
 
 
 def test_stress_repeated_keys_bf16_path_reported():
-    """Single-pass bf16 operands are validated on the workload distributions,
-    not on adversarial inputs: on the repeated-key stress input the error is
-    reported and bounded loosely (it is expected to exceed the bf16 tolerance)."""
+    """Single-pass bf16 operands are validated on the workload distributions, not
+    on adversarial inputs: on the repeated-key stress input (App. G.5's repeated
+    tokens with gates near one) the error exceeds the bf16 tolerance.  It is pinned
+    near its measured value (~0.13 with one repeated key) so that a regression shows."""
     x = W.repeated_key_inputs(1, 2, 512, 128, 128, pool=1, dtype="bf16")
     got = _gpu_forward(x, "bf16", 20, 64, precision=L.MESA_PREC_BF16)
     ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 20)["out"]
     e = rel_l2(got, ref)
     _say("stress pool=1 bf16 matrix-core products: %.3e" % e)
-    assert np.isfinite(got).all() and e <= 0.25
+    assert np.isfinite(got).all() and e <= 0.15
 
 
 def test_chunk_size_invariance():
@@ -352,36 +353,72 @@ def _decode_state_pool(w, n_pool):
     return H.astype(np.float32), G.astype(np.float32)   # [n_pool, H, d, d]
 
 
-def test_decode_full_size_sampled_steps():
+def test_decode_full_workload_1024_steps():
+    """The decode workload as specified: 256 sequences x 16 heads, d = 128, 15 CG
+    steps, 1024 consecutive steps, on the full layout and (separately) on the packed
+    symmetric state.  Every pair starts from an oracle-prefilled state (4096 gated
+    updates; 8 distinct sequences' states, sequence s taking those of s % 8) and
+    receives its own seeded token at every step.  Checked against the oracle:
+    every pair over the first 16 steps; 64 sampled pairs (four sequences with
+    distinct prefill states x 16 heads) at every one of the 1024 steps, and their
+    states after the last step."""
     w = W.DECODE_BF16
-    _say("decode full size %s" % w.name)
-    n_pool = 4
+    n_pool, n_all = 8, 16
+    _say("decode %s: 1024 steps on the full batch" % w.name)
     Hp, Gp = _decode_state_pool(w, n_pool)
-    # every sequence s starts from pool state s % n_pool (per head)
+    Hp = np.triu(Hp) + np.swapaxes(np.triu(Hp, 1), -1, -2)   # exactly symmetric fp32
     idx = np.arange(w.seqs) % n_pool
     H0 = np.ascontiguousarray(Hp[idx])
     G0 = np.ascontiguousarray(Gp[idx])
     lam = W.decode_lambda(w)
-    dH = torch.from_numpy(H0).cuda()
-    dG = torch.from_numpy(G0).cuda()
     dlam = torch.from_numpy(lam).cuda()
-    sample = [0, 1, 77, 255]
+    dH, dG = torch.from_numpy(H0).cuda(), torch.from_numpy(G0).cuda()
+    pH, pG = L.pack_state(dH), dG.clone()
+    sample = [0, 13, 130, 255]                # prefill states 0, 5, 2, 7
     rH = H0[sample].astype(np.float64)
     rG = G0[sample].astype(np.float64)
-    worst = 0.0
-    for step in range(8):
+    first_in, first_out = [], []
+    worst_full, worst_packed, worst_at = 0.0, 0.0, {}
+    for step in range(w.steps):
         x = W.decode_step_inputs(w, step)
         d = to_device(x, w.dtype)
-        out = L.decode_step(dH, dG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], dlam, w.n_cg)
+        of = L.decode_step(dH, dG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], dlam, w.n_cg)
+        op = L.decode_step(pH, pG, d["q"], d["k"], d["v"], d["gamma"], d["beta"], dlam, w.n_cg, packed=True)
         torch.cuda.synchronize()
+        of, op = of.cpu().numpy(), op.cpu().numpy()
+        assert np.isfinite(of).all() and np.isfinite(op).all(), step
+        if step < n_all:
+            first_in.append(x)
+            first_out.append((of, op))
         sx = {n: x[n][sample] for n in x}
         ro, rH, rG = oracle.decode_step(rH, rG, sx["q"], sx["k"], sx["v"], sx["gamma"], sx["beta"],
-                                        lam, w.n_cg)
-        worst = max(worst, rel_l2(out.cpu().numpy()[sample], ro))
-    _say("  decode worst step rel L2 %.3e" % worst)
-    assert worst <= TOL_BF16
-    assert rel_l2(dH.cpu().numpy()[sample], rH) <= 1e-5
-    assert rel_l2(dG.cpu().numpy()[sample], rG) <= 1e-5
+                                        lam, w.n_cg, threads=16)
+        ef, ep = rel_l2(of[sample], ro), rel_l2(op[sample], ro)
+        worst_full, worst_packed = max(worst_full, ef), max(worst_packed, ep)
+        if step + 1 in (1, 16, 64, 256, 1024):
+            worst_at[step + 1] = (ef, ep)
+        if (step + 1) % 128 == 0:
+            _say("  step %d: sampled pairs rel L2 full %.2e packed %.2e" % (step + 1, ef, ep))
+    _say("  worst over 1024 steps: full %.3e packed %.3e; at steps %s" % (worst_full, worst_packed, worst_at))
+    assert worst_full <= TOL_BF16 and worst_packed <= TOL_BF16
+    eH, eG = rel_l2(dH.cpu().numpy()[sample], rH), rel_l2(dG.cpu().numpy()[sample], rG)
+    ePH = rel_l2(L.unpack_state(pH).cpu().numpy()[sample], rH)
+    ePG = rel_l2(pG.cpu().numpy()[sample], rG)
+    _say("  final states rel L2: H %.2e G %.2e (packed H %.2e G %.2e)" % (eH, eG, ePH, ePG))
+    assert max(eH, eG, ePH, ePG) <= 1e-5
+    # every pair over the first 16 steps, the oracle run in slices of 32 sequences
+    worst_all = 0.0
+    for s0 in range(0, w.seqs, 32):
+        sl = slice(s0, s0 + 32)
+        qH, qG = H0[sl].astype(np.float64), G0[sl].astype(np.float64)
+        for step in range(n_all):
+            x = first_in[step]
+            ro, qH, qG = oracle.decode_step(qH, qG, x["q"][sl], x["k"][sl], x["v"][sl], x["gamma"][sl],
+                                            x["beta"][sl], lam, w.n_cg, threads=16)
+            of, op = first_out[step]
+            worst_all = max(worst_all, rel_l2(of[sl], ro), rel_l2(op[sl], ro))
+    _say("  all 4096 pairs, first %d steps: worst rel L2 %.3e" % (n_all, worst_all))
+    assert worst_all <= TOL_BF16
 
 
 def test_decode_f32_matches_oracle_tightly():

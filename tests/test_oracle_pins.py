@@ -201,7 +201,7 @@ def test_brute_force_per_token_solves_tiny(seed):
 
 
 def test_sherman_morrison_rls_for_unit_forget_gates():
-    """With gamma = 1 the Mesa layer is recursive least squares (App. F):
+    """With gamma = 1 the Mesa layer is recursive least squares (App. H):
     R_t^{-1} = R_{t-1}^{-1} - beta R^{-1} k k^T R^{-1} / (1 + beta k^T R^{-1} k), R_0^{-1} = Lambda^{-1}."""
     x = _inputs(B=1, H=1, T=15, dk=4, dv=3, seed=20)
     x["gamma"][:] = 1.0
@@ -362,7 +362,7 @@ def test_zero_cg_steps_is_jacobi_start():
 
 
 def test_gla_identity_with_query_start_and_no_steps():
-    """Sec. 4: with no CG steps and q* = q the layer is gated linear attention,
+    """Sec. 3: with no CG steps and q* = q the layer is gated linear attention,
     o_t = sum_i zeta_{t,i} beta_i v_i (k_i^T q_t)."""
     x = _inputs(B=1, H=1, T=8, dk=4, dv=3, seed=34)
     r = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 0, init="query")
