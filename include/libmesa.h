@@ -236,6 +236,26 @@ int mesa_pack_state(const float* state_H, float* state_HP, int64_t batch, int64_
 int mesa_unpack_state(const float* state_HP, float* state_H, int64_t batch, int64_t heads,
                       int64_t d_k, void* stream);
 
+/* Size of the device buffer behind mesa_forward_noalloc: 64 MiB. */
+#define MESA_NOALLOC_SCRATCH_BYTES 67108864
+
+/* mesa_forward without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results and precision (MESA_PREC_AUTO)
+ * as mesa_forward, minus workspace / workspace_bytes: the chunk states go to a
+ * fixed buffer of MESA_NOALLOC_SCRATCH_BYTES that the library holds on every GPU
+ * it runs on (part of its code object, kept until the process ends).  The call
+ * allocates nothing.  It returns MESA_ERR_WORKSPACE, and launches nothing, when
+ * mesa_forward_workspace_bytes(batch, heads, seq_len, d_k, d_v, chunk) exceeds
+ * that size (e.g. at d_k = d_v = 128 and chunk 64, at most 512 sequence-chunks:
+ * batch * heads * ceil(seq_len / 64) <= 512).  All calls on one GPU share the one
+ * buffer: calls that may overlap on a GPU (different streams, or different host
+ * threads without ordering) race on it and must not be issued. */
+int mesa_forward_noalloc(const void* q, const void* k, const void* v, const float* gamma,
+                         const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                         int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
+                         float* out, void* stream);
+
 /* Static text for a status code (never NULL). */
 const char* mesa_status_string(int status);
 

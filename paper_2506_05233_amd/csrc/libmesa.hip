@@ -7,6 +7,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "mesa_kernels.hpp"
 
 namespace {
@@ -561,6 +563,70 @@ int mesa_backward(const void* k, const void* v, const float* gamma, const float*
                                    precision, qstar, dout, dq, dk, dv, dgamma, dbeta, dlambda, workspace,
                                    workspace_bytes, stream, launched);
     return launched ? finish(st, stream) : st;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Chunk-state workspace of mesa_forward_noalloc: a fixed buffer in device memory
+// that comes with the library's code object, so each GPU the library runs on holds
+// one copy until the process ends.  In host code its name is only a stand-in for
+// the symbol: kernels get the device address that hipGetSymbolAddress returns on
+// the current device (each device's copy has its own address), never the name.
+// Nothing in it has to start at zero: the chunk-state scan writes every state (and
+// every segment total of the segmented scan) before anything reads it.
+__device__ __align__(256) unsigned char scratch[MESA_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up on the first call
+// per device (with that device current) and kept.
+int scratch_address(void** ptr)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MESA_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return MESA_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return MESA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mesa_forward_noalloc(const void* q, const void* k, const void* v, const float* gamma,
+                         const float* beta, const float* lambda, int64_t batch, int64_t heads,
+                         int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
+                         float* out, void* stream)
+{
+    if (!out) return MESA_ERR_NULL;
+    // every argument check except the workspace's, before the device is touched
+    FwdCall c{q, k, v, gamma, beta, lambda, batch, heads, seq_len, d_k, d_v, dtype, n_cg, chunk,
+              MESA_PREC_AUTO, out, nullptr, nullptr, nullptr, nullptr, 0, true, false};
+    int st = validate_forward(c);
+    if (st != MESA_OK || batch == 0 || heads == 0) return st;
+    const size_t need = mesa_forward_workspace_bytes(batch, heads, seq_len, d_k, d_v, chunk);
+    if (need > size_t(MESA_NOALLOC_SCRATCH_BYTES)) return MESA_ERR_WORKSPACE;
+    if (need > 0) {
+        st = scratch_address(const_cast<void**>(&c.workspace));
+        if (st != MESA_OK) return st;
+        c.workspace_bytes = MESA_NOALLOC_SCRATCH_BYTES;
+        c.needs_ws = true;
+        st = validate_forward(c);
+        if (st != MESA_OK) return st;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = launch_states(c, true, s);
+    if (st == MESA_OK) st = launch_solve(c, s);
+    return finish(st, stream);
 }
 
 }  // extern "C"

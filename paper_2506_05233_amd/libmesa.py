@@ -26,11 +26,12 @@ MESA_ERR_ARG = 4
 MESA_ERR_WORKSPACE = 5
 MESA_ERR_HIP = 6
 MESA_MAX_NCG = 1024
+MESA_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 EXPORTED = ("mesa_forward", "mesa_forward_ex", "mesa_forward_states", "mesa_forward_solve",
             "mesa_forward_tol", "mesa_forward_workspace_bytes", "mesa_decode_step",
             "mesa_decode_step_tol", "mesa_decode_step_packed", "mesa_pack_state", "mesa_unpack_state",
-            "mesa_backward", "mesa_backward_workspace_bytes",
+            "mesa_backward", "mesa_backward_workspace_bytes", "mesa_forward_noalloc",
             "mesa_status_string", "mesa_version")
 
 _lib = None
@@ -84,6 +85,8 @@ def load():
     lib.mesa_backward.argtypes = [vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, fp, fp,
                                   fp, fp, fp, fp, fp, fp, vp, sz, vp]
     lib.mesa_backward.restype = ci
+    lib.mesa_forward_noalloc.argtypes = [vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, fp, vp]
+    lib.mesa_forward_noalloc.restype = ci
     lib.mesa_status_string.argtypes = [ci]
     lib.mesa_status_string.restype = ctypes.c_char_p
     lib.mesa_version.argtypes = []
@@ -214,6 +217,32 @@ def forward(q, k, v, gamma, beta, lam, n_cg, chunk=64, precision=MESA_PREC_AUTO,
         res["H"] = fH
         res["G"] = fG
     return res
+
+
+def forward_noalloc(q, k, v, gamma, beta, lam, n_cg, chunk=64, out=None):
+    """mesa_forward_noalloc: the forward with the chunk states in the library's own
+    fixed device buffer (no workspace; MesaError with MESA_ERR_WORKSPACE when the
+    shape needs more than MESA_NOALLOC_SCRATCH_BYTES).  Same inputs as forward();
+    returns out [B,H,T,d_v] fp32 (allocated here unless given)."""
+    torch = _torch()
+    lib = load()
+    B, H, T, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    _check(q, "q", (B, H, T, dk), device=dev)
+    _check(k, "k", (B, H, T, dk), q.dtype, dev)
+    _check(v, "v", (B, H, T, dv), q.dtype, dev)
+    _check(gamma, "gamma", (B, H, T), torch.float32, dev)
+    _check(beta, "beta", (B, H, T), torch.float32, dev)
+    _check(lam, "lam", (H, dk), torch.float32, dev)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
+    _check(out, "out", (B, H, T, dv), torch.float32, dev)
+    st = lib.mesa_forward_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(gamma), _ptr(beta), _ptr(lam), B, H, T,
+                                  dk, dv, _dtype_code(q), int(n_cg), int(chunk), _ptr(out), _stream(dev))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_forward_noalloc")
+    return out
 
 
 class ForwardPlan:

@@ -269,3 +269,35 @@ def test_packed_state_entry_points_reject_bad_arguments(lib):
     assert lib.mesa_decode_step_packed(None, *args[1:], 0.0, P["out"], None, None) == L.MESA_ERR_NULL
     # the packed H of 8 pairs spans 8 * 65 * 128 floats: an output inside that extent overlaps
     assert lib.mesa_decode_step_packed(*args, 0.0, P["H"] + 8 * 65 * 128 * 4 - 4, None, None) == L.MESA_ERR_ARG
+
+
+def _noalloc(lib, **kw):
+    a = dict(q=P["q"], k=P["k"], v=P["v"], gamma=P["g"], beta=P["b"], lam=P["lam"], B=2, H=3, T=128,
+             dk=64, dv=64, dtype=0, n_cg=5, chunk=64, out=P["out"])
+    a.update(kw)
+    return lib.mesa_forward_noalloc(a["q"], a["k"], a["v"], a["gamma"], a["beta"], a["lam"], a["B"], a["H"],
+                                    a["T"], a["dk"], a["dv"], a["dtype"], a["n_cg"], a["chunk"], a["out"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(out=None), L.MESA_ERR_NULL),
+    (dict(q=None), L.MESA_ERR_NULL),
+    (dict(dk=96), L.MESA_ERR_UNSUPPORTED),
+    (dict(chunk=48), L.MESA_ERR_UNSUPPORTED),
+    (dict(n_cg=1025), L.MESA_ERR_ARG),
+    (dict(out=P["k"] + 16), L.MESA_ERR_ARG),          # out overlaps k
+    (dict(B=0), L.MESA_OK),                           # nothing to do, nothing touched
+    # more than MESA_NOALLOC_SCRATCH_BYTES of chunk states: 513 sequence-chunks at d = 128
+    (dict(B=1, H=1, T=513 * 64, dk=128, dv=128), L.MESA_ERR_WORKSPACE),
+    (dict(B=8, H=16, T=2048, dk=128, dv=128, dtype=1), L.MESA_ERR_WORKSPACE),
+])
+def test_noalloc_forward_rejects_before_touching_the_device(lib, kw, status):
+    """Every check of mesa_forward_noalloc, the buffer size included, runs before the
+    library looks up its device buffer: these calls need no GPU."""
+    assert _noalloc(lib, **kw) == status
+
+
+def test_noalloc_buffer_size_constant():
+    assert L.MESA_NOALLOC_SCRATCH_BYTES == 64 << 20
+    # exactly the buffer: 512 sequence-chunks of fp32 H_c and G_c at d_k = d_v = 128
+    assert L.forward_workspace_bytes(4, 16, 512, 128, 128, 64) == L.MESA_NOALLOC_SCRATCH_BYTES
