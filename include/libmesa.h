@@ -65,16 +65,26 @@ extern "C" {
 #define MESA_DTYPE_BF16 1
 
 /* Arithmetic of the matrix products inside CG and the read-out.
- *   MESA_PREC_AUTO : MESA_PREC_F32 for fp32 inputs, MESA_PREC_BF16 for bf16 inputs.
- *   MESA_PREC_F32  : fp32 products with fp32 accumulation (fp32-accurate).
- *   MESA_PREC_BF16 : matrix-core products with bf16 operands (the fp32 state and
- *                    the fp32 CG direction are rounded to bf16 as operands) and
- *                    fp32 accumulation; every CG vector, scalar and reduction
- *                    stays fp32 (App. G.5 keeps the solver in fp32; this mode
- *                    trades operand precision for matrix-core throughput). */
+ *   MESA_PREC_AUTO  : MESA_PREC_F32 for fp32 inputs, MESA_PREC_BF16 for bf16 inputs.
+ *   MESA_PREC_F32   : fp32 products with fp32 accumulation (fp32-accurate).
+ *   MESA_PREC_BF16  : matrix-core products with bf16 operands and fp32 accumulation:
+ *                     the chunk states are stored as bf16, and the fp32 CG
+ *                     direction, the fp32 intra-chunk weights and Lambda are
+ *                     rounded to bf16 as operands; every CG vector, scalar and
+ *                     reduction stays fp32.  Accurate to ~5e-3 on well-conditioned
+ *                     systems, ~1e-1 on repeated keys with gates near one (App. G.5
+ *                     keeps the solver in fp32; this mode trades operand precision
+ *                     for matrix-core throughput).
+ *   MESA_PREC_BF16X3: matrix-core products on split operands: each fp32 operand x
+ *                     is carried as bf16 hi = bf16(x) plus lo = bf16(x - hi), and
+ *                     a product as hi hi + hi lo + lo hi with fp32 accumulation
+ *                     (~2^-16 relative per term); chunk states fp32-accurate;
+ *                     Lambda p in fp32.  Accurate to ~1e-5 on well-conditioned
+ *                     systems and ~1e-4 on repeated keys.  bf16 inputs, chunk 64. */
 #define MESA_PREC_AUTO 0
 #define MESA_PREC_F32 1
 #define MESA_PREC_BF16 2
+#define MESA_PREC_BF16X3 3
 
 /* Status codes. */
 #define MESA_OK 0

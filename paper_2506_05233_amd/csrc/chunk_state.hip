@@ -441,7 +441,7 @@ struct SegPlan {
     float* dec;   // [B*H, total]: D_s
 };
 
-template <int DK, int DV, bool STORE, bool SPLIT, bool PLAIN = false>
+template <int DK, int DV, bool STORE, bool SPLIT, bool PLAIN = false, bool X3 = false>
 __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArgs a, SegPlan sg)
 {
     constexpr int C = 64;
@@ -588,13 +588,34 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
         // chunk n + 1 is staged (from Rn1) into the other buffer and chunk n + 3 loaded
         float dprod = 1.0f;  // decay across the chunks walked so far
         auto consume = [&](int n, float D, Regs& Rn1, Regs& Rfree, float& Dnext) {
-            if (frag_out) {
+            if (frag_out && X3 && part == 0) {
+                // H_c as fp32 fragments: half e of fragment f, lane l at [(2 f + e) 64 + l] x 4
+                float* base = static_cast<float*>(a.Hs) + (bh * s.n_chunks + n) * int64_t(kStateElems);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const int f = (ct0 + ct) * NS + sblk;
+                    *reinterpret_cast<f32x4*>(base + ((2 * f + 0) * kWave + lane) * 4) = acc[0][ct];
+                    *reinterpret_cast<f32x4*>(base + ((2 * f + 1) * kWave + lane) * 4) = acc[1][ct];
+                }
+            } else if (frag_out) {
+                // bf16 fragments; with X3 (G_c) the high parts, and the low parts
+                // bf16(x - hi) in a second plane of the same layout after all chunks' states
                 uint16_t* base = frag_base + (bh * s.n_chunks + n) * int64_t(kStateElems);
+                const int64_t lo_plane = s.batch * s.heads * int64_t(s.n_chunks) * kStateElems;
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     const uint4 pk = make_uint4(pack_bf16x2(acc[0][ct][0], acc[0][ct][1]), pack_bf16x2(acc[0][ct][2], acc[0][ct][3]),
                                                 pack_bf16x2(acc[1][ct][0], acc[1][ct][1]), pack_bf16x2(acc[1][ct][2], acc[1][ct][3]));
-                    *reinterpret_cast<uint4*>(base + (((ct0 + ct) * NS + sblk) * kWave + lane) * 8) = pk;
+                    const int64_t off = (((ct0 + ct) * NS + sblk) * kWave + lane) * 8;
+                    *reinterpret_cast<uint4*>(base + off) = pk;
+                    if constexpr (X3) {
+                        auto lo2 = [](float x0, float x1, uint32_t h) {
+                            return pack_bf16x2(x0 - __uint_as_float(h << 16), x1 - __uint_as_float(h & 0xffff0000u));
+                        };
+                        const uint4 pl = make_uint4(lo2(acc[0][ct][0], acc[0][ct][1], pk.x), lo2(acc[0][ct][2], acc[0][ct][3], pk.y),
+                                                    lo2(acc[1][ct][0], acc[1][ct][1], pk.z), lo2(acc[1][ct][2], acc[1][ct][3], pk.w));
+                        *reinterpret_cast<uint4*>(base + lo_plane + off) = pl;
+                    }
                 }
             }
             if constexpr (PLAIN) {
@@ -735,11 +756,11 @@ int wide_segments(int64_t bh, int n_chunks)
     return S;
 }
 
-template <int DK, int DV, bool STORE, bool SPLIT, bool PLAIN = false>
+template <int DK, int DV, bool STORE, bool SPLIT, bool PLAIN = false, bool X3 = false>
 void launch_wide_kernel(const StateArgs& a, const SegPlan& sg, int64_t bh, hipStream_t stream)
 {
     const unsigned blocks = unsigned(bh * 2 * sg.count);
-    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, STORE, SPLIT, PLAIN>), dim3(blocks), dim3(kWideThreads), 0, stream, a, sg);
+    hipLaunchKernelGGL((chunk_state_wide_kernel<DK, DV, STORE, SPLIT, PLAIN, X3>), dim3(blocks), dim3(kWideThreads), 0, stream, a, sg);
 }
 
 template <int DK, int DV>
@@ -764,7 +785,7 @@ hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
         SegPlan p1 = sg;
         p1.count = S - 1;
         p1.totals = true;
-        if (fin || a.Hs32)
+        if (fin || a.Hs32 || a.x3)
             launch_wide_kernel<DK, DV, false, true>(a, p1, bh, stream);
         else
             launch_wide_kernel<DK, DV, false, false>(a, p1, bh, stream);
@@ -776,7 +797,9 @@ hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
         sg.first = S - 1;
         sg.count = 1;
     }
-    if (a.store_chunks && a.frag && a.Hs32)  // fragments and fp32 plain states, fp32-accurate
+    if (a.store_chunks && a.x3)  // fp32 H_c fragments, G_c high and low planes, fp32-accurate
+        launch_wide_kernel<DK, DV, true, true, false, true>(a, sg, bh, stream);
+    else if (a.store_chunks && a.frag && a.Hs32)  // fragments and fp32 plain states, fp32-accurate
         launch_wide_kernel<DK, DV, true, true, true>(a, sg, bh, stream);
     else if (a.store_chunks && a.frag && !fin)
         launch_wide_kernel<DK, DV, true, false>(a, sg, bh, stream);
@@ -812,8 +835,8 @@ bool chunk_state_frag_supported(const ForwardShape& s)
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream)
 {
     const int64_t bh = a.s.batch * a.s.heads;
-    if (a.frag && !chunk_state_frag_supported(a.s)) return hipErrorInvalidValue;
-    if (chunk_state_frag_supported(a.s) && (a.frag || !a.store_chunks)) {
+    if ((a.frag || a.x3) && !chunk_state_frag_supported(a.s)) return hipErrorInvalidValue;
+    if (chunk_state_frag_supported(a.s) && (a.frag || a.x3 || !a.store_chunks)) {
         if (a.s.d_k == 64) return a.s.d_v == 64 ? launch_wide<64, 64>(a, stream) : launch_wide<64, 128>(a, stream);
         return a.s.d_v == 64 ? launch_wide<128, 64>(a, stream) : launch_wide<128, 128>(a, stream);
     }

@@ -87,11 +87,13 @@ int validate_forward(const FwdCall& c)
     if (st != MESA_OK) return st;
     if (!eps_ok(c.eps)) return MESA_ERR_ARG;
     if (!chunk_ok(c.chunk)) return MESA_ERR_UNSUPPORTED;
-    if (c.precision != MESA_PREC_AUTO && c.precision != MESA_PREC_F32 && c.precision != MESA_PREC_BF16)
+    if (c.precision != MESA_PREC_AUTO && c.precision != MESA_PREC_F32 && c.precision != MESA_PREC_BF16 &&
+        c.precision != MESA_PREC_BF16X3)
         return MESA_ERR_UNSUPPORTED;
     const ForwardShape probe{c.batch, c.heads, c.seq_len, int(c.d_k), int(c.d_v), c.chunk, 0,
                              c.dtype == MESA_DTYPE_BF16};
     if (c.precision == MESA_PREC_BF16 && !mesa::chunk_cg_bf16_supported(probe)) return MESA_ERR_UNSUPPORTED;
+    if (c.precision == MESA_PREC_BF16X3 && !mesa::chunk_cg_x3_supported(probe)) return MESA_ERR_UNSUPPORTED;
     if (c.batch == 0 || c.heads == 0) return MESA_OK;
     // Arrays with no elements (seq_len == 0) may be NULL; lambda never is empty.
     if (c.seq_len > 0 && (!c.k || !c.v || !c.gamma || !c.beta)) return MESA_ERR_NULL;
@@ -156,8 +158,9 @@ int resolve_precision(const FwdCall& c)
     return c.precision;
 }
 
-// Workspace: H states then G states, fp32 plain (MESA_PREC_F32) or bf16
-// fragments (MESA_PREC_BF16, half the bytes).
+// Workspace: H states then G states, fp32 plain (MESA_PREC_F32), bf16 fragments
+// (MESA_PREC_BF16, half the bytes) or the split-operand layout (MESA_PREC_BF16X3: fp32
+// H_c fragments, then G_c's bf16 high and low planes).
 void* ws_H(const FwdCall& c) { return const_cast<void*>(c.workspace); }
 void* ws_G(const FwdCall& c)
 {
@@ -180,6 +183,7 @@ int launch_states(const FwdCall& c, bool store_chunks, hipStream_t s)
     mesa::StateArgs sa{shape_of(c), c.k, c.v, c.gamma, c.beta,
                        store_chunks ? ws_H(c) : nullptr, store_chunks ? ws_G(c) : nullptr,
                        c.final_H, c.final_G, store_chunks, frag};
+    sa.x3 = store_chunks && resolve_precision(c) == MESA_PREC_BF16X3;
     // The bf16 chunk states fill half of the workspace (and a states-only call none
     // of it): the other half is scratch for the segmented scan of few sequences.
     if (c.workspace && (frag || !store_chunks)) {
@@ -197,8 +201,9 @@ int launch_solve(const FwdCall& c, hipStream_t s)
     const int prec = resolve_precision(c);
     mesa::CgArgs ca{shape, c.q, c.k, c.v, c.gamma, c.beta, c.lambda, ws_H(c), ws_G(c), c.n_cg, c.out, c.qstar,
                     c.eps * c.eps, c.steps};
-    const hipError_t e = prec == MESA_PREC_BF16 ? mesa::launch_chunk_cg_bf16(ca, s)
-                                                : mesa::launch_chunk_cg_f32(ca, s);
+    const hipError_t e = prec == MESA_PREC_BF16     ? mesa::launch_chunk_cg_bf16(ca, s)
+                         : prec == MESA_PREC_BF16X3 ? mesa::launch_chunk_cg_x3(ca, s)
+                                                    : mesa::launch_chunk_cg_f32(ca, s);
     return e == hipSuccess ? MESA_OK : MESA_ERR_HIP;
 }
 

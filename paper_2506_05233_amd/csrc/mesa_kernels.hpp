@@ -45,6 +45,11 @@ struct StateArgs {
     // the same fp32-accurate pass (may be null).
     float* Hs32 = nullptr;
     float* Gs32 = nullptr;
+    // Split-operand layout (bf16 inputs, chunk 64; instead of frag), fp32-accurate:
+    // Hs fp32 H_c fragments, half e of fragment f = (t, s), lane l at
+    // [B*H, n_chunks][(2 f + e) * 64 + l][4]; Gs the bf16 G_c fragments (high parts)
+    // followed by a second plane of the same shape with the low parts bf16(x - hi).
+    bool x3 = false;
 };
 bool chunk_state_frag_supported(const ForwardShape& s);
 hipError_t launch_chunk_state(const StateArgs& a, hipStream_t stream);
@@ -103,6 +108,10 @@ struct BwdArgs {
 hipError_t launch_backward_stage(const BwdArgs& a, int stage, hipStream_t stream);
 hipError_t launch_chunk_cg_bf16(const CgArgs& a, hipStream_t stream);
 bool chunk_cg_bf16_supported(const ForwardShape& s);
+// The same solve and read-out with split operands (hi + lo bf16 pairs, three matrix-core
+// passes per product) from the split-operand chunk-state layout.
+hipError_t launch_chunk_cg_x3(const CgArgs& a, hipStream_t stream);
+bool chunk_cg_x3_supported(const ForwardShape& s);
 
 // One recurrent decode step for batch*heads pairs.
 struct DecodeArgs {

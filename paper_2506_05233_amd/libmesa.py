@@ -18,6 +18,7 @@ MESA_DTYPE_BF16 = 1
 MESA_PREC_AUTO = 0
 MESA_PREC_F32 = 1
 MESA_PREC_BF16 = 2
+MESA_PREC_BF16X3 = 3
 MESA_OK = 0
 MESA_ERR_NULL = 1
 MESA_ERR_SHAPE = 2

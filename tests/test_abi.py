@@ -94,9 +94,12 @@ def _fwd(lib, **kw):
     (dict(chunk=128), L.MESA_ERR_UNSUPPORTED),
     (dict(dtype=2), L.MESA_ERR_UNSUPPORTED),
     (dict(prec=7), L.MESA_ERR_UNSUPPORTED),
+    (dict(prec=L.MESA_PREC_BF16X3), L.MESA_ERR_UNSUPPORTED),               # split operands need bf16 inputs
+    (dict(prec=L.MESA_PREC_BF16X3, dtype=1, chunk=32), L.MESA_ERR_UNSUPPORTED),  # ... and chunk 64
     (dict(n_cg=-1), L.MESA_ERR_ARG),
     (dict(n_cg=L.MESA_MAX_NCG + 1), L.MESA_ERR_ARG),
     (dict(ws_bytes=100), L.MESA_ERR_WORKSPACE),
+    (dict(prec=L.MESA_PREC_BF16X3, dtype=1, ws_bytes=100), L.MESA_ERR_WORKSPACE),
     (dict(out=P["q"] + 64), L.MESA_ERR_ARG),          # out overlaps q
     (dict(k=P["k"] + 2), L.MESA_ERR_ARG),             # k not 16-byte aligned
     (dict(ws=P["ws"] + 8), L.MESA_ERR_ARG),           # workspace not 16-byte aligned

@@ -1,0 +1,168 @@
+"""GPU parity of the split-operand matrix-core path (MESA_PREC_BF16X3) against the
+fp64 oracle's same-step CG.
+
+Every fp32 operand of a matrix-core product is carried as a bf16 high part plus a
+bf16 low part (App. G.5 keeps the CG products in fp32; this mode reaches that
+accuracy on the bf16 matrix cores), so the path is held to the fp32 tolerance on
+the workload distributions and pinned near its measured error on the repeated-key
+stress input, where single bf16 operands fail.  All calls go through the C ABI.
+"""
+import concurrent.futures as cf
+
+import numpy as np
+import pytest
+
+import oracle
+from mesa_testutil import TOL_BF16, TOL_F32, rel_l2, to_device
+from paper_2506_05233_amd import libmesa as L
+from paper_2506_05233_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+X3 = L.MESA_PREC_BF16X3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    L.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _gpu_forward(x, n_cg, prec=X3, **kw):
+    d = to_device(x, "bf16")
+    res = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], n_cg, 64, precision=prec, **kw)
+    torch.cuda.synchronize()
+    if isinstance(res, dict):
+        return {k: v.cpu().numpy() for k, v in res.items()}
+    return res.cpu().numpy()
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 64), (64, 128), (128, 64), (128, 128)])
+def test_x3_shapes_ragged_tail(dk, dv):
+    """Several chunks plus a ragged last one; every output and every q* within the
+    fp32 tolerance of the oracle, and the final states fp32-accurate."""
+    x = W.forward_inputs(2, 2, 3 * 64 + 29, dk, dv, "bf16", 4.0, seed=dk + 2 * dv)
+    got = _gpu_forward(x, 15, want_qstar=True, want_states=True)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 15, want_qstar=True,
+                         want_states=True)
+    e_out, e_q = rel_l2(got["out"], ref["out"]), rel_l2(got["qstar"], ref["qstar"])
+    _say("x3 d_k=%d d_v=%d: out %.3e qstar %.3e" % (dk, dv, e_out, e_q))
+    assert e_out <= TOL_F32 and e_q <= TOL_F32
+    assert rel_l2(got["H"], ref["H"]) <= 1e-5 and rel_l2(got["G"], ref["G"]) <= 1e-5
+
+
+def test_x3_edge_cases():
+    """Zero gates at a chunk's start, inside and at its end; q = 0; beta = 0 tokens;
+    n_cg from 0 (Jacobi start only) to 15."""
+    x = W.forward_inputs(2, 2, 150, 128, 128, "bf16", 4.0, seed=31)
+    x["gamma"][0, 1, 40] = 0.0
+    x["gamma"][1, 0, 64] = 0.0
+    x["gamma"][1, 1, 63] = 0.0
+    x["q"][0, 0, 10] = 0.0
+    x["beta"][1, 0, 5:9] = 0.0
+    for n_cg in (0, 1, 2, 3, 15):
+        got = _gpu_forward(x, n_cg)
+        ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], n_cg)["out"]
+        e = rel_l2(got, ref)
+        _say("x3 edge n_cg=%d: %.3e" % (n_cg, e))
+        assert e <= TOL_F32, n_cg
+        assert np.all(got[0, 0, 10] == 0.0)
+
+
+def test_x3_strong_decay():
+    """Gates in [0.25, 0.6]: later sub-chunk states are built without the chunk
+    state, earlier ones carry rank-update weights up to ~1e14."""
+    x = W.forward_inputs(2, 2, 4 * 64 + 17, 128, 128, "bf16", 4.0, seed=43)
+    rng = np.random.default_rng(4301)
+    x["gamma"][...] = rng.uniform(0.25, 0.6, size=x["gamma"].shape).astype(np.float32)
+    for n_cg in (0, 15):
+        got = _gpu_forward(x, n_cg, want_qstar=True)
+        ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], n_cg, want_qstar=True)
+        e_out, e_q = rel_l2(got["out"], ref["out"]), rel_l2(got["qstar"], ref["qstar"])
+        _say("x3 strong decay n_cg=%d: out %.3e qstar %.3e" % (n_cg, e_out, e_q))
+        assert e_out <= TOL_F32 and e_q <= TOL_F32, n_cg
+
+
+@pytest.mark.parametrize("pool,pin", [(1, 1e-3), (4, 5e-4)])
+def test_x3_stress_repeated_keys(pool, pin):
+    """App. G.5's hard case: keys from a pool of one or four vectors, gates near one
+    (condition numbers ~60-230).  Single bf16 operands reach ~0.13 (one key) and
+    ~0.04 (four); split operands stay near the fp32 products' error (~2e-4 and ~7e-5
+    measured), well inside the bf16-input tolerance and pinned near that value."""
+    x = W.repeated_key_inputs(1, 2, 512, 128, 128, pool=pool, dtype="bf16")
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 20)["out"]
+    e = rel_l2(_gpu_forward(x, 20), ref)
+    _say("stress pool=%d split operands: %.3e" % (pool, e))
+    assert e <= TOL_BF16 and e <= pin
+
+
+def test_x3_query_scale_is_exact():
+    """Each column solves for q scaled by a power of two (exact), so q * 2^k gives
+    out * 2^k bit for bit."""
+    x = W.forward_inputs(1, 2, 128 + 40, 128, 128, "bf16", 4.0, seed=47)
+    base = _gpu_forward(x, 15)
+    for k in (-60, -20, 7, 60):
+        y = dict(x)
+        y["q"] = (x["q"].astype(np.float64) * 2.0 ** k).astype(np.float32)
+        got = _gpu_forward(y, 15)
+        assert np.array_equal(got, (base.astype(np.float64) * 2.0 ** k).astype(np.float32)), k
+
+
+def test_x3_bitwise_deterministic_and_max_ncg():
+    x = W.forward_inputs(2, 4, 512, 128, 128, "bf16", 4.0, seed=9)
+    assert np.array_equal(_gpu_forward(x, 15), _gpu_forward(x, 15))
+    y = W.forward_inputs(1, 2, 70, 64, 64, "bf16", 4.0, seed=41)
+    n = L.MESA_MAX_NCG
+    ref = oracle.forward(y["q"], y["k"], y["v"], y["gamma"], y["beta"], y["lam"], n)["out"]
+    e = rel_l2(_gpu_forward(y, n), ref)
+    _say("x3 n_cg = %d: %.3e" % (n, e))
+    assert e <= TOL_F32
+
+
+@pytest.mark.parametrize("eps", [1e-2, 1e-4])
+def test_x3_tolerance_matches_oracle(eps):
+    """Alg. 1's relative test on the split-operand path: iteration counts agree with
+    the oracle's except within rounding of the threshold, outputs of equal counts to
+    the fp32 tolerance."""
+    x = W.forward_inputs(2, 2, 2 * 64 + 40, 128, 128, "bf16", 4.0, seed=62)
+    res = _gpu_forward(x, 40, eps=eps, want_steps=True)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 40, eps=eps, want_steps=True)
+    diff = np.abs(res["steps"].astype(np.int64) - ref["steps"].astype(np.int64))
+    _say("x3 eps=%g: steps equal %.4f, max |diff| %d" % (eps, np.mean(diff == 0), diff.max()))
+    assert diff.max() <= 1 and np.mean(diff == 0) >= 0.97
+    same = diff == 0
+    assert rel_l2(res["out"][same], ref["out"][same]) <= TOL_F32
+    assert rel_l2(res["out"], ref["out"]) <= 20 * eps + TOL_F32
+
+
+@pytest.mark.parametrize("w,pairs", [
+    (W.LAYER_1B_BF16, [(0, 0), (3, 7), (5, 12), (7, 15)]),
+    (W.LONG_BF16, [(0, 0), (0, 9)]),
+], ids=["layer1b", "longctx"])
+def test_x3_full_size_sampled(w, pairs):
+    """The two bf16 workloads at full size in the split-operand mode, sampled
+    sequences against the oracle from their first token."""
+    _say("x3 full-size forward %s, sampled %s" % (w.name, pairs))
+    x = W.workload_inputs(w)
+    got = _gpu_forward(x, w.n_cg)
+    assert np.isfinite(got).all()
+
+    def one(bh):
+        b, h = bh
+        sl = {n: x[n][b:b + 1, h:h + 1] for n in ("q", "k", "v", "gamma", "beta")}
+        return oracle.forward(sl["q"], sl["k"], sl["v"], sl["gamma"], sl["beta"], x["lam"][h:h + 1], w.n_cg,
+                              threads=1)["out"][0, 0]
+    with cf.ThreadPoolExecutor(max_workers=len(pairs)) as ex:
+        refs = list(ex.map(one, pairs))
+    e = rel_l2(np.stack([got[b, h] for b, h in pairs]), np.stack(refs))
+    _say("  sampled rel L2 %.3e" % e)
+    assert e <= TOL_F32
