@@ -28,15 +28,14 @@
 // Data: the chunk states come from the scan as fp32 H_c in matrix-core fragment
 // order (fragment f = 16-row tile mt x 32-column step ks; half e of lane l at
 // [(2 f + e) 64 + l] x 4 floats) and G_c as bf16 high and low planes of the
-// fragment layout.  H_c reaches LDS by direct global -> LDS loads issued during the
-// previous chunk's CG and is the starting value of the state build's accumulators
-// (H and B'_w are symmetric, so a fragment's two halves are the two 16x16 result
-// tiles it belongs to); the build then adds the rank update, keeps B'_w in fp32
-// until it is complete and stores its high and low parts as matrix-core operands
-// in the accumulation registers (256 of them at d_k = 128), where the state
-// products read them.  G_c is read from global memory by the read-out, after the
-// CG loop has requested it into the L2 cache.  q is read from global memory at
-// the Jacobi start.
+// fragment layout.  The state build reads H_c straight from global memory into its
+// accumulators, one row tile ahead (H and B'_w are symmetric, so a fragment's two
+// halves are the two 16x16 result tiles it belongs to; the previous chunk's CG loop
+// has requested H_c into the L2 cache), adds the rank update, and stores B'_w's
+// high and low parts as matrix-core operands in the accumulation registers (256 of
+// them at d_k = 128), where the state products read them.  G_c reaches LDS by
+// direct global -> LDS loads issued under the chunk's own CG loop, for the
+// read-out.  q is read from global memory at the Jacobi start.
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
 #include "mesa_mfma.hpp"
@@ -51,20 +50,26 @@ constexpr int kThreads = 256;  // four waves, 16 tokens each
 // their reciprocal (the sub-chunk states are then built without H_c).
 constexpr float kMinDecay = 1e-20f;
 
-__device__ __forceinline__ float bf16_value(__bf16 x) { return (float)x; }
+// High and low bf16 parts of two fp32 values, each pair packed in one word:
+// hi = bf16(x) (nearest even), lo = bf16(x - hi).  The high parts are widened back
+// to fp32 from the packed word (a shift and a mask) rather than converted again.
+__device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_t& lo)
+{
+    hi = pack_bf16x2(x0, x1);
+    lo = pack_bf16x2(x0 - __uint_as_float(hi << 16), x1 - __uint_as_float(hi & 0xffff0000u));
+}
 
-// hi = bf16(x) (nearest even), lo = bf16(x - hi), for the 8 values of two result tiles
-// that form one 8-wide operand (a -> elements 0..3, b -> elements 4..7).
+// The split of the 8 values of two result tiles that form one 8-wide operand
+// (a -> elements 0..3, b -> elements 4..7).
 __device__ __forceinline__ void split8(const f32x4& a, const f32x4& b, bf16x8& hi, bf16x8& lo)
 {
-    hi = pack8(a, b);
-    f32x4 ra, rb;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        ra[e] = a[e] - bf16_value(hi[e]);
-        rb[e] = b[e] - bf16_value(hi[4 + e]);
-    }
-    lo = pack8(ra, rb);
+    uint32_t h[4], l[4];
+    split2(a[0], a[1], h[0], l[0]);
+    split2(a[2], a[3], h[1], l[1]);
+    split2(b[0], b[1], h[2], l[2]);
+    split2(b[2], b[3], h[3], l[3]);
+    hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
+    lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
 }
 
 // Four values as one 8-wide operand: elements 0..3 their high parts, 4..7 their low
@@ -72,28 +77,21 @@ __device__ __forceinline__ void split8(const f32x4& a, const f32x4& b, bf16x8& h
 // product sums hi + lo.
 __device__ __forceinline__ bf16x8 split4_stacked(const f32x4& a)
 {
-    bf16x8 r;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        r[e] = (__bf16)a[e];
-        r[4 + e] = (__bf16)(a[e] - bf16_value(r[e]));
-    }
-    return r;
+    uint32_t h0, l0, h1, l1;
+    split2(a[0], a[1], h0, l0);
+    split2(a[2], a[3], h1, l1);
+    return __builtin_bit_cast(bf16x8, make_uint4(h0, h1, l0, l1));
 }
 
 // 8 bf16 (bits in v) times u, split into high and low bf16 parts.
 __device__ __forceinline__ void scale_split8(const uint4& v, float u, uint4& hi, uint4& lo)
 {
-    const bf16x8 x = __builtin_bit_cast(bf16x8, v);
-    bf16x8 h, l;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t h[4], l[4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const float y = (float)x[e] * u;
-        h[e] = (__bf16)y;
-        l[e] = (__bf16)(y - bf16_value(h[e]));
-    }
-    hi = __builtin_bit_cast(uint4, h);
-    lo = __builtin_bit_cast(uint4, l);
+    for (int q = 0; q < 4; ++q) split2(__uint_as_float(w[q] << 16) * u, __uint_as_float(w[q] & 0xffff0000u) * u, h[q], l[q]);
+    hi = make_uint4(h[0], h[1], h[2], h[3]);
+    lo = make_uint4(l[0], l[1], l[2], l[3]);
 }
 
 // beta_i prod_{s=i+1..j} gamma_s for the four tokens i = i4 .. i4+3 (i4 a multiple of 4)
@@ -123,9 +121,9 @@ __device__ __forceinline__ uint4 keep_if(bool c, const uint4& v)
 // Sum over the four lanes that hold one column (lanes n, n+16, n+32, n+48).
 __device__ __forceinline__ float col_sum(float v) { return row_pair_sums(v); }
 
-// LDS arena (byte offsets).  The next chunk's H_c lands in its own region while the
-// current chunk's CG runs; the next chunk's keys and values land on the key tiles
-// (sKT, sKUh, sKUl), which only the state build and the operand set-up before CG read.
+// LDS arena (byte offsets).  G_c lands in its own region under the chunk's CG loop;
+// the next chunk's keys and values land on the key tiles (sKT, sKUh, sKUl), which
+// only the state build and the operand set-up before CG read.
 template <int DK, int DV>
 struct CgX3Smem {
     static constexpr int LDK = DK + 8;  // row stride (elements) of token-major tiles
@@ -135,23 +133,22 @@ struct CgX3Smem {
     static constexpr int kRawSlots = 2 * (NKQ + NV);
     static constexpr int oK = 0;                              // k_i[b], token-major bf16
     static constexpr int oVT = oK + kC * LDK * 2;             // v_i[e], feature-major bf16
-    static constexpr int oLam = oVT + DV * LDC * 2;           // lambda
-    static constexpr int oLg = oLam + DK * 4;                 // gate log-cumsums
+    static constexpr int oLg = oVT + DV * LDC * 2;            // gate log-cumsums
     static constexpr int oBeta = oLg + kWave * 4;
     static constexpr int oZl = oBeta + kWave * 4;             // last zero gate
     static constexpr int oZ0 = oZl + kWave * 4;               // zeta_{c+j,c}
-    static constexpr int oHc = oZ0 + kC * 4;                  // H_c, fp32 fragments
-    static constexpr int oKT = oHc + DK * DK * 4;             // k_i[b], feature-major
+    static constexpr int oGc = oZ0 + kC * 4;                  // G_c, bf16 high then low fragments
+    static constexpr int oKT = oGc + DV * DK * 4;             // k_i[b], feature-major
     static constexpr int oKUh = oKT + DK * LDC * 2;           // hi(u_i k_i[b]), feature-major
     static constexpr int oKUl = oKUh + DK * LDC * 2;          // lo(u_i k_i[b])
-    static constexpr int oSink = oKUl + DK * LDC * 2;         // landing slot of the L2 requests for G_c
+    static constexpr int oSink = oKUl + DK * LDC * 2;         // landing slot of the L2 requests for H_c
     static constexpr int oDiag = oSink + kWave * 16;          // diag(B'_w) per wave, spare slots
     static constexpr int oRaw = oKT;                          // next chunk's staging slots
     static constexpr int kEnd = oDiag + (kThreads / kWave) * (DK + kWave) * 4;
     static constexpr int kRawEnd = oRaw + kRawSlots * kThreads * 16;
     static constexpr int kBytes = kEnd;
     static_assert(kRawEnd <= oSink, "staging slots run past the key tiles");
-    static_assert(oHc % 16 == 0 && oKT % 16 == 0 && oSink % 16 == 0, "misaligned LDS region");
+    static_assert(oGc % 16 == 0 && oKT % 16 == 0 && oSink % 16 == 0, "misaligned LDS region");
     static_assert(kBytes <= 160 * 1024, "LDS use exceeds 160 KiB");
 };
 
@@ -165,18 +162,21 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
     constexpr int MTV = DV / 16;   // 16-row tiles of an output column
     constexpr int LDK = L::LDK, LDC = L::LDC, NKQ = L::NKQ, NV = L::NV;
     constexpr int kWaves = kThreads / kWave;
-    constexpr int kHcLoads = DK * DK * 4 / 1024 / kWaves;  // 1-KiB H_c loads per wave
-    constexpr int kGLoads = DV * DK * 4 / 1024 / kWaves;   // 1-KiB L2 requests for G_c (hi + lo) per wave
+    constexpr int kHcReq = DK * DK * 4 / 1024 / kWaves;  // 1-KiB L2 requests for H_c per wave
+    constexpr int kGLoads = DV * DK * 4 / 1024 / kWaves;  // 1-KiB G_c loads (high + low) per wave
 
     __shared__ __attribute__((aligned(16))) unsigned char smem[L::kBytes];
+    // Lambda, read in every CG product, has an array of its own: the compiler can then
+    // tell its reads apart from the direct loads into smem that run under the CG loop
+    // and does not order them behind those loads.
+    __shared__ __attribute__((aligned(16))) float sLam[DK];
     uint16_t* sK = reinterpret_cast<uint16_t*>(smem + L::oK);
     uint16_t* sVT = reinterpret_cast<uint16_t*>(smem + L::oVT);
-    float* sLam = reinterpret_cast<float*>(smem + L::oLam);
     float* sLg = reinterpret_cast<float*>(smem + L::oLg);
     float* sBeta = reinterpret_cast<float*>(smem + L::oBeta);
     int* sZl = reinterpret_cast<int*>(smem + L::oZl);
     float* sZ0 = reinterpret_cast<float*>(smem + L::oZ0);
-    float* sHc = reinterpret_cast<float*>(smem + L::oHc);
+    uint16_t* sGc = reinterpret_cast<uint16_t*>(smem + L::oGc);
     uint16_t* sKT = reinterpret_cast<uint16_t*>(smem + L::oKT);
     uint16_t* sKUh = reinterpret_cast<uint16_t*>(smem + L::oKUh);
     uint16_t* sKUl = reinterpret_cast<uint16_t*>(smem + L::oKUl);
@@ -192,17 +192,20 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
     const int heads = int(s.heads);
     const int64_t n_g = int64_t(total) * DV * DK;  // elements of one G_c plane
 
-    // Chunk c (fewer than 2^31, checked at launch) is chunk c % n_chunks of sequence
-    // c / n_chunks; it is also the index of its entering state.  Its loads never sit
+    // Loads for chunk c (fewer than 2^31, checked at launch; chunk c % n_chunks of
+    // sequence c / n_chunks, and the index of its entering state).  They never sit
     // behind a branch: tokens past the end of the sequence read the last valid token
-    // and are zeroed once in registers.  Gates and lambda go to registers; keys and
-    // values to the thread's staging slots; H_c to sHc.  They are issued in pieces,
-    // one per CG iteration of the previous chunk: H_c in four pieces, the staging
-    // slots in pieces of four.
+    // and are zeroed once in registers.  Pieces 0-3 request a quarter of H_c each into
+    // the L2 cache (direct loads whose LDS copies land on a sink nobody reads; the
+    // state build reads H_c from there), the rest bring the keys and values into the
+    // thread's staging slots, four slots per piece.  One piece is issued per CG
+    // iteration of the previous chunk.  The gates and lambda go to registers with
+    // plain loads issued before that loop (load_gates), so that no register merge
+    // after a conditional piece waits for the loads in flight.
     constexpr int kRawSlots = L::kRawSlots;
     constexpr int kHcPieces = 4, kRawPer = 4;
     constexpr int kPieces = kHcPieces + (kRawSlots + kRawPer - 1) / kRawPer;
-    auto issue_piece = [&](int c, int piece, int tid_in, float& g_out, float& b_out, float& lam_out) {
+    auto issue_piece = [&](int c, int piece, int tid_in) {
         int tid = tid_in;
         asm volatile("" : "+v"(tid));
         const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -214,17 +217,11 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         const int valid_ = int(min<int64_t>(kC, s.seq_len - t0_));
         const int64_t tok0_ = int64_t(bh_) * s.seq_len + t0_;
         if (piece < kHcPieces) {
-            if (piece == 0) {
-                const int lt = min(lane, valid_ - 1);
-                g_out = a.gamma[tok0_ + lt];
-                b_out = a.beta[tok0_ + lt];
-                lam_out = a.lambda[(bh_ % heads) * DK + min(tid, DK - 1)];
-            }
             const float* Hf = static_cast<const float*>(a.Hs) + int64_t(c) * DK * DK;
 #pragma unroll
-            for (int u = piece * (kHcLoads / kHcPieces); u < (piece + 1) * (kHcLoads / kHcPieces); ++u) {
-                const int f = wave * kHcLoads + u;  // 1-KiB block of the chunk's H_c
-                load_lds16(Hf + (f * kWave + lane) * 4, sHc + f * kWave * 4);
+            for (int u = piece * (kHcReq / kHcPieces); u < (piece + 1) * (kHcReq / kHcPieces); ++u) {
+                const int f = wave * kHcReq + u;  // 1-KiB block of the chunk's H_c
+                load_lds16(Hf + (f * kWave + lane) * 4, sSink);
             }
             return;
         }
@@ -243,29 +240,42 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
             load_lds16(src, slot + q * kThreads);
         }
     };
-    auto issue_all = [&](int c, int tid_in, float& g_out, float& b_out, float& lam_out) {
+    auto issue_all = [&](int c, int tid_in) {
 #pragma unroll
-        for (int piece = 0; piece < kPieces; ++piece) issue_piece(c, piece, tid_in, g_out, b_out, lam_out);
+        for (int piece = 0; piece < kPieces; ++piece) issue_piece(c, piece, tid_in);
     };
-    // One quarter of this wave's share of the L2 requests for chunk c's G_c (high and
-    // low planes): direct loads whose LDS copies land on a sink nobody reads.
-    auto request_g = [&](int c, int quarter, int lane_in) {
+    // gate and input-gate value of token `lane` of chunk c, and lambda element tid of its head
+    auto load_gates = [&](int c, int tid_in, float& g_out, float& b_out, float& lam_out) {
+        const int lane = tid_in % kWave;
+        const int nn = c % n_chunks;
+        const int bh_ = c / n_chunks;
+        const int64_t t0_ = int64_t(nn) * kC;
+        const int valid_ = int(min<int64_t>(kC, s.seq_len - t0_));
+        const int64_t tok = int64_t(bh_) * s.seq_len + t0_ + min(lane, valid_ - 1);
+        g_out = a.gamma[tok];
+        b_out = a.beta[tok];
+        lam_out = a.lambda[(bh_ % heads) * DK + min(tid_in, DK - 1)];
+    };
+    // One quarter of this wave's share of chunk c's G_c (high and low planes) into sGc:
+    // the high plane's blocks first, then the low plane's.
+    auto load_g = [&](int c, int quarter, int lane_in) {
         int lane = lane_in;
         asm volatile("" : "+v"(lane));
         const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
         const uint16_t* G = static_cast<const uint16_t*>(a.Gs) + int64_t(c) * DV * DK;
+        constexpr int kPlaneBlocks = DV * DK * 2 / 1024;
 #pragma unroll
         for (int u = quarter * (kGLoads / 4); u < (quarter + 1) * (kGLoads / 4); ++u) {
-            const int f = wave * kGLoads + u;                  // 1-KiB block of the two planes
-            const int plane = f / (kGLoads * kWaves / 2);       // 0: high, 1: low
-            const int fb = f % (kGLoads * kWaves / 2);
-            load_lds16(G + plane * n_g + (fb * kWave + lane) * 8, sSink);
+            const int f = wave * kGLoads + u;
+            const int plane = f / kPlaneBlocks, fb = f % kPlaneBlocks;
+            load_lds16(G + plane * n_g + (fb * kWave + lane) * 8, sGc + f * kWave * 8);
         }
     };
 
     int cc = blockIdx.x;
     float g_cur = 1.0f, b_cur = 0.0f, lam_cur = 0.0f;
-    issue_all(cc, threadIdx.x, g_cur, b_cur, lam_cur);
+    load_gates(cc, threadIdx.x, g_cur, b_cur, lam_cur);
+    issue_all(cc, threadIdx.x);
     for (;;) {
         int tid = threadIdx.x;
         asm volatile("" : "+v"(tid));
@@ -285,8 +295,20 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         const int valid = int(min<int64_t>(kC, s.seq_len - t0));
         const int64_t tok0 = int64_t(bh) * s.seq_len + t0;
 
-        // ---- staging data, gates and H_c blocks of this thread have landed; the barrier
-        // publishes H_c and ends the previous chunk's read-out
+        // the first row tile of H_c (requested into L2 under the previous chunk's CG) is
+        // read now, so that its latency passes during the staging
+        const float* Hc = static_cast<const float*>(a.Hs) + int64_t(cc) * DK * DK;
+        f32x4 hc[2][KS][2];
+        auto load_hc = [&](int mt, f32x4 (&dst)[KS][2]) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                for (int e = 0; e < 2; ++e)
+                    dst[ks][e] = *reinterpret_cast<const f32x4*>(Hc + ((2 * (mt * KS + ks) + e) * kWave + lane) * 4);
+        };
+        load_hc(0, hc[0]);
+        // ---- this thread's staging data and gates have landed (and the previous chunk's
+        // G_c); the barrier ends the previous chunk's read-out
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         uint4 kv[NKQ][2], vv[NV][2];
 #pragma unroll
@@ -300,14 +322,6 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
             vv[m][1] = sRaw[(2 * NKQ + 2 * m + 1) * kThreads + tid];
         }
         __syncthreads();
-        // q of this lane's token (rows 16mt + 4g .. +3), read now and used at the Jacobi
-        // start; a token past the end reads the last valid one and is zeroed there
-        uint2 qraw[MT];
-        {
-            const int64_t qrow = tok0 + min(j, valid - 1);
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) qraw[mt] = *reinterpret_cast<const uint2*>(qp + qrow * DK + 16 * mt + 4 * g);
-        }
         const float gl = lane < valid ? g_cur : 1.0f;
         const float bl = lane < valid ? b_cur : 0.0f;
         if (valid < kC) {
@@ -368,10 +382,19 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         const f32x4 zw = decay_weights4(sLg, sBeta, lgj, zlj, 16 * wave + 4 * g, j);
 
         // ---- B'_w in fp32, then its high and low parts as A-fragments in the accumulation
-        // registers: hfh/hfl[mt][ks] cover rows 16mt.., columns 32ks..  The rank update's
-        // A operand is K^T with the tokens i >= 16w zeroed (element e of step u is token
-        // 32u + 4g + e (e < 4) or 32u + 16 + 4g + e - 4); its B operand the scaled keys,
+        // registers: hfh/hfl[mt][ks] cover rows 16mt.., columns 32ks..  The accumulators
+        // start from H_c (read from global memory one row tile ahead), the rank update's A
+        // operand is K^T with the tokens i >= 16w zeroed (element e of step u is token
+        // 32u + 4g + e (e < 4) or 32u + 16 + 4g + e - 4), its B operand the scaled keys,
         // high and low parts.
+        // q of this lane's token (rows 16mt + 4g .. +3), used at the Jacobi start; a token
+        // past the end reads the last valid one and is zeroed there
+        uint2 qraw[MT];
+        {
+            const int64_t qrow = tok0 + min(j, valid - 1);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) qraw[mt] = *reinterpret_cast<const uint2*>(qp + qrow * DK + 16 * mt + 4 * g);
+        }
         bf16x8 ka[KS][2][2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
@@ -394,12 +417,12 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
 #pragma unroll
                 for (int hh = 0; hh < 2; ++hh) uw[u][hh] = decay_weights4(sLg, sBeta, lgb, zlb, 32 * u + 16 * hh + 4 * g, jb);
         }
-        const float hmul = keepH ? 1.0f : 0.0f;
         const int e_diag = ln - 4 * g;
         const bool on_diag = e_diag >= 0 && e_diag < 4;
         bf16x8 hfh[MT][KS], hfl[MT][KS];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
+            if (mt + 1 < MT) load_hc(mt + 1, hc[(mt + 1) % 2]);
             // scaled keys of the tile's columns (features 16mt + ln), high and low parts
             bf16x8 bwh[2], bwl[2];
 #pragma unroll
@@ -418,11 +441,14 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
                     split8(y0, y1, bwh[u], bwl[u]);
                 }
             }
+            if (!keepH) {  // the state term is dropped (wave-uniform, rare)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) hc[mt % 2][ks][0] = hc[mt % 2][ks][1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                const int f = mt * KS + ks;
-                f32x4 lo = hmul * *reinterpret_cast<const f32x4*>(sHc + ((2 * f + 0) * kWave + lane) * 4);
-                f32x4 hi = hmul * *reinterpret_cast<const f32x4*>(sHc + ((2 * f + 1) * kWave + lane) * 4);
+                f32x4 lo = hc[mt % 2][ks][0];
+                f32x4 hi = hc[mt % 2][ks][1];
 #pragma unroll
                 for (int u = 0; u < 2; ++u) {
                     lo = mfma16(ka[ks][0][u], bwh[u], lo);
@@ -459,8 +485,6 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         //   W = zs_j (B'_w vec) + K_w^T (beta Z ⊙ (K_w vec)) + Lambda vec,
         // each matrix-core product on split operands.
         auto matvec = [&](const f32x4 (&vec)[MT], f32x4 (&w)[MT]) {
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) w[mt] = zero4;
             f32x4 sacc = zero4;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
@@ -468,7 +492,7 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
                 split8(vec[2 * ks], vec[2 * ks + 1], vh, vl);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    w[mt] = mfma16(hfh[mt][ks], vh, w[mt]);
+                    w[mt] = mfma16(hfh[mt][ks], vh, ks == 0 ? zero4 : w[mt]);
                     w[mt] = mfma16(hfh[mt][ks], vl, w[mt]);
                     w[mt] = mfma16(hfl[mt][ks], vh, w[mt]);
                 }
@@ -504,28 +528,20 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
             qsh = cg_scale_shift(col_sum(qq));
             const float qs = __builtin_ldexpf(1.0f, -qsh);
             const bf16x8 zws = split4_stacked(zw);  // (hi, lo) of the weights of tokens 4g + e
-            bf16x8 zwh;                             // (hi, hi)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                zwh[e] = zws[e];
-                zwh[4 + e] = zws[e];
-            }
+            const uint4 zwu = __builtin_bit_cast(uint4, zws);
+            const bf16x8 zwh = __builtin_bit_cast(bf16x8, make_uint4(zwu.x, zwu.y, zwu.x, zwu.y));  // (hi, hi)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                // k^2 of the sub-chunk tokens: (hi, hi) against (w_hi, w_lo), then (lo, -) ...
-                bf16x8 kh, kl;
-                {
-                    const bf16x8 kk = kf3[mt];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float v = (float)kk[e];
-                        const float v2 = v * v;
-                        kh[e] = (__bf16)v2;
-                        kh[4 + e] = kh[e];
-                        kl[e] = (__bf16)(v2 - bf16_value(kh[e]));
-                        kl[4 + e] = (__bf16)0.0f;
-                    }
-                }
+                // k^2 of the sub-chunk tokens, exact as (hi, lo): (hi, hi) against (w_hi, w_lo),
+                // then (lo, 0) against (w_hi, w_hi)
+                const uint4 kk = __builtin_bit_cast(uint4, kf3[mt]);
+                const float k0 = __uint_as_float(kk.x << 16), k1 = __uint_as_float(kk.x & 0xffff0000u);
+                const float k2 = __uint_as_float(kk.y << 16), k3 = __uint_as_float(kk.y & 0xffff0000u);
+                uint32_t h01, l01, h23, l23;
+                split2(k0 * k0, k1 * k1, h01, l01);
+                split2(k2 * k2, k3 * k3, h23, l23);
+                const bf16x8 kh = __builtin_bit_cast(bf16x8, make_uint4(h01, h23, h01, h23));
+                const bf16x8 kl = __builtin_bit_cast(bf16x8, make_uint4(l01, l23, 0u, 0u));
                 f32x4 dg2 = mfma16(kh, zws, zero4);   // k2_hi (w_hi + w_lo)
                 dg2 = mfma16(kl, zwh, dg2);          // + k2_lo w_hi
                 const f32x4 d = zs * *reinterpret_cast<const f32x4*>(&sDiag[wave * (DK + kWave) + 16 * mt + 4 * g]) + dg2 +
@@ -549,21 +565,23 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         bool active = delta >= kMinNormal;
         int steps = 0;
 
-        // ---- every wave is done with sHc, sKT, sKUh and sKUl: the next chunk's loads may
-        // land there while this chunk's CG runs
+        // ---- every wave is done with sKT, sKUh and sKUl: the next chunk's loads may land
+        // there while this chunk's CG runs (and G_c's loads run under it: no access of this
+        // chunk's build or Jacobi start is ordered behind them)
         if (more) __syncthreads();
-        float g_nx = 1.0f, b_nx = 0.0f, lam_nx = 0.0f;
+        float g_nx, b_nx, lam_nx;
+        load_gates(more ? cn : cc, tid, g_nx, b_nx, lam_nx);
         int pieces = 0;   // pieces of the next chunk's loads issued so far
-        int gq = 0;       // quarters of this chunk's G_c requested into L2 so far
+        int gq = 0;       // quarters of this chunk's G_c loaded so far
 
         // One CG step (App. C, Alg. 1), branch-free: a stopped column takes alpha = 0 and
         // beta = 0 and keeps x.  A column stops, after its x update, when the new squared
         // residual meets Alg. 1's relative test or falls below the smallest normal number
         // (relative to |q|^2), and without an update when p^T A p is not a positive normal
-        // number.
+        // number.  The vector updates are written as in-place fused multiply-adds.
         auto cg_step = [&]() {
-            if (READOUT && gq < 4) request_g(cc, gq++, lane);
-            else if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
+            if (READOUT && gq < 4) load_g(cc, gq++, lane);
+            else if (more && pieces < kPieces) issue_piece(cn, pieces++, tid);
             matvec(p, w);
             f32x4 acc = zero4;
 #pragma unroll
@@ -572,11 +590,14 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
             const bool act1 = active && pw >= kMinNormal;
             steps += act1 ? 1 : 0;
             const float alpha = act1 ? delta * __builtin_amdgcn_rcpf(pw) : 0.0f;
+            const float nalpha = -alpha;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                x[mt] += alpha * p[mt];
-                r[mt] -= alpha * w[mt];
-            }
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    asm("v_fmac_f32 %0, %1, %2" : "+v"(x[mt][e]) : "v"(alpha), "v"(p[mt][e]));
+                    asm("v_fmac_f32 %0, %1, %2" : "+v"(r[mt][e]) : "v"(nalpha), "v"(w[mt][e]));
+                }
             acc = zero4;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) acc += r[mt] * r[mt];
@@ -584,7 +605,9 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
             const bool act2 = act1 && dn >= kMinNormal && dn > thr;
             const float bcg = act2 ? dn * __builtin_amdgcn_rcpf(delta) : 0.0f;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) p[mt] = r[mt] + bcg * p[mt];
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) asm("v_fma_f32 %0, %1, %0, %2" : "+v"(p[mt][e]) : "v"(bcg), "v"(r[mt][e]));
             delta = act2 ? dn : delta;
             active = act2;
         };
@@ -598,9 +621,9 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
             for (int mt = 0; mt < MT; ++mt) x[mt] = us * x[mt];
         }
         if (READOUT)
-            while (gq < 4) request_g(cc, gq++, lane);
+            while (gq < 4) load_g(cc, gq++, lane);
         if (more)
-            while (pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
+            while (pieces < kPieces) issue_piece(cn, pieces++, tid);
 
         if (a.steps && g == 0 && j < valid) a.steps[tok0 + j] = steps;
         if (a.qstar && j < valid) {
@@ -609,24 +632,15 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
                 *reinterpret_cast<f32x4*>(a.qstar + (tok0 + j) * DK + 16 * mt + 4 * g) = x[mt];
         }
         // ---- read-out o_j = G_c (zeta_j x_j) + sum_i beta_i Z[i][j] v_i (k_i^T x_j), on
-        // split operands; G_c's high and low fragments are read from global memory, one row
-        // tile ahead of their products
+        // split operands.  This wave's G_c loads (and the next chunk's) have landed; the
+        // barrier publishes G_c to every wave.
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
         if constexpr (READOUT) {
             const float zeta = sZ0[j];
             f32x4 zo[4];
 #pragma unroll
             for (int it = 0; it < 4; ++it) zo[it] = decay_weights4(sLg, sBeta, lgj, zlj, 16 * it + 4 * g, j);
-            const uint16_t* Gh = static_cast<const uint16_t*>(a.Gs) + int64_t(cc) * DV * DK;
-            const uint16_t* Gl = Gh + n_g;
-            auto gfrag = [&](const uint16_t* P, int mt, int ks) {
-                return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(P + ((mt * KS + ks) * kWave + lane) * 8));
-            };
-            bf16x8 gh[2][KS], gl[2][KS];
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                gh[0][ks] = gfrag(Gh, 0, ks);
-                gl[0][ks] = gfrag(Gl, 0, ks);
-            }
             // S = K x over the chunk's four token tiles (every wave runs all four; zo is zero
             // past the causal ones)
             f32x4 sacc[4];
@@ -645,23 +659,19 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
                 }
                 split8(zeta * x[2 * ks], zeta * x[2 * ks + 1], xzh[ks], xzl[ks]);
             }
+            const uint16_t* Gl = sGc + DV * DK;  // low plane
             f32x4 o[MTV];
 #pragma unroll
             for (int mt = 0; mt < MTV; ++mt) {
-                const int cur = mt % 2;
-                if (mt + 1 < MTV) {
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) {
-                        gh[cur ^ 1][ks] = gfrag(Gh, mt + 1, ks);
-                        gl[cur ^ 1][ks] = gfrag(Gl, mt + 1, ks);
-                    }
-                }
                 o[mt] = zero4;
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    o[mt] = mfma16(gh[cur][ks], xzh[ks], o[mt]);
-                    o[mt] = mfma16(gh[cur][ks], xzl[ks], o[mt]);
-                    o[mt] = mfma16(gl[cur][ks], xzh[ks], o[mt]);
+                    const int off = ((mt * KS + ks) * kWave + lane) * 8;
+                    const bf16x8 gh = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sGc + off));
+                    const bf16x8 gl = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(Gl + off));
+                    o[mt] = mfma16(gh, xzh[ks], o[mt]);
+                    o[mt] = mfma16(gh, xzl[ks], o[mt]);
+                    o[mt] = mfma16(gl, xzh[ks], o[mt]);
                 }
             }
             // + V (beta Z ⊙ S): the values as A operand (32 tokens per step), S' split into
