@@ -3,21 +3,28 @@
 
 A step is one forward pass of the layer over one batch of the 1B-shaped
 workload (B=8, heads=16, T=2048, d_k=d_v=128, chunk 64, 15 CG steps, bf16
-q/k/v, fp32 state and CG): the chunk-state scan launch, then the chunked CG +
-read-out launch.  Inputs are resident in HBM before timing starts.  Each launch
-is bracketed by HIP events on the stream it runs on; the CG launch is the
-dominant kernel and its algorithmic flops per launch divided by its mean event
-time give the roofline entry.  Decode (256 sequences x 16 heads, d=128,
-15 CG steps, 1024 consecutive steps) is timed after the forward steps.
+q/k/v): the chunk-state scan launch, then the chunked CG + read-out launch.
+Inputs are resident in HBM before timing starts.  Each launch is bracketed by
+HIP events on the stream it runs on; the CG launch is the dominant kernel and
+its algorithmic flops per launch divided by its mean event time give the
+roofline entry.
 
-Two extra entries run the same forward and decode with Alg. 1's relative
+The timed steps (the metric) use the single-pass matrix-core products
+(MESA_PREC_BF16: chunk states stored in bf16, CG operands rounded to bf16, fp32
+accumulation and fp32 CG vectors), the fastest mode within the bf16-input
+tolerance on the workloads.  The same workload is also timed with the
+fp32-accurate split-operand products (MESA_PREC_BF16X3, the library's default
+for bf16 inputs; App. G.5 keeps the solver's products in fp32) and with fp32
+products (MESA_PREC_F32), each with its own roofline entry; and the
+long-context workload (B=1, heads=16, T=16384, 20 CG steps) in both
+matrix-core modes.  Decode (256 sequences x 16 heads, d=128, 15 CG steps,
+1024 consecutive steps) is timed after the forward steps.
+
+Context entries run the same forward and decode with Alg. 1's relative
 stopping test (eps = 1e-4, at most 30 iterations, the paper's dynamic
-test-time compute setting) and report tokens/s and the mean iterations used;
-they are context, not the metric.  A third times the backward pass
-(mesa_backward, App. D) of the same workload given dL/do and the forward's q*.
-
-The CPU baseline is the fp64 oracle (the sequential recurrence with fixed-step
-CG) on a bounded sample of the same workload, run on the host's cores.
+test-time compute setting) and time the backward pass (mesa_backward, App. D).
+The CPU baseline is the fp64 oracle (the sequential recurrence with
+fixed-step CG) on the same workload, run on the host's cores.
 
 Prints ONE JSON line.
 """
@@ -37,9 +44,22 @@ if ROOT not in sys.path:
 METRIC = "Mesa-layer forward tokens/s on 1 MI355X (+% MFMA peak); decode tokens/s"
 PEAKS = {  # MI355X published dense peaks
     "mfma_bf16_tflops": 2500.0,
-    "fp32_vector_tflops": 157.3,
+    "mfma_fp32_tflops": 157.3,
     "hbm_gbps": 8000.0,
 }
+
+# What each precision mode computes, as printed in the JSON line.
+PREC_TEXT = {
+    2: "bf16 q/k/v; chunk states stored as bf16 matrix-core fragments; CG and read-out products on "
+       "single bf16 operands (the fp32 state, direction, intra-chunk weights and Lambda rounded to bf16) "
+       "with fp32 accumulation; CG vectors, scalars and reductions fp32 (MESA_PREC_BF16)",
+    3: "bf16 q/k/v; chunk states fp32-accurate (H_c fp32, G_c as bf16 high + low parts); CG and read-out "
+       "products on split operands x = hi + lo (hi*hi + hi*lo + lo*hi, three bf16 matrix-core passes, fp32 "
+       "accumulation); Lambda p, CG vectors, scalars and reductions fp32 (MESA_PREC_BF16X3)",
+    1: "bf16 q/k/v; fp32 chunk states; fp32 products on the fp32 matrix cores (MESA_PREC_F32)",
+}
+# The CG kernel each mode runs, and the sources its traffic record is tied to.
+CG_KERNEL = {2: "chunk_cg_bf16", 3: "chunk_cg_x3", 1: "chunk_cg_f32"}
 
 
 def log(msg):
@@ -50,7 +70,9 @@ def cg_kernel_flops(B, H, T, dk, dv, C, n_cg):
     """Algorithmic flops of one launch of the chunked CG + read-out kernel.
     Per token-head: (n_cg + 1) products (H_t + Lambda) p, each 2 d_k^2 for the
     state term plus 2 (C + 1) d_k for the causal intra-chunk K^T(Z (K p)) term
-    (causal halves only), and the read-out 2 d_v d_k + (C + 1)(d_k + d_v)."""
+    (causal halves only), and the read-out 2 d_v d_k + (C + 1)(d_k + d_v).
+    The same count serves every precision mode: split operands issue more
+    matrix-core work for the same products."""
     per_th = (n_cg + 1) * (2 * dk * dk + 2 * (C + 1) * dk) + 2 * dv * dk + (C + 1) * (dk + dv)
     return B * H * T * per_th
 
@@ -58,56 +80,58 @@ def cg_kernel_flops(B, H, T, dk, dv, C, n_cg):
 def state_kernel_bytes(B, H, T, dk, dv, C, in_bytes, state_bytes):
     """Algorithmic HBM bytes of the chunk-state launch: the states entering every
     chunk written once (state_bytes per element: 2 for the bf16 fragments of the
-    bf16 path, 4 for fp32 states), plus k and v read once (gates ignored)."""
+    single-pass path, 4 for fp32 or split-operand states), plus k and v read once
+    (gates ignored)."""
     nc = (T + C - 1) // C
     return B * H * nc * dk * (dk + dv) * state_bytes + B * H * T * (dk + dv) * in_bytes
 
 
-def traffic_entry(kernel_src_hash):
-    """HBM traffic of the CG kernel from committed rocprofv3 --pmc summaries, or
-    None when absent or taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", "chunk_cg_layer1b_traffic.json")
+def source_hash(kernel):
+    """sha256 over the sources a CG kernel is built from."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2506_05233_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.startswith(kernel) or name in ("mesa_device.hpp", "mesa_mfma.hpp", "mesa_kernels.hpp"):
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()
+
+
+def traffic_entry(kernel):
+    """HBM bytes per launch of a CG kernel from its committed rocprofv3 --pmc record,
+    or None when absent or taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", "%s_layer1b_traffic.json" % kernel)
     if not os.path.exists(path):
         return None
     try:
         rec = json.load(open(path))
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_sha256") != kernel_src_hash:
+    if rec.get("kernel_source_sha256") != source_hash(kernel):
         return None
     return rec.get("hbm_bytes_per_launch")
 
 
-def source_hash():
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2506_05233_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.startswith("chunk_cg") or name in ("mesa_device.hpp", "mesa_mfma.hpp"):
-            h.update(open(os.path.join(csrc, name), "rb").read())
-    return h.hexdigest()
-
-
-def run_forward(args, torch, L, W):
-    w = W.LAYER_1B_BF16
-    log("generating %s inputs" % w.name)
-    x = W.workload_inputs(w)
+def device_inputs(torch, x):
     dev = torch.device("cuda:0")
-    tdt = torch.bfloat16
     d = {}
     for name, a in x.items():
         t = torch.from_numpy(a).to(dev)
-        d[name] = t.to(tdt) if name in ("q", "k", "v") else t
-    plan = L.ForwardPlan(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], w.n_cg, w.chunk,
-                         args.precision)
-    log("warmup %d" % args.warmup)
-    for _ in range(args.warmup):
+        d[name] = t.to(torch.bfloat16) if name in ("q", "k", "v") else t
+    return d
+
+
+def time_forward(torch, L, w, d, prec, steps, warmup):
+    """Times `steps` forward steps (scan launch + solve launch) after `warmup`
+    untimed ones: wall time between two synchronisations and the mean HIP-event
+    time of each launch (events on the launch stream)."""
+    plan = L.ForwardPlan(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], w.n_cg, w.chunk, prec)
+    for _ in range(warmup):
         plan()
     torch.cuda.synchronize()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    log("timing %d steps" % args.steps)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         ev[i][0].record()
         plan.states()
         ev[i][1].record()
@@ -115,20 +139,79 @@ def run_forward(args, torch, L, W):
         ev[i][2].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    state_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
-    cg_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
-    out = plan.out
-    if not bool(torch.isfinite(out).all()):
+    state_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+    cg_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / steps
+    if not bool(torch.isfinite(plan.out).all()):
         raise RuntimeError("non-finite output")
+    return {"plan": plan, "wall": wall, "state_ms": state_ms, "cg_ms": cg_ms}
+
+
+def roofline(L, w, prec, cg_ms):
+    """Roofline entry of the CG launch: algorithmic flops / mean launch time against
+    the peak of the matrix cores the mode runs on."""
+    flops = cg_kernel_flops(w.batch, w.heads, w.seq_len, w.d_k, w.d_v, w.chunk, w.n_cg)
+    achieved = flops / (cg_ms / 1e3) / 1e12
+    peak = PEAKS["mfma_fp32_tflops"] if prec == L.MESA_PREC_F32 else PEAKS["mfma_bf16_tflops"]
+    kernel = CG_KERNEL[prec]
+    return {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+            "traffic": traffic_entry(kernel), "kernel": kernel + " (chunked CG + read-out)",
+            "ms_per_launch": cg_ms, "flops_per_launch": flops}
+
+
+def mode_entry(L, w, prec, t):
     B, H, T, dk, dv = w.batch, w.heads, w.seq_len, w.d_k, w.d_v
-    bf16_states = args.precision == L.MESA_PREC_BF16 or (
-        args.precision == L.MESA_PREC_AUTO and L.bf16_path_available(dk, dv, w.chunk, T))
-    return {
-        "w": w, "wall": wall, "state_ms": state_ms, "cg_ms": cg_ms, "d": d, "plan": plan,
-        "flops": cg_kernel_flops(B, H, T, dk, dv, w.chunk, w.n_cg),
-        "state_bytes": state_kernel_bytes(B, H, T, dk, dv, w.chunk, 2, 2 if bf16_states else 4),
-        "x": x,
-    }
+    sb = 2 if prec == L.MESA_PREC_BF16 else 4
+    st_bytes = state_kernel_bytes(B, H, T, dk, dv, w.chunk, 2, sb)
+    return {"inputs": PREC_TEXT[prec], "tokens_per_s": B * T / (t["wall"] / t["steps"]),
+            "ms_per_step": t["wall"] / t["steps"] * 1e3,
+            "kernels_ms": {"chunk_state": t["state_ms"], "chunk_cg": t["cg_ms"]},
+            "state_kernel_hbm": {"GBps": st_bytes / (t["state_ms"] / 1e3) / 1e9,
+                                 "frac": st_bytes / (t["state_ms"] / 1e3) / 1e9 / PEAKS["hbm_gbps"]},
+            "roofline": roofline(L, w, prec, t["cg_ms"])}
+
+
+def run_forward(args, torch, L, W):
+    w = W.LAYER_1B_BF16
+    log("generating %s inputs" % w.name)
+    x = W.workload_inputs(w)
+    d = device_inputs(torch, x)
+    log("warmup %d, timing %d steps (precision %d)" % (args.warmup, args.steps, args.precision))
+    t = time_forward(torch, L, w, d, args.precision, args.steps, args.warmup)
+    t["steps"] = args.steps
+    return {"w": w, "x": x, "d": d, "plan": t["plan"], "t": t}
+
+
+def run_other_modes(args, torch, L, fw):
+    """The headline workload in the other precision modes (5 timed steps each)."""
+    w, d = fw["w"], fw["d"]
+    out = {}
+    for prec, key in ((L.MESA_PREC_BF16X3, "split_operands_bf16x3"), (L.MESA_PREC_F32, "fp32_products")):
+        if prec == args.precision:
+            continue
+        log("forward in precision mode %d" % prec)
+        t = time_forward(torch, L, w, d, prec, 5, 2)
+        t["steps"] = 5
+        out[key] = mode_entry(L, w, prec, t)
+        del t["plan"]
+    return out
+
+
+def run_long_context(args, torch, L, W):
+    """The long-context workload (B=1, heads=16, T=16384, 20 CG steps) in both
+    matrix-core modes: tokens/s and per-launch times."""
+    w = W.LONG_BF16
+    log("generating %s inputs" % w.name)
+    d = device_inputs(torch, W.workload_inputs(w))
+    res = {"workload": w.name, "batch": w.batch, "heads": w.heads, "seq_len": w.seq_len, "n_cg": w.n_cg}
+    for prec, key in ((L.MESA_PREC_BF16, "single_pass_bf16"), (L.MESA_PREC_BF16X3, "split_operands_bf16x3")):
+        log("long context, precision mode %d" % prec)
+        t = time_forward(torch, L, w, d, prec, 5, 2)
+        t["steps"] = 5
+        e = mode_entry(L, w, prec, t)
+        e["cg_fraction_of_step"] = t["cg_ms"] / (t["state_ms"] + t["cg_ms"])
+        del t["plan"]
+        res[key] = e
+    return res
 
 
 def run_forward_dynamic(args, torch, L, fw):
@@ -160,6 +243,8 @@ def run_backward(args, torch, L, fw):
     """mesa_backward on the forward workload: gradients of q, k, v, gamma, beta and
     Lambda given a seeded dL/do and the q* of the forward (computed before timing)."""
     w, d = fw["w"], fw["d"]
+    # the backward's solve runs on fp32 products or on the single-pass matrix cores
+    prec = L.MESA_PREC_F32 if args.precision == L.MESA_PREC_F32 else L.MESA_PREC_BF16
     res = L.forward(d["q"], d["k"], d["v"], d["gamma"], d["beta"], d["lam"], w.n_cg, w.chunk,
                     precision=args.precision, want_qstar=True)
     qstar = res["qstar"]
@@ -169,7 +254,7 @@ def run_backward(args, torch, L, fw):
                      dtype=torch.uint8, device="cuda")
     def call():
         return L.backward(d["k"], d["v"], d["gamma"], d["beta"], d["lam"], qstar, dout, w.n_cg,
-                          precision=args.precision, workspace=ws)
+                          precision=prec, workspace=ws)
     for _ in range(2):
         g = call()
     torch.cuda.synchronize()
@@ -186,7 +271,7 @@ def run_backward(args, torch, L, fw):
     ms = e0.elapsed_time(e1) / reps
     del ws
     return {"tokens_per_s": w.batch * w.seq_len / (ms / 1e3), "ms_per_call": ms, "n_cg": w.n_cg,
-            "solve": "matrix cores (bf16 operands)" if args.precision != L.MESA_PREC_F32 else "fp32",
+            "solve": "matrix cores (single-pass bf16 operands)" if prec == L.MESA_PREC_BF16 else "fp32 products",
             "launches": "fp32 and bf16 chunk states, rhs G^T e, CG solve for e*, reverse adjoint scan, "
                         "per-chunk gradients, Lambda sum"}
 
@@ -350,11 +435,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--precision", type=int, default=0, help="MESA_PREC_* (0 = auto)")
+    ap.add_argument("--precision", type=int, default=2, choices=(1, 2, 3),
+                    help="MESA_PREC_* of the timed steps: 2 single-pass bf16 (default), 3 split "
+                         "operands, 1 fp32 products")
     ap.add_argument("--decode-steps", type=int, default=1024)
     ap.add_argument("--cpu-sequences", type=int, default=128)
     ap.add_argument("--skip-decode", action="store_true")
     ap.add_argument("--skip-backward", action="store_true")
+    ap.add_argument("--skip-modes", action="store_true", help="skip the other precision modes")
+    ap.add_argument("--skip-long", action="store_true", help="skip the long-context workload")
     ap.add_argument("--eps", type=float, default=1e-4,
                     help="relative CG tolerance of the extra dynamic-stopping runs (0: skip them)")
     ap.add_argument("--dyn-max-cg", type=int, default=30, help="iteration limit of those runs")
@@ -377,7 +466,7 @@ def main():
     L.load()
 
     fw = run_forward(args, torch, L, W)
-    w = fw["w"]
+    w, t = fw["w"], fw["t"]
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -386,46 +475,36 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    head = mode_entry(L, w, args.precision, t)
+    modes = None if args.skip_modes else run_other_modes(args, torch, L, fw)
     dyn = run_forward_dynamic(args, torch, L, fw) if args.eps > 0 else None
     bwd = None if args.skip_backward else run_backward(args, torch, L, fw)
+    longctx = None if args.skip_long else run_long_context(args, torch, L, W)
     dec = None if args.skip_decode else run_decode(args, torch, L, W)
     cpu = None if args.skip_cpu else cpu_baseline(args, fw["x"], w)
 
-    prec = args.precision
-    bf16_path = prec == L.MESA_PREC_BF16 or (prec == L.MESA_PREC_AUTO and
-                                              L.bf16_path_available(w.d_k, w.d_v, w.chunk, w.seq_len))
     tokens = w.batch * w.seq_len
-    cg_s = fw["cg_ms"] / 1e3
-    achieved = fw["flops"] / cg_s / 1e12
-    if bf16_path:
-        roof = {"bound": "mfma", "peak": PEAKS["mfma_bf16_tflops"]}
-    else:
-        roof = {"bound": "alu", "peak": PEAKS["fp32_vector_tflops"]}
-    roof.update({"achieved": achieved, "unit": "TFLOP/s", "frac": achieved / roof["peak"],
-                 "traffic": traffic_entry(source_hash()),
-                 "kernel": "chunk_cg (chunked CG + read-out)", "ms_per_launch": fw["cg_ms"],
-                 "flops_per_launch": fw["flops"]})
     res = {
         "metric": METRIC,
-        "value": tokens * args.steps / fw["wall"],
+        "value": tokens * args.steps / t["wall"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": fw["wall"] / args.steps * 1e3,
+        "ms_per_step": t["wall"] / args.steps * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if bf16_path else "f32",
+        "dtype": "f32" if args.precision == L.MESA_PREC_F32 else "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "batch": w.batch, "heads": w.heads, "seq_len": w.seq_len,
                    "d_k": w.d_k, "d_v": w.d_v, "chunk": w.chunk, "n_cg": w.n_cg,
-                   "inputs": "bf16 q/k/v, fp32 gates/lambda/state/CG",
-                   "parallelism": "single GPU"},
-        "roofline": roof,
-        "kernels_ms": {"chunk_state": fw["state_ms"], "chunk_cg": fw["cg_ms"]},
-        "state_kernel_hbm": {"GBps": fw["state_bytes"] / (fw["state_ms"] / 1e3) / 1e9,
-                             "frac": fw["state_bytes"] / (fw["state_ms"] / 1e3) / 1e9 / PEAKS["hbm_gbps"]},
+                   "inputs": PREC_TEXT[args.precision], "parallelism": "single GPU"},
+        "roofline": head["roofline"],
+        "kernels_ms": head["kernels_ms"],
+        "state_kernel_hbm": head["state_kernel_hbm"],
+        "other_precision_modes": modes,
+        "long_context": longctx,
         "forward_dynamic_stopping": dyn,
         "backward": bwd,
         "decode": dec,

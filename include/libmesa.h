@@ -65,7 +65,8 @@ extern "C" {
 #define MESA_DTYPE_BF16 1
 
 /* Arithmetic of the matrix products inside CG and the read-out.
- *   MESA_PREC_AUTO  : MESA_PREC_F32 for fp32 inputs, MESA_PREC_BF16 for bf16 inputs.
+ *   MESA_PREC_AUTO  : MESA_PREC_BF16X3 for bf16 inputs at chunk 64 (fp32-accurate
+ *                     products, as the paper's solver keeps them), else MESA_PREC_F32.
  *   MESA_PREC_F32   : fp32 products with fp32 accumulation (fp32-accurate).
  *   MESA_PREC_BF16  : matrix-core products with bf16 operands and fp32 accumulation:
  *                     the chunk states are stored as bf16, and the fp32 CG

@@ -154,7 +154,7 @@ int resolve_precision(const FwdCall& c)
 {
     const ForwardShape s = shape_of(c);
     if (c.precision == MESA_PREC_AUTO)
-        return s.bf16 && mesa::chunk_cg_bf16_supported(s) ? MESA_PREC_BF16 : MESA_PREC_F32;
+        return s.bf16 && mesa::chunk_cg_x3_supported(s) ? MESA_PREC_BF16X3 : MESA_PREC_F32;
     return c.precision;
 }
 

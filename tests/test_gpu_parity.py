@@ -312,8 +312,8 @@ def test_segmented_state_scan_long_memory():
 
 def test_forward_is_bitwise_deterministic():
     x = W.forward_inputs(2, 4, 512, 128, 128, "bf16", 4.0, seed=9)
-    a = _gpu_forward(x, "bf16", 15, 64)
-    b = _gpu_forward(x, "bf16", 15, 64)
+    a = _gpu_forward(x, "bf16", 15, 64, precision=L.MESA_PREC_BF16)
+    b = _gpu_forward(x, "bf16", 15, 64, precision=L.MESA_PREC_BF16)
     assert np.array_equal(a, b)
 
 
@@ -333,9 +333,11 @@ def test_stress_repeated_keys_f32_path():
     (W.LONG_BF16, [(0, 0), (0, 9)]),
 ], ids=["layer1b", "longctx"])
 def test_forward_full_size_sampled(w, pairs):
+    """Single-pass matrix-core products (the benchmarked mode) at full size; the
+    split-operand mode has its own full-size test."""
     _say("full-size forward %s, sampled %s" % (w.name, pairs))
     x = W.workload_inputs(w)
-    got = _gpu_forward(x, w.dtype, w.n_cg, w.chunk)
+    got = _gpu_forward(x, w.dtype, w.n_cg, w.chunk, precision=L.MESA_PREC_BF16)
     assert np.isfinite(got).all()
     refs = _oracle_pairs(x, pairs, w.n_cg)
     g = np.stack([got[b, h] for b, h in pairs])
