@@ -106,9 +106,12 @@ extern "C" {
 /* Bytes of device workspace mesa_forward needs: the states entering every
  * chunk (App. D: states are kept only at chunk boundaries c = 0, C, 2C, ...),
  * H_c for [batch, heads, ceil(seq_len/chunk)] chunks (d_k x d_k each) followed
- * by G_c (d_v x d_k each), as fp32 (the upper bound; the bf16 path stores them
- * as bf16 and uses half).  The layout is internal to the library.  Returns 0
- * for unsupported or empty sizes. */
+ * by G_c (d_v x d_k each), as fp32 (the upper bound; MESA_PREC_BF16 stores them
+ * as bf16 and uses half), and, for few long sequences (batch * heads <= 64 and
+ * at least 16 chunks), room for the segment totals of the segmented scan:
+ * min(batch * heads * floor(chunks / 8), 128) * d_k * (d_k + d_v) + 128 floats
+ * more.  The layout is internal to the library.  Returns 0 for unsupported or
+ * empty sizes. */
 size_t mesa_forward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
                                     int64_t d_v, int chunk);
 

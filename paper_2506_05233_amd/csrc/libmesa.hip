@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "mesa_kernels.hpp"
@@ -62,6 +63,16 @@ int check_sizes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int6
 }  // namespace
 
 namespace {
+
+// fp32 bytes of the states entering every chunk (H_c then G_c), 0 for unsupported or
+// empty sizes.
+size_t states_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v, int chunk)
+{
+    if (batch <= 0 || heads <= 0 || seq_len <= 0) return 0;
+    if (!dim_ok(d_k) || !dim_ok(d_v) || !chunk_ok(chunk)) return 0;
+    const int64_t nc = n_chunks_of(seq_len, chunk);
+    return size_t(batch) * size_t(heads) * size_t(nc) * size_t(d_k) * size_t(d_k + d_v) * sizeof(float);
+}
 
 // Checks shared by the forward entry points.  `need_ws` is the workspace the
 // call reads or writes (0 when it uses none).  Returns a status code.
@@ -190,6 +201,14 @@ int launch_states(const FwdCall& c, bool store_chunks, hipStream_t s)
         const size_t full = mesa_forward_workspace_bytes(c.batch, c.heads, c.seq_len, c.d_k, c.d_v, c.chunk);
         sa.seg_ws = reinterpret_cast<float*>(static_cast<char*>(const_cast<void*>(c.workspace)) + full / 2);
         sa.seg_bytes = full - full / 2;
+    } else if (sa.x3 && c.workspace) {
+        // the split-operand states fill the fp32-sized part: the segment totals go after it
+        const size_t states = states_bytes(c.batch, c.heads, c.seq_len, c.d_k, c.d_v, c.chunk);
+        const size_t full = mesa_forward_workspace_bytes(c.batch, c.heads, c.seq_len, c.d_k, c.d_v, c.chunk);
+        if (full > states) {
+            sa.seg_ws = reinterpret_cast<float*>(static_cast<char*>(const_cast<void*>(c.workspace)) + states);
+            sa.seg_bytes = full - states;
+        }
     }
     return mesa::launch_chunk_state(sa, s) == hipSuccess ? MESA_OK : MESA_ERR_HIP;
 }
@@ -230,10 +249,15 @@ const char* mesa_status_string(int status)
 size_t mesa_forward_workspace_bytes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
                                     int64_t d_v, int chunk)
 {
-    if (batch <= 0 || heads <= 0 || seq_len <= 0) return 0;
-    if (!dim_ok(d_k) || !dim_ok(d_v) || !chunk_ok(chunk)) return 0;
-    const int64_t nc = n_chunks_of(seq_len, chunk);
-    return size_t(batch) * size_t(heads) * size_t(nc) * size_t(d_k) * size_t(d_k + d_v) * sizeof(float);
+    const size_t states = states_bytes(batch, heads, seq_len, d_k, d_v, chunk);
+    if (states == 0) return 0;
+    // Few long sequences (at most 64, at least 16 chunks each) are scanned in segments
+    // (at most 128 segment totals in all, none for a sequence's last segment, and at most
+    // one per 8 chunks): room for the totals and the segment decays after the states.
+    const int64_t bh = batch * heads, nc = n_chunks_of(seq_len, chunk);
+    if (bh > 64 || nc < 16) return states;
+    const int64_t totals = std::min<int64_t>(bh * (nc / 8), 128);
+    return states + size_t(totals) * size_t(d_k) * size_t(d_k + d_v) * sizeof(float) + 128 * sizeof(float);
 }
 
 int mesa_forward_ex(const void* q, const void* k, const void* v, const float* gamma,

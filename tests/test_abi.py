@@ -63,6 +63,12 @@ def test_workspace_bytes(lib):
     assert L.forward_workspace_bytes(1, 1, 0, 64, 64, 64) == 0
     assert L.forward_workspace_bytes(1, 1, 64, 96, 64, 64) == 0
     assert L.forward_workspace_bytes(1, 1, 64, 64, 64, 48) == 0
+    # few long sequences: room for the segment totals of the segmented scan after the
+    # states, min(B H floor(chunks / 8), 128) totals of d_k (d_k + d_v) floats, + 128 floats
+    states = 16 * 256 * 128 * 256 * 4
+    assert L.forward_workspace_bytes(1, 16, 16384, 128, 128, 64) == states + 128 * 128 * 256 * 4 + 512
+    assert L.forward_workspace_bytes(1, 2, 17 * 64 + 13, 64, 128, 64) == 2 * 18 * 64 * 192 * 4 + 4 * 64 * 192 * 4 + 512
+    assert L.forward_workspace_bytes(65, 1, 16 * 64, 128, 128, 64) == 65 * 16 * 128 * 256 * 4
 
 
 # fake, non-overlapping device addresses

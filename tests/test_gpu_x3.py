@@ -166,3 +166,26 @@ def test_x3_full_size_sampled(w, pairs):
     e = rel_l2(np.stack([got[b, h] for b, h in pairs]), np.stack(refs))
     _say("  sampled rel L2 %.3e" % e)
     assert e <= TOL_F32
+
+
+@pytest.mark.parametrize("dk,dv", [(128, 128), (64, 128)])
+def test_x3_segmented_scan_long_memory(dk, dv):
+    """Two sequences of 36 chunks: the split-operand scan runs in segments (the
+    totals in the output array, which the solve then overwrites), gates within 1e-3
+    of one keep every earlier segment visible, zero gates reset memory inside a
+    segment and on a segment's first token.  The output array starts filled with
+    ones, so a total read before it is written, or an output the solve leaves
+    unwritten, shows.  Every output and the final states against the oracle."""
+    T = 35 * 64 + 17
+    x = W.forward_inputs(1, 2, T, dk, dv, "bf16", 4.0, seed=81 + dk)
+    rng = np.random.default_rng(8101 + dk)
+    x["gamma"][...] = rng.uniform(0.999, 1.0, size=x["gamma"].shape).astype(np.float32)
+    x["gamma"][0, 0, 9 * 64 + 100] = 0.0
+    x["gamma"][0, 1, 18 * 64] = 0.0
+    out = torch.ones((1, 2, T, dv), dtype=torch.float32, device="cuda")
+    got = _gpu_forward(x, 15, want_states=True, out=out)
+    ref = oracle.forward(x["q"], x["k"], x["v"], x["gamma"], x["beta"], x["lam"], 15, want_states=True)
+    e_out = rel_l2(got["out"], ref["out"])
+    e_h, e_g = rel_l2(got["H"], ref["H"]), rel_l2(got["G"], ref["G"])
+    _say("x3 segmented d_k=%d d_v=%d: out %.3e H %.3e G %.3e" % (dk, dv, e_out, e_h, e_g))
+    assert e_out <= TOL_F32 and e_h <= 1e-5 and e_g <= 1e-5
