@@ -444,6 +444,9 @@ def main():
     ap.add_argument("--skip-backward", action="store_true")
     ap.add_argument("--skip-modes", action="store_true", help="skip the other precision modes")
     ap.add_argument("--skip-long", action="store_true", help="skip the long-context workload")
+    ap.add_argument("--long-only", action="store_true",
+                    help="time only the long-context workload and print its entry (a profiling aid; "
+                         "not the metric)")
     ap.add_argument("--eps", type=float, default=1e-4,
                     help="relative CG tolerance of the extra dynamic-stopping runs (0: skip them)")
     ap.add_argument("--dyn-max-cg", type=int, default=30, help="iteration limit of those runs")
@@ -465,6 +468,9 @@ def main():
         sys.exit(1)
     L.load()
 
+    if args.long_only:
+        print(json.dumps({"long_context": run_long_context(args, torch, L, W)}), flush=True)
+        return
     fw = run_forward(args, torch, L, W)
     w, t = fw["w"], fw["t"]
     if args.calib_copy_mib > 0:
