@@ -270,6 +270,50 @@ int mesa_forward_noalloc(const void* q, const void* k, const void* v, const floa
                          int64_t seq_len, int64_t d_k, int64_t d_v, int dtype, int n_cg, int chunk,
                          float* out, void* stream);
 
+/* The layer's front end (App. E; the gate cap and the Lambda floor of App. G.5),
+ * one launch, from the projections of the layer input e_t (the heads of a token
+ * side by side, as a projection produces them) to the inputs of mesa_forward:
+ *     q_t, k_t = normalize(SiLU(conv4(projection)))      per head
+ *     v_t      = SiLU(conv4(projection)) if conv_v, else the projection
+ *     beta_t   = sigmoid(a_beta_t)
+ *     gamma_t  = sigmoid(a_gamma_t) * (1 - (1 - gamma_cap) * beta_t^2)
+ *     Lambda   = 0.25 + softplus(theta)
+ * with conv4(x)_t = sum_{i=0..3} w[c][i] x_{t-i} per channel c (x_s = 0 for s < 0),
+ * SiLU(x) = x sigmoid(x), normalize(x) = x / sqrt(|x|^2 + l2_eps), softplus(x) =
+ * log(1 + exp(x)).
+ *   qp, kp        [batch, seq_len, heads, d_k]   dtype (the projections)
+ *   vp            [batch, seq_len, heads, d_v]   dtype
+ *   conv_q, conv_k [heads * d_k, 4]              fp32, w[c][i] multiplies x_{t-i}
+ *   conv_v        [heads * d_v, 4] fp32, or NULL (values pass through)
+ *   a_gamma, a_beta [batch, seq_len, heads]      fp32, gate pre-activations
+ *   theta         [heads, d_k]                   fp32
+ *   gamma_cap     in [0, 1] (App. G.5 uses 0.9975; 1 disables the cap)
+ *   l2_eps        >= 0 (a zero key or query stays zero when > 0)
+ *   q, k          [batch, heads, seq_len, d_k]   dtype (outputs)
+ *   v             [batch, heads, seq_len, d_v]   dtype
+ *   gamma, beta   [batch, heads, seq_len]        fp32
+ *   lambda        [heads, d_k]                   fp32
+ * d_k, d_v in {64, 128}.  Arrays need the alignment of their element type; outputs
+ * must overlap neither an input nor each other (MESA_ERR_ARG).  batch or seq_len 0
+ * writes lambda only; heads 0 is a no-op.  One kernel launch. */
+int mesa_frontend(const void* qp, const void* kp, const void* vp, const float* conv_q, const float* conv_k,
+                  const float* conv_v, const float* a_gamma, const float* a_beta, const float* theta,
+                  float gamma_cap, float l2_eps, int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
+                  int64_t d_v, int dtype, void* q, void* k, void* v, float* gamma, float* beta, float* lambda,
+                  void* stream);
+
+/* The layer's back end (App. E): each head's output through its RMSNorm before the
+ * output projection, y_t = o_t / sqrt(mean(o_t^2) + eps) * weight[h], with the heads
+ * of a token side by side for that projection.
+ *   o       [batch, heads, seq_len, d_v]   fp32 (the out of mesa_forward)
+ *   weight  [heads, d_v]                   fp32
+ *   eps     >= 0
+ *   y       [batch, seq_len, heads, d_v]   out_dtype (MESA_DTYPE_F32 or MESA_DTYPE_BF16,
+ *           rounded to nearest even)
+ * d_v in {64, 128}; y must not overlap o or weight.  One kernel launch. */
+int mesa_output_norm(const float* o, const float* weight, float eps, int64_t batch, int64_t heads,
+                     int64_t seq_len, int64_t d_v, int out_dtype, void* y, void* stream);
+
 /* Static text for a status code (never NULL). */
 const char* mesa_status_string(int status);
 

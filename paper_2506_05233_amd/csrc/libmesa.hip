@@ -659,3 +659,78 @@ int mesa_forward_noalloc(const void* q, const void* k, const void* v, const floa
 }
 
 }  // extern "C"
+
+extern "C" {
+
+int mesa_frontend(const void* qp, const void* kp, const void* vp, const float* conv_q, const float* conv_k,
+                  const float* conv_v, const float* a_gamma, const float* a_beta, const float* theta,
+                  float gamma_cap, float l2_eps, int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
+                  int64_t d_v, int dtype, void* q, void* k, void* v, float* gamma, float* beta, float* lambda,
+                  void* stream)
+{
+    int st = check_sizes(batch, heads, seq_len, d_k, d_v, dtype, 0);
+    if (st != MESA_OK) return st;
+    if (!(isfinite(gamma_cap) && gamma_cap >= 0.0f && gamma_cap <= 1.0f)) return MESA_ERR_ARG;
+    if (!(isfinite(l2_eps) && l2_eps >= 0.0f)) return MESA_ERR_ARG;
+    if (heads == 0) return MESA_OK;
+    if (!theta || !lambda) return MESA_ERR_NULL;
+    const int64_t tokens = batch * heads * seq_len;
+    if (tokens > 0 && (!qp || !kp || !vp || !conv_q || !conv_k || !a_gamma || !a_beta || !q || !k || !v ||
+                       !gamma || !beta))
+        return MESA_ERR_NULL;
+    if (tokens > (int64_t(1) << 40)) return MESA_ERR_SHAPE;
+    const int64_t es = dtype == MESA_DTYPE_BF16 ? 2 : 4;
+    for (const void* ptr : {qp, kp, vp, static_cast<const void*>(q), static_cast<const void*>(k),
+                            static_cast<const void*>(v)})
+        if (uintptr_t(ptr) % es != 0) return MESA_ERR_ARG;
+    for (const void* ptr : {static_cast<const void*>(conv_q), static_cast<const void*>(conv_k),
+                            static_cast<const void*>(conv_v), static_cast<const void*>(a_gamma),
+                            static_cast<const void*>(a_beta), static_cast<const void*>(theta),
+                            static_cast<const void*>(gamma), static_cast<const void*>(beta),
+                            static_cast<const void*>(lambda)})
+        if (uintptr_t(ptr) % 4 != 0) return MESA_ERR_ARG;
+    const Range ins[] = {range_of(qp, tokens * d_k * es), range_of(kp, tokens * d_k * es),
+                         range_of(vp, tokens * d_v * es), range_of(conv_q, heads * d_k * 16),
+                         range_of(conv_k, heads * d_k * 16), range_of(conv_v, conv_v ? heads * d_v * 16 : 0),
+                         range_of(a_gamma, tokens * 4), range_of(a_beta, tokens * 4),
+                         range_of(theta, heads * d_k * 4)};
+    const Range outs[] = {range_of(q, tokens * d_k * es), range_of(k, tokens * d_k * es),
+                          range_of(v, tokens * d_v * es), range_of(gamma, tokens * 4),
+                          range_of(beta, tokens * 4), range_of(lambda, heads * d_k * 4)};
+    for (const Range& o : outs) {
+        if (o.lo == o.hi) continue;
+        for (const Range& i : ins)
+            if (i.lo != i.hi && overlaps(o, i)) return MESA_ERR_ARG;
+    }
+    for (int x = 0; x < 6; ++x)
+        for (int y = x + 1; y < 6; ++y)
+            if (outs[x].lo != outs[x].hi && outs[y].lo != outs[y].hi && overlaps(outs[x], outs[y]))
+                return MESA_ERR_ARG;
+    mesa::FrontArgs fa{batch, heads, seq_len, int(d_k), int(d_v), dtype == MESA_DTYPE_BF16, qp, kp, vp,
+                       conv_q, conv_k, conv_v, a_gamma, a_beta, theta, gamma_cap, l2_eps, q, k, v, gamma,
+                       beta, lambda};
+    const hipError_t e = mesa::launch_frontend(fa, static_cast<hipStream_t>(stream));
+    return finish(e == hipSuccess ? MESA_OK : MESA_ERR_HIP, stream);
+}
+
+int mesa_output_norm(const float* o, const float* weight, float eps, int64_t batch, int64_t heads,
+                     int64_t seq_len, int64_t d_v, int out_dtype, void* y, void* stream)
+{
+    int st = check_sizes(batch, heads, seq_len, 64, d_v, out_dtype, 0);
+    if (st != MESA_OK) return st;
+    if (!(isfinite(eps) && eps >= 0.0f)) return MESA_ERR_ARG;
+    const int64_t tokens = batch * heads * seq_len;
+    if (tokens == 0) return MESA_OK;
+    if (!o || !weight || !y) return MESA_ERR_NULL;
+    if (tokens > (int64_t(1) << 40)) return MESA_ERR_SHAPE;
+    const int64_t es = out_dtype == MESA_DTYPE_BF16 ? 2 : 4;
+    if (uintptr_t(o) % 4 != 0 || uintptr_t(weight) % 4 != 0 || uintptr_t(y) % es != 0) return MESA_ERR_ARG;
+    const Range out = range_of(y, tokens * d_v * es);
+    if (overlaps(out, range_of(o, tokens * d_v * 4)) || overlaps(out, range_of(weight, heads * d_v * 4)))
+        return MESA_ERR_ARG;
+    mesa::NormArgs na{batch, heads, seq_len, int(d_v), out_dtype == MESA_DTYPE_BF16, o, weight, eps, y};
+    const hipError_t e = mesa::launch_output_norm(na, static_cast<hipStream_t>(stream));
+    return finish(e == hipSuccess ? MESA_OK : MESA_ERR_HIP, stream);
+}
+
+}  // extern "C"

@@ -141,4 +141,45 @@ hipError_t launch_decode_step(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_pack_state(const float* H, float* HP, int64_t pairs, int d_k, hipStream_t stream);
 hipError_t launch_unpack_state(const float* HP, float* H, int64_t pairs, int d_k, hipStream_t stream);
 
+// The layer's front end (App. E; gate cap and Lambda floor of App. G.5), one launch:
+// q, k [B, H, T, d_k] and v [B, H, T, d_v] (element type of the projections) from the
+// projections qp, kp [B, T, H, d_k], vp [B, T, H, d_v]; gamma, beta [B, H, T] from the
+// gate projections a_gamma, a_beta [B, T, H]; lambda [H, d_k] from theta [H, d_k].
+// conv_q, conv_k [H * d_k, 4], conv_v [H * d_v, 4] or null (values unchanged).
+struct FrontArgs {
+    int64_t batch, heads, seq_len;
+    int d_k, d_v;
+    bool bf16;
+    const void* qp;
+    const void* kp;
+    const void* vp;
+    const float* conv_q;
+    const float* conv_k;
+    const float* conv_v;
+    const float* a_gamma;
+    const float* a_beta;
+    const float* theta;
+    float gamma_cap, l2_eps;
+    void* q;
+    void* k;
+    void* v;
+    float* gamma;
+    float* beta;
+    float* lambda;
+};
+hipError_t launch_frontend(const FrontArgs& a, hipStream_t stream);
+
+// The back end: per-head RMSNorm, o [B, H, T, d_v] fp32 -> y [B, T, H, d_v] (fp32 or
+// bf16), weight [H, d_v].
+struct NormArgs {
+    int64_t batch, heads, seq_len;
+    int d_v;
+    bool bf16_out;
+    const float* o;
+    const float* weight;
+    float eps;
+    void* y;
+};
+hipError_t launch_output_norm(const NormArgs& a, hipStream_t stream);
+
 }  // namespace mesa

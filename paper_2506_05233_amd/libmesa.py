@@ -33,6 +33,7 @@ EXPORTED = ("mesa_forward", "mesa_forward_ex", "mesa_forward_states", "mesa_forw
             "mesa_forward_tol", "mesa_forward_workspace_bytes", "mesa_decode_step",
             "mesa_decode_step_tol", "mesa_decode_step_packed", "mesa_pack_state", "mesa_unpack_state",
             "mesa_backward", "mesa_backward_workspace_bytes", "mesa_forward_noalloc",
+            "mesa_frontend", "mesa_output_norm",
             "mesa_status_string", "mesa_version")
 
 _lib = None
@@ -88,6 +89,11 @@ def load():
     lib.mesa_backward.restype = ci
     lib.mesa_forward_noalloc.argtypes = [vp, vp, vp, fp, fp, fp, i64, i64, i64, i64, i64, ci, ci, ci, fp, vp]
     lib.mesa_forward_noalloc.restype = ci
+    lib.mesa_frontend.argtypes = [vp, vp, vp, fp, fp, fp, fp, fp, fp, cf, cf, i64, i64, i64, i64, i64, ci,
+                                   vp, vp, vp, fp, fp, fp, vp]
+    lib.mesa_frontend.restype = ci
+    lib.mesa_output_norm.argtypes = [fp, fp, cf, i64, i64, i64, i64, ci, vp, vp]
+    lib.mesa_output_norm.restype = ci
     lib.mesa_status_string.argtypes = [ci]
     lib.mesa_status_string.restype = ctypes.c_char_p
     lib.mesa_version.argtypes = []
@@ -218,6 +224,61 @@ def forward(q, k, v, gamma, beta, lam, n_cg, chunk=64, precision=MESA_PREC_AUTO,
         res["H"] = fH
         res["G"] = fG
     return res
+
+
+def frontend(qp, kp, vp, conv_q, conv_k, conv_v, a_gamma, a_beta, theta, gamma_cap=0.9975, l2_eps=1e-6):
+    """mesa_frontend: the layer's inputs from the projections (App. E, App. G.5).
+    qp, kp [B,T,H,d_k], vp [B,T,H,d_v] (fp32 or bf16, one dtype); conv_q, conv_k
+    [H*d_k,4], conv_v [H*d_v,4] or None; a_gamma, a_beta [B,T,H]; theta [H,d_k] (fp32).
+    Returns a dict: q, k [B,H,T,d_k], v [B,H,T,d_v] (the projections' dtype), gamma,
+    beta [B,H,T], lam [H,d_k] (fp32)."""
+    torch = _torch()
+    lib = load()
+    B, T, H, dk = qp.shape
+    dv = vp.shape[-1]
+    dev = qp.device
+    f32 = torch.float32
+    _check(qp, "qp", (B, T, H, dk), device=dev)
+    _check(kp, "kp", (B, T, H, dk), qp.dtype, dev)
+    _check(vp, "vp", (B, T, H, dv), qp.dtype, dev)
+    _check(conv_q, "conv_q", (H * dk, 4), f32, dev)
+    _check(conv_k, "conv_k", (H * dk, 4), f32, dev)
+    if conv_v is not None:
+        _check(conv_v, "conv_v", (H * dv, 4), f32, dev)
+    _check(a_gamma, "a_gamma", (B, T, H), f32, dev)
+    _check(a_beta, "a_beta", (B, T, H), f32, dev)
+    _check(theta, "theta", (H, dk), f32, dev)
+    res = {"q": torch.empty((B, H, T, dk), dtype=qp.dtype, device=dev),
+           "k": torch.empty((B, H, T, dk), dtype=qp.dtype, device=dev),
+           "v": torch.empty((B, H, T, dv), dtype=qp.dtype, device=dev),
+           "gamma": torch.empty((B, H, T), dtype=f32, device=dev),
+           "beta": torch.empty((B, H, T), dtype=f32, device=dev),
+           "lam": torch.empty((H, dk), dtype=f32, device=dev)}
+    st = lib.mesa_frontend(_ptr(qp), _ptr(kp), _ptr(vp), _ptr(conv_q), _ptr(conv_k), _ptr(conv_v), _ptr(a_gamma),
+                           _ptr(a_beta), _ptr(theta), float(gamma_cap), float(l2_eps), B, H, T, dk, dv,
+                           _dtype_code(qp), _ptr(res["q"]), _ptr(res["k"]), _ptr(res["v"]), _ptr(res["gamma"]),
+                           _ptr(res["beta"]), _ptr(res["lam"]), _stream(dev))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_frontend")
+    return res
+
+
+def output_norm(o, weight, eps=1e-6, out_dtype=None):
+    """mesa_output_norm: per-head RMSNorm of the layer output o [B,H,T,d_v] fp32 with
+    weight [H,d_v], into [B,T,H,d_v] of out_dtype (torch.bfloat16 by default)."""
+    torch = _torch()
+    lib = load()
+    B, H, T, dv = o.shape
+    dev = o.device
+    _check(o, "o", (B, H, T, dv), torch.float32, dev)
+    _check(weight, "weight", (H, dv), torch.float32, dev)
+    out_dtype = torch.bfloat16 if out_dtype is None else out_dtype
+    y = torch.empty((B, T, H, dv), dtype=out_dtype, device=dev)
+    st = lib.mesa_output_norm(_ptr(o), _ptr(weight), float(eps), B, H, T, dv, _dtype_code(y), _ptr(y),
+                              _stream(dev))
+    if st != MESA_OK:
+        raise MesaError(st, "mesa_output_norm")
+    return y
 
 
 def forward_noalloc(q, k, v, gamma, beta, lam, n_cg, chunk=64, out=None):

@@ -310,3 +310,42 @@ def test_noalloc_buffer_size_constant():
     assert L.MESA_NOALLOC_SCRATCH_BYTES == 64 << 20
     # exactly the buffer: 512 sequence-chunks of fp32 H_c and G_c at d_k = d_v = 128
     assert L.forward_workspace_bytes(4, 16, 512, 128, 128, 64) == L.MESA_NOALLOC_SCRATCH_BYTES
+
+
+def _front(lib, **kw):
+    a = dict(qp=P["q"], kp=P["k"], vp=P["v"], cq=P["g"], ck=P["b"], cv=None, ag=P["lam"], ab=P["H"],
+             th=P["G"], cap=0.9975, eps=1e-6, B=2, H=3, T=100, dk=128, dv=64, dtype=1, q=P["out"], k=P["qs"],
+             v=P["fh"], gam=P["fg"], bet=P["ws"], lam=P["st"])
+    a.update(kw)
+    return lib.mesa_frontend(a["qp"], a["kp"], a["vp"], a["cq"], a["ck"], a["cv"], a["ag"], a["ab"], a["th"],
+                             a["cap"], a["eps"], a["B"], a["H"], a["T"], a["dk"], a["dv"], a["dtype"], a["q"],
+                             a["k"], a["v"], a["gam"], a["bet"], a["lam"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(qp=None), L.MESA_ERR_NULL),
+    (dict(th=None), L.MESA_ERR_NULL),
+    (dict(lam=None, T=0), L.MESA_ERR_NULL),          # Lambda is written even without tokens
+    (dict(dk=96), L.MESA_ERR_UNSUPPORTED),
+    (dict(dtype=5), L.MESA_ERR_UNSUPPORTED),
+    (dict(B=-1), L.MESA_ERR_SHAPE),
+    (dict(cap=1.5), L.MESA_ERR_ARG),
+    (dict(cap=float("nan")), L.MESA_ERR_ARG),
+    (dict(eps=-1.0), L.MESA_ERR_ARG),
+    (dict(qp=P["q"] + 1), L.MESA_ERR_ARG),            # bf16 needs 2-byte alignment
+    (dict(q=P["k"] + 64), L.MESA_ERR_ARG),            # output overlaps an input
+    (dict(k=P["out"] + 64), L.MESA_ERR_ARG),          # two outputs overlap
+    (dict(H=0), L.MESA_OK),
+])
+def test_frontend_rejects_bad_arguments(lib, kw, status):
+    assert _front(lib, **kw) == status
+
+
+def test_output_norm_rejects_bad_arguments(lib):
+    f = lib.mesa_output_norm
+    assert f(None, P["lam"], 1e-6, 1, 2, 10, 128, 1, P["out"], None) == L.MESA_ERR_NULL
+    assert f(P["q"], P["lam"], -1e-6, 1, 2, 10, 128, 1, P["out"], None) == L.MESA_ERR_ARG
+    assert f(P["q"], P["lam"], 1e-6, 1, 2, 10, 96, 1, P["out"], None) == L.MESA_ERR_UNSUPPORTED
+    assert f(P["q"], P["lam"], 1e-6, 1, 2, 10, 128, 3, P["out"], None) == L.MESA_ERR_UNSUPPORTED
+    assert f(P["q"], P["lam"], 1e-6, 1, 2, 10, 128, 1, P["q"] + 64, None) == L.MESA_ERR_ARG
+    assert f(P["q"], P["lam"], 1e-6, 0, 2, 10, 128, 1, P["out"], None) == L.MESA_OK
