@@ -22,7 +22,8 @@ matrix-core modes.  Decode (256 sequences x 16 heads, d=128, 15 CG steps,
 
 Context entries run the same forward and decode with Alg. 1's relative
 stopping test (eps = 1e-4, at most 30 iterations, the paper's dynamic
-test-time compute setting) and time the backward pass (mesa_backward, App. D).
+test-time compute setting), time the backward pass (mesa_backward, App. D) and
+the layer's front and back end (App. E) at the same shapes.
 The CPU baseline is the fp64 oracle (the sequential recurrence with
 fixed-step CG) on the same workload, run on the host's cores.
 
@@ -212,6 +213,54 @@ def run_long_context(args, torch, L, W):
         del t["plan"]
         res[key] = e
     return res
+
+
+def run_layer_ends(args, torch, L, fw):
+    """The layer's front end (mesa_frontend: projections -> q, k, v, gates, Lambda) and back
+    end (mesa_output_norm: per-head RMSNorm) at the headline workload's shapes, bf16
+    projections with a value filter, bf16 normed output.  Both are HBM-bound; the entry
+    gives time per call and algorithmic bytes over time against the 8 TB/s peak."""
+    w = fw["w"]
+    B, H, T, dk, dv = w.batch, w.heads, w.seq_len, w.d_k, w.d_v
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(11)
+    bf = torch.bfloat16
+    qp = torch.randn((B, T, H, dk), generator=g, device=dev).to(bf)
+    kp = torch.randn((B, T, H, dk), generator=g, device=dev).to(bf)
+    vp = torch.randn((B, T, H, dv), generator=g, device=dev).to(bf)
+    cq, ck = (0.5 * torch.randn((H * dk, 4), generator=g, device=dev) for _ in range(2))
+    cv = 0.5 * torch.randn((H * dv, 4), generator=g, device=dev)
+    ag = 4.0 + torch.randn((B, T, H), generator=g, device=dev)
+    ab = torch.randn((B, T, H), generator=g, device=dev)
+    th = torch.randn((H, dk), generator=g, device=dev)
+    o = fw["plan"].out
+    wt = torch.ones((H, dv), device=dev)
+
+    def timed(fn, reps=10):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    ms_f = timed(lambda: L.frontend(qp, kp, vp, cq, ck, cv, ag, ab, th))
+    ms_n = timed(lambda: L.output_norm(o, wt, 1e-6))
+    th_ = B * H * T
+    bytes_f = th_ * (2 * (2 * dk + dv) * 2 + 4 * 4) + 4 * (H * (2 * dk + dv) * 4 + 2 * H * dk)
+    bytes_n = th_ * dv * (4 + 2)
+    gbps = lambda b, ms: b / (ms / 1e3) / 1e9
+    return {"frontend": {"ms_per_call": ms_f, "tokens_per_s": B * T / (ms_f / 1e3), "bytes": bytes_f,
+                         "hbm_GBps": gbps(bytes_f, ms_f), "hbm_frac": gbps(bytes_f, ms_f) / PEAKS["hbm_gbps"],
+                         "what": "window-4 convolution + SiLU (q, k, v), unit norm (q, k), gates with the cap, "
+                                 "Lambda; bf16 projections [B,T,H,d] -> bf16 [B,H,T,d]"},
+            "output_norm": {"ms_per_call": ms_n, "tokens_per_s": B * T / (ms_n / 1e3), "bytes": bytes_n,
+                            "hbm_GBps": gbps(bytes_n, ms_n), "hbm_frac": gbps(bytes_n, ms_n) / PEAKS["hbm_gbps"],
+                            "what": "per-head RMSNorm, fp32 [B,H,T,d_v] -> bf16 [B,T,H,d_v]"}}
 
 
 def run_forward_dynamic(args, torch, L, fw):
@@ -444,6 +493,7 @@ def main():
     ap.add_argument("--skip-backward", action="store_true")
     ap.add_argument("--skip-modes", action="store_true", help="skip the other precision modes")
     ap.add_argument("--skip-long", action="store_true", help="skip the long-context workload")
+    ap.add_argument("--skip-layer-ends", action="store_true", help="skip the front and back end")
     ap.add_argument("--long-only", action="store_true",
                     help="time only the long-context workload and print its entry (a profiling aid; "
                          "not the metric)")
@@ -483,6 +533,7 @@ def main():
         del src, dst
     head = mode_entry(L, w, args.precision, t)
     modes = None if args.skip_modes else run_other_modes(args, torch, L, fw)
+    ends = None if args.skip_layer_ends else run_layer_ends(args, torch, L, fw)
     dyn = run_forward_dynamic(args, torch, L, fw) if args.eps > 0 else None
     bwd = None if args.skip_backward else run_backward(args, torch, L, fw)
     longctx = None if args.skip_long else run_long_context(args, torch, L, W)
@@ -511,6 +562,7 @@ def main():
         "state_kernel_hbm": head["state_kernel_hbm"],
         "other_precision_modes": modes,
         "long_context": longctx,
+        "layer_front_and_back_end": ends,
         "forward_dynamic_stopping": dyn,
         "backward": bwd,
         "decode": dec,
