@@ -293,9 +293,10 @@ int mesa_forward_noalloc(const void* q, const void* k, const void* v, const floa
  *   v             [batch, heads, seq_len, d_v]   dtype
  *   gamma, beta   [batch, heads, seq_len]        fp32
  *   lambda        [heads, d_k]                   fp32
- * d_k, d_v in {64, 128}.  Arrays need the alignment of their element type; outputs
- * must overlap neither an input nor each other (MESA_ERR_ARG).  batch or seq_len 0
- * writes lambda only; heads 0 is a no-op.  One kernel launch. */
+ * d_k, d_v in {64, 128}.  qp, kp, vp, q, k, v and the three filters must be 16-byte
+ * aligned (they are moved in 16-byte pieces), the other arrays 4-byte aligned; outputs
+ * must overlap neither an input nor each other (MESA_ERR_ARG for either).  batch or
+ * seq_len 0 writes lambda only; heads 0 is a no-op.  One kernel launch. */
 int mesa_frontend(const void* qp, const void* kp, const void* vp, const float* conv_q, const float* conv_k,
                   const float* conv_v, const float* a_gamma, const float* a_beta, const float* theta,
                   float gamma_cap, float l2_eps, int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k,
@@ -310,7 +311,8 @@ int mesa_frontend(const void* qp, const void* kp, const void* vp, const float* c
  *   eps     >= 0
  *   y       [batch, seq_len, heads, d_v]   out_dtype (MESA_DTYPE_F32 or MESA_DTYPE_BF16,
  *           rounded to nearest even)
- * d_v in {64, 128}; y must not overlap o or weight.  One kernel launch. */
+ * d_v in {64, 128}; o, weight and y must be 16-byte aligned and y must not overlap
+ * o or weight (MESA_ERR_ARG).  One kernel launch. */
 int mesa_output_norm(const float* o, const float* weight, float eps, int64_t batch, int64_t heads,
                      int64_t seq_len, int64_t d_v, int out_dtype, void* y, void* stream);
 

@@ -680,14 +680,14 @@ int mesa_frontend(const void* qp, const void* kp, const void* vp, const float* c
         return MESA_ERR_NULL;
     if (tokens > (int64_t(1) << 40)) return MESA_ERR_SHAPE;
     const int64_t es = dtype == MESA_DTYPE_BF16 ? 2 : 4;
+    // the kernel moves projections, outputs and filter rows in 16-byte pieces
     for (const void* ptr : {qp, kp, vp, static_cast<const void*>(q), static_cast<const void*>(k),
-                            static_cast<const void*>(v)})
-        if (uintptr_t(ptr) % es != 0) return MESA_ERR_ARG;
-    for (const void* ptr : {static_cast<const void*>(conv_q), static_cast<const void*>(conv_k),
-                            static_cast<const void*>(conv_v), static_cast<const void*>(a_gamma),
-                            static_cast<const void*>(a_beta), static_cast<const void*>(theta),
-                            static_cast<const void*>(gamma), static_cast<const void*>(beta),
-                            static_cast<const void*>(lambda)})
+                            static_cast<const void*>(v), static_cast<const void*>(conv_q),
+                            static_cast<const void*>(conv_k), static_cast<const void*>(conv_v)})
+        if (uintptr_t(ptr) % 16 != 0) return MESA_ERR_ARG;
+    for (const void* ptr : {static_cast<const void*>(a_gamma), static_cast<const void*>(a_beta),
+                            static_cast<const void*>(theta), static_cast<const void*>(gamma),
+                            static_cast<const void*>(beta), static_cast<const void*>(lambda)})
         if (uintptr_t(ptr) % 4 != 0) return MESA_ERR_ARG;
     const Range ins[] = {range_of(qp, tokens * d_k * es), range_of(kp, tokens * d_k * es),
                          range_of(vp, tokens * d_v * es), range_of(conv_q, heads * d_k * 16),
@@ -724,7 +724,7 @@ int mesa_output_norm(const float* o, const float* weight, float eps, int64_t bat
     if (!o || !weight || !y) return MESA_ERR_NULL;
     if (tokens > (int64_t(1) << 40)) return MESA_ERR_SHAPE;
     const int64_t es = out_dtype == MESA_DTYPE_BF16 ? 2 : 4;
-    if (uintptr_t(o) % 4 != 0 || uintptr_t(weight) % 4 != 0 || uintptr_t(y) % es != 0) return MESA_ERR_ARG;
+    if (uintptr_t(o) % 16 != 0 || uintptr_t(weight) % 16 != 0 || uintptr_t(y) % 16 != 0) return MESA_ERR_ARG;
     const Range out = range_of(y, tokens * d_v * es);
     if (overlaps(out, range_of(o, tokens * d_v * 4)) || overlaps(out, range_of(weight, heads * d_v * 4)))
         return MESA_ERR_ARG;

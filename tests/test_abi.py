@@ -332,7 +332,11 @@ def _front(lib, **kw):
     (dict(cap=1.5), L.MESA_ERR_ARG),
     (dict(cap=float("nan")), L.MESA_ERR_ARG),
     (dict(eps=-1.0), L.MESA_ERR_ARG),
-    (dict(qp=P["q"] + 1), L.MESA_ERR_ARG),            # bf16 needs 2-byte alignment
+    (dict(qp=P["q"] + 1), L.MESA_ERR_ARG),            # projections move in 16-byte pieces
+    (dict(vp=P["v"] + 8), L.MESA_ERR_ARG),
+    (dict(v=P["fh"] + 8), L.MESA_ERR_ARG),
+    (dict(ck=P["b"] + 4), L.MESA_ERR_ARG),            # so do the filter rows
+    (dict(ag=P["lam"] + 2), L.MESA_ERR_ARG),          # gate projections: 4-byte alignment
     (dict(q=P["k"] + 64), L.MESA_ERR_ARG),            # output overlaps an input
     (dict(k=P["out"] + 64), L.MESA_ERR_ARG),          # two outputs overlap
     (dict(H=0), L.MESA_OK),
@@ -349,3 +353,6 @@ def test_output_norm_rejects_bad_arguments(lib):
     assert f(P["q"], P["lam"], 1e-6, 1, 2, 10, 128, 3, P["out"], None) == L.MESA_ERR_UNSUPPORTED
     assert f(P["q"], P["lam"], 1e-6, 1, 2, 10, 128, 1, P["q"] + 64, None) == L.MESA_ERR_ARG
     assert f(P["q"], P["lam"], 1e-6, 0, 2, 10, 128, 1, P["out"], None) == L.MESA_OK
+    assert f(P["q"] + 4, P["lam"], 1e-6, 1, 2, 10, 128, 1, P["out"], None) == L.MESA_ERR_ARG
+    assert f(P["q"], P["lam"] + 4, 1e-6, 1, 2, 10, 128, 1, P["out"], None) == L.MESA_ERR_ARG
+    assert f(P["q"], P["lam"], 1e-6, 1, 2, 10, 128, 1, P["out"] + 8, None) == L.MESA_ERR_ARG
