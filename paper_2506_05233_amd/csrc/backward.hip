@@ -40,51 +40,67 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kC = 64;       // tokens per chunk of the backward
-constexpr int kLdT = 130;    // row stride of [token][feature] tiles
-constexpr int kLdC = 66;     // row stride of [token][token] matrices
+constexpr int kLdT = 132;    // row stride of [token][feature] tiles (16-byte aligned rows)
+constexpr int kLdC = 68;     // row stride of [token][token] matrices (16-byte aligned rows)
 
 // One 16 x 16 output tile += A (16 x K) B (K x 16) on the matrix cores, fp32:
 // A(m, k) = A[m * AM + k * AK], B(k, n) = B[k * BK + n * BN].  With
-// v_mfma_f32_16x16x4f32 lane l supplies A(l % 16, k0 + l / 16) and B(k0 + l / 16, l % 16);
-// element i of the result holds row 4 (l / 16) + i, column l % 16.
-template <int K, int AM, int AK, int BK, int BN>
-__device__ __forceinline__ f32x4 mma16(const float* A, const float* B, f32x4 acc)
+// v_mfma_f32_16x16x4f32 lane l supplies one A(l % 16, k) and one B(k, l % 16) per step;
+// element i of the result holds row 4 (l / 16) + i, column l % 16.  Step s of lane group
+// sl = l / 16 contracts k = 16 (s / 4) + 4 sl + s % 4 (any assignment of the K indices to
+// (step, group) gives the same product as long as A and B agree): a lane's four
+// consecutive steps take four consecutive k, so an operand whose k runs along a row (stride
+// 1, rows 16-byte aligned) comes in one 16-byte load per four steps.
+template <int K, int M, int S>
+__device__ __forceinline__ void load_opnd(const float* X, float (&v)[K / 4], int k0 = 0)
 {
+    static_assert(K % 16 == 0 && (S != 1 || M % 4 == 0), "16-byte operand rows");
     const int lane = threadIdx.x % kWave, r = lane % 16, sl = lane / 16;
-    const float* a = A + r * AM + sl * AK;
-    const float* b = B + sl * BK + r * BN;
-    // all operand loads first (one round trip for the whole contraction), then the products
-    float av[K / 4], bv[K / 4];
+    // all loads first (one round trip for the whole contraction); steps below k0 skipped
 #pragma unroll
-    for (int i = 0; i < K / 4; ++i) {
-        av[i] = a[4 * i * AK];
-        bv[i] = b[4 * i * BK];
+    for (int j = 0; j < K / 16; ++j) {
+        if (16 * j + 16 <= k0) continue;
+        if constexpr (S == 1) {
+            const float4 f = *reinterpret_cast<const float4*>(X + r * M + 16 * j + 4 * sl);
+            v[4 * j] = f.x;
+            v[4 * j + 1] = f.y;
+            v[4 * j + 2] = f.z;
+            v[4 * j + 3] = f.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[4 * j + e] = X[(16 * j + 4 * sl + e) * S + r * M];
+        }
     }
+}
+
+template <int K>
+__device__ __forceinline__ f32x4 mma_steps(const float (&av)[K / 4], const float (&bv)[K / 4], f32x4 acc, int k0 = 0)
+{
 #pragma unroll
-    for (int i = 0; i < K / 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[i], acc, 0, 0, 0);
+    for (int i = 0; i < K / 4; ++i)
+        if (16 * (i / 4) + 16 > k0) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[i], acc, 0, 0, 0);
     return acc;
 }
 
-// mma16 over contraction indices k0 .. K - 1 only (k0 a multiple of 4): for products
+template <int K, int AM, int AK, int BK, int BN>
+__device__ __forceinline__ f32x4 mma16(const float* A, const float* B, f32x4 acc)
+{
+    float av[K / 4], bv[K / 4];
+    load_opnd<K, AM, AK>(A, av);
+    load_opnd<K, BN, BK>(B, bv);
+    return mma_steps<K>(av, bv, acc);
+}
+
+// mma16 over contraction indices k0 .. K - 1 only (k0 a multiple of 16): for products
 // with a causally masked matrix whose entries below k0 are zero.  The skipped steps are
 // resolved at compile time wherever k0 is a constant of an unrolled loop.
 template <int K, int AM, int AK, int BK, int BN>
 __device__ __forceinline__ f32x4 mma16_from(const float* A, const float* B, int k0, f32x4 acc)
 {
-    const int lane = threadIdx.x % kWave, r = lane % 16, sl = lane / 16;
-    const float* a = A + r * AM + sl * AK;
-    const float* b = B + sl * BK + r * BN;
     float av[K / 4], bv[K / 4];
-#pragma unroll
-    for (int i = 0; i < K / 4; ++i) {
-        if (4 * i < k0) continue;
-        av[i] = a[4 * i * AK];
-        bv[i] = b[4 * i * BK];
-    }
-#pragma unroll
-    for (int i = 0; i < K / 4; ++i)
-        if (4 * i >= k0) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[i], acc, 0, 0, 0);
-    return acc;
+    load_opnd<K, AM, AK>(A, av, k0);
+    load_opnd<K, BN, BK>(B, bv, k0);
+    return mma_steps<K>(av, bv, acc, k0);
 }
 
 // The same product split in two: the B operand values of one tile (a global matrix,
@@ -93,22 +109,14 @@ __device__ __forceinline__ f32x4 mma16_from(const float* A, const float* B, int 
 template <int K, int BK, int BN>
 __device__ __forceinline__ void load_b(const float* B, float (&bv)[K / 4])
 {
-    const int lane = threadIdx.x % kWave, r = lane % 16, sl = lane / 16;
-    const float* b = B + sl * BK + r * BN;
-#pragma unroll
-    for (int i = 0; i < K / 4; ++i) bv[i] = b[4 * i * BK];
+    load_opnd<K, BN, BK>(B, bv);
 }
 template <int K, int AM, int AK>
 __device__ __forceinline__ f32x4 mma16_b(const float* A, const float (&bv)[K / 4], f32x4 acc)
 {
-    const int lane = threadIdx.x % kWave, r = lane % 16, sl = lane / 16;
-    const float* a = A + r * AM + sl * AK;
     float av[K / 4];
-#pragma unroll
-    for (int i = 0; i < K / 4; ++i) av[i] = a[4 * i * AK];
-#pragma unroll
-    for (int i = 0; i < K / 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[i], acc, 0, 0, 0);
-    return acc;
+    load_opnd<K, AM, AK>(A, av);
+    return mma_steps<K>(av, bv, acc);
 }
 
 constexpr f32x4 kZero4 = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -256,8 +264,8 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     const int w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave, g = lane / 16, ln = lane % 16;
     const int t = 16 * w + ln;  // this lane's token (column of the transposed products)
 
-    __shared__ float sE[kC * kLdT];   // e_t [t][a]
-    __shared__ float sX[kC * kLdT];   // v_i, then k_i
+    __shared__ __attribute__((aligned(16))) float sE[kC * kLdT];   // e_t [t][a]
+    __shared__ __attribute__((aligned(16))) float sX[kC * kLdT];   // v_i, then k_i
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
 
@@ -553,12 +561,12 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     const float* Gc = a.Gs + mat * int64_t(DV) * DK;
     const float* Hc = a.Hs + mat * int64_t(DK) * DK;
 
-    __shared__ float sT0[kC * kLdT];
-    __shared__ float sT1[kC * kLdT];
-    __shared__ float sM0[kC * kLdC];  // KQ, then M1 = Z ⊙ KQ, then W
-    __shared__ float sM1[kC * kLdC];  // VE, then M2 = Z ⊙ (VE - KE)
-    __shared__ float sM2[kC * kLdC];  // KE, then Qm = beta_p (VE - KE) KQ
-    __shared__ float sZ[kC * kLdC];   // Z[s][t] = zeta_{t,s} (s <= t)
+    __shared__ __attribute__((aligned(16))) float sT0[kC * kLdT];
+    __shared__ __attribute__((aligned(16))) float sT1[kC * kLdT];
+    __shared__ __attribute__((aligned(16))) float sM0[kC * kLdC];  // KQ, then M1 = Z ⊙ KQ, then W
+    __shared__ __attribute__((aligned(16))) float sM1[kC * kLdC];  // VE, then M2 = Z ⊙ (VE - KE)
+    __shared__ __attribute__((aligned(16))) float sM2[kC * kLdC];  // KE, then Qm = beta_p (VE - KE) KQ
+    __shared__ __attribute__((aligned(16))) float sZ[kC * kLdC];   // Z[s][t] = zeta_{t,s} (s <= t)
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
     __shared__ float sBeta[kC], sZe[kC], sPhi[kC];
@@ -690,13 +698,18 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
 
     // ---- dk_s = beta_s (sum_t M2[s][t] q*_t - sum_t M1[s][t] e*_t + zeta_E[s] ((A^G)^T v_s + S^H k_s)),
     //      with v^T A^G k and k^T A^H k = (1/2) k^T S^H k per token
+    // The inter part's operands: lane (sl, n) of the wave of column tile bt holds
+    // A^G[k][16 bt + n] and S^H[16 bt + n][k] (S^H is symmetric; its rows are contiguous)
+    // for the lane's contraction indices k.  The g and h products below load G_c and H_c in
+    // the same patterns, so the Frobenius products of F are the lanes' own sums over their
+    // registers (every element of the four matrices is read once).
+    float bag[DV / 4], bsh[DK / 4];  // in flight during the intra part
     {
         using S = GradSplit<DK>;
         const int bt = S::col(w);
         f32x4 in[4];
-        float bag[DV / 4], bsh[DK / 4];  // the inter part's operands, in flight during the intra part
         load_b<DV, DK, 1>(AG + 16 * bt, bag);  // B(k, n) = A^G[k][16 bt + n]
-        load_b<DK, DK, 1>(SH + 16 * bt, bsh);  // B(k, n) = S^H[k][16 bt + n]
+        load_b<DK, 1, DK>(SH + 16 * bt * DK, bsh);  // B(k, n) = S^H[16 bt + n][k] = S^H[k][16 bt + n]
         __syncthreads();
         tq.put(sT0, valid);
         te.put(sT1, valid);
@@ -742,11 +755,15 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         float bg[DV / 4], bh_[DK / 4];
         load_b<DV, DK, 1>(Gc + 16 * bt, bg);  // B(k, n) = G_c[k][16 bt + n], before the barriers
         __syncthreads();
+        // F = <A^G, G_c> + (1/2) <S^H, H_c>, this lane's elements (A^G and S^H held since dk)
+        float fr = 0.0f;
+#pragma unroll
+        for (int i = 0; i < DV / 4; ++i) fr = fmaf(bag[i], bg[i], fr);
         tq.put(sT0, valid);
         td.put(sT1, valid);
         te.fetch(a.estar, tok0, valid);
         __syncthreads();
-        load_b<DK, DK, 1>(Hc + 16 * bt, bh_);  // B(k, n) = H_c[k][16 bt + n], in flight during g
+        load_b<DK, 1, DK>(Hc + 16 * bt * DK, bh_);  // B(k, n) = H_c[16 bt + n][k] = H_c[k][16 bt + n], in flight during g
         float pg[4][4] = {}, ph[4][4] = {};
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
@@ -758,6 +775,12 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         __syncthreads();  // every wave is done with d in sT1 (g's token sums wait for h's)
         te.put(sT1, valid);
         __syncthreads();
+        {
+            float fh = 0.0f;
+#pragma unroll
+            for (int i = 0; i < DK / 4; ++i) fh = fmaf(bsh[i], bh_[i], fh);
+            fr = fmaf(0.5f, fh, fr);
+        }
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
             if (!S::own(w, st)) continue;
@@ -766,28 +789,8 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
             for (int r = 0; r < 4; ++r) ph[st][r] += eh[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
         }
         reduce_tokens2(pg, ph, sTok[3], sTok[4]);
-        // F: every thread a strided slice of the two Frobenius products, 16-byte loads,
-        // all issued before the products
-        float fr = 0.0f;
-        {
-            constexpr int NG = DV * DK / 4 / kGradThreads, NH = DK * DK / 4 / kGradThreads;
-            float4 x[NG], y[NG], u[NH], v[NH];
-#pragma unroll
-            for (int m = 0; m < NG; ++m) {
-                x[m] = *reinterpret_cast<const float4*>(AG + 4 * (tid + kGradThreads * m));
-                y[m] = *reinterpret_cast<const float4*>(Gc + 4 * (tid + kGradThreads * m));
-            }
-#pragma unroll
-            for (int m = 0; m < NH; ++m) {
-                u[m] = *reinterpret_cast<const float4*>(SH + 4 * (tid + kGradThreads * m));
-                v[m] = *reinterpret_cast<const float4*>(Hc + 4 * (tid + kGradThreads * m));
-            }
-#pragma unroll
-            for (int m = 0; m < NG; ++m) fr += x[m].x * y[m].x + x[m].y * y[m].y + x[m].z * y[m].z + x[m].w * y[m].w;
-#pragma unroll
-            for (int m = 0; m < NH; ++m) fr += 0.5f * (u[m].x * v[m].x + u[m].y * v[m].y + u[m].z * v[m].z + u[m].w * v[m].w);
-        }
-        fr = wave_sum(fr);
+        // (with d_k = 64 two waves share a column tile: the first of them counts it)
+        fr = wave_sum(w % S::WPC == 0 ? fr : 0.0f);
         if (lane == 0) sPart[w] = fr;
         // dLambda of the chunk, -sum_t q*_t e*_t per feature: the tokens split into
         // kGradThreads / DK slices, one per thread of a feature, partial sums through sRed
