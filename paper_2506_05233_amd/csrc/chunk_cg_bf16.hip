@@ -659,6 +659,21 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         }
         if constexpr (READOUT) {
             const float zeta = sZ0[j];
+            // Operands come from LDS in batches issued ahead of their products (the CG
+            // vectors and the state fragments are dead here, so registers are plentiful):
+            // the keys of all four token tiles and the first half of G_c, then the rest of
+            // G_c and the values while the first products run.
+            constexpr int MTH = MTV / 2;
+            bf16x8 kq[4][KS], g0[MTH][KS], g1[MTH][KS], vq[2][MTV];
+#pragma unroll
+            for (int it = 0; it < 4; ++it)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) kq[it][ks] = lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g);
+#pragma unroll
+            for (int mt = 0; mt < MTH; ++mt)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    g0[mt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sGf + ((mt * KS + ks) * kWave + lane) * 8));
             f32x4 zo[4];  // beta_i Z[i][j] over the four token tiles (0 past the causal ones)
 #pragma unroll
             for (int it = 0; it < 4; ++it) zo[it] = decay_weights4(sLg, sBeta, lgj, zlj, 16 * it + 4 * g, j);
@@ -668,30 +683,39 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
                 xb[ks] = pack8(x[2 * ks], x[2 * ks + 1]);
                 xz[ks] = pack8(zeta * x[2 * ks], zeta * x[2 * ks + 1]);
             }
+#pragma unroll
+            for (int mt = 0; mt < MTH; ++mt)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    g1[mt][ks] = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const uint4*>(sGf + (((MTH + mt) * KS + ks) * kWave + lane) * 8));
+            // (the scheduler keeps these loads ahead of the products)
+            __builtin_amdgcn_sched_barrier(0);
             // every wave runs all four token tiles (zo is zero past the causal ones)
             f32x4 sacc[4];
 #pragma unroll
             for (int it = 0; it < 4; ++it) {
                 sacc[it] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks)
-                    sacc[it] = mfma16(lds_frag(sK + (16 * it + ln) * LDK + 32 * ks + 4 * g), xb[ks], sacc[it]);
+                for (int ks = 0; ks < KS; ++ks) sacc[it] = mfma16(kq[it][ks], xb[ks], sacc[it]);
             }
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int mt = 0; mt < MTV; ++mt) vq[u][mt] = lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g);
+            __builtin_amdgcn_sched_barrier(0);
             f32x4 o[MTV];
 #pragma unroll
             for (int mt = 0; mt < MTV; ++mt) {
                 o[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks)
-                    o[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(sGf + ((mt * KS + ks) * kWave + lane) * 8)),
-                                   xz[ks], o[mt]);
+                for (int ks = 0; ks < KS; ++ks) o[mt] = mfma16(mt < MTH ? g0[mt][ks] : g1[mt - MTH][ks], xz[ks], o[mt]);
             }
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
                 const bf16x8 sb = pack8(sacc[2 * u] * zo[2 * u], sacc[2 * u + 1] * zo[2 * u + 1]);
 #pragma unroll
-                for (int mt = 0; mt < MTV; ++mt)
-                    o[mt] = mfma16(lds_frag(sVT + (16 * mt + ln) * LDC + 32 * u + 4 * g), sb, o[mt]);
+                for (int mt = 0; mt < MTV; ++mt) o[mt] = mfma16(vq[u][mt], sb, o[mt]);
             }
 
             if (j < valid) {
