@@ -495,13 +495,22 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         // hardware reciprocal is exact to an ulp.
         {
             const bf16x8 zwb = pack8(zw, zero4);
+            // every LDS operand of the start in one batch: q_j, diag(B'_w) and lambda
+            uint2 qv[MT];
+            f32x4 dgl[MT], lml[MT];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                qv[mt] = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
+                dgl[mt] = *reinterpret_cast<const f32x4*>(&sDiag[wave][16 * mt + 4 * g]);
+                lml[mt] = *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
+            }
+            __builtin_amdgcn_sched_barrier(0);
             f32x4 qf[MT];
             float qq = 0.0f;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                const uint2 qv2 = *reinterpret_cast<const uint2*>(sQ + j * LDK + 16 * mt + 4 * g);
-                qf[mt] = f32x4{bf16_bits_to_f32(qv2.x & 0xffffu), bf16_bits_to_f32(qv2.x >> 16),
-                               bf16_bits_to_f32(qv2.y & 0xffffu), bf16_bits_to_f32(qv2.y >> 16)};
+                qf[mt] = f32x4{bf16_bits_to_f32(qv[mt].x & 0xffffu), bf16_bits_to_f32(qv[mt].x >> 16),
+                               bf16_bits_to_f32(qv[mt].y & 0xffffu), bf16_bits_to_f32(qv[mt].y >> 16)};
                 qq += qf[mt][0] * qf[mt][0] + qf[mt][1] * qf[mt][1] + qf[mt][2] * qf[mt][2] + qf[mt][3] * qf[mt][3];
             }
             qsh = __builtin_amdgcn_frexp_expf(col_sum(qq)) >> 1;  // |q|^2 = m 2^e, m in [1/2, 1)
@@ -515,8 +524,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
                     ksq[e] = (__bf16)(v * v);
                 }
                 const f32x4 dg2 = mfma16(ksq, zwb, zero4);
-                const f32x4 d = zs * *reinterpret_cast<const f32x4*>(&sDiag[wave][16 * mt + 4 * g]) + dg2 +
-                                *reinterpret_cast<const f32x4*>(sLam + 16 * mt + 4 * g);
+                const f32x4 d = zs * dgl[mt] + dg2 + lml[mt];
                 qf[mt] = qs * qf[mt];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) x[mt][e] = qf[mt][e] * __builtin_amdgcn_rcpf(d[e]);
