@@ -121,6 +121,103 @@ __device__ __forceinline__ f32x4 mma16_b(const float* A, const float (&bv)[K / 4
 
 constexpr f32x4 kZero4 = {0.0f, 0.0f, 0.0f, 0.0f};
 
+// bf16 matrix-core products of the bf16 route (v_mfma_f32_16x16x32_bf16): in step b
+// lane (g = l / 16, m = l % 16) supplies A(m, k) and B(k, m) for the eight k = 32 b + 4g +
+// {0..3} and 32 b + 16 + 4g + {0..3}; the result tile has the layout of the fp32
+// products above.  An fp32 operand enters split into bf16 high and low parts (x = hi +
+// lo to ~2^-16 relative): a product of two split operands takes hi*hi + hi*lo + lo*hi, a
+// product with an operand that is exact in bf16 (the route's keys and values) x*hi + x*lo.
+// Operand values are held as fp32, [D / 32][8] per lane.
+
+// Row operand: v[b] = row[32 b + 4g .. +3], row[32 b + 16 + 4g .. +3] (16-byte aligned rows).
+template <int D>
+__device__ __forceinline__ void load_row8(const float* row, float (&v)[D / 32][8])
+{
+    const int g = (threadIdx.x % kWave) / 16;
+#pragma unroll
+    for (int b = 0; b < D / 32; ++b) {
+        const float4 x = *reinterpret_cast<const float4*>(row + 32 * b + 4 * g);
+        const float4 y = *reinterpret_cast<const float4*>(row + 32 * b + 16 + 4 * g);
+        v[b][0] = x.x;
+        v[b][1] = x.y;
+        v[b][2] = x.z;
+        v[b][3] = x.w;
+        v[b][4] = y.x;
+        v[b][5] = y.y;
+        v[b][6] = y.z;
+        v[b][7] = y.w;
+    }
+}
+// Column operand of a row-major matrix: v[b][e] = col[k(b, e) * ld] for the lane's k.
+template <int D>
+__device__ __forceinline__ void load_col8(const float* col, int ld, float (&v)[D / 32][8])
+{
+    const int g = (threadIdx.x % kWave) / 16;
+#pragma unroll
+    for (int b = 0; b < D / 32; ++b)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[b][e] = col[(32 * b + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4)) * ld];
+}
+// The split operand of every step, hi[b] and lo[b].
+template <int D>
+__device__ __forceinline__ void split_steps(const float (&v)[D / 32][8], bf16x8 (&hi)[D / 32], bf16x8 (&lo)[D / 32])
+{
+#pragma unroll
+    for (int b = 0; b < D / 32; ++b)
+        split8(f32x4{v[b][0], v[b][1], v[b][2], v[b][3]}, f32x4{v[b][4], v[b][5], v[b][6], v[b][7]}, hi[b], lo[b]);
+}
+// The A values of step b from a row: row[32 b + 4g .. +3], row[32 b + 16 + 4g .. +3].
+__device__ __forceinline__ void row_step(const float* row, int b, f32x4& x, f32x4& y)
+{
+    const int g = (threadIdx.x % kWave) / 16;
+    x = *reinterpret_cast<const f32x4*>(row + 32 * b + 4 * g);
+    y = *reinterpret_cast<const f32x4*>(row + 32 * b + 16 + 4 * g);
+}
+// acc += A B, A from the rows of an LDS tile holding values exact in bf16, B split
+template <int D>
+__device__ __forceinline__ f32x4 mma_xs(const float* arow, const bf16x8 (&bhi)[D / 32], const bf16x8 (&blo)[D / 32],
+                                        f32x4 acc)
+{
+#pragma unroll
+    for (int b = 0; b < D / 32; ++b) {
+        f32x4 x0, x1;
+        row_step(arow, b, x0, x1);
+        const bf16x8 x = pack8(x0, x1);
+        acc = mfma16(x, bhi[b], acc);
+        acc = mfma16(x, blo[b], acc);
+    }
+    return acc;
+}
+// acc += A B with both split (A from the rows of an fp32 LDS tile)
+template <int D>
+__device__ __forceinline__ f32x4 mma_ss(const float* arow, const bf16x8 (&bhi)[D / 32], const bf16x8 (&blo)[D / 32],
+                                        f32x4 acc)
+{
+#pragma unroll
+    for (int b = 0; b < D / 32; ++b) {
+        f32x4 x0, x1;
+        row_step(arow, b, x0, x1);
+        bf16x8 ahi, alo;
+        split8(x0, x1, ahi, alo);
+        acc = mfma16(ahi, bhi[b], acc);
+        acc = mfma16(ahi, blo[b], acc);
+        acc = mfma16(alo, bhi[b], acc);
+    }
+    return acc;
+}
+// sum over the lane's elements of (hi + lo) y: a Frobenius product with the split
+// values standing for the fp32 ones (to ~2^-16 relative)
+template <int D>
+__device__ __forceinline__ float dot_split(const bf16x8 (&hi)[D / 32], const bf16x8 (&lo)[D / 32], const float (&y)[D / 32][8])
+{
+    float s = 0.0f;
+#pragma unroll
+    for (int b = 0; b < D / 32; ++b)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s = fmaf((float)hi[b][e] + (float)lo[b][e], y[b][e], s);
+    return s;
+}
+
 // Sum over the 16 lanes of a lane row (the columns of a result tile); every lane of
 // the row receives it.
 __device__ __forceinline__ float row16_sum(float x)
@@ -576,6 +673,10 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     __shared__ float sRed2[kGW][kC];  // the same for a second quantity
     __shared__ float sF;
 
+    // The products with the d x d matrices (A^G, S^H, G_c, H_c) run on the bf16 matrix cores
+    // with split operands on the bf16 route (keys and values exact in bf16), on the fp32
+    // matrix cores otherwise.
+    constexpr bool kSplit = std::is_same<Tin, bf16_t>::value;
     // Token tiles in registers: each phase's tiles are fetched while the phase before it
     // computes, then put into sT0 / sT1 once those are free.
     Tile<DK, Tin, kGradThreads> tk;
@@ -600,13 +701,31 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
 
     // ---- gram matrices [p][t] of the chunk's tokens: wave w forms row tile w % 4,
     // column tiles 2 (w / 4) and 2 (w / 4) + 1
+    // (on the bf16 route sT0 holds keys or values, exact in bf16, and the other side
+    // enters split)
     auto gram = [&](float* dst, auto d_tag) {
         constexpr int D = decltype(d_tag)::value;
         const int rt = w % 4;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int tt = 2 * (w / 4) + h;
-            const f32x4 gm = mma16<D, kLdT, 1, 1, kLdT>(sT0 + 16 * rt * kLdT, sT1 + 16 * tt * kLdT, kZero4);
+            f32x4 gm;
+            if constexpr (kSplit) {
+                gm = kZero4;
+#pragma unroll
+                for (int b = 0; b < D / 32; ++b) {
+                    f32x4 a0, a1, b0, b1;
+                    row_step(sT0 + (16 * rt + ln) * kLdT, b, a0, a1);
+                    row_step(sT1 + (16 * tt + ln) * kLdT, b, b0, b1);
+                    bf16x8 bhi, blo;
+                    split8(b0, b1, bhi, blo);
+                    const bf16x8 x = pack8(a0, a1);
+                    gm = mfma16(x, bhi, gm);
+                    gm = mfma16(x, blo, gm);
+                }
+            } else {
+                gm = mma16<D, kLdT, 1, 1, kLdT>(sT0 + 16 * rt * kLdT, sT1 + 16 * tt * kLdT, kZero4);
+            }
 #pragma unroll
             for (int r = 0; r < 4; ++r) dst[(16 * rt + 4 * g + r) * kLdC + 16 * tt + ln] = gm[r];
         }
@@ -675,19 +794,29 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     {
         using S = GradSplit<DV>;
         const int at = S::col(w);
-        float bv[DK / 4];
-        load_b<DK, 1, DK>(AG + 16 * at * DK, bv);  // B(k, n) = A^G[16 at + n][k], before the barriers
+        float bv[DK / 4];                       // fp32 route: B(k, n) = A^G[16 at + n][k]
+        float agr[DK / 32][8];                  // bf16 route: the same, split below
+        bf16x8 arh[DK / 32], arl[DK / 32];
+        if constexpr (kSplit)
+            load_row8<DK>(AG + (16 * at + ln) * DK, agr);  // before the barriers
+        else
+            load_b<DK, 1, DK>(AG + 16 * at * DK, bv);
         __syncthreads();
         tk.put(sT0, valid);
         tq.fetch(a.qstar, tok0, valid);
         te.fetch(a.estar, tok0, valid);
         __syncthreads();
+        if constexpr (kSplit) split_steps<DK>(agr, arh, arl);
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
             if (!S::own(w, st)) continue;
             // M1[s][t] = 0 for t < s: the token sum of row tile st starts at 16 st
             const f32x4 in = mma16_from<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * at, 16 * st, kZero4);
-            const f32x4 ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv, kZero4);  // (K A^G^T)[s][a]
+            f32x4 ex;  // (K A^G^T)[s][a]
+            if constexpr (kSplit)
+                ex = mma_xs<DK>(sT0 + (16 * st + ln) * kLdT, arh, arl, kZero4);
+            else
+                ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv, kZero4);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int t = tok(st, r);
@@ -703,13 +832,20 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     // for the lane's contraction indices k.  The g and h products below load G_c and H_c in
     // the same patterns, so the Frobenius products of F are the lanes' own sums over their
     // registers (every element of the four matrices is read once).
-    float bag[DV / 4], bsh[DK / 4];  // in flight during the intra part
+    float bag[DV / 4], bsh[DK / 4];            // fp32 route, in flight during the intra part
+    bf16x8 agh[DV / 32], agl[DV / 32], shh[DK / 32], shl[DK / 32];  // bf16 route, split
     {
         using S = GradSplit<DK>;
         const int bt = S::col(w);
         f32x4 in[4];
-        load_b<DV, DK, 1>(AG + 16 * bt, bag);  // B(k, n) = A^G[k][16 bt + n]
-        load_b<DK, 1, DK>(SH + 16 * bt * DK, bsh);  // B(k, n) = S^H[16 bt + n][k] = S^H[k][16 bt + n]
+        float agc[DV / 32][8], shr[DK / 32][8];  // bf16 route, in flight during the intra part
+        if constexpr (kSplit) {
+            load_col8<DV>(AG + 16 * bt + ln, DK, agc);     // B(k, n) = A^G[k][16 bt + n]
+            load_row8<DK>(SH + (16 * bt + ln) * DK, shr);  // B(k, n) = S^H[16 bt + n][k]
+        } else {
+            load_b<DV, DK, 1>(AG + 16 * bt, bag);       // B(k, n) = A^G[k][16 bt + n]
+            load_b<DK, 1, DK>(SH + 16 * bt * DK, bsh);  // B(k, n) = S^H[16 bt + n][k] = S^H[k][16 bt + n]
+        }
         __syncthreads();
         tq.put(sT0, valid);
         te.put(sT1, valid);
@@ -729,12 +865,22 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         tq.fetch(a.qstar, tok0, valid);
         td.fetch(a.dout, tok0, valid);
         __syncthreads();
+        if constexpr (kSplit) {
+            split_steps<DV>(agc, agh, agl);
+            split_steps<DK>(shr, shh, shl);
+        }
         float pa[4][4] = {}, pk[4][4] = {};
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
             if (!S::own(w, st)) continue;
-            const f32x4 ag = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bag, kZero4);
-            const f32x4 sh = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bsh, kZero4);
+            f32x4 ag, sh;
+            if constexpr (kSplit) {
+                ag = mma_xs<DV>(sT1 + (16 * st + ln) * kLdT, agh, agl, kZero4);
+                sh = mma_xs<DK>(sT0 + (16 * st + ln) * kLdT, shh, shl, kZero4);
+            } else {
+                ag = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bag, kZero4);
+                sh = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bsh, kZero4);
+            }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int t = tok(st, r), b = 16 * bt + ln;
@@ -752,23 +898,43 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     {
         using S = GradSplit<DK>;
         const int bt = S::col(w);
-        float bg[DV / 4], bh_[DK / 4];
-        load_b<DV, DK, 1>(Gc + 16 * bt, bg);  // B(k, n) = G_c[k][16 bt + n], before the barriers
-        __syncthreads();
-        // F = <A^G, G_c> + (1/2) <S^H, H_c>, this lane's elements (A^G and S^H held since dk)
+        float bg[DV / 4], bh_[DK / 4];                             // fp32 route
+        bf16x8 gch[DV / 32], gcl[DV / 32], hch[DK / 32], hcl[DK / 32];  // bf16 route, split
         float fr = 0.0f;
-#pragma unroll
-        for (int i = 0; i < DV / 4; ++i) fr = fmaf(bag[i], bg[i], fr);
+        float gcc[DV / 32][8];
+        if constexpr (kSplit)
+            load_col8<DV>(Gc + 16 * bt + ln, DK, gcc);  // B(k, n) = G_c[k][16 bt + n], before the barriers
+        else
+            load_b<DV, DK, 1>(Gc + 16 * bt, bg);
+        __syncthreads();
         tq.put(sT0, valid);
         td.put(sT1, valid);
         te.fetch(a.estar, tok0, valid);
         __syncthreads();
-        load_b<DK, 1, DK>(Hc + 16 * bt * DK, bh_);  // B(k, n) = H_c[16 bt + n][k] = H_c[k][16 bt + n], in flight during g
+        // F = <A^G, G_c> + (1/2) <S^H, H_c>, this lane's elements (A^G and S^H held since dk;
+        // on the bf16 route split, standing for the fp32 values to ~2^-16)
+        if constexpr (kSplit) {
+            fr = dot_split<DV>(agh, agl, gcc);
+            split_steps<DV>(gcc, gch, gcl);
+        } else {
+#pragma unroll
+            for (int i = 0; i < DV / 4; ++i) fr = fmaf(bag[i], bg[i], fr);
+        }
+        // B(k, n) = H_c[16 bt + n][k] = H_c[k][16 bt + n], in flight during g
+        float hcr[DK / 32][8];
+        if constexpr (kSplit)
+            load_row8<DK>(Hc + (16 * bt + ln) * DK, hcr);
+        else
+            load_b<DK, 1, DK>(Hc + 16 * bt * DK, bh_);
         float pg[4][4] = {}, ph[4][4] = {};
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
             if (!S::own(w, st)) continue;
-            const f32x4 eg = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bg, kZero4);
+            f32x4 eg;
+            if constexpr (kSplit)
+                eg = mma_ss<DV>(sT1 + (16 * st + ln) * kLdT, gch, gcl, kZero4);
+            else
+                eg = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bg, kZero4);
 #pragma unroll
             for (int r = 0; r < 4; ++r) pg[st][r] += eg[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
         }
@@ -777,14 +943,23 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         __syncthreads();
         {
             float fh = 0.0f;
+            if constexpr (kSplit) {
+                fh = dot_split<DK>(shh, shl, hcr);
+                split_steps<DK>(hcr, hch, hcl);
+            } else {
 #pragma unroll
-            for (int i = 0; i < DK / 4; ++i) fh = fmaf(bsh[i], bh_[i], fh);
+                for (int i = 0; i < DK / 4; ++i) fh = fmaf(bsh[i], bh_[i], fh);
+            }
             fr = fmaf(0.5f, fh, fr);
         }
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
             if (!S::own(w, st)) continue;
-            const f32x4 eh = mma16_b<DK, kLdT, 1>(sT1 + 16 * st * kLdT, bh_, kZero4);
+            f32x4 eh;
+            if constexpr (kSplit)
+                eh = mma_ss<DK>(sT1 + (16 * st + ln) * kLdT, hch, hcl, kZero4);
+            else
+                eh = mma16_b<DK, kLdT, 1>(sT1 + 16 * st * kLdT, bh_, kZero4);
 #pragma unroll
             for (int r = 0; r < 4; ++r) ph[st][r] += eh[r] * sT0[tok(st, r) * kLdT + 16 * bt + ln];
         }

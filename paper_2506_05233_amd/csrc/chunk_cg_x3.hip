@@ -50,28 +50,6 @@ constexpr int kThreads = 256;  // four waves, 16 tokens each
 // their reciprocal (the sub-chunk states are then built without H_c).
 constexpr float kMinDecay = 1e-20f;
 
-// High and low bf16 parts of two fp32 values, each pair packed in one word:
-// hi = bf16(x) (nearest even), lo = bf16(x - hi).  The high parts are widened back
-// to fp32 from the packed word (a shift and a mask) rather than converted again.
-__device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_t& lo)
-{
-    hi = pack_bf16x2(x0, x1);
-    lo = pack_bf16x2(x0 - __uint_as_float(hi << 16), x1 - __uint_as_float(hi & 0xffff0000u));
-}
-
-// The split of the 8 values of two result tiles that form one 8-wide operand
-// (a -> elements 0..3, b -> elements 4..7).
-__device__ __forceinline__ void split8(const f32x4& a, const f32x4& b, bf16x8& hi, bf16x8& lo)
-{
-    uint32_t h[4], l[4];
-    split2(a[0], a[1], h[0], l[0]);
-    split2(a[2], a[3], h[1], l[1]);
-    split2(b[0], b[1], h[2], l[2]);
-    split2(b[2], b[3], h[3], l[3]);
-    hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
-    lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
-}
-
 // Four values as one 8-wide operand: elements 0..3 their high parts, 4..7 their low
 // parts.  Against an operand that repeats its four k-values in both halves, one
 // product sums hi + lo.

@@ -54,6 +54,29 @@ __device__ __forceinline__ uint2 pack4(const f32x4& v)
     return make_uint2(u.x, u.y);
 }
 
+// Split of two fp32 values into bf16 high parts hi = bf16(x) (nearest even) and low
+// parts lo = bf16(x - hi), each pair packed as a | b << 16: hi + lo carries x to
+// ~2^-16 relative, so a product of two split operands, hi*hi + hi*lo + lo*hi with fp32
+// accumulation, is accurate to that order.  The high parts are widened back to fp32
+// from the packed word (a shift and a mask) rather than converted again.
+__device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_t& lo)
+{
+    hi = pack_bf16x2(x0, x1);
+    lo = pack_bf16x2(x0 - __uint_as_float(hi << 16), x1 - __uint_as_float(hi & 0xffff0000u));
+}
+
+// The split of the 8 values of one 8-wide operand (a -> elements 0..3, b -> 4..7).
+__device__ __forceinline__ void split8(const f32x4& a, const f32x4& b, bf16x8& hi, bf16x8& lo)
+{
+    uint32_t h[4], l[4];
+    split2(a[0], a[1], h[0], l[0]);
+    split2(a[2], a[3], h[1], l[1]);
+    split2(b[0], b[1], h[2], l[2]);
+    split2(b[2], b[3], h[3], l[3]);
+    hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
+    lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
+}
+
 // 8 bf16 from LDS: base[0..3] and base[16..19] (the k-index map above).
 __device__ __forceinline__ bf16x8 lds_frag(const uint16_t* base)
 {
