@@ -506,8 +506,8 @@ def main():
                          "(reference dispatch for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (--gpus 1); the (batch, head) sharding "
-              "across GPUs is described in DESIGN.md but not built.", file=sys.stderr)
+        print("bench.py: runs on one GPU only (--gpus 1); sharding the (batch, head) "
+              "sequences across GPUs is not built.", file=sys.stderr)
         sys.exit(2)
 
     import torch

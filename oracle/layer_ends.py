@@ -19,7 +19,7 @@ and App. G.5 ("Notes on precision used in the CG-solver"), per head h:
   back end: the head's output through its RMSNorm before the output projection,
     y_t = o_t / sqrt(mean(o_t^2) + eps) * w_h.
 
-Readings where the paper is silent (listed in the design doc):
+Readings where the paper is silent:
   - the convolution is depthwise (one 4-tap filter per channel of every head) and
     causal with zeros before the sequence start; the paper's w_{i+1} multiplies x_{t-i};
   - the values take the convolution and SiLU only when a filter for them is given

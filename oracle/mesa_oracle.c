@@ -20,7 +20,7 @@
  *     - an exact Cholesky solve (the closed form of Eq. mesa-layer-objective).
  *   Nothing is chunked: this is the sequential recurrence, token by token.
  *
- * Readings adopted where the paper is ambiguous (all listed in the design doc):
+ * Readings adopted where the paper is ambiguous:
  *   - the Jacobi diagonal is that of the system being solved, H_t + Lambda;
  *   - n_cg counts loop iterations, so a solve does n_cg + 1 products;
  *   - the loop stops, after updating x, when the new residual meets Alg. 1's
