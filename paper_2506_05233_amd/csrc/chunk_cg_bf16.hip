@@ -45,6 +45,8 @@
 // state build and the Jacobi start use (so HBM traffic is spread over the whole
 // kernel instead of arriving in bursts at every chunk start); G_c is loaded the
 // same way during the chunk's own build and CG.
+#include <atomic>
+
 #include "mesa_device.hpp"
 #include "mesa_kernels.hpp"
 #include "mesa_mfma.hpp"
@@ -741,26 +743,14 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
     }
 }
 
-// Compute units of the current device (one workgroup of the kernel fills a CU's LDS).
-int device_cus()
-{
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 1;
-    if (dev < 64 && cached[dev] > 0) return cached[dev];
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 1;
-    if (dev < 64) cached[dev] = n;
-    return n;
-}
-
 template <int DK, int DV>
 hipError_t launch_shape(const CgArgs& a, hipStream_t stream)
 {
     const int64_t total = a.s.batch * a.s.heads * a.s.n_chunks;
     if (total <= 0) return hipSuccess;
     if (total > INT32_MAX) return hipErrorInvalidValue;
-    const int64_t cus = device_cus();
+    // one workgroup fills a compute unit's LDS
+    const int64_t cus = device_compute_units();
     const unsigned blocks = unsigned(total < cus ? total : cus);
     // without an output the read-out (and the loads of G_c and v it needs) is skipped
     if (a.out)
@@ -771,6 +761,21 @@ hipError_t launch_shape(const CgArgs& a, hipStream_t stream)
 }
 
 }  // namespace
+
+int device_compute_units()
+{
+    static std::atomic<int> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 1;
+    if (dev < 64) {
+        const int c = cached[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 1;
+    if (dev < 64) cached[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
 
 bool chunk_cg_bf16_supported(const ForwardShape& s)
 {

@@ -680,26 +680,14 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
     }
 }
 
-// Compute units of the current device (one workgroup of the kernel fills a CU's LDS).
-int device_cus_x3()
-{
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 1;
-    if (dev < 64 && cached[dev] > 0) return cached[dev];
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 1;
-    if (dev < 64) cached[dev] = n;
-    return n;
-}
-
 template <int DK, int DV>
 hipError_t launch_shape(const CgArgs& a, hipStream_t stream)
 {
     const int64_t total = a.s.batch * a.s.heads * a.s.n_chunks;
     if (total <= 0) return hipSuccess;
     if (total > INT32_MAX) return hipErrorInvalidValue;
-    const int64_t cus = device_cus_x3();
+    // one workgroup fills a compute unit's LDS
+    const int64_t cus = device_compute_units();
     const unsigned blocks = unsigned(total < cus ? total : cus);
     if (a.out)
         hipLaunchKernelGGL((chunk_cg_x3_kernel<DK, DV, true>), dim3(blocks), dim3(kThreads), 0, stream, a, int(total));

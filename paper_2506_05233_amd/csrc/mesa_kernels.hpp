@@ -182,4 +182,8 @@ struct NormArgs {
 };
 hipError_t launch_output_norm(const NormArgs& a, hipStream_t stream);
 
+// Compute units of the current device (queried once per device), for the persistent
+// kernels that launch one workgroup per unit.
+int device_compute_units();
+
 }  // namespace mesa
