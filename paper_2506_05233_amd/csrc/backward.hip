@@ -448,9 +448,14 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
 // Few long sequences walk in segments, in time reverse of the forward scan's: a first
 // launch computes each later segment's contribution from a zero state, T_s, and its decay
 // D_s; the second starts segment s from E_s = sum_{t>s} (D_{s+1} ... D_{t-1}) T_t.
+// On the bf16 route (SPLIT) the rank-64 products run on the bf16 matrix cores with both
+// operands split into high and low parts (hi*hi + hi*lo + lo*hi, ~2^-16 relative; the
+// fp32 route keeps exact fp32 products): the operands are staged transposed, one bf16
+// plane each for the high and low parts, two tokens per 32-bit word.
 constexpr int kAdjRows = 64;
 constexpr int kLdX = 144;   // row stride of the [token][column] operands (16 banks apart)
 constexpr int kLdR = 80;    // row stride of the [token][row] operands
+constexpr int kLdP = 36;    // row stride in 32-bit words of the split [feature][token] planes
 
 struct AdjSeg {
     int len;      // chunks per segment (the last may be shorter)
@@ -462,7 +467,7 @@ struct AdjSeg {
     float* dec;   // [B*H, total]: D_s
 };
 
-template <int DK, int DV>
+template <int DK, int DV, bool SPLIT>
 __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, AdjSeg sg)
 {
     constexpr int NCT = DK / 16;                  // column tiles
@@ -488,8 +493,16 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, Adj
     // One pass per rank-64 product: the token tile goes to sX, the weighted row slice to
     // sYr.  A^G has one pass per chunk (q*, zeta e), S^H two (q*, -zeta e*) and (e*, -zeta q*).
     // The inputs of the next pass are fetched into registers while this one multiplies.
-    __shared__ float sX[kC * kLdX];   // token tile [j][c]
-    __shared__ float sYr[kC * kLdR];  // weighted row slice [j][r] (rows r0..)
+    // fp32: token tile [j][c] (sX) and weighted row slice [j][r] (rows r0.., sYr);
+    // SPLIT: the same transposed as bf16 planes, [c][j] and [r][j], high then low parts
+    constexpr int kFloats = SPLIT ? 2 * (DK + kAdjRows) * kLdP : kC * (kLdX + kLdR);
+    __shared__ __attribute__((aligned(16))) float sBuf[kFloats];
+    float* const sX = sBuf;
+    float* const sYr = sBuf + kC * kLdX;
+    uint32_t* const pXh = reinterpret_cast<uint32_t*>(sBuf);
+    uint32_t* const pXl = pXh + DK * kLdP;
+    uint32_t* const pYh = pXl + DK * kLdP;
+    uint32_t* const pYl = pYh + kAdjRows * kLdP;
     __shared__ float sW[kC];
     __shared__ float sLg[kC];
     __shared__ int sZl[kC];
@@ -514,6 +527,20 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, Adj
     struct PassRegs {
         float4 t[VT], r[VR];
     };
+    // The thread's 16-byte pieces: piece m is token j, columns (rows) f .. f + 3.  SPLIT
+    // pairs the pieces, tokens 2q and 2q + 1 at the same columns, so a column's two values
+    // form one 32-bit word of the transposed planes; consecutive lanes take consecutive
+    // token pairs, so a wave's stores of one column fall in distinct banks.
+    auto tile_piece = [&](int m, int& j, int& f) {
+        const int e = tid + kThreads * (SPLIT ? m / 2 : m);
+        j = SPLIT ? 2 * (e % (kC / 2)) + m % 2 : e / (DK / 4);
+        f = 4 * (SPLIT ? e / (kC / 2) : e % (DK / 4));
+    };
+    auto row_piece = [&](int m, int& j, int& r) {
+        const int e = tid + kThreads * (SPLIT ? m / 2 : m);
+        j = SPLIT ? 2 * (e % (kC / 2)) + m % 2 : e / (kAdjRows / 4);
+        r = 4 * (SPLIT ? e / (kC / 2) : e % (kAdjRows / 4));
+    };
     // pass p of chunk n: tokens past the end re-read the last valid one (zeroed in put)
     auto fetch = [&](int n, int p, PassRegs& R) {
         const int64_t t0 = int64_t(n) * kC;
@@ -524,18 +551,54 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, Adj
         const int rd = isG ? DV : DK;
 #pragma unroll
         for (int m = 0; m < VT; ++m) {
-            const int e = tid + kThreads * m, j = e / (DK / 4), f = 4 * (e % (DK / 4));
+            int j, f;
+            tile_piece(m, j, f);
             R.t[m] = *reinterpret_cast<const float4*>(ts + (tok0 + min(j, valid - 1)) * DK + f);
         }
 #pragma unroll
         for (int m = 0; m < VR; ++m) {
-            const int e = tid + kThreads * m, j = e / (kAdjRows / 4), r = 4 * (e % (kAdjRows / 4));
+            int j, r;
+            row_piece(m, j, r);
             R.r[m] = *reinterpret_cast<const float4*>(rs + (tok0 + min(j, valid - 1)) * rd + r0 + r);
         }
     };
     // tile rows past `valid` zeroed; row slice weighted by zeta_{j,c-1} (zero past the end),
     // negated for S^H
     auto put = [&](const PassRegs& R, int valid) {
+        if constexpr (SPLIT) {
+#pragma unroll
+            for (int m = 0; m < VT; m += 2) {
+                int j, f;
+                tile_piece(m, j, f);
+                const float4 x0 = j < valid ? R.t[m] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+                const float4 x1 = j + 1 < valid ? R.t[m + 1] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+                const float a0[4] = {x0.x, x0.y, x0.z, x0.w}, a1[4] = {x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    uint32_t hi, lo;
+                    split2(a0[i], a1[i], hi, lo);
+                    pXh[(f + i) * kLdP + j / 2] = hi;
+                    pXl[(f + i) * kLdP + j / 2] = lo;
+                }
+            }
+#pragma unroll
+            for (int m = 0; m < VR; m += 2) {
+                int j, r;
+                row_piece(m, j, r);
+                const float w0 = j < valid ? (isG ? sW[j] : -sW[j]) : 0.0f;
+                const float w1 = j + 1 < valid ? (isG ? sW[j + 1] : -sW[j + 1]) : 0.0f;
+                const float a0[4] = {R.r[m].x, R.r[m].y, R.r[m].z, R.r[m].w};
+                const float a1[4] = {R.r[m + 1].x, R.r[m + 1].y, R.r[m + 1].z, R.r[m + 1].w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    uint32_t hi, lo;
+                    split2(w0 * a0[i], w1 * a1[i], hi, lo);
+                    pYh[(r + i) * kLdP + j / 2] = hi;
+                    pYl[(r + i) * kLdP + j / 2] = lo;
+                }
+            }
+            return;
+        }
 #pragma unroll
         for (int m = 0; m < VT; ++m) {
             const int e = tid + kThreads * m, j = e / (DK / 4), f = 4 * (e % (DK / 4));
@@ -558,9 +621,31 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, Adj
         }
     };
     // X[r][c] += sum_j Yr[j][r] T[j][c]  (A(m, k) = sYr[k][m], B(k, n) = sX[k][n])
+    // SPLIT: in step b lane (g, m) takes tokens 32 b + 4g .. + 3 and 32 b + 16 + 4g .. + 3
+    // of plane row m (the bf16 product convention above), two 8-byte reads per plane
+    auto frag = [&](const uint32_t* plane, int row, int b) {
+        const uint32_t* q = plane + row * kLdP + 16 * b + 2 * g;
+        const uint2 u0 = *reinterpret_cast<const uint2*>(q);
+        const uint2 u1 = *reinterpret_cast<const uint2*>(q + 8);
+        return __builtin_bit_cast(bf16x8, make_uint4(u0.x, u0.y, u1.x, u1.y));
+    };
     auto multiply = [&](f32x4 (&acc)[NCT]) {
+        if constexpr (SPLIT) {
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) acc[ct] = mma16<kC, 1, kLdR, kLdX, 1>(sYr + 16 * w, sX + 16 * ct, acc[ct]);
+            for (int b = 0; b < kC / 32; ++b) {
+                const bf16x8 ah = frag(pYh, 16 * w + ln, b), al = frag(pYl, 16 * w + ln, b);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const bf16x8 bh_ = frag(pXh, 16 * ct + ln, b), bl = frag(pXl, 16 * ct + ln, b);
+                    acc[ct] = mfma16(ah, bh_, acc[ct]);
+                    acc[ct] = mfma16(ah, bl, acc[ct]);
+                    acc[ct] = mfma16(al, bh_, acc[ct]);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) acc[ct] = mma16<kC, 1, kLdR, kLdX, 1>(sYr + 16 * w, sX + 16 * ct, acc[ct]);
+        }
     };
     float dprod = 1.0f;
     float* out = isG ? a.AG : a.SH;
@@ -1077,6 +1162,7 @@ hipError_t launch_bwd_dims(const BwdArgs& a, hipStream_t stream, int stage)
 {
     const int64_t bh = a.s.batch * a.s.heads;
     const unsigned chunks = unsigned(bh * a.s.n_chunks);
+    constexpr bool kSplit = std::is_same<Tin, bf16_t>::value;  // the bf16 route's split products
     switch (stage) {
         case 0:
             hipLaunchKernelGGL((bwd_rhs_kernel<Tin, DK, DV>), dim3(chunks), dim3(kThreads), 0, stream, a);
@@ -1097,12 +1183,12 @@ hipError_t launch_bwd_dims(const BwdArgs& a, hipStream_t stream, int stage)
                 p1.first = 1;
                 p1.count = S - 1;
                 p1.totals = true;
-                hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV>), dim3(unsigned(bh * NTILE * p1.count)), dim3(kThreads), 0,
+                hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV, kSplit>), dim3(unsigned(bh * NTILE * p1.count)), dim3(kThreads), 0,
                                    stream, a, p1);
                 const hipError_t e = hipGetLastError();
                 if (e != hipSuccess) return e;
             }
-            hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV>), dim3(unsigned(bh * NTILE * sg.count)), dim3(kThreads), 0,
+            hipLaunchKernelGGL((bwd_adjoint_kernel<DK, DV, kSplit>), dim3(unsigned(bh * NTILE * sg.count)), dim3(kThreads), 0,
                                stream, a, sg);
             break;
         }
