@@ -344,10 +344,11 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         const f32x4 zw = decay_weights4(sLg, sBeta, lgj, zlj, 16 * wave + 4 * g, j);
 
         // ---- B'_w as bf16 A-fragments: hf[mt][s] covers rows 16mt.., columns 32s..
-        // Every wave runs the same straight-line code: both 32-token steps of the rank update,
-        // with the tokens i >= 16w zeroed in its A operand (rows 32s + 16h.., independent of mt,
-        // loaded once).  Element e of step u is token 32u + 4g + e (e < 4) or 32u + 16 + 4g + e - 4,
-        // so whole halves are in or out: the lower half of step u iff 32u + 16 <= 16w, the upper
+        // Every wave runs the same straight-line code: both 32-token steps of the rank update
+        // (of the second only its lower half: no sub-chunk state takes tokens 48..63), with the
+        // tokens i >= 16w zeroed in its A operand (rows 32s + 16h.., independent of mt, loaded
+        // once).  Element e of step u is token 32u + 4g + e (e < 4) or 32u + 16 + 4g + e - 4, so
+        // whole halves are in or out: the lower half of step u iff 32u + 16 <= 16w, the upper
         // half iff 32u + 32 <= 16w.
         bf16x8 ka[KS][2][2];
 #pragma unroll
@@ -373,17 +374,22 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
 #pragma unroll
                 for (int hh = 0; hh < 2; ++hh) uw[u][hh] = decay_weights4(sLg, sBeta, lgb, zlb, 32 * u + 16 * hh + 4 * g, jb);
         }
-        // Identity operands that copy an A-fragment of H_c, read as a B operand, into the two
-        // 16x16 result tiles (rows 32s + {0..15} and 32s + {16..31}) it belongs to; zero when
-        // the state term is dropped.
-        bf16x8 id_lo, id_hi;
-        const float one = keepH ? 1.0f : 0.0f;
+        // H_c enters through the contraction of the second rank step: no sub-chunk uses the
+        // tokens 48..63 (its upper k-half), so that half carries an identity in the A operand
+        // and an A-fragment half of H_c in the B operand, which adds H_c's rows 32s + {0..15}
+        // or 32s + {16..31} to the 16x16 result tile they belong to (zero when the state term
+        // is dropped).  Two products per result tile: step 0, then step 1's lower half with H_c.
+        uint2 id_up;
+        {
+            bf16x8 t;
+            const float one = keepH ? 1.0f : 0.0f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            id_lo[e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
-            id_lo[4 + e] = (__bf16)0.0f;
-            id_hi[e] = (__bf16)0.0f;
-            id_hi[4 + e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
+            for (int e = 0; e < 4; ++e) {
+                t[e] = (__bf16)0.0f;
+                t[4 + e] = (__bf16)(4 * g + e == ln ? one : 0.0f);
+            }
+            const uint4 u = __builtin_bit_cast(uint4, t);
+            id_up = make_uint2(u.z, u.w);
         }
         // diag(B'_w) goes to sDiag[wave][r]; lanes off the diagonal write a spare slot instead
         const int e_diag = ln - 4 * g;
@@ -411,15 +417,17 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
 #pragma unroll
                     for (int e = 0; e < 8; ++e) bw[u][e] = (__bf16)((float)bw[u][e] * uw[u][e / 4][e % 4]);
             }
+            const uint4 b1 = __builtin_bit_cast(uint4, bw[1]);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                f32x4 lo = mfma16(id_lo, hcs[ks], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
-                f32x4 hi = mfma16(id_hi, hcs[ks], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    lo = mfma16(ka[ks][0][u], bw[u], lo);
-                    hi = mfma16(ka[ks][1][u], bw[u], hi);
-                }
+                const uint4 h = __builtin_bit_cast(uint4, hcs[ks]);
+                const uint4 a0 = __builtin_bit_cast(uint4, ka[ks][0][1]), a1 = __builtin_bit_cast(uint4, ka[ks][1][1]);
+                f32x4 lo = mfma16(ka[ks][0][0], bw[0], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+                f32x4 hi = mfma16(ka[ks][1][0], bw[0], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+                lo = mfma16(__builtin_bit_cast(bf16x8, make_uint4(a0.x, a0.y, id_up.x, id_up.y)),
+                            __builtin_bit_cast(bf16x8, make_uint4(b1.x, b1.y, h.x, h.y)), lo);
+                hi = mfma16(__builtin_bit_cast(bf16x8, make_uint4(a1.x, a1.y, id_up.x, id_up.y)),
+                            __builtin_bit_cast(bf16x8, make_uint4(b1.x, b1.y, h.z, h.w)), hi);
                 hf[mt][ks] = pack8(lo, hi);
                 // B'_w is read only as the A operand of the state products.  Those accept the
                 // accumulation registers directly, so it goes there as it is formed: the loop's
