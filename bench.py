@@ -88,12 +88,13 @@ def state_kernel_bytes(B, H, T, dk, dv, C, in_bytes, state_bytes):
 
 
 def source_hash(kernel):
-    """sha256 over the sources a CG kernel is built from."""
+    """sha256 over the sources a CG kernel is built from and the build script (its flags)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2506_05233_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
         if name.startswith(kernel) or name in ("mesa_device.hpp", "mesa_mfma.hpp", "mesa_kernels.hpp"):
             h.update(open(os.path.join(csrc, name), "rb").read())
+    h.update(open(os.path.join(ROOT, "paper_2506_05233_amd", "build.py"), "rb").read())
     return h.hexdigest()
 
 
