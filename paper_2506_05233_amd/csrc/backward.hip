@@ -346,7 +346,10 @@ struct Tile<D, bf16_t, NT> {
 // tile it, k-slot g stands for token i = 16 it + 4 g + r, exactly the element lane
 // (g, n) holds), and u^T = zeta ⊙ (G_c^T E^T) + K^T S^T comes out as [feature][token]
 // tiles, four consecutive features of one token per lane.  No C x C matrix goes
-// through LDS, so two workgroups share a compute unit.
+// through LDS, so two workgroups share a compute unit.  On the bf16 route the three
+// products run on the bf16 matrix cores with split operands: V E^T and K^T S^T with E and
+// S^T split (values and keys are exact in bf16, two passes per 32-long step), G_c^T E^T
+// with both split (three passes).
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
 {
@@ -374,24 +377,45 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     __syncthreads();
     // S^T[i][t] = beta_i zeta_{t,i} (v_i . e_t) for i <= t (0 otherwise and past the end);
     // row tiles it > w lie wholly above this wave's tokens and are zero
+    constexpr bool kSplit = std::is_same<Tin, bf16_t>::value;
     f32x4 sT[kC / 16];
+    bf16x8 ehi[DV / 32], elo[DV / 32];  // bf16 route: e_t, this lane's token, split
+    if constexpr (kSplit) {
+        float ev[DV / 32][8];
+        load_row8<DV>(sE + (16 * w + ln) * kLdT, ev);
+        split_steps<DV>(ev, ehi, elo);
+    }
 #pragma unroll
     for (int it = 0; it < kC / 16; ++it) {
         if (it > w) {
             sT[it] = kZero4;
             continue;
         }
-        const f32x4 ve = mma16<DV, kLdT, 1, 1, kLdT>(sX + 16 * it * kLdT, sE + 16 * w * kLdT, kZero4);
+        f32x4 ve;
+        if constexpr (kSplit)
+            ve = mma_xs<DV>(sX + (16 * it + ln) * kLdT, ehi, elo, kZero4);
+        else
+            ve = mma16<DV, kLdT, 1, 1, kLdT>(sX + 16 * it * kLdT, sE + 16 * w * kLdT, kZero4);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int i = 16 * it + 4 * g + r;
             sT[it][r] = (i <= t && i < valid) ? a.beta[tok0 + i] * decay_between(sLg, sZl, i, t) * ve[r] : 0.0f;
         }
     }
-    // E^T as the B operand of every G_c^T E^T tile: B(k = a, n = t) = e_t[a]
+    // E^T as the B operand of every G_c^T E^T tile: B(k = a, n = t) = e_t[a] (fp32 route;
+    // the bf16 route has it split in ehi, elo)
     float eb[DV / 4];
+    if constexpr (!kSplit) {
 #pragma unroll
-    for (int i = 0; i < DV / 4; ++i) eb[i] = sE[t * kLdT + 4 * i + g];
+        for (int i = 0; i < DV / 4; ++i) eb[i] = sE[t * kLdT + 4 * i + g];
+    }
+    // bf16 route: S^T as the B operand of K^T S^T, step s = token tiles 2s, 2s + 1 (the
+    // k-slots of lane group g are exactly the tokens this lane holds), split
+    bf16x8 shi[2], slo[2];
+    if constexpr (kSplit) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) split8(sT[2 * u], sT[2 * u + 1], shi[u], slo[u]);
+    }
     __syncthreads();
     tk.put(sX, valid);
     __syncthreads();
@@ -400,8 +424,13 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     // tile ahead
     const float* Gc = a.Gs + (bh * nc + n) * int64_t(DV) * DK;
     auto load_ga = [&](int bt, float (&ga)[DV / 4]) {
+        if constexpr (kSplit) {
+            // the bf16 k-map: step b takes a = 32 b + 4g + {0..3} and 32 b + 16 + 4g + {0..3}
+            load_col8<DV>(Gc + 16 * bt + ln, DK, reinterpret_cast<float (&)[DV / 32][8]>(ga));
+        } else {
 #pragma unroll
-        for (int i = 0; i < DV / 4; ++i) ga[i] = Gc[(4 * i + g) * DK + 16 * bt + ln];
+            for (int i = 0; i < DV / 4; ++i) ga[i] = Gc[(4 * i + g) * DK + 16 * bt + ln];
+        }
     };
     float ga[2][DV / 4];
     load_ga(0, ga[0]);
@@ -409,23 +438,51 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     for (int bt = 0; bt < DK / 16; ++bt) {
         if (bt + 1 < DK / 16) load_ga(bt + 1, ga[(bt + 1) % 2]);
         f32x4 eg = kZero4;
+        if constexpr (kSplit) {
+            bf16x8 ghi[DV / 32], glo[DV / 32];
+            split_steps<DV>(reinterpret_cast<const float (&)[DV / 32][8]>(ga[bt % 2]), ghi, glo);
 #pragma unroll
-        for (int i = 0; i < DV / 4; ++i) eg = __builtin_amdgcn_mfma_f32_16x16x4f32(ga[bt % 2][i], eb[i], eg, 0, 0, 0);
+            for (int b = 0; b < DV / 32; ++b) {
+                eg = mfma16(ghi[b], ehi[b], eg);
+                eg = mfma16(ghi[b], elo[b], eg);
+                eg = mfma16(glo[b], ehi[b], eg);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < DV / 4; ++i) eg = __builtin_amdgcn_mfma_f32_16x16x4f32(ga[bt % 2][i], eb[i], eg, 0, 0, 0);
+        }
         // K^T S^T: A(m = b, k = i) = k_i[16 bt + m] with i = 16 it + 4 g + r (the zero
         // tiles it > w skipped)
-        float ka[kC / 4];
-#pragma unroll
-        for (int it = 0; it < kC / 16; ++it) {
-            if (it > w) continue;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) ka[4 * it + r] = sX[(16 * it + 4 * g + r) * kLdT + 16 * bt + ln];
-        }
         f32x4 sk = kZero4;
+        if constexpr (kSplit) {
+            // step u: tokens 32u + 4g + e and 32u + 16 + 4g + e (exact in bf16)
 #pragma unroll
-        for (int it = 0; it < kC / 16; ++it) {
-            if (it > w) continue;
+            for (int u = 0; u < 2; ++u) {
+                if (2 * u > w) continue;
+                f32x4 k0, k1;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sk = __builtin_amdgcn_mfma_f32_16x16x4f32(ka[4 * it + r], sT[it][r], sk, 0, 0, 0);
+                for (int e = 0; e < 4; ++e) {
+                    k0[e] = sX[(32 * u + 4 * g + e) * kLdT + 16 * bt + ln];
+                    k1[e] = sX[(32 * u + 16 + 4 * g + e) * kLdT + 16 * bt + ln];
+                }
+                const bf16x8 kb = pack8(k0, k1);
+                sk = mfma16(kb, shi[u], sk);
+                sk = mfma16(kb, slo[u], sk);
+            }
+        } else {
+            float ka[kC / 4];
+#pragma unroll
+            for (int it = 0; it < kC / 16; ++it) {
+                if (it > w) continue;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) ka[4 * it + r] = sX[(16 * it + 4 * g + r) * kLdT + 16 * bt + ln];
+            }
+#pragma unroll
+            for (int it = 0; it < kC / 16; ++it) {
+                if (it > w) continue;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) sk = __builtin_amdgcn_mfma_f32_16x16x4f32(ka[4 * it + r], sT[it][r], sk, 0, 0, 0);
+            }
         }
         // lane (g, n): u_t[16 bt + 4g + r], r = 0..3
         if (t < valid) {
