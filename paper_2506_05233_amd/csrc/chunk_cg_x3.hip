@@ -464,18 +464,32 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         // each matrix-core product on split operands.
         auto matvec = [&](const f32x4 (&vec)[MT], f32x4 (&w)[MT]) {
             f32x4 sacc = zero4;
+            bf16x8 vh[KS], vl[KS];
+            split8(vec[0], vec[1], vh[0], vl[0]);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                bf16x8 vh, vl;
-                split8(vec[2 * ks], vec[2 * ks + 1], vh, vl);
+                // the next step's split runs among this step's products
+                if (ks + 1 < KS) split8(vec[2 * ks + 2], vec[2 * ks + 3], vh[ks + 1], vl[ks + 1]);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    w[mt] = mfma16(hfh[mt][ks], vh, ks == 0 ? zero4 : w[mt]);
-                    w[mt] = mfma16(hfh[mt][ks], vl, w[mt]);
-                    w[mt] = mfma16(hfl[mt][ks], vh, w[mt]);
+                    w[mt] = mfma16(hfh[mt][ks], vh[ks], ks == 0 ? zero4 : w[mt]);
+                    w[mt] = mfma16(hfh[mt][ks], vl[ks], w[mt]);
+                    w[mt] = mfma16(hfl[mt][ks], vh[ks], w[mt]);
                 }
-                sacc = mfma16(kf2[ks], vh, sacc);
-                sacc = mfma16(kf2[ks], vl, sacc);
+                sacc = mfma16(kf2[ks], vh[ks], sacc);
+                sacc = mfma16(kf2[ks], vl[ks], sacc);
+                // one matrix-core op, one vector op, ... (the split's vector ops under this
+                // step's products; with one wave per SIMD the wave's own vector work is all
+                // that can fill the matrix cores' latency)
+                if (ks + 1 < KS) {
+#pragma unroll
+                    for (int i = 0; i < 3 * MT; ++i) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+                    }
+                    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
             const bf16x8 sb = split4_stacked(sacc * zw);
 #pragma unroll
