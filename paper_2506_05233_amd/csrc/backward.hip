@@ -129,9 +129,29 @@ constexpr f32x4 kZero4 = {0.0f, 0.0f, 0.0f, 0.0f};
 // product with an operand that is exact in bf16 (the route's keys and values) x*hi + x*lo.
 // Operand values are held as fp32, [D / 32][8] per lane.
 
-// Row operand: v[b] = row[32 b + 4g .. +3], row[32 b + 16 + 4g .. +3] (16-byte aligned rows).
+// Row operand from global memory: v[b] = row[32 b + 4g .. +3], row[32 b + 16 + 4g .. +3] of
+// the row that starts at base + off (16-byte aligned rows).
 template <int D>
-__device__ __forceinline__ void load_row8(const float* row, float (&v)[D / 32][8])
+__device__ __forceinline__ void load_row8(const float* base, int off, float (&v)[D / 32][8])
+{
+    const int g = (threadIdx.x % kWave) / 16;
+#pragma unroll
+    for (int b = 0; b < D / 32; ++b) {
+        const float4 x = load_at<float4>(base, 4u * (off + 32 * b + 4 * g));
+        const float4 y = load_at<float4>(base, 4u * (off + 32 * b + 16 + 4 * g));
+        v[b][0] = x.x;
+        v[b][1] = x.y;
+        v[b][2] = x.z;
+        v[b][3] = x.w;
+        v[b][4] = y.x;
+        v[b][5] = y.y;
+        v[b][6] = y.z;
+        v[b][7] = y.w;
+    }
+}
+// The same from a row of an LDS tile.
+template <int D>
+__device__ __forceinline__ void lds_row8(const float* row, float (&v)[D / 32][8])
 {
     const int g = (threadIdx.x % kWave) / 16;
 #pragma unroll
@@ -148,15 +168,16 @@ __device__ __forceinline__ void load_row8(const float* row, float (&v)[D / 32][8
         v[b][7] = y.w;
     }
 }
-// Column operand of a row-major matrix: v[b][e] = col[k(b, e) * ld] for the lane's k.
+// Column operand of a row-major matrix: v[b][e] = base[k(b, e) * ld + col] for the lane's k.
 template <int D>
-__device__ __forceinline__ void load_col8(const float* col, int ld, float (&v)[D / 32][8])
+__device__ __forceinline__ void load_col8(const float* base, int col, int ld, float (&v)[D / 32][8])
 {
     const int g = (threadIdx.x % kWave) / 16;
 #pragma unroll
     for (int b = 0; b < D / 32; ++b)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[b][e] = col[(32 * b + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4)) * ld];
+        for (int e = 0; e < 8; ++e)
+            v[b][e] = load_at<float>(base, 4u * ((32 * b + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4)) * ld + col));
 }
 // The split operand of every step, hi[b] and lo[b].
 template <int D>
@@ -291,7 +312,7 @@ struct Tile<D, float, NT> {
 #pragma unroll
         for (int m = 0; m < V; ++m) {
             const int e = threadIdx.x + NT * m, i = e / (D / 4), f = 4 * (e % (D / 4));
-            x[m] = *reinterpret_cast<const float4*>(src + (tok0 + min(i, valid - 1)) * D + f);
+            x[m] = load_at<float4>(src + tok0 * D, 4u * (min(i, valid - 1) * D + f));
         }
     }
     __device__ __forceinline__ void put(float* dst, int valid) const
@@ -317,7 +338,7 @@ struct Tile<D, bf16_t, NT> {
 #pragma unroll
         for (int m = 0; m < V; ++m) {
             const int e = threadIdx.x + NT * m, i = e / (D / 8), f = 8 * (e % (D / 8));
-            x[m] = *reinterpret_cast<const uint4*>(src + (tok0 + min(i, valid - 1)) * D + f);
+            x[m] = load_at<uint4>(src + tok0 * D, 2u * (min(i, valid - 1) * D + f));
         }
     }
     __device__ __forceinline__ void put(float* dst, int valid) const
@@ -382,7 +403,7 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     bf16x8 ehi[DV / 32], elo[DV / 32];  // bf16 route: e_t, this lane's token, split
     if constexpr (kSplit) {
         float ev[DV / 32][8];
-        load_row8<DV>(sE + (16 * w + ln) * kLdT, ev);
+        lds_row8<DV>(sE + (16 * w + ln) * kLdT, ev);
         split_steps<DV>(ev, ehi, elo);
     }
 #pragma unroll
@@ -426,7 +447,7 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
     auto load_ga = [&](int bt, float (&ga)[DV / 4]) {
         if constexpr (kSplit) {
             // the bf16 k-map: step b takes a = 32 b + 4g + {0..3} and 32 b + 16 + 4g + {0..3}
-            load_col8<DV>(Gc + 16 * bt + ln, DK, reinterpret_cast<float (&)[DV / 32][8]>(ga));
+            load_col8<DV>(Gc, 16 * bt + ln, DK, reinterpret_cast<float (&)[DV / 32][8]>(ga));
         } else {
 #pragma unroll
             for (int i = 0; i < DV / 4; ++i) ga[i] = Gc[(4 * i + g) * DK + 16 * bt + ln];
@@ -512,7 +533,12 @@ __global__ __launch_bounds__(kThreads) void bwd_rhs_kernel(BwdArgs a)
 constexpr int kAdjRows = 64;
 constexpr int kLdX = 144;   // row stride of the [token][column] operands (16 banks apart)
 constexpr int kLdR = 80;    // row stride of the [token][row] operands
-constexpr int kLdP = 36;    // row stride in 32-bit words of the split [feature][token] planes
+// Row stride in 32-bit words of the split [feature][token] planes.  An 8-byte LDS read
+// serves 16 lanes at a time from 32 four-byte banks; the 16 rows of an operand fragment then
+// start 2 banks apart (34 = 2 mod 32) and fill the banks once.  With 36 (4 apart) rows 8
+// apart shared banks and every fragment read took twice its cycles (14.2k of ~160k cycles
+// per wave were bank-conflict stalls at d = 128; 0.4k with 34).
+constexpr int kLdP = 34;
 
 struct AdjSeg {
     int len;      // chunks per segment (the last may be shorter)
@@ -940,7 +966,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         float agr[DK / 32][8];                  // bf16 route: the same, split below
         bf16x8 arh[DK / 32], arl[DK / 32];
         if constexpr (kSplit)
-            load_row8<DK>(AG + (16 * at + ln) * DK, agr);  // before the barriers
+            load_row8<DK>(AG, (16 * at + ln) * DK, agr);  // before the barriers
         else
             load_b<DK, 1, DK>(AG + 16 * at * DK, bv);
         __syncthreads();
@@ -982,8 +1008,8 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         f32x4 in[4];
         float agc[DV / 32][8], shr[DK / 32][8];  // bf16 route, in flight during the intra part
         if constexpr (kSplit) {
-            load_col8<DV>(AG + 16 * bt + ln, DK, agc);     // B(k, n) = A^G[k][16 bt + n]
-            load_row8<DK>(SH + (16 * bt + ln) * DK, shr);  // B(k, n) = S^H[16 bt + n][k]
+            load_col8<DV>(AG, 16 * bt + ln, DK, agc);     // B(k, n) = A^G[k][16 bt + n]
+            load_row8<DK>(SH, (16 * bt + ln) * DK, shr);  // B(k, n) = S^H[16 bt + n][k]
         } else {
             load_b<DV, DK, 1>(AG + 16 * bt, bag);       // B(k, n) = A^G[k][16 bt + n]
             load_b<DK, 1, DK>(SH + 16 * bt * DK, bsh);  // B(k, n) = S^H[16 bt + n][k] = S^H[k][16 bt + n]
@@ -1045,7 +1071,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         float fr = 0.0f;
         float gcc[DV / 32][8];
         if constexpr (kSplit)
-            load_col8<DV>(Gc + 16 * bt + ln, DK, gcc);  // B(k, n) = G_c[k][16 bt + n], before the barriers
+            load_col8<DV>(Gc, 16 * bt + ln, DK, gcc);  // B(k, n) = G_c[k][16 bt + n], before the barriers
         else
             load_b<DV, DK, 1>(Gc + 16 * bt, bg);
         __syncthreads();
@@ -1065,7 +1091,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         // B(k, n) = H_c[16 bt + n][k] = H_c[k][16 bt + n], in flight during g
         float hcr[DK / 32][8];
         if constexpr (kSplit)
-            load_row8<DK>(Hc + (16 * bt + ln) * DK, hcr);
+            load_row8<DK>(Hc, (16 * bt + ln) * DK, hcr);
         else
             load_b<DK, 1, DK>(Hc + 16 * bt * DK, bh_);
         float pg[4][4] = {}, ph[4][4] = {};

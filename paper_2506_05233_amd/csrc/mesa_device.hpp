@@ -142,4 +142,17 @@ __device__ __forceinline__ int xcd_major_block(int b, int n)
     return x * per + min(x, rem) + local;
 }
 
+// A global load from a base address that every lane shares, at a 32-bit byte offset of the
+// lane's own: the address is an SGPR base plus a 32-bit VGPR offset.  The empty asm makes
+// the offset opaque, so it is formed next to its load; otherwise the compiler may form the
+// offsets of loads that repeat (a tile fetched in several phases) once, as 64-bit
+// addresses, and hold them across the kernel, which spilled in the backward gradient
+// kernel (and each reload of a spilled address waited for every load in flight).
+template <typename T>
+__device__ __forceinline__ T load_at(const void* base, uint32_t byte_off)
+{
+    asm volatile("" : "+v"(byte_off));
+    return *reinterpret_cast<const T*>(static_cast<const char*>(base) + byte_off);
+}
+
 }  // namespace mesa
