@@ -113,8 +113,13 @@ __device__ __forceinline__ float col_sum(float v) { return row_pair_sums(v); }
 // every thread reads back its own slots.
 template <int DK, int DV>
 struct CgSmem {
-    static constexpr int LDK = DK + 8;  // row stride (elements) of token-major tiles
-    static constexpr int LDC = kC + 8;  // row stride of feature-major tiles
+    // Row strides (bf16 elements) of the token-major and feature-major tiles.  A fragment
+    // read (two 8-byte LDS reads per lane) is served 16 lanes at a time from 32 four-byte
+    // banks; rows 2 banks apart (a stride of 2 mod 32 words) give its 16 rows distinct bank
+    // pairs, where rows 4 apart (+8 elements) made every such read take twice its cycles.
+    // The rows are then 8-byte aligned only, so 16-byte stores into them are split.
+    static constexpr int LDK = DK + 4;
+    static constexpr int LDC = kC + 4;
     static constexpr int NKQ = DK / 64;  // staging passes over the key features
     static constexpr int NV = DV / 64;
     static constexpr int kRawSlots = 2 * (2 * NKQ + NV);
@@ -315,10 +320,10 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
 #pragma unroll
         for (int m = 0; m < NKQ; ++m) {
             const int f0 = 64 * m + 8 * fg;
-            *reinterpret_cast<uint4*>(sK + i0 * LDK + f0) = kv[m][0];
-            *reinterpret_cast<uint4*>(sK + i1 * LDK + f0) = kv[m][1];
-            *reinterpret_cast<uint4*>(sQ + i0 * LDK + f0) = qv[m][0];
-            *reinterpret_cast<uint4*>(sQ + i1 * LDK + f0) = qv[m][1];
+            put8x2(sK + i0 * LDK + f0, kv[m][0]);
+            put8x2(sK + i1 * LDK + f0, kv[m][1]);
+            put8x2(sQ + i0 * LDK + f0, qv[m][0]);
+            put8x2(sQ + i1 * LDK + f0, qv[m][1]);
             stage_token_pair(reinterpret_cast<uint32_t*>(sKT), LDC / 2, f0, p2, kv[m][0], kv[m][1]);
             stage_token_pair(reinterpret_cast<uint32_t*>(sKU), LDC / 2, f0, p2, scale_bf16x8(kv[m][0], u0),
                              scale_bf16x8(kv[m][1], u1));

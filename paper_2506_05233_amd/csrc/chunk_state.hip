@@ -120,7 +120,9 @@ __global__ __launch_bounds__(kThreads) void chunk_state_mfma_kernel(StateArgs a)
 {
     constexpr int C = 64;
     constexpr int KST = C / 32;   // 32-token contraction steps per chunk
-    constexpr int LDT = C + 8;    // row stride (elements) of the token-minor LDS tiles
+    // row stride (elements) of the token-minor LDS tiles: 34 words, so the 16 rows of a fragment
+    // read (8 bytes per lane, 16 lanes at a time over 32 banks) fall in distinct bank pairs
+    constexpr int LDT = C + 4;
     const ForwardShape s = a.s;
     const int dk = s.d_k, dv = s.d_v;
     const int nrt = (dk + dv) / 64, nct = dk / 32;
@@ -445,7 +447,7 @@ template <int DK, int DV, bool STORE, bool SPLIT, bool PLAIN = false, bool X3 = 
 __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArgs a, SegPlan sg)
 {
     constexpr int C = 64;
-    constexpr int LDT = C + 8;           // row stride of the [feature][token] tiles
+    constexpr int LDT = C + 4;           // row stride of the [feature][token] tiles (34 words: see above)
     constexpr int NS = DK / 32;          // 32-row blocks of the key features
     constexpr int CS = kWideThreads / kWave / NS;  // column shares per row block
     constexpr int FPP = 8 * kWideThreads / 32;     // features staged per pass (8 per thread group)

@@ -85,6 +85,13 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t* base)
     return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
 }
 
+// 16 bytes into an LDS row that is only 8-byte aligned, as two 8-byte stores.
+__device__ __forceinline__ void put8x2(uint16_t* dst, const uint4& x)
+{
+    reinterpret_cast<uint2*>(dst)[0] = make_uint2(x.x, x.y);
+    reinterpret_cast<uint2*>(dst)[1] = make_uint2(x.z, x.w);
+}
+
 // 8 fp32 from global memory, base[0..3] and base[16..19], rounded to bf16.
 __device__ __forceinline__ bf16x8 gmem_frag(const float* base)
 {
