@@ -309,12 +309,16 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_mma_kernel(CgArgs a)
         float4 hv[NV];
 #pragma unroll
         for (int m = 0; m < NV; ++m) hv[m] = load4(Hc + 4 * (tid + kThreads * m));
+        // keys: lane l stages token l, features 4 (w + 4m) .. + 3, so that consecutive lanes
+        // write consecutive words of the transposed tile sKT (a lane per token of a feature
+        // row; lanes along the features of one token put 16 lanes on each bank)
         constexpr int NKV = C * DK / 4 / kThreads;
+        static_assert(C == kWave, "one token per lane");
         f32x4 kv[NKV];
 #pragma unroll
         for (int m = 0; m < NKV; ++m) {
-            const int e = 4 * (tid + kThreads * m), i = e / DK;
-            kv[m] = load_vec4<DK>(kp + (tok0 + min(i, valid - 1)) * DK + e % DK);
+            const int f = 4 * (w + (kThreads / kWave) * m);
+            kv[m] = load_vec4<DK>(kp + (tok0 + min(lane, valid - 1)) * DK + f);
         }
 #pragma unroll
         for (int m = 0; m < NV; ++m) {
@@ -323,7 +327,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_mma_kernel(CgArgs a)
         }
 #pragma unroll
         for (int m = 0; m < NKV; ++m) {
-            const int e = 4 * (tid + kThreads * m), i = e / DK, f = e % DK;
+            const int i = lane, f = 4 * (w + (kThreads / kWave) * m);
             const f32x4 kk = i < valid ? kv[m] : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
             *reinterpret_cast<float4*>(sK + i * LDH + f) = float4{kk[0], kk[1], kk[2], kk[3]};
 #pragma unroll
@@ -502,13 +506,11 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_mma_kernel(CgArgs a)
         float4 gv[NG];
 #pragma unroll
         for (int m = 0; m < NG; ++m) gv[m] = load4(Gc + 4 * (tid + kThreads * m));
-        constexpr int NVV = C * DV / 4 / kThreads;
+        constexpr int NVV = C * DV / 4 / kThreads;  // values: token per lane, as the keys
         f32x4 vv[NVV];
 #pragma unroll
-        for (int m = 0; m < NVV; ++m) {
-            const int e = 4 * (tid + kThreads * m), i = e / DV;
-            vv[m] = load_vec4<DV>(vp + (tok0 + min(i, valid - 1)) * DV + e % DV);
-        }
+        for (int m = 0; m < NVV; ++m)
+            vv[m] = load_vec4<DV>(vp + (tok0 + min(lane, valid - 1)) * DV + 4 * (w + (kThreads / kWave) * m));
 #pragma unroll
         for (int m = 0; m < NG; ++m) {
             const int e = 4 * (tid + kThreads * m);
@@ -516,7 +518,7 @@ __global__ __launch_bounds__(kThreads) void chunk_cg_f32_mma_kernel(CgArgs a)
         }
 #pragma unroll
         for (int m = 0; m < NVV; ++m) {
-            const int e = 4 * (tid + kThreads * m), i = e / DV, c = e % DV;
+            const int i = lane, c = 4 * (w + (kThreads / kWave) * m);
 #pragma unroll
             for (int q = 0; q < 4; ++q) sKT[(c + q) * LDT + i] = i < valid ? vv[m][q] : 0.0f;
         }
