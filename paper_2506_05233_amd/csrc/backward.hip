@@ -613,11 +613,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, Adj
     // The thread's 16-byte pieces: piece m is token j, columns (rows) f .. f + 3.  SPLIT
     // pairs the pieces, tokens 2q and 2q + 1 at the same columns, so a column's two values
     // form one 32-bit word of the transposed planes; consecutive lanes take consecutive
-    // token pairs, so a wave's stores of one column fall in distinct banks.
+    // token pairs, so a wave's stores of one column fall in distinct banks.  SPLIT also
+    // starts the tile's columns at r0 (mod d_k), so that pieces 0 .. 3 hold this workgroup's
+    // row slice r0 .. r0 + 63 (S^H takes its row operand from them).
     auto tile_piece = [&](int m, int& j, int& f) {
         const int e = tid + kThreads * (SPLIT ? m / 2 : m);
         j = SPLIT ? 2 * (e % (kC / 2)) + m % 2 : e / (DK / 4);
-        f = 4 * (SPLIT ? e / (kC / 2) : e % (DK / 4));
+        f = SPLIT ? (4 * (e / (kC / 2)) + r0) % DK : 4 * (e % (DK / 4));
     };
     auto row_piece = [&](int m, int& j, int& r) {
         const int e = tid + kThreads * (SPLIT ? m / 2 : m);
@@ -732,12 +734,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, Adj
     };
     float dprod = 1.0f;
     float* out = isG ? a.AG : a.SH;
-    PassRegs P0, P1;
-    if (nend > nbeg) fetch(nend - 1, 0, P0);
-    for (int n = nend - 1; n >= nbeg; --n) {
-        const int64_t t0 = int64_t(n) * kC;
-        const int valid = int(min<int64_t>(kC, s.seq_len - t0));
-        const int64_t tok0 = bh * s.seq_len + t0;
+    // the adjoint arriving at this chunk's end goes out; the chunk's gates into sLg, sZl, sW
+    auto chunk_head = [&](int n, int valid, int64_t tok0) {
         if (!sg.totals) {
             float* dst = out + ((bh * nc + n) * nrow + r0 + 16 * w) * int64_t(DK);
 #pragma unroll
@@ -749,31 +747,157 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_adjoint_kernel(BwdArgs a, Adj
             chunk_log_decays(a.gamma + tok0, valid, sLg, sZl);
             sW[tid] = tid < valid ? decay_from_start(sLg, sZl, tid) : 0.0f;  // own lane's values
         }
-        __syncthreads();  // the gates are published; the previous pass is done with sX, sYr
-        put(P0, valid);
-        if (!isG)
-            fetch(n, 1, P1);
-        else if (n > nbeg)
-            fetch(n - 1, 0, P1);
-        __syncthreads();
-        const float D = decay_from_start(sLg, sZl, kC - 1);
-        dprod *= D;
-        f32x4 acc[NCT];
+    };
+    if constexpr (SPLIT) {
+        // A chunk's q* and e* tiles are fetched once for both passes of S^H: each is the token
+        // tile of one pass and, where its features fall in this workgroup's row slice, the
+        // weighted row operand of the other (the row slice r0 .. r0 + 63 is a column range of
+        // the tile: its pieces 0 .. 3).  A^G takes the q* tile
+        // and its own rows of dout.  The next chunk's data is fetched once this chunk's last
+        // put has read the registers, and is in flight during its last product.
+        float4 TA[VT], TB[VT];  // S^H: q*, e*; A^G: q*, dout rows (TB[0 .. VR - 1])
+        auto fetch_chunk = [&](int n) {
+            const int64_t t0 = int64_t(n) * kC;
+            const int valid = int(min<int64_t>(kC, s.seq_len - t0));
+            const int64_t tok0 = bh * s.seq_len + t0;
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) acc[ct] = st[ct] * D;
-        multiply(acc);
-        if (!isG) {
+            for (int m = 0; m < VT; ++m) {
+                int j, f;
+                tile_piece(m, j, f);
+                TA[m] = *reinterpret_cast<const float4*>(a.qstar + (tok0 + min(j, valid - 1)) * DK + f);
+            }
+            if (!isG) {
+#pragma unroll
+                for (int m = 0; m < VT; ++m) {
+                    int j, f;
+                    tile_piece(m, j, f);
+                    TB[m] = *reinterpret_cast<const float4*>(a.estar + (tok0 + min(j, valid - 1)) * DK + f);
+                }
+            } else {
+#pragma unroll
+                for (int m = 0; m < VR; ++m) {
+                    int j, r;
+                    row_piece(m, j, r);
+                    TB[m] = *reinterpret_cast<const float4*>(a.dout + (tok0 + min(j, valid - 1)) * DV + r0 + r);
+                }
+            }
+        };
+        // token tile planes from T (rows past `valid` zero)
+        auto put_x = [&](const float4 (&T)[VT], int valid) {
+#pragma unroll
+            for (int m = 0; m < VT; m += 2) {
+                int j, f;
+                tile_piece(m, j, f);
+                const float4 x0 = j < valid ? T[m] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+                const float4 x1 = j + 1 < valid ? T[m + 1] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+                const float a0[4] = {x0.x, x0.y, x0.z, x0.w}, a1[4] = {x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    uint32_t hi, lo;
+                    split2(a0[i], a1[i], hi, lo);
+                    pXh[(f + i) * kLdP + j / 2] = hi;
+                    pXl[(f + i) * kLdP + j / 2] = lo;
+                }
+            }
+        };
+        // row planes: pieces (m, m + 1) of T hold rows r .. r + 3 of tokens j, j + 1, each
+        // weighted by sgn zeta_{j,c-1} (zero past `valid`)
+        auto put_y_pair = [&](const float4& y0, const float4& y1, int j, int r, int valid, float sgn) {
+            const float w0 = j < valid ? sgn * sW[j] : 0.0f;
+            const float w1 = j + 1 < valid ? sgn * sW[j + 1] : 0.0f;
+            const float a0[4] = {y0.x, y0.y, y0.z, y0.w}, a1[4] = {y1.x, y1.y, y1.z, y1.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                uint32_t hi, lo;
+                split2(w0 * a0[i], w1 * a1[i], hi, lo);
+                pYh[(r + i) * kLdP + j / 2] = hi;
+                pYl[(r + i) * kLdP + j / 2] = lo;
+            }
+        };
+        auto put_y_rows = [&](const float4 (&R)[VT], int valid) {  // A^G: dout rows, +zeta
+#pragma unroll
+            for (int m = 0; m < VR; m += 2) {
+                int j, r;
+                row_piece(m, j, r);
+                put_y_pair(R[m], R[m + 1], j, r, valid, 1.0f);
+            }
+        };
+        auto put_y_tile = [&](const float4 (&T)[VT], int valid) {  // S^H: the tile's slice, -zeta
+#pragma unroll
+            for (int m = 0; m < 4; m += 2) {
+                int j, f;
+                tile_piece(m, j, f);
+                put_y_pair(T[m], T[m + 1], j, f - r0, valid, -1.0f);
+            }
+        };
+        static_assert(kAdjRows == 64 && VR == 4 && VT % 4 == 0, "row slices of 64: two tile piece pairs each");
+        if (nend > nbeg) fetch_chunk(nend - 1);
+        for (int n = nend - 1; n >= nbeg; --n) {
+            const int64_t t0 = int64_t(n) * kC;
+            const int valid = int(min<int64_t>(kC, s.seq_len - t0));
+            const int64_t tok0 = bh * s.seq_len + t0;
+            chunk_head(n, valid, tok0);
+            __syncthreads();  // the gates are published; the previous pass is done with the planes
+            put_x(TA, valid);  // q*
+            if (isG) {
+                put_y_rows(TB, valid);  // zeta dout
+                if (n > nbeg) fetch_chunk(n - 1);
+            } else {
+                put_y_tile(TB, valid);  // -zeta e*
+            }
             __syncthreads();
-            put(P1, valid);
-            if (n > nbeg) fetch(n - 1, 0, P0);
-            __syncthreads();
+            const float D = decay_from_start(sLg, sZl, kC - 1);
+            dprod *= D;
+            f32x4 acc[NCT];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) acc[ct] = st[ct] * D;
             multiply(acc);
-        } else {
-            P0 = P1;
-        }
+            if (!isG) {
+                __syncthreads();
+                put_x(TB, valid);       // e*
+                put_y_tile(TA, valid);  // -zeta q*
+                if (n > nbeg) fetch_chunk(n - 1);
+                __syncthreads();
+                multiply(acc);
+            }
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) st[ct] = acc[ct];
-        __syncthreads();  // every wave is done with this chunk's gates before they are rewritten
+            for (int ct = 0; ct < NCT; ++ct) st[ct] = acc[ct];
+            __syncthreads();  // every wave is done with this chunk's gates before they are rewritten
+        }
+    } else {
+        PassRegs P0, P1;
+        if (nend > nbeg) fetch(nend - 1, 0, P0);
+        for (int n = nend - 1; n >= nbeg; --n) {
+            const int64_t t0 = int64_t(n) * kC;
+            const int valid = int(min<int64_t>(kC, s.seq_len - t0));
+            const int64_t tok0 = bh * s.seq_len + t0;
+            chunk_head(n, valid, tok0);
+            __syncthreads();  // the gates are published; the previous pass is done with sX, sYr
+            put(P0, valid);
+            if (!isG)
+                fetch(n, 1, P1);
+            else if (n > nbeg)
+                fetch(n - 1, 0, P1);
+            __syncthreads();
+            const float D = decay_from_start(sLg, sZl, kC - 1);
+            dprod *= D;
+            f32x4 acc[NCT];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) acc[ct] = st[ct] * D;
+            multiply(acc);
+            if (!isG) {
+                __syncthreads();
+                put(P1, valid);
+                if (n > nbeg) fetch(n - 1, 0, P0);
+                __syncthreads();
+                multiply(acc);
+            } else {
+                P0 = P1;
+            }
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) st[ct] = acc[ct];
+            __syncthreads();  // every wave is done with this chunk's gates before they are rewritten
+        }
     }
     if (sg.totals) {
         float* tb = seg_tile(seg);
