@@ -240,6 +240,9 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
     int cc = blockIdx.x;
     float g_cur = 1.0f, b_cur = 0.0f, lam_cur = 0.0f;
     issue_all(cc, threadIdx.x, g_cur, b_cur, lam_cur);
+    // the first chunk's staging data has landed; later chunks' data is waited for before the
+    // previous chunk's read-out (the staging then does not wait for the read-out's stores)
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     for (;;) {
         // The thread's index values are re-derived for every chunk from a copy the
         // compiler cannot see through, so the many per-lane LDS addresses below are
@@ -266,7 +269,6 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
 
         // ---- this thread's staging data, its gates and this wave's H_c fragments have
         // landed; the barrier publishes H_c and ends the previous chunk's read-out
-        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         uint4 kv[NKQ][2], qv[NKQ][2], vv[NV][2];
 #pragma unroll
         for (int m = 0; m < NKQ; ++m) {
@@ -316,7 +318,7 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         // u_i = beta_i / zeta_{c+i,c}; 0 where zeta_{c+i,c} <= kMinDecay (those tokens
         // only enter sub-chunk states built without H_c, below).
         const float u_l = zeta_l > kMinDecay ? bl * __expf(-lgl) : 0.0f;
-        const float u0 = __shfl(u_l, i0), u1 = __shfl(u_l, i1);
+        const float u0 = shfl_lane(u_l, i0), u1 = shfl_lane(u_l, i1);
 #pragma unroll
         for (int m = 0; m < NKQ; ++m) {
             const int f0 = 64 * m + 8 * fg;

@@ -259,6 +259,9 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
     float g_cur = 1.0f, b_cur = 0.0f, lam_cur = 0.0f;
     load_gates(cc, threadIdx.x, g_cur, b_cur, lam_cur);
     issue_all(cc, threadIdx.x);
+    // the first chunk's staging data has landed; later chunks' data is waited for before the
+    // previous chunk's read-out (the staging then does not wait for the read-out's stores)
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     for (;;) {
         int tid = threadIdx.x;
         asm volatile("" : "+v"(tid));
@@ -292,7 +295,6 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         load_hc(0, hc[0]);
         // ---- this thread's staging data and gates have landed (and the previous chunk's
         // G_c); the barrier ends the previous chunk's read-out
-        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         uint4 kv[NKQ][2], vv[NV][2];
 #pragma unroll
         for (int m = 0; m < NKQ; ++m) {
@@ -335,7 +337,7 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         // rank-update weight relative to the chunk's entering state, u_i = beta_i /
         // zeta_{c+i,c}; 0 where that decay is <= kMinDecay
         const float u_l = zeta_l > kMinDecay ? bl * __expf(-lgl) : 0.0f;
-        const float u0 = __shfl(u_l, i0), u1 = __shfl(u_l, i1);
+        const float u0 = shfl_lane(u_l, i0), u1 = shfl_lane(u_l, i1);
 #pragma unroll
         for (int m = 0; m < NKQ; ++m) {
             const int f0 = 64 * m + 8 * fg;

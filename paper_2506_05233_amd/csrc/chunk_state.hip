@@ -341,7 +341,7 @@ __global__ __launch_bounds__(kThreads) void chunk_state_f32_kernel(StateArgs a)
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const float w = __shfl(wl, tq + 16 * r);
+            const float w = shfl_lane(wl, tq + 16 * r);
             *reinterpret_cast<f32x4*>(wx + (tq + 16 * r) * 16 + q4) = R.x[r];
             *reinterpret_cast<f32x4*>(wy + (tq + 16 * r) * 16 + q4) = w * R.y[r];
         }
@@ -534,7 +534,7 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
             const float lgE = lane_value(lg, C - 1);
             const int zlE = lane_value(zl, C - 1);
             const float wl = live ? R.bet * (zlE > lane ? 0.0f : expf(lgE - lg)) : 0.0f;
-            return Gate{__shfl(wl, 2 * p), __shfl(wl, 2 * p + 1), zlE >= 0 ? 0.0f : expf(lgE)};
+            return Gate{shfl_lane(wl, 2 * p), shfl_lane(wl, 2 * p + 1), zlE >= 0 ? 0.0f : expf(lgE)};
         };
         auto stage_k = [&](const Regs& R, int b) {
             const bool k0 = 2 * p < R.valid, k1 = 2 * p + 1 < R.valid;

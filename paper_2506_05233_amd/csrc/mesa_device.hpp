@@ -86,6 +86,13 @@ __device__ __forceinline__ int wave_scan_max(int x)
 // Value of lane `l` (a wave-uniform index) in every lane.
 __device__ __forceinline__ float lane_value(float x, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l)); }
 __device__ __forceinline__ int lane_value(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
+// x of lane src (0..63, per lane) through ds_bpermute.  HIP's __shfl also forms
+// (lane & ~63) + src for its width argument, a per-lane value that the compiler keeps live
+// (in the larger kernels, in a spill slot).
+__device__ __forceinline__ float shfl_lane(float x, int src)
+{
+    return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(x)));
+}
 
 // Gate log-cumsums of one chunk (Sec. 2: zeta_{t,s} = prod_{s<i<=t} gamma_i).
 // Called by the 64 lanes of ONE wave, for C <= 64 tokens starting at `gamma`
