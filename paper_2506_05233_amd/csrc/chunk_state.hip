@@ -675,7 +675,12 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
         };
 
         constexpr int64_t kSegElems = int64_t(DK) * (DK + DV);  // one segment total, H then G
-        auto seg_total = [&](int t) -> float* { return sg.tot + (bh * (sg.total - 1) + t) * kSegElems + (part ? DK * DK : 0); };
+        // Segment totals are stored in this workgroup's own register order: value (rt, ct, ii)
+        // of thread tid at [(rt NCT + ct) kWideThreads + tid] * 4 + ii of the half's region, so
+        // the walk that adds them reads 16 contiguous bytes per value quadruple (the totals
+        // launch has the walk's work split, so both see the same order)
+        auto seg_total = [&](int t) -> float* { return sg.tot + (bh * (sg.total - 1) + t) * kSegElems + half * (DK * DK); };
+        auto tot_at = [&](int rt, int ct) { return ((rt * NCT + ct) * kWideThreads + tid) * 4; };
         // inputs of the first three chunks (the walk keeps three chunks in flight)
         Regs R0, R1, R2;
         load(nbeg, R0);
@@ -699,12 +704,12 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
 #pragma unroll
                 for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-                    for (int ct = 0; ct < NCT; ++ct)
+                    for (int ct = 0; ct < NCT; ++ct) {
+                        const f32x4 v0 = *reinterpret_cast<const f32x4*>(tb0 + tot_at(rt, ct));
+                        const f32x4 v1 = *reinterpret_cast<const f32x4*>(tb1 + tot_at(rt, ct));
 #pragma unroll
-                        for (int ii = 0; ii < 4; ++ii) {
-                            const int o = tile_off(rt, ct, ii);
-                            acc[rt][ct][ii] += c[0] * tb0[o] + c[1] * tb1[o];
-                        }
+                        for (int ii = 0; ii < 4; ++ii) acc[rt][ct][ii] += c[0] * v0[ii] + c[1] * v1[ii];
+                    }
             }
         }
         float D0, D1 = 1.0f, D2 = 1.0f;
@@ -724,7 +729,11 @@ __global__ __launch_bounds__(kWideThreads) void chunk_state_wide_kernel(StateArg
         // final states
         float* dst = nullptr;
         if (sg.totals) {
-            dst = seg_total(seg);
+            float* tb = seg_total(seg);
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) *reinterpret_cast<f32x4*>(tb + tot_at(rt, ct)) = acc[rt][ct];
             if (half == 0 && tid == 0) sg.dec[bh * sg.total + seg] = dprod;
         } else if (seg == sg.total - 1) {
             float* fin = part ? a.final_G : a.final_H;
@@ -784,13 +793,17 @@ hipError_t launch_wide(const StateArgs& a, hipStream_t stream)
     if (S > 1) {
         // segment totals T_0 .. T_{S-2} (the last one is never needed); fp32-accurate
         // (split products) when fp32 final states come out
+        // (the totals are kept in the walk's thread order, so they take the walk's product
+        // form, which fixes its work split: single products only for the bf16 fragments
+        // without fp32 outputs)
         SegPlan p1 = sg;
         p1.count = S - 1;
         p1.totals = true;
-        if (fin || a.Hs32 || a.x3)
-            launch_wide_kernel<DK, DV, false, true>(a, p1, bh, stream);
-        else
+        const bool single = a.store_chunks && !a.x3 && a.frag && !a.Hs32 && !fin;
+        if (single)
             launch_wide_kernel<DK, DV, false, false>(a, p1, bh, stream);
+        else
+            launch_wide_kernel<DK, DV, false, true>(a, p1, bh, stream);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
