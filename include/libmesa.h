@@ -46,7 +46,18 @@
  *   - Argument checks run on the host before any launch; a failed check
  *     returns its status code and neither launches nor writes anything.
  *   - Value ranges are preconditions and are not checked (that would read
- *     device memory): gamma, beta in [0, 1], Lambda > 0, finite inputs.
+ *     device memory): gamma, beta in [0, 1], Lambda > 0, finite inputs.  When
+ *     the environment variable MESA_CHECK_FINITE is set to anything other than
+ *     "" or "0" (read once, at the library's first call), the forward and decode
+ *     calls (mesa_forward, mesa_forward_ex, mesa_forward_tol, mesa_decode_step,
+ *     mesa_decode_step_tol, mesa_decode_step_packed) check them: before their
+ *     launches they read q, k, v, gamma, beta, lambda and the decode states and
+ *     return MESA_ERR_ARG, having launched nothing of the layer, if a value is
+ *     not finite, a gate lies outside [0, 1] or a lambda is below the smallest
+ *     normal float; after their launches they synchronise `stream` and return
+ *     MESA_ERR_NONFINITE if an output (out, q*, the final or decode states)
+ *     holds a NaN or an infinity.  A debugging aid: it reads device memory and
+ *     serialises the caller with the GPU.
  *   - Outputs must not overlap inputs.  Calls on different streams are
  *     independent; calls that share output or workspace memory must not overlap.
  */
@@ -95,6 +106,7 @@ extern "C" {
 #define MESA_ERR_ARG 4           /* n_cg or eps out of range, misaligned, overlapping  */
 #define MESA_ERR_WORKSPACE 5     /* workspace too small                                */
 #define MESA_ERR_HIP 6           /* the HIP runtime refused a launch                   */
+#define MESA_ERR_NONFINITE 7     /* MESA_CHECK_FINITE: an output holds a NaN or an inf */
 
 /* Supported sizes: d_k, d_v in {64, 128}; chunk in {16, 32, 64}; 0 <= n_cg <= 1024.
  * Any seq_len >= 0 is accepted; a last chunk shorter than `chunk` is handled.

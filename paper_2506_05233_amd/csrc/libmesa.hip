@@ -2,12 +2,14 @@
 // The contract of every entry point is documented in include/libmesa.h.
 #include "libmesa.h"
 
+#include <float.h>
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
+#include <initializer_list>
 #include <mutex>
 
 #include "mesa_kernels.hpp"
@@ -46,6 +48,87 @@ int finish(int status, void* stream)
     if (status != MESA_OK || !sync_after_launch()) return status;
     if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return MESA_ERR_HIP;
     return hipGetLastError() == hipSuccess ? MESA_OK : MESA_ERR_HIP;
+}
+
+// MESA_CHECK_FINITE (read once, at the first call): when set to anything but "" or
+// "0", the forward and decode calls check the values of their inputs before their
+// launches and of their outputs after them (a debugging aid that reads device memory
+// and synchronises the stream).
+bool check_values_on()
+{
+    static const bool on = [] {
+        const char* e = getenv("MESA_CHECK_FINITE");
+        return e != nullptr && e[0] != '\0' && strcmp(e, "0") != 0;
+    }();
+    return on;
+}
+
+// A device array to check: n values (fp32, or bf16 bits), each to lie in [lo, hi] (a NaN
+// lies in no range).
+struct ValueRange {
+    const void* p;
+    int64_t n;
+    bool bf16;
+    float lo, hi;
+};
+constexpr float kFinite = FLT_MAX;
+
+// Set by value_range_kernel when a value lies outside its range; one per device, in the
+// library's code object (host code takes its address from hipGetSymbolAddress).
+__device__ int value_flag;
+
+__global__ __launch_bounds__(64) void value_flag_clear_kernel(int* flag)
+{
+    if (threadIdx.x == 0) flag[0] = 0;
+}
+
+__global__ __launch_bounds__(256) void value_range_kernel(const void* p, int64_t n, int bf16, float lo, float hi,
+                                                          int* flag)
+{
+    bool bad = false;
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const float x = bf16 ? __uint_as_float(uint32_t(static_cast<const uint16_t*>(p)[i]) << 16)
+                             : static_cast<const float*>(p)[i];
+        bad = bad || !(x >= lo && x <= hi);
+    }
+    if (bad) flag[0] = 1;
+}
+
+constexpr int kMaxFlagDevices = 64;
+std::mutex g_flag_mutex;
+int* g_flag_ptr[kMaxFlagDevices] = {};
+
+// Checks `vals` on `stream` (when MESA_CHECK_FINITE is on): returns `bad` if a value lies
+// outside its range, MESA_OK if none does or the checks are off.  Synchronises the stream.
+int check_values(std::initializer_list<ValueRange> vals, void* stream, int bad)
+{
+    if (!check_values_on()) return MESA_OK;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxFlagDevices) return MESA_ERR_HIP;
+    int* flag = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_flag_mutex);
+        if (g_flag_ptr[dev] == nullptr) {
+            void* ptr = nullptr;
+            if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(value_flag)) != hipSuccess || ptr == nullptr) return MESA_ERR_HIP;
+            g_flag_ptr[dev] = static_cast<int*>(ptr);
+        }
+        flag = g_flag_ptr[dev];
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(value_flag_clear_kernel, dim3(1), dim3(64), 0, s, flag);
+    for (const ValueRange& v : vals) {
+        if (v.p == nullptr || v.n <= 0) continue;
+        const int64_t blocks = std::min<int64_t>((v.n + 255) / 256, 1024);
+        hipLaunchKernelGGL(value_range_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, v.p, v.n, int(v.bf16), v.lo,
+                           v.hi, flag);
+    }
+    if (hipGetLastError() != hipSuccess) return MESA_ERR_HIP;
+    int h = 0;
+    if (hipMemcpyAsync(&h, flag, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess) return MESA_ERR_HIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return MESA_ERR_HIP;
+    return h ? bad : MESA_OK;
 }
 
 int check_sizes(int64_t batch, int64_t heads, int64_t seq_len, int64_t d_k, int64_t d_v,
@@ -153,6 +236,26 @@ int validate_forward(const FwdCall& c)
     return MESA_OK;
 }
 
+// MESA_CHECK_FINITE: the forward's inputs (before its launches) and outputs (after them)
+int check_forward_inputs(const FwdCall& c, void* stream)
+{
+    const int64_t nt = c.batch * c.heads * c.seq_len;
+    const bool b16 = c.dtype == MESA_DTYPE_BF16;
+    return check_values({{c.needs_q ? c.q : nullptr, nt * c.d_k, b16, -kFinite, kFinite},
+                         {c.k, nt * c.d_k, b16, -kFinite, kFinite}, {c.v, nt * c.d_v, b16, -kFinite, kFinite},
+                         {c.gamma, nt, false, 0.0f, 1.0f}, {c.beta, nt, false, 0.0f, 1.0f},
+                         {c.needs_q ? c.lambda : nullptr, c.heads * c.d_k, false, FLT_MIN, kFinite}},
+                        stream, MESA_ERR_ARG);
+}
+int check_forward_outputs(const FwdCall& c, void* stream)
+{
+    const int64_t nt = c.batch * c.heads * c.seq_len, bh = c.batch * c.heads;
+    return check_values({{c.out, nt * c.d_v, false, -kFinite, kFinite}, {c.qstar, nt * c.d_k, false, -kFinite, kFinite},
+                         {c.final_H, bh * c.d_k * c.d_k, false, -kFinite, kFinite},
+                         {c.final_G, bh * c.d_v * c.d_k, false, -kFinite, kFinite}},
+                        stream, MESA_ERR_NONFINITE);
+}
+
 ForwardShape shape_of(const FwdCall& c)
 {
     return ForwardShape{c.batch, c.heads, c.seq_len, int(c.d_k), int(c.d_v), c.chunk,
@@ -242,6 +345,7 @@ const char* mesa_status_string(int status)
         case MESA_ERR_ARG: return "n_cg or eps out of range, a misaligned pointer, or an output overlapping an input";
         case MESA_ERR_WORKSPACE: return "workspace too small";
         case MESA_ERR_HIP: return "the HIP runtime refused a launch";
+        case MESA_ERR_NONFINITE: return "an output holds a NaN or an infinity (MESA_CHECK_FINITE)";
         default: return "unknown status";
     }
 }
@@ -274,10 +378,13 @@ int mesa_forward_ex(const void* q, const void* k, const void* v, const float* ga
               !states_only, !states_only || workspace != nullptr};
     int st = validate_forward(c);
     if (st != MESA_OK || batch == 0 || heads == 0) return st;
+    st = check_forward_inputs(c, stream);
+    if (st != MESA_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     st = launch_states(c, !states_only, s);
     if (st == MESA_OK && !states_only) st = launch_solve(c, s);
-    return finish(st, stream);
+    st = finish(st, stream);
+    return st == MESA_OK ? check_forward_outputs(c, stream) : st;
 }
 
 int mesa_forward(const void* q, const void* k, const void* v, const float* gamma,
@@ -363,11 +470,22 @@ int decode_step(float* state_H, float* state_G, const void* q, const void* k, co
                 if (outs[x].lo != outs[x].hi && outs[y].lo != outs[y].hi && overlaps(outs[x], outs[y]))
                     return MESA_ERR_ARG;
     }
-    mesa::DecodeArgs da{batch, heads, int(d_k), int(d_v), dtype == MESA_DTYPE_BF16, state_H, state_G,
+    const bool b16 = dtype == MESA_DTYPE_BF16;
+    const int64_t h_elems = pairs * (packed ? d_k / 2 + 1 : d_k) * d_k, g_elems = pairs * d_v * d_k;
+    st = check_values({{q, pairs * d_k, b16, -kFinite, kFinite}, {k, pairs * d_k, b16, -kFinite, kFinite},
+                       {v, pairs * d_v, b16, -kFinite, kFinite}, {gamma, pairs, false, 0.0f, 1.0f},
+                       {beta, pairs, false, 0.0f, 1.0f}, {lambda, heads * d_k, false, FLT_MIN, kFinite},
+                       {state_H, h_elems, false, -kFinite, kFinite}, {state_G, g_elems, false, -kFinite, kFinite}},
+                      stream, MESA_ERR_ARG);
+    if (st != MESA_OK) return st;
+    mesa::DecodeArgs da{batch, heads, int(d_k), int(d_v), b16, state_H, state_G,
                         q, k, v, gamma, beta, lambda, max_cg, out, eps * eps, steps_out, packed};
-    return finish(mesa::launch_decode_step(da, static_cast<hipStream_t>(stream)) == hipSuccess ? MESA_OK
-                                                                                              : MESA_ERR_HIP,
-                  stream);
+    st = finish(mesa::launch_decode_step(da, static_cast<hipStream_t>(stream)) == hipSuccess ? MESA_OK : MESA_ERR_HIP,
+                stream);
+    if (st != MESA_OK) return st;
+    return check_values({{out, pairs * d_v, false, -kFinite, kFinite}, {state_H, h_elems, false, -kFinite, kFinite},
+                         {state_G, g_elems, false, -kFinite, kFinite}},
+                        stream, MESA_ERR_NONFINITE);
 }
 
 // pack (to_packed) or unpack the symmetric decode state H of batch x heads pairs
@@ -432,10 +550,13 @@ int mesa_forward_tol(const void* q, const void* k, const void* v, const float* g
               eps, steps_out};
     int st = validate_forward(c);
     if (st != MESA_OK || batch == 0 || heads == 0) return st;
+    st = check_forward_inputs(c, stream);
+    if (st != MESA_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     st = launch_states(c, true, s);
     if (st == MESA_OK) st = launch_solve(c, s);
-    return finish(st, stream);
+    st = finish(st, stream);
+    return st == MESA_OK ? check_forward_outputs(c, stream) : st;
 }
 
 }  // extern "C"

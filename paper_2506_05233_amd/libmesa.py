@@ -26,6 +26,7 @@ MESA_ERR_UNSUPPORTED = 3
 MESA_ERR_ARG = 4
 MESA_ERR_WORKSPACE = 5
 MESA_ERR_HIP = 6
+MESA_ERR_NONFINITE = 7
 MESA_MAX_NCG = 1024
 MESA_NOALLOC_SCRATCH_BYTES = 64 << 20
 
