@@ -601,7 +601,6 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
         // so no vector is copied.
         float alpha_d = 0.0f;  // the pending x update: x += alpha_d * (previous direction)
         auto cg_step = [&](f32x4 (&pc)[MT], f32x4 (&pn)[MT]) {
-            if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
             {
                 bf16x8 pb[KS];
 #pragma unroll
@@ -638,19 +637,24 @@ void chunk_cg_bf16_kernel(CgArgs a, int total)
             delta = act2 ? dn : delta;
             active = act2;
         };
-        // Pairs of iterations (an odd count ends with one more); the wave leaves as soon
-        // as every column has stopped.
+        // Pairs of iterations (an odd count ends with one more), the pass's two pieces of the
+        // next chunk's loads issued first: no branch between the two iterations, so the
+        // compiler schedules the end of the first (the direction update) together with the
+        // start of the second (its first products).  The wave leaves at a pass boundary once
+        // every column has stopped (a stopped column takes alpha = 0, so a second iteration
+        // after the last column stopped changes nothing).
         int it = 0;
         bool last_pa = false;  // the last iteration run read its direction from pa
         for (; it + 2 <= a.n_cg; it += 2) {
             if (!__any(active)) break;
+            if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
+            if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
             cg_step(p, pa);
-            last_pa = false;
-            if (!__any(active)) break;
             cg_step(pa, p);
             last_pa = true;
         }
         if (it + 2 > a.n_cg && it < a.n_cg && __any(active)) {
+            if (more && pieces < kPieces) issue_piece(cn, pieces++, tid, g_nx, b_nx, lam_nx);
             cg_step(p, pa);
             last_pa = false;
         }

@@ -579,8 +579,6 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
         // (relative to |q|^2), and without an update when p^T A p is not a positive normal
         // number.  The vector updates are written as in-place fused multiply-adds.
         auto cg_step = [&]() {
-            if (READOUT && gq < 4) load_g(cc, gq++, lane);
-            else if (more && pieces < kPieces) issue_piece(cn, pieces++, tid);
             matvec(p, w);
             f32x4 acc = zero4;
 #pragma unroll
@@ -610,8 +608,25 @@ void chunk_cg_x3_kernel(CgArgs a, int total)
             delta = act2 ? dn : delta;
             active = act2;
         };
-        for (int it = 0; it < a.n_cg; ++it) {
+        // the next loads are issued between iterations
+        auto issue_next = [&]() {
+            if (READOUT && gq < 4) load_g(cc, gq++, lane);
+            else if (more && pieces < kPieces) issue_piece(cn, pieces++, tid);
+        };
+        // two iterations per pass with no branch between them, so the compiler schedules
+        // the end of the first (the direction update) together with the start of the second
+        // (its first products); a stopped column takes alpha = 0, so a wave whose columns have
+        // all stopped after the first loses nothing but time in the second
+        int it = 0;
+        for (; it + 2 <= a.n_cg; it += 2) {
             if (!__any(active)) break;
+            issue_next();
+            issue_next();
+            cg_step();
+            cg_step();
+        }
+        if (it + 2 > a.n_cg && it < a.n_cg && __any(active)) {
+            issue_next();
             cg_step();
         }
         {
