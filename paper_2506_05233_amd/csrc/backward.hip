@@ -209,6 +209,20 @@ __device__ __forceinline__ f32x4 mma_xs(const float* arow, const bf16x8 (&bhi)[D
     }
     return acc;
 }
+// acc += A B, A from the rows of a bf16 LDS tile (exact), B split
+template <int D>
+__device__ __forceinline__ f32x4 mma_bs(const uint16_t* arow, const bf16x8 (&bhi)[D / 32], const bf16x8 (&blo)[D / 32],
+                                        f32x4 acc)
+{
+    const int g = (threadIdx.x % kWave) / 16;
+#pragma unroll
+    for (int b = 0; b < D / 32; ++b) {
+        const bf16x8 x = lds_frag(arow + 32 * b + 4 * g);
+        acc = mfma16(x, bhi[b], acc);
+        acc = mfma16(x, blo[b], acc);
+    }
+    return acc;
+}
 // acc += A B with both split (A from the rows of an fp32 LDS tile)
 template <int D>
 __device__ __forceinline__ f32x4 mma_ss(const float* arow, const bf16x8 (&bhi)[D / 32], const bf16x8 (&blo)[D / 32],
@@ -333,6 +347,18 @@ template <int D, int NT>
 struct Tile<D, bf16_t, NT> {
     static constexpr int V = kC * D / 8 / NT;
     uint4 x[V];
+    // the tile as bf16, rows of `ld` elements (8-byte aligned), rows past `valid` zero
+    __device__ __forceinline__ void put_bf16(uint16_t* dst, int ld, int valid) const
+    {
+#pragma unroll
+        for (int m = 0; m < V; ++m) {
+            const int e = threadIdx.x + NT * m, i = e / (D / 8), f = 8 * (e % (D / 8));
+            const uint4 v = i < valid ? x[m] : make_uint4(0u, 0u, 0u, 0u);
+            uint2* o = reinterpret_cast<uint2*>(dst + i * ld + f);
+            o[0] = make_uint2(v.x, v.y);
+            o[1] = make_uint2(v.z, v.w);
+        }
+    }
     __device__ __forceinline__ void fetch(const bf16_t* src, int64_t tok0, int valid)
     {
 #pragma unroll
@@ -964,6 +990,11 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     __shared__ float sRed[kGW][kC];   // per-wave partial sums per token
     __shared__ float sRed2[kGW][kC];  // the same for a second quantity
     __shared__ float sF;
+    // bf16 route: the chunk's keys stay in LDS as bf16 for the whole kernel (rows of
+    // kLdKb elements: 2 mod 32 words, so the 16 rows of a fragment read fall in distinct
+    // banks), read as matrix-core operands straight from there
+    constexpr int kLdKb = DK + 4;
+    __shared__ __attribute__((aligned(16))) uint16_t sKb[std::is_same<Tin, bf16_t>::value ? kC * kLdKb : 1];
 
     // The products with the d x d matrices (A^G, S^H, G_c, H_c) run on the bf16 matrix cores
     // with split operands on the bf16 route (keys and values exact in bf16), on the fp32
@@ -995,8 +1026,10 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
     // column tiles 2 (w / 4) and 2 (w / 4) + 1
     // (on the bf16 route sT0 holds keys or values, exact in bf16, and the other side
     // enters split)
-    auto gram = [&](float* dst, auto d_tag) {
+    // (A_KEYS: on the bf16 route the A operand, the keys, comes from sKb)
+    auto gram = [&](float* dst, auto d_tag, auto keys_tag) {
         constexpr int D = decltype(d_tag)::value;
+        constexpr bool A_KEYS = decltype(keys_tag)::value;
         const int rt = w % 4;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -1006,12 +1039,18 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
                 gm = kZero4;
 #pragma unroll
                 for (int b = 0; b < D / 32; ++b) {
-                    f32x4 a0, a1, b0, b1;
-                    row_step(sT0 + (16 * rt + ln) * kLdT, b, a0, a1);
+                    f32x4 b0, b1;
                     row_step(sT1 + (16 * tt + ln) * kLdT, b, b0, b1);
                     bf16x8 bhi, blo;
                     split8(b0, b1, bhi, blo);
-                    const bf16x8 x = pack8(a0, a1);
+                    bf16x8 x;
+                    if constexpr (A_KEYS) {
+                        x = lds_frag(sKb + (16 * rt + ln) * kLdKb + 32 * b + 4 * g);
+                    } else {
+                        f32x4 a0, a1;
+                        row_step(sT0 + (16 * rt + ln) * kLdT, b, a0, a1);
+                        x = pack8(a0, a1);
+                    }
                     gm = mfma16(x, bhi, gm);
                     gm = mfma16(x, blo, gm);
                 }
@@ -1022,23 +1061,28 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
             for (int r = 0; r < 4; ++r) dst[(16 * rt + 4 * g + r) * kLdC + 16 * tt + ln] = gm[r];
         }
     };
-    tk.put(sT0, valid);
+    using KeysA = std::integral_constant<bool, kSplit>;
+    using NoKeys = std::integral_constant<bool, false>;
+    if constexpr (kSplit)
+        tk.put_bf16(sKb, kLdKb, valid);
+    else
+        tk.put(sT0, valid);
     tq.put(sT1, valid);
     te.fetch(a.estar, tok0, valid);
     __syncthreads();
-    gram(sM0, std::integral_constant<int, DK>{});  // KQ[p][t] = k_p . q*_t
+    gram(sM0, std::integral_constant<int, DK>{}, KeysA{});  // KQ[p][t] = k_p . q*_t
     __syncthreads();
     te.put(sT1, valid);
     tv.fetch(vp, tok0, valid);
     td.fetch(a.dout, tok0, valid);
     __syncthreads();
-    gram(sM2, std::integral_constant<int, DK>{});  // KE[p][t] = k_p . e*_t
+    gram(sM2, std::integral_constant<int, DK>{}, KeysA{});  // KE[p][t] = k_p . e*_t
     __syncthreads();
     tv.put(sT0, valid);
     td.put(sT1, valid);
-    tk.fetch(kp, tok0, valid);
+    if constexpr (!kSplit) tk.fetch(kp, tok0, valid);
     __syncthreads();
-    gram(sM1, std::integral_constant<int, DV>{});  // VE[p][t] = v_p . e_t
+    gram(sM1, std::integral_constant<int, DV>{}, NoKeys{});  // VE[p][t] = v_p . e_t
     __syncthreads();
 
     // ---- C x C combinations, one row p per wave pass (lane = t): DVK = VE - KE;
@@ -1094,7 +1138,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         else
             load_b<DK, 1, DK>(AG + 16 * at * DK, bv);
         __syncthreads();
-        tk.put(sT0, valid);
+        if constexpr (!kSplit) tk.put(sT0, valid);  // (the bf16 route reads the keys from sKb)
         tq.fetch(a.qstar, tok0, valid);
         te.fetch(a.estar, tok0, valid);
         __syncthreads();
@@ -1106,7 +1150,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
             const f32x4 in = mma16_from<kC, kLdC, 1, kLdT, 1>(sM0 + 16 * st * kLdC, sT1 + 16 * at, 16 * st, kZero4);
             f32x4 ex;  // (K A^G^T)[s][a]
             if constexpr (kSplit)
-                ex = mma_xs<DK>(sT0 + (16 * st + ln) * kLdT, arh, arl, kZero4);
+                ex = mma_bs<DK>(sKb + (16 * st + ln) * kLdKb, arh, arl, kZero4);
             else
                 ex = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bv, kZero4);
 #pragma unroll
@@ -1141,7 +1185,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         __syncthreads();
         tq.put(sT0, valid);
         te.put(sT1, valid);
-        tk.fetch(kp, tok0, valid);
+        if constexpr (!kSplit) tk.fetch(kp, tok0, valid);
         tv.fetch(vp, tok0, valid);
         __syncthreads();
 #pragma unroll
@@ -1152,9 +1196,10 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
             in[st] = pq - pe;
         }
         __syncthreads();
-        tk.put(sT0, valid);
+        // the bf16 route keeps q* in sT0 for the g/h phase (its keys come from sKb)
+        if constexpr (!kSplit) tk.put(sT0, valid);
         tv.put(sT1, valid);
-        tq.fetch(a.qstar, tok0, valid);
+        if constexpr (!kSplit) tq.fetch(a.qstar, tok0, valid);
         td.fetch(a.dout, tok0, valid);
         __syncthreads();
         if constexpr (kSplit) {
@@ -1168,7 +1213,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
             f32x4 ag, sh;
             if constexpr (kSplit) {
                 ag = mma_xs<DV>(sT1 + (16 * st + ln) * kLdT, agh, agl, kZero4);
-                sh = mma_xs<DK>(sT0 + (16 * st + ln) * kLdT, shh, shl, kZero4);
+                sh = mma_bs<DK>(sKb + (16 * st + ln) * kLdKb, shh, shl, kZero4);
             } else {
                 ag = mma16_b<DV, kLdT, 1>(sT1 + 16 * st * kLdT, bag, kZero4);
                 sh = mma16_b<DK, kLdT, 1>(sT0 + 16 * st * kLdT, bsh, kZero4);
@@ -1176,7 +1221,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int t = tok(st, r), b = 16 * bt + ln;
-                const float kb = sT0[t * kLdT + b];
+                const float kb = kSplit ? __uint_as_float(uint32_t(sKb[t * kLdKb + b]) << 16) : sT0[t * kLdT + b];
                 if (t < valid) a.dk[(tok0 + t) * DK + b] = sBeta[t] * (in[st][r] + sZe[t] * (ag[r] + sh[r]));
                 pa[st][r] += kb * ag[r];
                 pk[st][r] += 0.5f * kb * sh[r];
@@ -1199,7 +1244,7 @@ __global__ __launch_bounds__(kGradThreads) void bwd_grad_kernel(BwdArgs a)
         else
             load_b<DV, DK, 1>(Gc + 16 * bt, bg);
         __syncthreads();
-        tq.put(sT0, valid);
+        if constexpr (!kSplit) tq.put(sT0, valid);  // (on the bf16 route q* is still in sT0)
         td.put(sT1, valid);
         te.fetch(a.estar, tok0, valid);
         __syncthreads();
